@@ -1,0 +1,139 @@
+/*
+ * cfo.h -- the oracle: a plain, slow, single-threaded CPU implementation of
+ * the statistical plan evaluation of Cornfigurator (arXiv 2512.14098), used
+ * ONLY as test infrastructure (pytest, the smoke check and the CPU-baseline
+ * leg of the benchmark).  Nothing in the product path may link or call it.
+ *
+ * It shares no code, header, table or helper with the HIP library: every
+ * structure below is the oracle's own.  All floating point is IEEE fp64,
+ * compiled with -ffp-contract=off, and every formula is evaluated in the
+ * written order with one rounding per operation.
+ *
+ * What is computed, and where the paper defines it:
+ *   - request traces (workload with per-type fractions pi_t, Sec. 3.1);
+ *   - phase 1 flow-based throughput R_d, bottleneck and redundancy pruning
+ *     (Sec. 4.3, Alg. 2 phase 1);
+ *   - phase 3 request-level simulation of a physical plan at a given rate
+ *     (Sec. 4.3, Alg. 2 phase 3; Sec. 5.2 CPU-GPU overlap and communication
+ *     overhead);
+ *   - per-type goodput = throughput of requests meeting their latency target
+ *     (Sec. 3.2), maximum achievable goodput over a rate grid (Sec. 6.1),
+ *     argmax selection (Alg. 2, final step).
+ * Where the paper is silent, the readings are the ones listed in the design
+ * notes of this repository (scheduling policy, tie-breaking, gating).
+ */
+#ifndef CFO_H
+#define CFO_H
+#include <stdint.h>
+#include <stddef.h>
+
+#define CFO_MAXC 8   /* components */
+#define CFO_MAXT 8   /* request types */
+#define CFO_MAXV 16  /* nodes per plan */
+#define CFO_MAXA 2   /* alternative paths per type (k_s = 2, Sec. 4.2) */
+#define CFO_MAXX 64  /* executors per plan */
+#define CFO_MAXB 256 /* max batch */
+
+enum { CFO_ENC = 0, CFO_LLM = 1, CFO_GEN = 2 };
+
+/* per-request attributes (index into the attribute vector) */
+enum {
+  CFO_A_PROMPT = 0, CFO_A_OUT = 1, CFO_A_PATCHES = 2, CFO_A_AUDIN_MS = 3,
+  CFO_A_AUDOUT_MS = 4, CFO_A_AUDIN_TOK = 5, CFO_A_AUDOUT_TOK = 6, CFO_NATTR = 7
+};
+
+/* length distributions */
+enum { CFO_D_NONE = 0, CFO_D_CONST = 1, CFO_D_LOGNORMAL = 2, CFO_D_EXP = 3 };
+/* image-count distributions */
+enum { CFO_I_NONE = 0, CFO_I_CONST = 1, CFO_I_UNIFORM = 2 };
+
+/* per-triple status bits */
+#define CFO_ST_INVALID 1u   /* route does not fit the plan */
+#define CFO_ST_DEADLOCK 2u  /* event queue drained with requests unfinished */
+
+typedef struct {
+  int32_t kind;      /* CFO_D_* */
+  int32_t pad;
+  double p0, p1;     /* CONST: value p0; LOGNORMAL: mu=p0 sigma=p1; EXP: mean p0 */
+  double scale;      /* multiplier applied before rounding (1 tokens, 1000 ms) */
+  int64_t lo, hi;    /* clamp */
+} cfo_dist;
+
+typedef struct {
+  int32_t n_comp, n_types;
+  int32_t kind[CFO_MAXC];
+  double k0[CFO_MAXC], k1[CFO_MAXC], k2[CFO_MAXC]; /* batch: (k0 + k1*X) + k2*n */
+  double d0[CFO_MAXC], d1[CFO_MAXC];               /* LLM decode: d0 + d1*n   */
+  uint32_t x_sel[CFO_MAXC];     /* bitmask of attributes summed into X     */
+  int32_t nout_attr[CFO_MAXC];  /* LLM: attribute giving the output length */
+  int32_t gate_src[CFO_MAXC];   /* LLM gated by this component, or -1      */
+  int32_t batch_cap[CFO_MAXC];  /* stage batch = min(node batch, cap)      */
+  double comm_s, cpu_pre_s;
+  uint32_t weight[CFO_MAXT];
+  uint32_t path_mask[CFO_MAXT], out_mask[CFO_MAXT], prefill_only[CFO_MAXT];
+  uint32_t parents[CFO_MAXT][CFO_MAXC];
+  int32_t img_kind[CFO_MAXT], img_lo[CFO_MAXT], img_hi[CFO_MAXT];
+  int32_t patch_lo, patch_hi;
+  cfo_dist len[CFO_MAXT][4];    /* prompt, out, aud_in_ms, aud_out_ms */
+  double slo[CFO_MAXT][4];      /* ttft, tpot, e2e, media (<=; +inf = none) */
+  uint32_t theta_num, theta_den;
+} cfo_model;
+
+typedef struct {
+  int32_t n_seeds, n_req;
+  uint64_t *arr_ticks;            /* [S][n] inclusive prefix of gap ticks */
+  uint8_t *type, *n_img;          /* [S][n] */
+  uint16_t *patches, *prompt, *out;
+  uint32_t *aud_in_ms, *aud_out_ms;
+  uint64_t *rkey0, *rkey1;        /* 16-bit replica keys, component c at bits 16*(c%4) of word c/4 */
+  uint32_t *akey;                 /* alternative-choice key */
+} cfo_trace;
+
+/* plan table: structure of arrays, field-slot major ([slot][P]) */
+typedef struct {
+  int32_t P;
+  const uint8_t *n_nodes;     /* [P] */
+  const uint8_t *node_comp;   /* [16][P] component bitmask */
+  const uint8_t *node_rep;    /* [16][P] replicas m_v */
+  const uint16_t *node_batch; /* [16][P] max batch B_v */
+  const uint8_t *node_gpus;   /* [16][P] GPUs per replica */
+  const uint8_t *n_alt;       /* [8][P] */
+  const uint8_t *alt_w;       /* [8][2][P] weight in tenths */
+  const uint8_t *alt_node;    /* [8][2][8][P] node per component, 255 = none */
+} cfo_plans;
+
+/* --- primitives (exposed for the tests that pin them) --- */
+void cfo_philox(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]);
+double cfo_log(double x);
+double cfo_exp(double x);
+double cfo_uniform(uint64_t x);
+
+/* --- hot-path steps --- */
+int cfo_trace_gen(const cfo_model *m, const uint64_t *seeds, int32_t n_seeds, int32_t n_req,
+                  cfo_trace *tr, uint64_t *moments /* [S][T][8] */);
+
+int cfo_eval_coarse(const cfo_model *m, const cfo_plans *pl, const uint64_t *moments /* [T][8] */,
+                    int32_t n_gpus, double *rd, int32_t *bottleneck, uint8_t *flags);
+
+int cfo_select_topk(const double *rd, const uint8_t *flags, int32_t P, int32_t k,
+                    int32_t *ids, int32_t *n_selected);
+
+int cfo_rate_grid(const double *rd, const int32_t *ids, int32_t n, int32_t K,
+                  double alpha_max, double *rates);
+
+/* One (plan, rate, seed) simulation.  met/cnt are [T]; lat (optional, may be
+ * NULL) is [n_req][4] = ttft, tpot, e2e, media; diag (optional) is
+ * [4] = integral of number-in-system over time, last completion time,
+ * number of instants, total executor busy time. */
+int cfo_sim_triple(const cfo_model *m, const cfo_plans *pl, int32_t plan_id, double rate,
+                   const cfo_trace *tr, int32_t seed_idx, uint32_t *met, uint32_t *cnt,
+                   uint64_t *events, uint32_t *status, double *lat, double *diag);
+
+int cfo_goodput_reduce(const uint32_t *met, const uint32_t *cnt, int32_t n_plans, int32_t K,
+                       int32_t S, int32_t T, const double *rates, uint32_t theta_num,
+                       uint32_t theta_den, int32_t n_req, int32_t *kstar, double *goodput_t,
+                       double *goodput);
+
+int32_t cfo_argmax(const double *goodput, int32_t n);
+
+#endif

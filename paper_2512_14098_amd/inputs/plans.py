@@ -1,0 +1,286 @@
+"""Physical-plan tables (Sec. 4.2, Alg. 1 and Eq. 1 of the paper).
+
+A plan is a set of nodes, each hosting a set of model components (a
+colocated group when more than one), with ``replicas`` executors of
+``gpus`` GPUs each and a maximum batch, plus per request type at most two
+alternative paths (parallel subplans, k_s = 2) with routing weights in
+tenths (step 0.1).  Each alternative maps every component on the type's
+path to the node that serves it.
+
+Layout (structure of arrays, field slot major, plan index fastest, so that
+one GPU thread per plan reads coalesced):
+
+=============  =======  ===========  ==========================================
+field          dtype    shape        meaning
+=============  =======  ===========  ==========================================
+n_nodes        uint8    [P]          nodes in the plan (<= 16)
+node_comp      uint8    [16, P]      component bitmask hosted by node v
+node_rep       uint8    [16, P]      executors (replicas) of node v
+node_batch     uint16   [16, P]      max batch of node v (<= 256)
+node_gpus      uint8    [16, P]      GPUs per executor of node v
+n_alt          uint8    [8, P]       alternatives of type t (1 or 2)
+alt_w          uint8    [16, P]      slot 2t+a: weight of alternative a, tenths
+alt_node       uint8    [128, P]     slot (2t+a)*8+c: node serving component c
+=============  =======  ===========  ==========================================
+
+Three families are produced: fully colocated (every component in one node),
+fully disaggregated (one node per component; replicas by coin change,
+Eq. 1), and seeded samples of mixed / compound plans: one or two subplans,
+each covering a subset of the types, each edge of a subplan kept or merged,
+optional node sharing between the two subplans, replicas drawn within the
+GPU budget, batches from the knob set, routing weights in tenths.
+"""
+import hashlib
+import itertools
+import os
+
+import numpy as np
+
+MAXV, MAXT, MAXC = 16, 8, 8
+
+
+class PlanTable:
+    FIELDS = ("n_nodes", "node_comp", "node_rep", "node_batch", "node_gpus", "n_alt", "alt_w",
+              "alt_node")
+
+    def __init__(self, P):
+        self.P = int(P)
+        self.n_nodes = np.zeros(P, np.uint8)
+        self.node_comp = np.zeros((MAXV, P), np.uint8)
+        self.node_rep = np.zeros((MAXV, P), np.uint8)
+        self.node_batch = np.zeros((MAXV, P), np.uint16)
+        self.node_gpus = np.zeros((MAXV, P), np.uint8)
+        self.n_alt = np.zeros((MAXT, P), np.uint8)
+        self.alt_w = np.zeros((2 * MAXT, P), np.uint8)
+        self.alt_node = np.full((2 * MAXT * MAXC, P), 255, np.uint8)
+
+    def subset(self, ids):
+        ids = np.asarray(ids, dtype=np.int64)
+        out = PlanTable(len(ids))
+        for f in self.FIELDS:
+            a = getattr(self, f)
+            setattr(out, f, np.ascontiguousarray(a[..., ids]))
+        return out
+
+    def plan(self, p):
+        """Readable dict of plan p (for reports and tests)."""
+        nv = int(self.n_nodes[p])
+        nodes = [dict(comp=int(self.node_comp[v, p]), rep=int(self.node_rep[v, p]),
+                      batch=int(self.node_batch[v, p]), gpus=int(self.node_gpus[v, p]))
+                 for v in range(nv)]
+        routes = []
+        for t in range(MAXT):
+            na = int(self.n_alt[t, p])
+            if na == 0:
+                break
+            routes.append([dict(w=int(self.alt_w[2 * t + a, p]),
+                                node=[int(self.alt_node[(2 * t + a) * 8 + c, p]) for c in range(MAXC)])
+                           for a in range(na)])
+        return dict(nodes=nodes, routes=routes)
+
+
+def _model_index(model):
+    names = [c["name"] for c in model["components"]]
+    idx = {n: i for i, n in enumerate(names)}
+    paths = [sorted(idx[c] for c in t["comps"]) for t in model["types"]]
+    edges = [sorted((idx[a], idx[b]) for a, b in t.get("edges", [])) for t in model["types"]]
+    return names, idx, paths, edges
+
+
+def plan_table_from_list(plans, P=None):
+    """plans: list of dict(nodes=[(comp_mask, rep, batch, gpus)], routes=[[(w, {c: node})]])."""
+    P = len(plans) if P is None else P
+    tab = PlanTable(P)
+    for p, pl in enumerate(plans):
+        tab.n_nodes[p] = len(pl["nodes"])
+        for v, (cm, rep, b, g) in enumerate(pl["nodes"]):
+            tab.node_comp[v, p] = cm
+            tab.node_rep[v, p] = rep
+            tab.node_batch[v, p] = b
+            tab.node_gpus[v, p] = g
+        for t, alts in enumerate(pl["routes"]):
+            tab.n_alt[t, p] = len(alts)
+            for a, (w, cmap) in enumerate(alts):
+                tab.alt_w[2 * t + a, p] = w
+                for c, v in cmap.items():
+                    tab.alt_node[(2 * t + a) * 8 + c, p] = v
+    return tab
+
+
+def _single_route(paths, node_of):
+    return [[(10, {c: node_of[c] for c in path})] for path in paths]
+
+
+def _colocated(model, fam, gpus):
+    names, idx, paths, _ = _model_index(model)
+    mask = (1 << len(names)) - 1
+    lo, hi = fam["replicas"]
+    out = []
+    for rep in range(lo, hi + 1):
+        if rep > gpus:
+            continue
+        for b in fam["batch"]:
+            out.append(dict(nodes=[(mask, rep, b, 1)],
+                            routes=_single_route(paths, {c: 0 for c in range(len(names))})))
+    return out
+
+
+def _disaggregated(model, fam, gpus):
+    names, idx, paths, _ = _model_index(model)
+    C = len(names)
+    maxt = min(int(fam.get("max_total", gpus)), gpus)
+    out = []
+    reps_all = [r for r in itertools.product(range(1, maxt + 1), repeat=C) if sum(r) <= maxt]
+    for reps in reps_all:
+        if fam.get("same_batch", False):
+            bsets = [(b,) * C for b in fam["batch"]]
+        else:
+            bsets = list(itertools.product(fam["batch"], repeat=C))
+        for bs in bsets:
+            nodes = [(1 << c, reps[c], bs[c], 1) for c in range(C)]
+            out.append(dict(nodes=nodes, routes=_single_route(paths, {c: c for c in range(C)})))
+    return out
+
+
+def _canon(pl):
+    parts = [tuple(n) for n in pl["nodes"]]
+    routes = tuple(tuple((w, tuple(sorted(m.items()))) for w, m in alts) for alts in pl["routes"])
+    return (tuple(parts), routes)
+
+
+def _sample(model, spec, gpus, have, total):
+    """Seeded mixed / compound plans until ``total`` distinct plans exist."""
+    names, idx, paths, edges = _model_index(model)
+    T, C = len(paths), len(names)
+    colocatable = model.get("colocatable")
+    if colocatable is not None:
+        colocatable = {(idx[a], idx[b]) for a, b in colocatable}
+    knobs = [spec["batch"][n] for n in names]
+    rng = np.random.Generator(np.random.Philox(key=int(spec["seed"])))
+    out = []
+    seen = set(_canon(p) for p in have)
+    tries = 0
+    while len(have) + len(out) < total:
+        tries += 1
+        if tries > 50 * total + 1000:
+            raise RuntimeError("plan sampler could not reach the requested count")
+        ns = 1 if rng.random() < 0.5 or T == 1 else 2
+        if ns == 1:
+            cover = [list(range(T))]
+        else:
+            while True:
+                assign = rng.integers(0, 3, size=T)
+                s0 = [t for t in range(T) if assign[t] in (0, 2)]
+                s1 = [t for t in range(T) if assign[t] in (1, 2)]
+                if s0 and s1:
+                    break
+            cover = [s0, s1]
+        nodes, node_of, sub_nodes = [], [], []
+        for si, types_s in enumerate(cover):
+            comps = sorted(set(c for t in types_s for c in paths[t]))
+            es = sorted(set(e for t in types_s for e in edges[t]))
+            par = {c: c for c in comps}
+
+            def find(c):
+                while par[c] != c:
+                    c = par[c]
+                return c
+            for (a, b) in es:
+                if colocatable is not None and (a, b) not in colocatable:
+                    continue
+                if rng.random() < 0.5:
+                    ra, rb = find(a), find(b)
+                    if ra != rb:
+                        par[max(ra, rb)] = min(ra, rb)
+            groups = {}
+            for c in comps:
+                groups.setdefault(find(c), 0)
+                groups[find(c)] |= 1 << c
+            nmap, mine = {}, []
+            for root in sorted(groups):
+                mask = groups[root]
+                shared = None
+                if si == 1 and rng.random() < 0.5:
+                    for v in sub_nodes[0]:
+                        if nodes[v] == mask:
+                            shared = v
+                            break
+                if shared is None:
+                    shared = len(nodes)
+                    nodes.append(mask)
+                mine.append(shared)
+                for c in range(C):
+                    if (mask >> c) & 1:
+                        nmap[c] = shared
+            node_of.append(nmap)
+            sub_nodes.append(mine)
+        V = len(nodes)
+        if V > gpus or V > MAXV:
+            continue
+        reps = [1] * V
+        extra = gpus - V
+        k = int(rng.integers(0, extra + 1))
+        for _ in range(k):
+            reps[int(rng.integers(0, V))] += 1
+        batch = []
+        for mask in nodes:
+            first = (mask & -mask).bit_length() - 1
+            batch.append(int(knobs[first][int(rng.integers(0, len(knobs[first])))]))
+        routes = []
+        for t in range(T):
+            alts = [si for si in range(ns) if t in cover[si]]
+            if len(alts) == 1:
+                routes.append([(10, {c: node_of[alts[0]][c] for c in paths[t]})])
+            else:
+                w0 = int(rng.integers(1, 10))
+                routes.append([(w0, {c: node_of[alts[0]][c] for c in paths[t]}),
+                               (10 - w0, {c: node_of[alts[1]][c] for c in paths[t]})])
+        pl = dict(nodes=[(nodes[v], reps[v], batch[v], 1) for v in range(V)], routes=routes)
+        key = _canon(pl)
+        if key in seen:
+            continue
+        seen.add(key)
+        out.append(pl)
+    return out
+
+
+def _cache_path(cfg):
+    h = hashlib.sha1(repr((cfg["model"], cfg["plans"], cfg["gpus"])).encode()).hexdigest()[:16]
+    d = os.environ.get("CF_PLAN_CACHE", os.path.join(os.path.expanduser("~"), ".cache", "cf_plans"))
+    return os.path.join(d, "%s_%s.npz" % (cfg.get("name", "cfg"), h))
+
+
+def make_plans(cfg, cache=True):
+    """Plan table for a configuration (deterministic; cached on disk when large)."""
+    cpath = _cache_path(cfg)
+    if cache and os.path.exists(cpath):
+        z = np.load(cpath)
+        tab = PlanTable(int(z["n_nodes"].shape[0]))
+        for f in PlanTable.FIELDS:
+            setattr(tab, f, np.ascontiguousarray(z[f]))
+        return tab
+    model, spec, gpus = cfg["model"], cfg["plans"], int(cfg["gpus"])
+    plans = []
+    for fam in spec.get("families", []):
+        if fam["family"] == "colocated":
+            plans += _colocated(model, fam, gpus)
+        elif fam["family"] == "disaggregated":
+            plans += _disaggregated(model, fam, gpus)
+        else:
+            raise ValueError(fam["family"])
+    seen, uniq = set(), []
+    for p in plans:
+        k = _canon(p)
+        if k not in seen:
+            seen.add(k)
+            uniq.append(p)
+    plans = uniq
+    if "sampled" in spec:
+        plans += _sample(model, spec["sampled"], gpus, plans, int(spec["sampled"]["total"]))
+    tab = plan_table_from_list(plans)
+    if cache and tab.P >= 5000:
+        os.makedirs(os.path.dirname(cpath), exist_ok=True)
+        tmp = cpath + ".tmp%d.npz" % os.getpid()
+        np.savez(tmp, **{f: getattr(tab, f) for f in PlanTable.FIELDS})
+        os.replace(tmp, cpath)
+    return tab
