@@ -1,0 +1,133 @@
+"""Benchmark: simulated request-events/s and plans fully evaluated/s on one GPU.
+
+A step is one pass of the whole evaluated path over one synthetic workload:
+trace generation, phase-1 screening of every plan, top-K selection, rate
+grid, phase-3 simulation of every (plan, rate, seed) triple, goodput
+reduction and selection.  Default workload: c1 (E->L on 8 simulated GPUs,
+1000 plans screened, the kept ones simulated at 16 rates x 32 seeds x 10^4
+requests).  Prints one JSON line.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "simulated request-events/sec and candidate plans fully evaluated/sec, 1 GPU"
+PEAK_LANE_OPS = 256 * 4 * 16 * 2.4e9 / 1e12  # T lane-ops/s: CUs x SIMDs x lanes x clock
+OPS_PER_EVENT = 4.0  # algorithmic lane-ops per request-event
+
+
+def cpu_baseline(w, ids, rates, budget_s):
+    """The oracle, single-threaded on this host, on a bounded sample of the
+    same workload's triples (spread over plans, rates and seeds)."""
+    import numpy as np
+
+    from oracle import oracle as O
+    m = O.make_model(w.cfg["model"])
+    S = len(w.seeds)
+    order = []
+    rng = np.random.default_rng(0)
+    for _ in range(4096):
+        order.append((int(rng.integers(len(ids))), int(rng.integers(rates.shape[1])), int(rng.integers(S))))
+    seeds_needed = sorted({s for _, _, s in order[:256]})
+    otr = O.trace_gen(m, [w.seeds[s] for s in seeds_needed], w.n_req)
+    pst, tst = O.plans_struct(w.tab), O.trace_struct(otr)
+    ev, n, t0 = 0, 0, time.perf_counter()
+    for (i, k, s) in order:
+        if s not in seeds_needed:
+            continue
+        o = O.sim_triple(m, w.tab, int(ids[i]), float(rates[i, k]), otr, seeds_needed.index(s),
+                         _pst=pst, _tst=tst)
+        ev += o["events"]
+        n += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": ev / dt, "unit": "request-events/s", "cores": 1, "kind": "oracle",
+            "sample": "%d triples of this workload drawn uniformly over plans, rates and seeds "
+                      "(%d request-events in %.1f s, single thread)" % (n, ev, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="c1")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(sharding by plan blocks is described in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2512_14098_amd import cf, pipeline
+
+    torch.cuda.set_device(0)
+    print("bench: loading workload %s" % args.config, file=sys.stderr, flush=True)
+    w = pipeline.Workload(args.config)
+    for i in range(args.warmup):
+        out = pipeline.run_step(w)
+        torch.cuda.synchronize()
+        print("bench: warmup %d done, %d request-events" % (i, pipeline.events_total(out)),
+              file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    events, plans, fine_ms, timers_all = 0, 0, [], []
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        timers = {}
+        out = pipeline.run_step(w, timers=timers)
+        timers_all.append(timers)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for i, timers in enumerate(timers_all):
+        s, e = timers["fine"]
+        fine_ms.append(s.elapsed_time(e))
+    events = pipeline.events_total(out) * args.steps
+    plans = int(out["ids"].numel()) * args.steps
+    st = pipeline.status_summary(out)
+    elapsed = t1 - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+    ev_step = events / args.steps
+    fine_avg_s = sum(fine_ms) / len(fine_ms) / 1e3
+    achieved = OPS_PER_EVENT * ev_step / fine_avg_s / 1e12
+    n_sel = int(out["ids"].numel())
+    res = {
+        "metric": METRIC,
+        "value": events / elapsed,
+        "unit": "request-events/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "plans_per_s": plans / elapsed,
+        "config": {"workload": "%s: %s" % (args.config, w.cfg["summary"]), "plans_screened": w.tab.P,
+                   "plans_simulated": n_sel, "rates": w.K, "seeds": len(w.seeds), "requests": w.n_req,
+                   "triples": n_sel * w.K * len(w.seeds), "request_events_per_step": ev_step,
+                   "status_counts": st, "fine_ms": fine_ms},
+        "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_LANE_OPS, "unit": "TOP/s",
+                     "frac": achieved / PEAK_LANE_OPS, "traffic": None,
+                     "kernel": "k_fine", "ops_per_event": OPS_PER_EVENT,
+                     "kernel_ms": sum(fine_ms) / len(fine_ms)},
+    }
+    if not args.no_cpu_baseline:
+        print("bench: cpu baseline (oracle, %.0f s budget)" % args.cpu_budget, file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(w, out["ids"].cpu().numpy(), out["rates"].cpu().numpy(),
+                                           args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

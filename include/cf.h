@@ -1,0 +1,241 @@
+/*
+ * cf.h -- C ABI of libcf, the MI355X (gfx950) implementation of the
+ * statistical plan evaluation of Cornfigurator (arXiv 2512.14098):
+ * request traces, flow-based screening (Sec. 4.3, Alg. 2 phase 1),
+ * request-level simulation (Alg. 2 phase 3) and goodput selection
+ * (Sec. 3.2, Sec. 6.1).
+ *
+ * Conventions
+ *  - Pointers named *_dev are device pointers (HIP global memory), owned and
+ *    allocated by the caller; the library never frees them.  Pointers named
+ *    *_host, and every descriptor struct, live in host memory and are read
+ *    during the call only.
+ *  - Every call is asynchronous on `stream` (a hipStream_t; NULL = the
+ *    default stream) unless its comment says it synchronises.
+ *  - Errors detectable on the host (bad descriptor, sizes, capacity limits)
+ *    are returned before anything is launched; nothing is written then.
+ *    Conditions found on the device are reported in per-triple status words
+ *    and never trap.  cf_last_error() returns the text of the calling
+ *    thread's last error.
+ *  - Layouts are structure-of-arrays; every multi-dimensional array is
+ *    row-major with the last index fastest.
+ *  - The library allocates internal scratch (per-wave simulation state) on
+ *    first use and keeps it for later calls; cf_release_scratch() frees it.
+ */
+#ifndef CF_H
+#define CF_H
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t cf_status;
+#define CF_OK 0
+#define CF_EINVAL (-1)        /* invalid descriptor or argument */
+#define CF_ENOMEM (-2)        /* device allocation of scratch failed */
+#define CF_EHIP (-3)          /* HIP runtime error */
+#define CF_ECAPACITY (-4)     /* static limit exceeded (see CF_MAX_*) */
+#define CF_EUNSUPPORTED (-6)  /* feature combination not supported */
+
+#define CF_MAX_COMP 8     /* model components */
+#define CF_MAX_TYPES 8    /* request types */
+#define CF_MAX_NODES 16   /* nodes per plan */
+#define CF_MAX_EXEC 64    /* executors (replicas) per plan */
+#define CF_MAX_BATCH 256  /* max batch of a node */
+
+/* component kinds */
+#define CF_ENC 0
+#define CF_LLM 1
+#define CF_GEN 2
+
+/* per-request attributes, used as bit positions of cf_model_desc.x_sel and
+ * as values of cf_model_desc.nout_attr */
+#define CF_ATTR_PROMPT 0
+#define CF_ATTR_OUT 1
+#define CF_ATTR_PATCHES 2
+#define CF_ATTR_AUDIN_MS 3
+#define CF_ATTR_AUDOUT_MS 4
+#define CF_ATTR_AUDIN_TOK 5  /* ceil(aud_in_ms / 80) */
+#define CF_ATTR_AUDOUT_TOK 6 /* ceil(aud_out_ms / 80) */
+
+/* length distributions */
+#define CF_DIST_NONE 0
+#define CF_DIST_CONST 1     /* value p0 */
+#define CF_DIST_LOGNORMAL 2 /* clamp(rint(scale * exp(p0 + p1 Z)), lo, hi) */
+#define CF_DIST_EXP 3       /* clamp(rint(p0 * Exp(1)), lo, hi) */
+
+/* image-count distributions */
+#define CF_IMG_NONE 0
+#define CF_IMG_CONST 1
+#define CF_IMG_UNIFORM 2
+
+/* cf_eval_coarse flag bits */
+#define CF_FLAG_KEEP 1u
+#define CF_FLAG_OVER_BUDGET 2u
+#define CF_FLAG_INVALID 4u
+#define CF_FLAG_REDUNDANT 8u
+
+/* cf_eval_fine per-triple status bits */
+#define CF_ST_INVALID 1u   /* a request's route does not fit the plan */
+#define CF_ST_DEADLOCK 2u  /* nothing pending but requests unfinished */
+#define CF_ST_OVERFLOW 4u  /* an internal capacity of the simulator was exceeded */
+
+typedef struct cf_dist {
+  int32_t kind;        /* CF_DIST_* */
+  int32_t reserved;
+  double p0, p1;       /* parameters (see CF_DIST_*) */
+  double scale;        /* LOGNORMAL: multiplier before rounding (1 tokens, 1000 ms) */
+  int64_t lo, hi;      /* clamp after rounding */
+} cf_dist;
+
+/* Model definition, configuration space and workload (Sec. 3.1): the
+ * component graph with one latency model per component, request types with
+ * their weight (pi_t proportional to weight), path, outputs, lengths and
+ * latency targets.  Host memory, copied by every call that takes it. */
+typedef struct cf_model_desc {
+  int32_t n_comp;                    /* 1..CF_MAX_COMP, topological index order */
+  int32_t n_types;                   /* 1..CF_MAX_TYPES */
+  int32_t kind[CF_MAX_COMP];         /* CF_ENC / CF_LLM / CF_GEN */
+  double k0[CF_MAX_COMP];            /* batch iteration: (k0 + k1*X) + k2*n seconds */
+  double k1[CF_MAX_COMP];
+  double k2[CF_MAX_COMP];
+  double d0[CF_MAX_COMP];            /* LLM decode step: d0 + d1*n seconds */
+  double d1[CF_MAX_COMP];
+  uint32_t x_sel[CF_MAX_COMP];       /* bitmask of CF_ATTR_* summed into X */
+  int32_t nout_attr[CF_MAX_COMP];    /* LLM: CF_ATTR_* giving the output length */
+  int32_t gate_src[CF_MAX_COMP];     /* LLM gated by that component's tokens, or -1 */
+  int32_t batch_cap[CF_MAX_COMP];    /* stage batch = min(node batch, cap) */
+  double comm_s;                     /* delay of every inter-executor edge (Sec. 5.2) */
+  double cpu_pre_s;                  /* CPU preprocessing of an idle-start encoder batch */
+  uint32_t weight[CF_MAX_TYPES];     /* type weights (>= 0, sum >= 1) */
+  uint32_t path_mask[CF_MAX_TYPES];  /* components on the type's path */
+  uint32_t out_mask[CF_MAX_TYPES];   /* output components of the type */
+  uint32_t prefill_only[CF_MAX_TYPES]; /* LLM components with one output token */
+  uint32_t parents[CF_MAX_TYPES][CF_MAX_COMP]; /* parent mask of each component on the path */
+  int32_t img_kind[CF_MAX_TYPES];    /* CF_IMG_* */
+  int32_t img_lo[CF_MAX_TYPES], img_hi[CF_MAX_TYPES]; /* images per request (<= 4) */
+  int32_t patch_lo, patch_hi;        /* patches per image, uniform integer */
+  cf_dist len[CF_MAX_TYPES][4];      /* prompt, out, aud_in_ms, aud_out_ms */
+  double slo[CF_MAX_TYPES][4];       /* bounds on TTFT, TPOT, E2E, MEDIA (<=; +inf = none) */
+  uint32_t theta_num, theta_den;     /* attainment threshold (e.g. 9/10) */
+} cf_model_desc;
+
+/* Request trace: device arrays of n_seeds * n_req elements, seed-major. */
+typedef struct cf_trace {
+  int32_t n_seeds, n_req;
+  uint64_t *arr_ticks_dev;  /* inclusive prefix sum of gaps, 2^-32 s at rate 1 */
+  uint8_t *type_dev;
+  uint8_t *n_img_dev;
+  uint16_t *patches_dev;    /* sum over the request's images */
+  uint16_t *prompt_dev;
+  uint16_t *out_dev;
+  uint32_t *aud_in_ms_dev;
+  uint32_t *aud_out_ms_dev;
+  uint64_t *rkey0_dev;      /* 16-bit replica keys of components 0..3 */
+  uint64_t *rkey1_dev;      /* 16-bit replica keys of components 4..7 */
+  uint32_t *akey_dev;       /* alternative-choice key */
+} cf_trace;
+
+/* Physical plans (Sec. 4.2): device arrays, field-slot major [slot][P]. */
+typedef struct cf_plan_table {
+  int32_t P;
+  const uint8_t *n_nodes_dev;    /* [P] */
+  const uint8_t *node_comp_dev;  /* [16][P] component bitmask */
+  const uint8_t *node_rep_dev;   /* [16][P] executors of the node */
+  const uint16_t *node_batch_dev;/* [16][P] max batch */
+  const uint8_t *node_gpus_dev;  /* [16][P] GPUs per executor */
+  const uint8_t *n_alt_dev;      /* [8][P] alternatives per type (1 or 2) */
+  const uint8_t *alt_w_dev;      /* [16][P] slot 2t+a: routing weight in tenths */
+  const uint8_t *alt_node_dev;   /* [128][P] slot (2t+a)*8+c: node serving c */
+} cf_plan_table;
+
+/* Outputs of cf_eval_fine, device arrays, triple (i, k, s) = plan i, rate k,
+ * seed s. */
+typedef struct cf_fine_out {
+  uint32_t *met_dev;      /* [n_plans][K][S][T] requests meeting every bound */
+  uint32_t *cnt_dev;      /* [n_plans][K][S][T] requests of the type */
+  uint64_t *events_dev;   /* [n_plans][K][S] request-events simulated */
+  uint32_t *status_dev;   /* [n_plans][K][S] CF_ST_* bits */
+  double *lat_dev;        /* optional [n_lat][n_req][4]: TTFT, TPOT, E2E, MEDIA; NULL = off */
+  const int32_t *lat_triples_dev; /* [n_lat] linear triple ids ((i*K)+k)*S+s to dump */
+  int32_t n_lat;
+} cf_fine_out;
+
+/* Error text of the calling thread's last failed call (empty if none);
+ * writes at most n bytes including the terminator, returns the full length. */
+size_t cf_last_error(char *buf, size_t n);
+const char *cf_status_str(cf_status s);
+const char *cf_version(void);
+
+/* Synthetic Any-to-Any trace (workload of Sec. 3.1, Poisson arrivals).
+ * For seed seeds_host[s] and request i: Philox4x64-10 blocks keyed
+ * (seeds_host[s], 0) with counter (i, field, attempt, 0) give the gap, type,
+ * image count, patches, lengths and route keys.  moments_dev receives
+ * [n_seeds][n_types][8] u64: count, then sums of prompt, out, patches,
+ * aud_in_ms, aud_out_ms, aud_in tokens, aud_out tokens.
+ * Errors: CF_EINVAL for a bad descriptor, n_seeds < 1 or n_req < 0. */
+cf_status cf_trace_gen(const cf_model_desc *model, const uint64_t *seeds_host, int32_t n_seeds,
+                       int32_t n_req, const cf_trace *out, uint64_t *moments_dev, void *stream);
+
+/* Phase 1 of the plan evaluation (Sec. 4.3, Alg. 2): per plan, the
+ * per-node demand u_v from the latency models at the node's batch and the
+ * per-type means in moments_dev ([n_types][8], one seed), R_d = min_v
+ * m_v/u_v, the bottleneck node (-1 if invalid) and CF_FLAG_* bits (budget of
+ * Eq. (1) is n_gpus).  Output arrays have P elements. */
+cf_status cf_eval_coarse(const cf_model_desc *model, const cf_plan_table *plans,
+                         const uint64_t *moments_dev, int32_t n_gpus, double *rd_dev,
+                         int32_t *bottleneck_dev, uint8_t *flags_dev, void *stream);
+
+/* Plans with CF_FLAG_KEEP ordered by R_d descending, ties by plan id
+ * ascending; the first min(k, kept) ids go to ids_dev[k].  Synchronises the
+ * stream and writes the number selected to *n_selected_host.
+ * Limits: 1 <= k <= 65536, P <= 2^24. */
+cf_status cf_select_topk(const double *rd_dev, const uint8_t *flags_dev, int32_t P, int32_t k,
+                         int32_t *ids_dev, int32_t *n_selected_host, void *stream);
+
+/* rates_dev[i][k] = (R_d[ids_dev[i]] * alpha_max * (k+1)) / K, i < n, k < K. */
+cf_status cf_rate_grid(const double *rd_dev, const int32_t *ids_dev, int32_t n, int32_t K,
+                       double alpha_max, double *rates_dev, void *stream);
+
+/* Phase 3 (Sec. 4.3, Alg. 2): request-level simulation of every triple
+ * (plan plan_ids_dev[i], rate rates_dev[i][k], trace seed s) for i <
+ * n_plans, k < K, s < trace->n_seeds, one wavefront per triple.  flags: 0.
+ * Errors: CF_EINVAL (descriptor, sizes), CF_ECAPACITY, CF_ENOMEM. */
+cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_table *plans,
+                       const int32_t *plan_ids_dev, int32_t n_plans, const double *rates_dev,
+                       int32_t K, const cf_trace *trace, uint32_t flags, const cf_fine_out *out,
+                       void *stream);
+
+/* Goodput (Sec. 3.2) at the highest feasible rate (Sec. 6.1): M_t, N_t
+ * pooled over seeds; rate k feasible iff theta_den*M_t >= theta_num*N_t for
+ * every type with N_t > 0; kstar = first infeasible - 1; goodput_t =
+ * (rates[i][kstar] * M_t) / (S * n_req) (0 if kstar < 0); goodput = sum_t.
+ * Outputs: kstar_dev[n_plans], goodput_t_dev[n_plans][T], goodput_dev[n_plans]. */
+cf_status cf_goodput_reduce(const uint32_t *met_dev, const uint32_t *cnt_dev, int32_t n_plans,
+                            int32_t K, int32_t S, int32_t T, const double *rates_dev,
+                            uint32_t theta_num, uint32_t theta_den, int32_t n_req,
+                            int32_t *kstar_dev, double *goodput_t_dev, double *goodput_dev,
+                            void *stream);
+
+/* Selection (Alg. 2, last step): index of the largest goodput, ties to the
+ * lowest index, written to best_dev[0]. */
+cf_status cf_select_best(const double *goodput_dev, int32_t n, int32_t *best_dev, void *stream);
+
+/* Diagnostics for tests: the device primitives applied element-wise.
+ * op 0: cf_log(x)  1: cf_exp(x)  2: sqrt(x)  3: x / y  4: uniform(bits of x)
+ * y_dev is only read by op 3; out_dev[n]. */
+cf_status cf_math_eval(int32_t op, const double *x_dev, const double *y_dev, double *out_dev,
+                       int64_t n, void *stream);
+/* Philox4x64-10 blocks: ctr_dev[n][4], key_dev[n][2] -> out_dev[n][4]. */
+cf_status cf_philox_eval(const uint64_t *ctr_dev, const uint64_t *key_dev, uint64_t *out_dev,
+                         int64_t n, void *stream);
+
+/* Frees the internal scratch (synchronises the device). */
+cf_status cf_release_scratch(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -136,4 +136,8 @@ int cfo_goodput_reduce(const uint32_t *met, const uint32_t *cnt, int32_t n_plans
 
 int32_t cfo_argmax(const double *goodput, int32_t n);
 
+/* element-wise helpers for the tests: op 0 log, 1 exp, 2 sqrt, 3 x/y, 4 uniform(bits of x) */
+void cfo_math_n(int32_t op, const double *x, const double *y, double *out, int64_t n);
+void cfo_philox_n(const uint64_t *ctr, const uint64_t *key, uint64_t *out, int64_t n);
+
 #endif

@@ -215,3 +215,23 @@ int cfo_trace_gen(const cfo_model *m, const uint64_t *seeds, int32_t n_seeds, in
   }
   return 0;
 }
+
+/* ---------------- element-wise helpers for the tests ---------------- */
+void cfo_math_n(int32_t op, const double *x, const double *y, double *out, int64_t n) {
+  for (int64_t i = 0; i < n; i++) {
+    double a = x[i], r = 0.0;
+    switch (op) {
+    case 0: r = cfo_log(a); break;
+    case 1: r = cfo_exp(a); break;
+    case 2: r = sqrt(a); break;
+    case 3: r = a / y[i]; break;
+    case 4: { uint64_t b; memcpy(&b, &a, 8); r = cfo_uniform(b); } break;
+    default: break;
+    }
+    out[i] = r;
+  }
+}
+
+void cfo_philox_n(const uint64_t *ctr, const uint64_t *key, uint64_t *out, int64_t n) {
+  for (int64_t i = 0; i < n; i++) cfo_philox(ctr + 4 * i, key + 2 * i, out + 4 * i);
+}

@@ -311,3 +311,23 @@ def goodput_reduce(met, cnt, rates, theta, n_req):
 def argmax(goodput):
     g = np.ascontiguousarray(goodput, np.float64)
     return int(lib().cfo_argmax(_ptr(g), len(g)))
+
+
+def math_n(op, x, y=None):
+    L = lib()
+    L.cfo_math_n.argtypes = [C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64]
+    x = np.ascontiguousarray(x, np.float64)
+    yy = np.ascontiguousarray(y, np.float64) if y is not None else None
+    out = np.zeros_like(x)
+    L.cfo_math_n(int(op), _ptr(x), _ptr(yy) if yy is not None else None, _ptr(out), x.size)
+    return out
+
+
+def philox_n(ctr, key):
+    L = lib()
+    L.cfo_philox_n.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64]
+    ctr = np.ascontiguousarray(ctr, np.uint64)
+    key = np.ascontiguousarray(key, np.uint64)
+    out = np.zeros_like(ctr)
+    L.cfo_philox_n(_ptr(ctr), _ptr(key), _ptr(out), ctr.shape[0])
+    return out

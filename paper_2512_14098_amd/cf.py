@@ -1,0 +1,334 @@
+"""Python binding of libcf (``include/cf.h``): argument marshalling only.
+
+Every function has the name of the C entry point it calls.  Device arrays
+are torch tensors on the current HIP device; each call runs on torch's
+current stream.  Nothing is computed here: the library runs every step in
+its HIP kernels, and a missing library raises at import.
+"""
+import ctypes as C
+import math
+import os
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcf.so")
+
+MAX_COMP, MAX_TYPES, MAX_NODES = 8, 8, 16
+KIND = {"ENC": 0, "LLM": 1, "GEN": 2}
+ATTR = {"prompt": 0, "out": 1, "patches": 2, "aud_in_ms": 3, "aud_out_ms": 4, "aud_in_tok": 5,
+        "aud_out_tok": 6}
+FLAG_KEEP, FLAG_OVER_BUDGET, FLAG_INVALID, FLAG_REDUNDANT = 1, 2, 4, 8
+ST_INVALID, ST_DEADLOCK, ST_OVERFLOW = 1, 2, 4
+
+
+class CfError(RuntimeError):
+    pass
+
+
+class cf_dist(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("reserved", C.c_int32), ("p0", C.c_double), ("p1", C.c_double),
+                ("scale", C.c_double), ("lo", C.c_int64), ("hi", C.c_int64)]
+
+
+class cf_model_desc(C.Structure):
+    _fields_ = [
+        ("n_comp", C.c_int32), ("n_types", C.c_int32), ("kind", C.c_int32 * MAX_COMP),
+        ("k0", C.c_double * MAX_COMP), ("k1", C.c_double * MAX_COMP), ("k2", C.c_double * MAX_COMP),
+        ("d0", C.c_double * MAX_COMP), ("d1", C.c_double * MAX_COMP),
+        ("x_sel", C.c_uint32 * MAX_COMP), ("nout_attr", C.c_int32 * MAX_COMP),
+        ("gate_src", C.c_int32 * MAX_COMP), ("batch_cap", C.c_int32 * MAX_COMP),
+        ("comm_s", C.c_double), ("cpu_pre_s", C.c_double),
+        ("weight", C.c_uint32 * MAX_TYPES), ("path_mask", C.c_uint32 * MAX_TYPES),
+        ("out_mask", C.c_uint32 * MAX_TYPES), ("prefill_only", C.c_uint32 * MAX_TYPES),
+        ("parents", (C.c_uint32 * MAX_COMP) * MAX_TYPES),
+        ("img_kind", C.c_int32 * MAX_TYPES), ("img_lo", C.c_int32 * MAX_TYPES),
+        ("img_hi", C.c_int32 * MAX_TYPES), ("patch_lo", C.c_int32), ("patch_hi", C.c_int32),
+        ("len", (cf_dist * 4) * MAX_TYPES), ("slo", (C.c_double * 4) * MAX_TYPES),
+        ("theta_num", C.c_uint32), ("theta_den", C.c_uint32),
+    ]
+
+
+class cf_trace(C.Structure):
+    _fields_ = [("n_seeds", C.c_int32), ("n_req", C.c_int32)] + [
+        (f + "_dev", C.c_void_p) for f in ("arr_ticks", "type", "n_img", "patches", "prompt", "out",
+                                           "aud_in_ms", "aud_out_ms", "rkey0", "rkey1", "akey")]
+
+
+class cf_plan_table(C.Structure):
+    _fields_ = [("P", C.c_int32)] + [
+        (f + "_dev", C.c_void_p) for f in ("n_nodes", "node_comp", "node_rep", "node_batch",
+                                           "node_gpus", "n_alt", "alt_w", "alt_node")]
+
+
+class cf_fine_out(C.Structure):
+    _fields_ = [("met_dev", C.c_void_p), ("cnt_dev", C.c_void_p), ("events_dev", C.c_void_p),
+                ("status_dev", C.c_void_p), ("lat_dev", C.c_void_p), ("lat_triples_dev", C.c_void_p),
+                ("n_lat", C.c_int32)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise CfError("libcf.so is not built (%s); run __graft_entry__.build()" % LIB_PATH)
+    L = C.CDLL(LIB_PATH)
+    vp, i32, i64, u32, dbl = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_double
+    sigs = {
+        "cf_last_error": ([vp, C.c_size_t], C.c_size_t),
+        "cf_status_str": ([i32], C.c_char_p),
+        "cf_version": ([], C.c_char_p),
+        "cf_trace_gen": ([vp, vp, i32, i32, vp, vp, vp], i32),
+        "cf_eval_coarse": ([vp, vp, vp, i32, vp, vp, vp, vp], i32),
+        "cf_select_topk": ([vp, vp, i32, i32, vp, vp, vp], i32),
+        "cf_rate_grid": ([vp, vp, i32, i32, dbl, vp, vp], i32),
+        "cf_eval_fine": ([vp, vp, vp, i32, vp, i32, vp, u32, vp, vp], i32),
+        "cf_goodput_reduce": ([vp, vp, i32, i32, i32, i32, vp, u32, u32, i32, vp, vp, vp, vp], i32),
+        "cf_select_best": ([vp, i32, vp, vp], i32),
+        "cf_math_eval": ([i32, vp, vp, vp, i64, vp], i32),
+        "cf_philox_eval": ([vp, vp, vp, i64, vp], i32),
+        "cf_release_scratch": ([], i32),
+    }
+    for name, (args, res) in sigs.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = res
+    return L
+
+
+_lib = _load()
+EXPORTED = ("cf_last_error", "cf_status_str", "cf_version", "cf_trace_gen", "cf_eval_coarse",
+            "cf_select_topk", "cf_rate_grid", "cf_eval_fine", "cf_goodput_reduce", "cf_select_best",
+            "cf_math_eval", "cf_philox_eval", "cf_release_scratch")
+
+
+def lib():
+    return _lib
+
+
+def _check(rc, what):
+    if rc != 0:
+        buf = C.create_string_buffer(512)
+        _lib.cf_last_error(buf, 512)
+        raise CfError("%s: %s (%s)" % (what, _lib.cf_status_str(rc).decode(), buf.value.decode()))
+
+
+def _stream():
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _p(t):
+    if t is None:
+        return None
+    if not t.is_cuda or not t.is_contiguous():
+        raise CfError("expected a contiguous device tensor")
+    return C.c_void_p(t.data_ptr())
+
+
+# ------------------------------------------------------------------ model
+def _dist(spec, audio):
+    d = cf_dist()
+    d.scale, d.lo, d.hi = 1.0, 1, (600000 if audio else 32767)
+    if not spec:
+        return d
+    (k, v), = spec.items()
+    if k == "const":
+        d.kind, d.p0 = 1, float(v)
+    elif k in ("lognormal", "lognormal_s"):
+        d.kind, d.p0, d.p1 = 2, float(v[0]), float(v[1])
+        d.scale = 1000.0 if k == "lognormal_s" else 1.0
+    elif k == "exp":
+        d.kind, d.p0 = 3, float(v)
+    else:
+        raise CfError("unknown length distribution " + k)
+    return d
+
+
+def model_desc(mcfg):
+    """cf_model_desc from a model description (JSON dict)."""
+    d = cf_model_desc()
+    comps = mcfg["components"]
+    idx = {c["name"]: i for i, c in enumerate(comps)}
+    d.n_comp, d.n_types = len(comps), len(mcfg["types"])
+    for i, c in enumerate(comps):
+        d.kind[i] = KIND[c["kind"]]
+        d.k0[i], d.k1[i], d.k2[i] = (float(v) for v in c["k"])
+        dec = c.get("decode", [0.0, 0.0])
+        d.d0[i], d.d1[i] = float(dec[0]), float(dec[1])
+        d.x_sel[i] = sum(1 << ATTR[a] for a in c.get("x", []))
+        d.nout_attr[i] = ATTR[c.get("n_out", "out")]
+        d.gate_src[i] = idx[c["gate"]] if c.get("gate") else -1
+        d.batch_cap[i] = int(c.get("batch_cap", 256))
+    d.comm_s = float(mcfg["comm_s"])
+    d.cpu_pre_s = float(mcfg.get("cpu_pre_s", 0.0))
+    for t, ty in enumerate(mcfg["types"]):
+        d.weight[t] = int(ty["weight"])
+        d.path_mask[t] = sum(1 << idx[c] for c in ty["comps"])
+        d.out_mask[t] = sum(1 << idx[c] for c in ty["outputs"])
+        d.prefill_only[t] = sum(1 << idx[c] for c in ty.get("prefill_only", []))
+        for a, b in ty.get("edges", []):
+            d.parents[t][idx[b]] |= 1 << idx[a]
+        img = ty.get("images")
+        if img and "const" in img:
+            d.img_kind[t], d.img_lo[t], d.img_hi[t] = 1, int(img["const"]), int(img["const"])
+        elif img:
+            d.img_kind[t], d.img_lo[t], d.img_hi[t] = 2, int(img["uniform"][0]), int(img["uniform"][1])
+        for j, (key, audio) in enumerate((("prompt", False), ("out", False), ("aud_in", True),
+                                          ("aud_out", True))):
+            d.len[t][j] = _dist(ty.get(key), audio)
+        slo = ty.get("slo", {})
+        for j, key in enumerate(("ttft", "tpot", "e2e", "media")):
+            d.slo[t][j] = float(slo[key]) if key in slo else math.inf
+    d.patch_lo, d.patch_hi = (int(v) for v in mcfg.get("patches_per_image", [256, 1024]))
+    th = mcfg.get("theta", [9, 10])
+    d.theta_num, d.theta_den = int(th[0]), int(th[1])
+    return d
+
+
+# ------------------------------------------------------------------ device containers
+TRACE_FIELDS = [("arr_ticks", torch.int64), ("type", torch.uint8), ("n_img", torch.uint8),
+                ("patches", torch.int16), ("prompt", torch.int16), ("out", torch.int16),
+                ("aud_in_ms", torch.int32), ("aud_out_ms", torch.int32), ("rkey0", torch.int64),
+                ("rkey1", torch.int64), ("akey", torch.int32)]
+
+
+class DeviceTrace:
+    """Trace arrays in HBM (seed-major [S * n]) and their cf_trace view."""
+
+    def __init__(self, n_seeds, n_req, device="cuda"):
+        self.n_seeds, self.n_req = int(n_seeds), int(n_req)
+        self.t = {f: torch.empty(self.n_seeds * self.n_req, dtype=dt, device=device)
+                  for f, dt in TRACE_FIELDS}
+        self.c = cf_trace()
+        self.c.n_seeds, self.c.n_req = self.n_seeds, self.n_req
+        for f, _ in TRACE_FIELDS:
+            setattr(self.c, f + "_dev", self.t[f].data_ptr())
+
+    def to_numpy(self):
+        """Host copy with the unsigned dtypes of the C layout."""
+        unsigned = {"arr_ticks": np.uint64, "type": np.uint8, "n_img": np.uint8, "patches": np.uint16,
+                    "prompt": np.uint16, "out": np.uint16, "aud_in_ms": np.uint32,
+                    "aud_out_ms": np.uint32, "rkey0": np.uint64, "rkey1": np.uint64, "akey": np.uint32}
+        out = {f: self.t[f].cpu().numpy().view(unsigned[f]) for f, _ in TRACE_FIELDS}
+        out["n_seeds"], out["n_req"] = self.n_seeds, self.n_req
+        return out
+
+    @staticmethod
+    def from_numpy(tr, device="cuda"):
+        d = DeviceTrace(tr["n_seeds"], tr["n_req"], device)
+        for f, dt in TRACE_FIELDS:
+            a = np.ascontiguousarray(tr[f])
+            d.t[f].copy_(torch.from_numpy(a.view({torch.int64: np.int64, torch.uint8: np.uint8,
+                                                  torch.int16: np.int16,
+                                                  torch.int32: np.int32}[dt])))
+        return d
+
+
+class DevicePlans:
+    """Plan table (paper_2512_14098_amd.inputs.PlanTable) copied to HBM."""
+
+    FIELDS = ("n_nodes", "node_comp", "node_rep", "node_batch", "node_gpus", "n_alt", "alt_w",
+              "alt_node")
+
+    def __init__(self, tab, device="cuda"):
+        self.P = tab.P
+        self.t = {}
+        self.c = cf_plan_table()
+        self.c.P = tab.P
+        for f in self.FIELDS:
+            a = np.ascontiguousarray(getattr(tab, f))
+            if a.dtype == np.uint16:
+                a = a.view(np.int16)
+            self.t[f] = torch.from_numpy(a).to(device)
+            setattr(self.c, f + "_dev", self.t[f].data_ptr())
+
+
+# ------------------------------------------------------------------ entry points
+def cf_trace_gen(desc, seeds, n_req, device="cuda"):
+    tr = DeviceTrace(len(seeds), n_req, device)
+    moments = torch.empty((len(seeds), desc.n_types, 8), dtype=torch.int64, device=device)
+    s = (C.c_uint64 * len(seeds))(*[int(v) for v in seeds])
+    _check(_lib.cf_trace_gen(C.byref(desc), s, len(seeds), int(n_req), C.byref(tr.c), _p(moments),
+                             _stream()), "cf_trace_gen")
+    return tr, moments
+
+
+def cf_eval_coarse(desc, plans, moments_seed, n_gpus):
+    P = plans.P
+    dev = moments_seed.device
+    rd = torch.empty(P, dtype=torch.float64, device=dev)
+    bott = torch.empty(P, dtype=torch.int32, device=dev)
+    flags = torch.empty(P, dtype=torch.uint8, device=dev)
+    _check(_lib.cf_eval_coarse(C.byref(desc), C.byref(plans.c), _p(moments_seed.contiguous()),
+                               int(n_gpus), _p(rd), _p(bott), _p(flags), _stream()), "cf_eval_coarse")
+    return rd, bott, flags
+
+
+def cf_select_topk(rd, flags, k):
+    ids = torch.empty(max(int(k), 1), dtype=torch.int32, device=rd.device)
+    n = C.c_int32(0)
+    _check(_lib.cf_select_topk(_p(rd), _p(flags), int(rd.numel()), int(k), _p(ids), C.byref(n),
+                               _stream()), "cf_select_topk")
+    return ids[:n.value]
+
+
+def cf_rate_grid(rd, ids, K, alpha_max=1.0):
+    rates = torch.empty((ids.numel(), int(K)), dtype=torch.float64, device=rd.device)
+    _check(_lib.cf_rate_grid(_p(rd), _p(ids.contiguous()), int(ids.numel()), int(K),
+                             float(alpha_max), _p(rates), _stream()), "cf_rate_grid")
+    return rates
+
+
+def cf_eval_fine(desc, plans, plan_ids, rates, trace, lat_triples=None):
+    n_plans, K = rates.shape
+    S, T, dev = trace.n_seeds, desc.n_types, rates.device
+    met = torch.empty((n_plans, K, S, T), dtype=torch.int32, device=dev)
+    cnt = torch.empty((n_plans, K, S, T), dtype=torch.int32, device=dev)
+    events = torch.empty((n_plans, K, S), dtype=torch.int64, device=dev)
+    status = torch.empty((n_plans, K, S), dtype=torch.int32, device=dev)
+    out = cf_fine_out()
+    out.met_dev, out.cnt_dev = met.data_ptr(), cnt.data_ptr()
+    out.events_dev, out.status_dev = events.data_ptr(), status.data_ptr()
+    lat = None
+    if lat_triples is not None and len(lat_triples) > 0:
+        lt = torch.as_tensor(np.asarray(lat_triples, np.int32), device=dev)
+        lat = torch.zeros((len(lat_triples), trace.n_req, 4), dtype=torch.float64, device=dev)
+        out.lat_dev, out.lat_triples_dev, out.n_lat = lat.data_ptr(), lt.data_ptr(), len(lat_triples)
+    _check(_lib.cf_eval_fine(C.byref(desc), C.byref(plans.c), _p(plan_ids.contiguous()), int(n_plans),
+                             _p(rates.contiguous()), int(K), C.byref(trace.c), 0, C.byref(out),
+                             _stream()), "cf_eval_fine")
+    return dict(met=met, cnt=cnt, events=events, status=status, lat=lat)
+
+
+def cf_goodput_reduce(met, cnt, rates, theta, n_req):
+    n_plans, K, S, T = met.shape
+    dev = met.device
+    kstar = torch.empty(n_plans, dtype=torch.int32, device=dev)
+    gt = torch.empty((n_plans, T), dtype=torch.float64, device=dev)
+    g = torch.empty(n_plans, dtype=torch.float64, device=dev)
+    _check(_lib.cf_goodput_reduce(_p(met), _p(cnt), n_plans, K, S, T, _p(rates.contiguous()),
+                                  int(theta[0]), int(theta[1]), int(n_req), _p(kstar), _p(gt), _p(g),
+                                  _stream()), "cf_goodput_reduce")
+    return kstar, gt, g
+
+
+def cf_select_best(goodput):
+    best = torch.empty(1, dtype=torch.int32, device=goodput.device)
+    _check(_lib.cf_select_best(_p(goodput), int(goodput.numel()), _p(best), _stream()), "cf_select_best")
+    return best
+
+
+def cf_math_eval(op, x, y=None):
+    out = torch.empty_like(x)
+    _check(_lib.cf_math_eval(int(op), _p(x), _p(y), _p(out), int(x.numel()), _stream()), "cf_math_eval")
+    return out
+
+
+def cf_philox_eval(ctr, key):
+    out = torch.empty_like(ctr)
+    _check(_lib.cf_philox_eval(_p(ctr), _p(key), _p(out), int(ctr.shape[0]), _stream()),
+           "cf_philox_eval")
+    return out
+
+
+def cf_release_scratch():
+    _check(_lib.cf_release_scratch(), "cf_release_scratch")

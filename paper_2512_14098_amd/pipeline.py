@@ -1,0 +1,94 @@
+"""One pass of the evaluated path on the GPU for a workload configuration.
+
+trace generation -> phase 1 screening (Alg. 2) -> top-K by R_d -> rate grid
+-> phase 3 simulation of every (plan, rate, seed) -> goodput reduction ->
+selection.  Every step is a libcf call on torch's current stream; this
+module only allocates device tensors and sequences the calls.
+"""
+import numpy as np
+import torch
+
+from . import cf
+from .inputs import load_config, make_plans, seeds_of
+
+
+class Workload:
+    """Device-resident inputs of one configuration (plans, model, seeds)."""
+
+    def __init__(self, cfg, n_req=None, seeds=None, device="cuda"):
+        if isinstance(cfg, str):
+            cfg = load_config(cfg)
+        self.cfg = cfg
+        self.desc = cf.model_desc(cfg["model"])
+        self.tab = make_plans(cfg)
+        self.plans = cf.DevicePlans(self.tab, device)
+        self.seeds = seeds if seeds is not None else seeds_of(cfg)
+        self.n_req = int(cfg["n_req"] if n_req is None else n_req)
+        self.n_gpus = int(cfg["gpus"])
+        self.theta = cfg["model"].get("theta", [9, 10])
+        r = cfg["rates"]
+        self.explicit_rates = r.get("explicit")
+        self.K = len(self.explicit_rates) if self.explicit_rates else int(r["grid"])
+        self.alpha_max = float(r.get("alpha_max", 1.0))
+        top = cfg.get("top_k")
+        self.top_k = int(top) if top else self.tab.P
+        self.device = device
+
+
+def run_step(w, timers=None):
+    """One pass over the whole path; returns every intermediate on the device.
+
+    ``timers`` (optional dict) receives (start, end) torch.cuda.Event pairs
+    recorded around each step on the current stream."""
+    ev = {}
+
+    def mark(name):
+        if timers is None:
+            return None
+        e = torch.cuda.Event(enable_timing=True)
+        e.record()
+        ev.setdefault(name, []).append(e)
+        return e
+
+    mark("trace")
+    trace, moments = cf.cf_trace_gen(w.desc, w.seeds, w.n_req, w.device)
+    mark("trace")
+    mark("coarse")
+    rd, bott, flags = cf.cf_eval_coarse(w.desc, w.plans, moments[0], w.n_gpus)
+    mark("coarse")
+    mark("select")
+    ids = cf.cf_select_topk(rd, flags, w.top_k)
+    if w.explicit_rates:
+        rates = torch.tensor(w.explicit_rates, dtype=torch.float64, device=w.device).repeat(ids.numel(), 1)
+    else:
+        rates = cf.cf_rate_grid(rd, ids, w.K, w.alpha_max)
+    mark("select")
+    mark("fine")
+    fine = cf.cf_eval_fine(w.desc, w.plans, ids, rates, trace)
+    mark("fine")
+    mark("reduce")
+    kstar, gt, g = cf.cf_goodput_reduce(fine["met"], fine["cnt"], rates, w.theta, w.n_req)
+    best = cf.cf_select_best(g) if ids.numel() > 0 else None
+    mark("reduce")
+    if timers is not None:
+        timers.update(ev)
+    return dict(trace=trace, moments=moments, rd=rd, bottleneck=bott, flags=flags, ids=ids,
+                rates=rates, fine=fine, kstar=kstar, goodput_t=gt, goodput=g, best=best)
+
+
+def best_plan(out):
+    """Host-side summary of a step's selection."""
+    if out["best"] is None:
+        return None
+    b = int(out["best"].item())
+    return dict(index=b, plan_id=int(out["ids"][b].item()), goodput=float(out["goodput"][b].item()),
+                kstar=int(out["kstar"][b].item()))
+
+
+def events_total(out):
+    return int(out["fine"]["events"].sum().item())
+
+
+def status_summary(out):
+    st = out["fine"]["status"].cpu().numpy()
+    return {int(k): int(v) for k, v in zip(*np.unique(st, return_counts=True))}

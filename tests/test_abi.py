@@ -1,0 +1,50 @@
+"""The C-ABI library loads and exports every function include/cf.h declares
+(no compute call: this runs without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cf.h")
+LIB = os.path.join(ROOT, "paper_2512_14098_amd", "libcf.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][\w\s\*]*?\b(cf_\w+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declares_the_path():
+    names = declared_functions()
+    for f in ("cf_trace_gen", "cf_eval_coarse", "cf_select_topk", "cf_rate_grid", "cf_eval_fine",
+              "cf_goodput_reduce", "cf_select_best"):
+        assert f in names
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="libcf.so not built")
+def test_library_exports_every_declared_function():
+    lib = ctypes.CDLL(LIB)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="libcf.so not built")
+def test_binding_has_the_same_names():
+    from paper_2512_14098_amd import cf
+    for n in declared_functions():
+        assert n in cf.EXPORTED
+        if n not in ("cf_last_error", "cf_status_str", "cf_version"):
+            assert callable(getattr(cf, n)), n
+
+
+def test_product_path_does_not_import_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2512_14098_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in re.sub(r"#.*|//.*", "", text).lower() or f == "__init__.py", f
