@@ -980,10 +980,12 @@ extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_tabl
   memset(&a, 0, sizeof a);
   cf_status st = lower_model(model, &a.m);
   if (st != CF_OK) return st;
-  if (!plans || !plan_ids_dev || !rates_dev || !trace || !out) return set_error(CF_EINVAL, "NULL argument");
+  if (!plans || !trace || !out) return set_error(CF_EINVAL, "NULL argument");
   if (flags != 0) return set_error(CF_EUNSUPPORTED, "flags must be 0");
   if (n_plans < 0 || K < 1 || trace->n_seeds < 1 || trace->n_req < 0 || plans->P < 0)
     return set_error(CF_EINVAL, "sizes");
+  if (n_plans == 0) return CF_OK;
+  if (!plan_ids_dev || !rates_dev) return set_error(CF_EINVAL, "NULL argument");
   if (!out->met_dev || !out->cnt_dev || !out->events_dev || !out->status_dev)
     return set_error(CF_EINVAL, "NULL output array");
   if (out->lat_dev && (out->n_lat < 0 || (out->n_lat > 0 && !out->lat_triples_dev)))

@@ -96,10 +96,10 @@ def test_coarse_select_grid_parity(cf, name):
     assert np.array_equal(rd.cpu().numpy(), want[0])
     assert np.array_equal(bn.cpu().numpy(), want[1])
     assert np.array_equal(fl.cpu().numpy(), want[2])
-    for k in sorted({1, 7, 1000, tab.P}):
+    for k in sorted({1, 7, 1000, min(tab.P, 65536)}):
         ids = cf.cf_select_topk(rd, fl, k).cpu().numpy()
         assert np.array_equal(ids, O.select_topk(want[0], want[2], k)), k
-    ids = cf.cf_select_topk(rd, fl, tab.P)
+    ids = cf.cf_select_topk(rd, fl, min(tab.P, 65536))
     for K, alpha in ((16, 1.0), (32, 0.75)):
         got = cf.cf_rate_grid(rd, ids, K, alpha).cpu().numpy()
         assert np.array_equal(got, O.rate_grid(want[0], ids.cpu().numpy(), K, alpha))
