@@ -15,9 +15,13 @@
 // deliveries due at t then arrivals at t are applied, and every executor
 // whose state changed since it went idle may start one iteration.
 //
-// Memory: executor state and the plan in LDS; stage queues as chunked
-// lists in a per-wavefront pool in HBM; LLM running sets as ordered slot
-// arrays; per-request state in HBM, indexed by request id.
+// Memory: the plan, executor state and every stage's queue / running-set
+// descriptor live in LDS (sized per launch from the largest plan); queue
+// entries (chunked lists in a per-wavefront pool), running slots and the
+// 16-byte per-request records live in HBM.  The members of a completed
+// iteration are processed lane-parallel, 64 at a time: delay-line appends,
+// queue appends and running-set appends keep the member order through
+// wavefront prefix sums, and SLO counts are ballot + popcount per type.
 //
 // Decode steps of a non-gated LLM stage cost O(1): a running request's
 // token count is (decode steps of its stage since it joined) + 1, so each
@@ -39,16 +43,24 @@ constexpr int kChunk = 64;                          // queue chunk entries
 constexpr int kHist = 64;                           // thinker step-time ring
 constexpr uint32_t kNone = 0xFFFFFFFFu;
 
-enum { IT_BATCH = 0, IT_PREFILL = 1, IT_DECODE = 2 };
+enum { IT_BATCH = 0, IT_PREFILL = 1, IT_DECODE = 2, IT_FINISH = 3 };
 enum { DL_DELIVER = 0, DL_TICK = 1 };
-constexpr uint32_t FL_TH_DONE = 16u;   // rs_flags: thinker finished; low 4 bits: outputs left
-constexpr uint32_t MARK = 0x80000000u; // gated running slot: in the current decode step
+constexpr uint32_t MISC_OUTS = 15u;     // outputs still to finish
+constexpr uint32_t MISC_TH_DONE = 16u;  // thinker finished
+constexpr uint32_t MARK = 0x80000000u;  // gated running slot: in the current decode step
+constexpr uint32_t EX_RUN = 1u << 21;   // executor state: busy with a multi-step decode run
+// stage flags
+constexpr uint8_t SF_LLM = 1, SF_GATED = 2, SF_THINKER = 4, SF_ENC = 8, SF_GEN = 16;
+
+struct __attribute__((aligned(16))) Rec {
+  uint64_t ex;    // executor of each component of the path (byte c), 0xFF off the path
+  uint32_t join;  // deliveries received per component (4 bits each)
+  uint32_t misc;  // outputs left (4 bits), thinker done (bit 4), type (bits 8..10)
+};
 
 struct Layout {
-  size_t si_comp, si_exec, si_beff, si_qhc, si_qhp, si_qtc, si_qtp, si_qn, si_roff, si_rn, si_iter, si_minfin,
-      si_hist;
+  size_t rec, tfirst, tlast, tmedia, thjoin;
   size_t run_r, run_k, hist, mem, dl_t, dl_v, pool, pool_next, pool_free;
-  size_t rs_ex, rs_join, rs_flags, rs_tfirst, rs_tlast, rs_tmedia, rs_thjoin;
   size_t bytes;
   int run_cap, hist_slots, n_chunks;
   uint32_t dl_mask;
@@ -56,7 +68,6 @@ struct Layout {
 
 struct FineArgs {
   KModel m;
-  // plans
   int P;
   const uint8_t *n_nodes, *node_comp, *node_rep, *n_alt, *alt_w, *alt_node;
   const uint16_t *node_batch;
@@ -64,28 +75,38 @@ struct FineArgs {
   int n_plans;
   const double *rates;
   int K;
-  // trace
   const uint64_t *ticks, *rkey0, *rkey1;
   const uint8_t *type;
   const uint16_t *patches, *prompt, *out;
   const uint32_t *aud_in, *aud_out, *akey;
   int S, n;
-  // outputs
   uint32_t *met, *cnt, *status;
   uint64_t *events;
   double *lat;
   const int32_t *lat_triples;
   int n_lat;
-  // scratch
   char *slab;
   Layout L;
   unsigned int *ticket;
   unsigned int total;
+  int nsi_cap;  // stage instances provided in LDS
+};
+
+// model tables read with per-lane (divergent) indices
+struct ModelLds {
+  uint8_t child[CF_MAX_TYPES][CF_MAX_COMP], npar[CF_MAX_TYPES][CF_MAX_COMP];
+  int8_t ttft_c[CF_MAX_TYPES], th_c[CF_MAX_TYPES], ta_c[CF_MAX_TYPES];
+  uint8_t outm[CF_MAX_TYPES], pfo[CF_MAX_TYPES], gen_out[CF_MAX_TYPES];
+  uint8_t kind[CF_MAX_COMP], nout_attr[CF_MAX_COMP];
+  double slo[CF_MAX_TYPES][4];
 };
 
 struct WaveShared {
   double ex_tend[CF_MAX_EXEC];
   double ex_last[CF_MAX_EXEC];
+  double ex_t0[CF_MAX_EXEC];    // decode run: start of its first step
+  double ex_dur[CF_MAX_EXEC];   // decode run: duration of every step
+  uint32_t ex_itgt[CF_MAX_EXEC];  // decode run: step counter of its stage at ex_tend
   uint32_t ex_st[CF_MAX_EXEC];  // busy:1 ran:1 kind:2 rr:4 cur:4 nmem:9
   uint16_t ex_first[CF_MAX_EXEC];
   uint8_t ex_ns[CF_MAX_EXEC], ex_node[CF_MAX_EXEC];
@@ -94,7 +115,18 @@ struct WaveShared {
   uint8_t vbase[CF_MAX_NODES + 1], vrep[CF_MAX_NODES], vminc[CF_MAX_NODES], vcomp[CF_MAX_NODES];
   uint16_t vbatch[CF_MAX_NODES];
   uint32_t met[CF_MAX_TYPES], cnt[CF_MAX_TYPES];
+  ModelLds ml;
 };
+
+// stage-instance descriptors, structure of arrays in dynamic LDS
+struct SiLds {
+  uint8_t *comp, *flags, *qhp, *qtp;
+  uint16_t *beff;
+  int16_t *hist;
+  int *qhc, *qtc, *qn, *roff, *rn;
+  uint32_t *iter, *minfin;
+};
+constexpr size_t kSiBytes = 1 + 1 + 1 + 1 + 2 + 2 + 4 * 7;
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x; }
 __device__ __forceinline__ uint32_t ru(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -102,12 +134,13 @@ __device__ __forceinline__ int ri(int v) { return __builtin_amdgcn_readfirstlane
 __device__ __forceinline__ uint64_t ru64(uint64_t v) {
   return ((uint64_t)ru((uint32_t)(v >> 32)) << 32) | ru((uint32_t)v);
 }
-__device__ __forceinline__ double rd(double v) { return __longlong_as_double((long long)ru64((uint64_t)__double_as_longlong(v))); }
-
+__device__ __forceinline__ double rdb(double v) {
+  return __longlong_as_double((long long)ru64((uint64_t)__double_as_longlong(v)));
+}
 __device__ __forceinline__ double wave_min(double v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
-    double w = __shfl_xor(v, o, 64);
+    const double w = __shfl_xor(v, o, 64);
     v = w < v ? w : v;
   }
   return v;
@@ -115,7 +148,7 @@ __device__ __forceinline__ double wave_min(double v) {
 __device__ __forceinline__ uint32_t wave_min_u(uint32_t v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
-    uint32_t w = __shfl_xor(v, o, 64);
+    const uint32_t w = __shfl_xor(v, o, 64);
     v = w < v ? w : v;
   }
   return v;
@@ -125,25 +158,36 @@ __device__ __forceinline__ uint32_t wave_sum_u(uint32_t v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
 }
+__device__ __forceinline__ uint32_t wave_or_u(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v |= __shfl_xor(v, o, 64);
+  return v;
+}
 __device__ __forceinline__ uint32_t lanes_below(uint64_t bal) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
 }
+// exclusive prefix sum of v over the lanes, and the total
+__device__ __forceinline__ uint32_t wave_excl_scan(uint32_t v, uint32_t &total) {
+  uint32_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t o = __shfl_up(x, d, 64);
+    if (lane_id() >= d) x += o;
+  }
+  total = ru(__shfl(x, 63, 64));
+  return x - v;
+}
 
-// All mutable per-triple state that is not in LDS; lives in registers.
 struct Sim {
   const FineArgs *A;
   WaveShared *sh;
-  // slab arrays
-  uint8_t *si_comp, *si_exec;
-  uint16_t *si_beff;
-  int *si_qhc, *si_qhp, *si_qtc, *si_qtp, *si_qn, *si_roff, *si_rn, *si_hist;
-  uint32_t *si_iter, *si_minfin, *run_r, *run_k, *mem, *dl_v, *pool, *rs_join, *rs_flags, *rs_thjoin;
+  SiLds si;
+  Rec *rec;
+  double *tfirst, *tlast, *tmedia, *hist, *dl_t;
+  uint32_t *thjoin, *run_r, *run_k, *mem, *dl_v, *pool;
   int *pool_next, *pool_free;
-  double *hist, *dl_t, *rs_tfirst, *rs_tlast, *rs_tmedia;
-  uint64_t *rs_ex;
-  // scalars
   size_t soff;
-  double lam, now;
+  double lam, now, dl_head_t, t_arr;
   uint64_t events, dirty, ta_exec_mask;
   uint32_t status, dl_head, dl_tail;
   int pool_top, pool_fresh, n_done, nx, lat_slot;
@@ -165,9 +209,8 @@ __device__ __forceinline__ uint32_t attr(const Sim &S, uint32_t r, int a) {
     default: return 0;
   }
 }
-
-__device__ __forceinline__ uint32_t x_of(const Sim &S, uint32_t r, int c) {
-  uint32_t sel = S.A->m.xsel[c], x = 0;
+__device__ __forceinline__ uint32_t x_of(const Sim &S, uint32_t r, uint32_t sel) {
+  uint32_t x = 0;
   while (sel) {
     const int a = __ffs(sel) - 1;
     sel &= sel - 1;
@@ -175,21 +218,16 @@ __device__ __forceinline__ uint32_t x_of(const Sim &S, uint32_t r, int c) {
   }
   return x;
 }
-
-__device__ __forceinline__ int type_of(const Sim &S, uint32_t r) { return S.A->type[S.soff + r]; }
-
 __device__ __forceinline__ uint32_t nout_of(const Sim &S, uint32_t r, int t, int c) {
-  if ((S.A->m.pfo[t] >> c) & 1u) return 1;
-  const uint32_t v = attr(S, r, S.A->m.nout_attr[c]);
+  if ((S.sh->ml.pfo[t] >> c) & 1u) return 1;
+  const uint32_t v = attr(S, r, S.sh->ml.nout_attr[c]);
   return v < 1 ? 1 : v;
 }
-
 __device__ __forceinline__ double arrival_time(const Sim &S, uint32_t r) {
   return ((double)S.A->ticks[S.soff + r] * 0x1p-32) / S.lam;
 }
-
-__device__ __forceinline__ int exec_of(const Sim &S, uint32_t r, int c) { return (int)((S.rs_ex[r] >> (8 * c)) & 0xFFu); }
-
+__device__ __forceinline__ int ex_byte(uint64_t ex, int c) { return (int)((ex >> (8 * c)) & 0xFFu); }
+__device__ __forceinline__ int rtype(uint32_t misc) { return (int)((misc >> 8) & 7u); }
 __device__ __forceinline__ int stage_of(const Sim &S, int x, int c) {
   const int v = S.sh->ex_node[x];
   return S.sh->ex_first[x] + __popc((uint32_t)S.sh->vcomp[v] & ((1u << c) - 1u));
@@ -197,18 +235,25 @@ __device__ __forceinline__ int stage_of(const Sim &S, int x, int c) {
 
 // ------------------------------------------------------------------ pool / queues
 __device__ __forceinline__ int chunk_alloc(Sim &S) {
-  if (S.pool_top > 0) return S.pool_free[--S.pool_top];
+  if (S.pool_top > 0) return ri(S.pool_free[--S.pool_top]);
   if (S.pool_fresh < S.A->L.n_chunks) return S.pool_fresh++;
   S.status |= CF_ST_OVERFLOW;
   return -1;
 }
 __device__ __forceinline__ void chunk_free(Sim &S, int c) {
-  if (c >= 0 && c < S.A->L.n_chunks && S.pool_top < S.A->L.n_chunks) S.pool_free[S.pool_top++] = c;
-  else S.status |= CF_ST_OVERFLOW;
+  if (c >= 0 && c < S.A->L.n_chunks && S.pool_top < S.A->L.n_chunks) {
+    if (lane_id() == 0) S.pool_free[S.pool_top] = c;
+    S.pool_top++;
+  } else {
+    S.status |= CF_ST_OVERFLOW;
+  }
 }
 
-__device__ void q_push(Sim &S, int si, uint32_t r) {
-  int qn = S.si_qn[si], tc = S.si_qtc[si], tp = S.si_qtp[si];
+// appends, in lane order, the requests r of the lanes set in bal to stage si's queue
+__device__ void q_push_lanes(Sim &S, int si, uint64_t bal, uint32_t r) {
+  const int cnt = __popcll(bal);
+  if (cnt == 0) return;
+  int qn = S.si.qn[si], tc = S.si.qtc[si], tp = S.si.qtp[si];
   if (qn > 0 && (tc < 0 || tc >= S.A->L.n_chunks || tp < 0 || tp > kChunk)) {
     S.status |= CF_ST_OVERFLOW;
     return;
@@ -216,29 +261,41 @@ __device__ void q_push(Sim &S, int si, uint32_t r) {
   if (qn == 0) {
     const int c = chunk_alloc(S);
     if (c < 0) return;
-    S.si_qhc[si] = c;
-    S.si_qhp[si] = 0;
-    tc = c;
-    tp = 0;
-  } else if (tp == kChunk) {
-    const int c = chunk_alloc(S);
-    if (c < 0) return;
-    S.pool_next[tc] = c;
+    S.si.qhc[si] = c;
+    S.si.qhp[si] = 0;
     tc = c;
     tp = 0;
   }
-  S.pool[(size_t)tc * kChunk + tp] = r;
-  S.si_qtc[si] = tc;
-  S.si_qtp[si] = tp + 1;
-  S.si_qn[si] = qn + 1;
+  // the entries fill the tail chunk, then at most one fresh chunk (cnt <= 64)
+  const int room = kChunk - tp;
+  int c1 = -1;
+  if (cnt > room) {
+    c1 = chunk_alloc(S);
+    if (c1 < 0) return;
+    if (lane_id() == 0) S.pool_next[tc] = c1;
+  }
+  if ((bal >> lane_id()) & 1ull) {
+    const int k = (int)lanes_below(bal);
+    const int ch = k < room ? tc : c1;
+    const int pos = k < room ? tp + k : k - room;
+    S.pool[(size_t)ch * kChunk + pos] = r;
+  }
+  if (cnt <= room) {
+    S.si.qtc[si] = tc;
+    S.si.qtp[si] = (uint8_t)(tp + cnt);
+  } else {
+    S.si.qtc[si] = c1;
+    S.si.qtp[si] = (uint8_t)(cnt - room);
+  }
+  S.si.qn[si] = qn + cnt;
 }
 
-// pops the first k entries of stage si's queue into mem[dst..dst+k)
+// pops the first k entries of stage si's queue into dst[0..k)
 __device__ void q_pop(Sim &S, int si, int k, uint32_t *dst) {
-  int hc = S.si_qhc[si], hp = S.si_qhp[si];
-  const int tc = S.si_qtc[si], tp = S.si_qtp[si];
+  int hc = S.si.qhc[si], hp = S.si.qhp[si];
+  const int tc = S.si.qtc[si], tp = S.si.qtp[si];
   if (k <= 0) return;
-  if (k > S.si_qn[si] || hc < 0 || hc >= S.A->L.n_chunks) {  // never on a consistent queue
+  if (k > S.si.qn[si] || hc < 0 || hc >= S.A->L.n_chunks) {
     S.status |= CF_ST_OVERFLOW;
     return;
   }
@@ -255,122 +312,108 @@ __device__ void q_pop(Sim &S, int si, int k, uint32_t *dst) {
     got += take;
     hp += take;
     if (hp == kChunk && got < k) {
-      const int nx = S.pool_next[hc];
+      const int nx = ri(S.pool_next[hc]);
       chunk_free(S, hc);
       hc = nx;
       hp = 0;
     }
   }
-  if (got < k) {
-    __syncthreads();
-    return;
-  }
-  const int qn = S.si_qn[si] - k;
-  S.si_qn[si] = qn;
+  __syncthreads();
+  if (got < k) return;
+  const int qn = S.si.qn[si] - k;
+  S.si.qn[si] = qn;
   if (qn == 0) {
     chunk_free(S, hc);
+    hc = -1;
+    hp = 0;
   } else if (hp == kChunk) {
-    const int nx = S.pool_next[hc];
+    const int nx = ri(S.pool_next[hc]);
     if (nx < 0 || nx >= S.A->L.n_chunks) S.status |= CF_ST_OVERFLOW;
     chunk_free(S, hc);
     hc = nx;
     hp = 0;
   }
-  S.si_qhc[si] = hc;
-  S.si_qhp[si] = hp;
-  __syncthreads();
+  S.si.qhc[si] = hc;
+  S.si.qhp[si] = (uint8_t)hp;
 }
 
-__device__ __forceinline__ void dl_push(Sim &S, double due, uint32_t v) {
+__device__ __forceinline__ void enqueue1(Sim &S, uint32_t r, int c, int x) {
+  S.events++;
+  q_push_lanes(S, stage_of(S, x, c), 1ull, r);
+  S.dirty |= 1ull << x;
+}
+
+// ------------------------------------------------------------------ delay line
+__device__ __forceinline__ void dl_push1(Sim &S, double due, uint32_t v) {
   if (S.dl_tail - S.dl_head > S.A->L.dl_mask) {
     S.status |= CF_ST_OVERFLOW;
     return;
   }
-  S.dl_t[S.dl_tail & S.A->L.dl_mask] = due;
-  S.dl_v[S.dl_tail & S.A->L.dl_mask] = v;
+  if (lane_id() == 0) {
+    S.dl_t[S.dl_tail & S.A->L.dl_mask] = due;
+    S.dl_v[S.dl_tail & S.A->L.dl_mask] = v;
+  }
+  if (S.dl_head == S.dl_tail) S.dl_head_t = due;
   S.dl_tail++;
 }
 
-// ------------------------------------------------------------------ request flow
-__device__ void enqueue(Sim &S, uint32_t r, int c, int x) {
-  S.events++;
-  q_push(S, stage_of(S, x, c), r);
-  S.dirty |= 1ull << x;
-}
-
-__device__ void join(Sim &S, uint32_t r, int c) {
-  const uint32_t j = S.rs_join[r] + (1u << (4 * c));
-  S.rs_join[r] = j;
-  const int t = type_of(S, r);
-  if (((j >> (4 * c)) & 15u) == S.A->m.npar[t][c]) enqueue(S, r, c, exec_of(S, r, c));
-}
-
-__device__ __forceinline__ void deliver(Sim &S, uint32_t r, int c2, int xfrom) {
-  if (exec_of(S, r, c2) == xfrom) join(S, r, c2);
-  else dl_push(S, S.now + S.A->m.comm, (r << 4) | (DL_DELIVER << 3) | (uint32_t)c2);
-}
-
-__device__ void complete_request(Sim &S, uint32_t r) {
-  const KModel &m = S.A->m;
-  S.events++;
-  S.n_done++;
-  const int t = type_of(S, r);
-  const double a = arrival_time(S, r);
-  double ttft = 0.0, tpot = 0.0, media = 0.0;
-  const int tc = m.ttft_c[t];
-  if (tc >= 0) {
-    const double tf = S.rs_tfirst[r];
-    ttft = tf - a;
-    const uint32_t n1 = nout_of(S, r, t, tc);
-    if (n1 > 1) tpot = (S.rs_tlast[r] - tf) / (double)(n1 - 1);
+// ------------------------------------------------------------------ gating
+__device__ __forceinline__ bool token_visible(const Sim &S, uint32_t r, uint32_t misc, int th, int xth, int x,
+                                              uint32_t k, uint32_t nth, bool &undecided) {
+  const double delta = (xth == x) ? 0.0 : S.A->m.comm;
+  double e;
+  if (k <= 1) {
+    e = S.tfirst[r];
+  } else if ((misc & MISC_TH_DONE) && k == nth) {
+    e = S.tlast[r];
+  } else {
+    const int si = stage_of(S, xth, th);
+    const uint32_t q = S.thjoin[r] + k - 1u;
+    const uint32_t it = S.si.iter[si];
+    if (q > it) return false;
+    const double *h = S.hist + (size_t)S.si.hist[si] * kHist;
+    if (it - q < (uint32_t)kHist) {
+      e = h[q & (kHist - 1)];
+    } else {
+      e = h[(it - (kHist - 1)) & (kHist - 1)];  // oldest kept step: token k is no later
+      if (!(e + delta <= S.now)) {
+        undecided = true;
+        return false;
+      }
+    }
   }
-  const double e2e = S.now - a;
-  if (m.gen_out[t]) media = S.rs_tmedia[r] - a;
-  const bool ok = ttft <= m.slo[t][0] && tpot <= m.slo[t][1] && e2e <= m.slo[t][2] && media <= m.slo[t][3];
-  S.sh->cnt[t] += 1;
-  if (ok) S.sh->met[t] += 1;
-  if (S.lat_slot >= 0) {
-    double *L = S.A->lat + ((size_t)S.lat_slot * S.A->n + r) * 4;
-    L[0] = ttft;
-    L[1] = tpot;
-    L[2] = e2e;
-    L[3] = media;
-  }
+  return e + delta <= S.now;
 }
 
-// request r finishes component c on executor x at S.now
-__device__ void finish(Sim &S, uint32_t r, int c, int x) {
-  const KModel &m = S.A->m;
-  const int t = type_of(S, r);
-  uint32_t ch = m.child[t][c];
-  while (ch) {
-    const int c2 = __ffs(ch) - 1;
-    ch &= ch - 1;
-    deliver(S, r, c2, x);
-  }
-  if (c == m.th_c[t]) S.rs_flags[r] |= FL_TH_DONE;
-  if ((m.outm[t] >> c) & 1u) {
-    if (m.kind[c] == CF_GEN) S.rs_tmedia[r] = S.now;
-    const uint32_t f = S.rs_flags[r] - 1u;
-    S.rs_flags[r] = f;
-    if ((f & 15u) == 0) complete_request(S, r);
-  }
+__device__ __forceinline__ bool slot_eligible(const Sim &S, uint32_t r, uint32_t tok, int c, int x, bool &undecided) {
+  const Rec R = S.rec[r];
+  const int t = rtype(R.misc);
+  if (S.sh->ml.ta_c[t] != c) return true;
+  const int th = S.sh->ml.th_c[t];
+  const uint32_t nth = nout_of(S, r, t, th);
+  const uint32_t k = tok + 1u < nth ? tok + 1u : nth;
+  return token_visible(S, r, R.misc, th, ex_byte(R.ex, th), x, k, nth, undecided);
 }
 
+// ------------------------------------------------------------------ requests
 __device__ void arrive(Sim &S, uint32_t r) {
   const KModel &m = S.A->m;
   const FineArgs &A = *S.A;
   const WaveShared &sh = *S.sh;
   S.events++;
   const size_t o = S.soff + r;
-  const int t = A.type[o];
-  if (t >= m.nt) { S.status |= CF_ST_INVALID; return; }
+  const int t = ri(A.type[o]);
+  if (t >= m.nt) {
+    S.status |= CF_ST_INVALID;
+    return;
+  }
+  const uint64_t k0 = ru64(A.rkey0[o]), k1 = ru64(A.rkey1[o]);
+  const uint32_t ak = ru(A.akey[o]);
   int alt = 0;
   if (sh.nalt[t] == 2) {
     const uint64_t w0 = sh.aw[t][0], w1 = sh.aw[t][1];
-    alt = ((((uint64_t)A.akey[o]) * (w0 + w1)) >> 32) < w0 ? 0 : 1;
+    alt = ((((uint64_t)ak) * (w0 + w1)) >> 32) < w0 ? 0 : 1;
   }
-  const uint64_t k0 = A.rkey0[o], k1 = A.rkey1[o];
   uint64_t ex = ~0ull;
   uint32_t path = m.path[t];
   while (path) {
@@ -382,94 +425,262 @@ __device__ void arrive(Sim &S, uint32_t r) {
     const int x = sh.vbase[v] + (int)((key * sh.vrep[v]) >> 16);
     ex = (ex & ~(0xFFull << (8 * c))) | ((uint64_t)x << (8 * c));
   }
-  S.rs_ex[r] = ex;
-  S.rs_join[r] = 0;
-  S.rs_flags[r] = (uint32_t)__popc(m.outm[t]);
+  Rec R;
+  R.ex = ex;
+  R.join = 0;
+  R.misc = (uint32_t)__popc(m.outm[t]) | ((uint32_t)t << 8);
+  if (lane_id() == 0) S.rec[r] = R;
   uint32_t src = m.srcm[t];
   while (src) {
     const int c = __ffs(src) - 1;
     src &= src - 1;
-    enqueue(S, r, c, exec_of(S, r, c));
+    enqueue1(S, r, c, ex_byte(ex, c));
   }
 }
 
-// ------------------------------------------------------------------ gating
-// Is thinker token k of request r (gate source th on executor xth) visible
-// at S.now to a talker on executor x?
-__device__ __forceinline__ bool token_visible(const Sim &S, uint32_t r, int t, int th, int xth, int x, uint32_t k,
-                                              uint32_t nth, bool &undecided) {
-  const double delta = (xth == x) ? 0.0 : S.A->m.comm;
-  double e;
-  if (k <= 1) {
-    e = S.rs_tfirst[r];
-  } else if ((S.rs_flags[r] & FL_TH_DONE) && k == nth) {
-    e = S.rs_tlast[r];
-  } else {
-    const int si = stage_of(S, xth, th);
-    const uint32_t q = S.rs_thjoin[r] + k - 1u;
-    const uint32_t it = S.si_iter[si];
-    if (q > it) return false;
-    const double *h = S.hist + (size_t)S.si_hist[si] * kHist;
-    if (it - q < (uint32_t)kHist) {
-      e = h[q & (kHist - 1)];
-    } else {
-      e = h[(it - (kHist - 1)) & (kHist - 1)];  // oldest kept: token k is no later
-      if (!(e + delta <= S.now)) { undecided = true; return false; }
+// step 2: a delayed delivery of request r to component c2
+__device__ void dl_deliver(Sim &S, uint32_t r, int c2) {
+  const Rec R = S.rec[r];
+  const uint64_t ex = ru64(R.ex);
+  const uint32_t join = ru(R.join) + (1u << (4 * c2));
+  const uint32_t misc = ru(R.misc);
+  if (lane_id() == 0) S.rec[r].join = join;
+  const int t = rtype(misc);
+  if (((join >> (4 * c2)) & 15u) == S.A->m.npar[t][c2]) enqueue1(S, r, c2, ex_byte(ex, c2));
+}
+
+// Lane-parallel processing of the n members mem[0..n) of a completed
+// iteration of stage si (component c) on executor x, in member order.
+//   IT_BATCH:   ENC/GEN members finish c;
+//   IT_PREFILL: members get their first token (TTFT stamps, thinker's
+//               streaming delivery to the talker) and finish or join Run;
+//   IT_FINISH:  decode members that produced their last token finish c.
+__device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, const uint32_t *mem) {
+  const KModel &m = S.A->m;
+  const ModelLds &ml = S.sh->ml;
+  const bool gated = S.si.flags[si] & SF_GATED;
+  const uint32_t iter_s = S.si.iter[si];
+  const double now = S.now;
+  for (int b = 0; b < n; b += 64) {
+    const int j = b + lane_id();
+    const bool valid = j < n;
+    uint32_t r = 0;
+    Rec R = {0, 0, 0};
+    if (valid) {
+      r = mem[j];
+      R = S.rec[r];
     }
+    const int t = rtype(R.misc);
+    bool fin = valid;
+    bool stream = false;  // thinker: deliver to the talker now
+    int ta = 0;
+    uint32_t key = 0;
+    if (valid && kind == IT_PREFILL) {
+      const uint32_t no = nout_of(S, r, t, c);
+      if (c == ml.ttft_c[t]) {
+        S.tfirst[r] = now;
+        S.tlast[r] = now;
+      }
+      if (c == ml.th_c[t]) {
+        S.thjoin[r] = iter_s;
+        stream = true;
+        ta = ml.ta_c[t];
+      }
+      fin = no == 1;
+      key = gated ? 1u : iter_s + no - 1u;
+    } else if (valid && kind == IT_FINISH) {
+      if (c == ml.ttft_c[t]) S.tlast[r] = now;
+    }
+    const bool append = valid && kind == IT_PREFILL && !fin;
+    // delayed deliveries: the streaming one first, then remote children
+    const uint32_t ch = fin ? ml.child[t][c] : 0u;
+    uint32_t rc = 0, lc = 0;
+    for (uint32_t cc = ch; cc;) {
+      const int c2 = __ffs(cc) - 1;
+      cc &= cc - 1;
+      if (ex_byte(R.ex, c2) == x) lc |= 1u << c2;
+      else rc |= 1u << c2;
+    }
+    const bool stream_remote = stream && ex_byte(R.ex, ta) != x;
+    if (stream && !stream_remote) lc |= 1u << ta;
+    uint32_t dl_total;
+    const uint32_t dl_off = wave_excl_scan((stream_remote ? 1u : 0u) + (uint32_t)__popc(rc), dl_total);
+    if (dl_total) {
+      if (S.dl_tail - S.dl_head + dl_total > S.A->L.dl_mask + 1u) {
+        S.status |= CF_ST_OVERFLOW;
+        return;
+      }
+      const double due = now + m.comm;
+      uint32_t pos = S.dl_tail + dl_off;
+      if (stream_remote) {
+        S.dl_t[pos & S.A->L.dl_mask] = due;
+        S.dl_v[pos & S.A->L.dl_mask] = (r << 4) | (DL_DELIVER << 3) | (uint32_t)ta;
+        pos++;
+      }
+      for (uint32_t cc = rc; cc;) {
+        const int c2 = __ffs(cc) - 1;
+        cc &= cc - 1;
+        S.dl_t[pos & S.A->L.dl_mask] = due;
+        S.dl_v[pos & S.A->L.dl_mask] = (r << 4) | (DL_DELIVER << 3) | (uint32_t)c2;
+        pos++;
+      }
+      if (S.dl_head == S.dl_tail) S.dl_head_t = due;
+      S.dl_tail += dl_total;
+    }
+    // local deliveries: join counters, components whose inputs are complete
+    uint32_t join = R.join, ready = 0;
+    for (uint32_t cc = lc; cc;) {
+      const int c2 = __ffs(cc) - 1;
+      cc &= cc - 1;
+      join += 1u << (4 * c2);
+      if (((join >> (4 * c2)) & 15u) == ml.npar[t][c2]) ready |= 1u << c2;
+    }
+    // outputs and completion
+    uint32_t misc = R.misc;
+    bool done = false;
+    if (fin && valid) {
+      if (c == ml.th_c[t]) misc |= MISC_TH_DONE;
+      if ((ml.outm[t] >> c) & 1u) {
+        if (ml.kind[c] == CF_GEN) S.tmedia[r] = now;
+        misc -= 1u;
+        done = (misc & MISC_OUTS) == 0;
+      }
+    }
+    if (valid) {
+      S.rec[r].join = join;
+      S.rec[r].misc = misc;
+    }
+    // running-set appends (prefill), in member order
+    const uint64_t abal = __ballot(append);
+    if (abal) {
+      const int rn = S.si.rn[si];
+      if (append) {
+        const int pos = rn + (int)lanes_below(abal);
+        S.run_r[S.si.roff[si] + pos] = r;
+        S.run_k[S.si.roff[si] + pos] = key;
+      }
+      S.si.rn[si] = rn + __popcll(abal);
+      if (!gated) {
+        const uint32_t mn = ru(wave_min_u(append ? key : kNone));
+        if (mn < S.si.minfin[si]) S.si.minfin[si] = mn;
+      }
+    }
+    // queue appends per ready component, in member order
+    const uint32_t any_ready = ru(wave_or_u(ready));
+    for (uint32_t cc = any_ready; cc;) {
+      const int c2 = __ffs(cc) - 1;
+      cc &= cc - 1;
+      const uint64_t bal = __ballot((ready >> c2) & 1u);
+      S.events += (uint64_t)__popcll(bal);
+      q_push_lanes(S, stage_of(S, x, c2), bal, r);
+      S.dirty |= 1ull << x;
+    }
+    // completed requests: latencies, SLO check, per-type counts
+    const uint64_t dbal = __ballot(done);
+    if (dbal) {
+      bool ok = false;
+      if (done) {
+        const double a = arrival_time(S, r);
+        double ttft = 0.0, tpot = 0.0, media = 0.0;
+        const int tc = ml.ttft_c[t];
+        if (tc >= 0) {
+          const double tf = S.tfirst[r];
+          ttft = tf - a;
+          const uint32_t n1 = nout_of(S, r, t, tc);
+          if (n1 > 1) tpot = (S.tlast[r] - tf) / (double)(n1 - 1);
+        }
+        const double e2e = now - a;
+        if (ml.gen_out[t]) media = S.tmedia[r] - a;
+        ok = ttft <= ml.slo[t][0] && tpot <= ml.slo[t][1] && e2e <= ml.slo[t][2] && media <= ml.slo[t][3];
+        if (S.lat_slot >= 0) {
+          double *Lp = S.A->lat + ((size_t)S.lat_slot * S.A->n + r) * 4;
+          Lp[0] = ttft;
+          Lp[1] = tpot;
+          Lp[2] = e2e;
+          Lp[3] = media;
+        }
+      }
+      for (int tt = 0; tt < m.nt; tt++) {
+        const uint64_t bc = __ballot(done && t == tt);
+        if (bc) {
+          const uint64_t bm = __ballot(done && ok && t == tt);
+          S.sh->cnt[tt] += (uint32_t)__popcll(bc);
+          S.sh->met[tt] += (uint32_t)__popcll(bm);
+        }
+      }
+      S.events += (uint64_t)__popcll(dbal);
+      S.n_done += __popcll(dbal);
+    }
+    __syncthreads();
   }
-  return e + delta <= S.now;
 }
 
 // ------------------------------------------------------------------ iterations
-__device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind) {
+__device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool lazy) {
   const KModel &m = S.A->m;
   WaveShared &sh = *S.sh;
   double dur;
   int nmem = 0;
   if (kind != IT_DECODE) {
-    const int qn = S.si_qn[si];
-    const int beff = S.si_beff[si];
-    const int room = kind == IT_PREFILL ? beff - S.si_rn[si] : beff;
+    const int qn = S.si.qn[si];
+    const int beff = S.si.beff[si];
+    const int room = kind == IT_PREFILL ? beff - S.si.rn[si] : beff;
     const int n = qn < room ? qn : room;
     uint32_t *dst = S.mem + (size_t)x * CF_MAX_BATCH;
     q_pop(S, si, n, dst);
     if (S.status & CF_ST_OVERFLOW) return;  // the triple is abandoned at the end of this instant
     uint32_t xs = 0;
+    const uint32_t sel = m.xsel[c];
     for (int b = 0; b < n; b += 64) {
       const int j = b + lane_id();
-      xs += (j < n) ? x_of(S, dst[j], c) : 0u;
+      xs += (j < n) ? x_of(S, dst[j], sel) : 0u;
     }
     xs = ru(wave_sum_u(xs));
     dur = (m.k0[c] + m.k1[c] * (double)xs) + m.k2[c] * (double)n;
-    if (m.kind[c] == CF_ENC) {
+    if (S.si.flags[si] & SF_ENC) {
       const bool ran = (sh.ex_st[x] >> 1) & 1u;
       if (!ran || sh.ex_last[x] < S.now) dur = dur + m.cpu_pre;
     }
     nmem = n;
-  } else if (!((m.gated_mask >> c) & 1u)) {
-    const int rn = S.si_rn[si];
+  } else if (!(S.si.flags[si] & SF_GATED)) {
+    const int rn = S.si.rn[si];
     dur = m.d0[c] + m.d1[c] * (double)rn;
     nmem = rn;
+    // Decode run: while no input reaches this executor, its next steps are
+    // decode steps of this stage with the same members, so the end of every
+    // step follows by repeated addition.  Run to the first finishing step or
+    // to the first step ending at or after the next pending input, whichever
+    // comes first; an input arriving earlier cuts the run (cut_run).
+    const uint32_t it0 = S.si.iter[si];
+    uint32_t itgt = it0 + 1u;
+    double tend = S.now + dur;
+    if (lazy && dur > 0.0) {
+      const uint32_t fin = S.si.minfin[si];
+      const double horizon = S.dl_head_t < S.t_arr ? S.dl_head_t : S.t_arr;
+      while (itgt < fin && tend < horizon && itgt - it0 < 65536u) {
+        tend = tend + dur;
+        itgt++;
+      }
+    }
+    sh.ex_t0[x] = S.now;
+    sh.ex_dur[x] = dur;
+    sh.ex_itgt[x] = itgt;
+    sh.ex_tend[x] = tend;
+    sh.ex_st[x] = (sh.ex_st[x] & 2u) | 1u | ((uint32_t)kind << 2) | ((uint32_t)l << 4) | ((uint32_t)l << 8) |
+                  ((uint32_t)nmem << 12) | (itgt > it0 + 1u ? EX_RUN : 0u);
+    return;
   } else {
     // gated stage: mark the eligible running requests
-    const int rn = S.si_rn[si];
-    uint32_t *rr = S.run_r + S.si_roff[si];
-    uint32_t *rk = S.run_k + S.si_roff[si];
+    const int rn = S.si.rn[si];
+    uint32_t *rr = S.run_r + S.si.roff[si];
+    uint32_t *rk = S.run_k + S.si.roff[si];
     uint32_t cntm = 0;
     bool undecided = false;
     for (int b = 0; b < rn; b += 64) {
       const int j = b + lane_id();
       if (j < rn) {
-        const uint32_t r = rr[j];
         const uint32_t tok = rk[j] & 0xFFFFu;
-        const int t = type_of(S, r);
-        bool el = true;
-        if (S.A->m.ta_c[t] == c) {
-          const int th = S.A->m.th_c[t];
-          const uint32_t nth = nout_of(S, r, t, th);
-          const uint32_t k = tok + 1u < nth ? tok + 1u : nth;
-          el = token_visible(S, r, t, th, exec_of(S, r, th), x, k, nth, undecided);
-        }
+        const bool el = slot_eligible(S, rr[j], tok, c, x, undecided);
         rk[j] = el ? (tok | MARK) : tok;
         cntm += el ? 1u : 0u;
       }
@@ -480,39 +691,27 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind) {
     dur = m.d0[c] + m.d1[c] * (double)cntm;
     nmem = (int)cntm;
   }
-  const double tend = S.now + dur;
-  sh.ex_tend[x] = tend;
+  sh.ex_tend[x] = S.now + dur;
+  sh.ex_itgt[x] = S.si.iter[si] + 1u;
   sh.ex_st[x] = (sh.ex_st[x] & 2u) | 1u | ((uint32_t)kind << 2) | ((uint32_t)l << 4) | ((uint32_t)l << 8) |
                 ((uint32_t)nmem << 12);
 }
 
-// does stage si (component c) of executor x have runnable work now?
 __device__ int runnable_kind(Sim &S, int x, int si, int c) {
-  const KModel &m = S.A->m;
-  const int qn = S.si_qn[si];
-  if (m.kind[c] != CF_LLM) return qn > 0 ? IT_BATCH : -1;
-  const int rn = S.si_rn[si];
-  if (qn > 0 && rn < (int)S.si_beff[si]) return IT_PREFILL;
+  const uint8_t fl = S.si.flags[si];
+  const int qn = S.si.qn[si];
+  if (!(fl & SF_LLM)) return qn > 0 ? IT_BATCH : -1;
+  const int rn = S.si.rn[si];
+  if (qn > 0 && rn < (int)S.si.beff[si]) return IT_PREFILL;
   if (rn == 0) return -1;
-  if (!((m.gated_mask >> c) & 1u)) return IT_DECODE;
-  const uint32_t *rr = S.run_r + S.si_roff[si];
-  const uint32_t *rk = S.run_k + S.si_roff[si];
+  if (!(fl & SF_GATED)) return IT_DECODE;
+  const uint32_t *rr = S.run_r + S.si.roff[si];
+  const uint32_t *rk = S.run_k + S.si.roff[si];
   bool any = false, undecided = false;
   for (int b = 0; b < rn && !any; b += 64) {
     const int j = b + lane_id();
     bool el = false;
-    if (j < rn) {
-      const uint32_t r = rr[j];
-      const int t = type_of(S, r);
-      el = true;
-      if (m.ta_c[t] == c) {
-        const int th = m.th_c[t];
-        const uint32_t nth = nout_of(S, r, t, th);
-        const uint32_t tok = rk[j] & 0xFFFFu;
-        const uint32_t k = tok + 1u < nth ? tok + 1u : nth;
-        el = token_visible(S, r, t, th, exec_of(S, r, th), x, k, nth, undecided);
-      }
-    }
+    if (j < rn) el = slot_eligible(S, rr[j], rk[j] & 0xFFFFu, c, x, undecided);
     any = __ballot(el) != 0;
   }
   if (__ballot(undecided)) S.status |= CF_ST_OVERFLOW;
@@ -527,25 +726,54 @@ __device__ void try_start(Sim &S, int x) {
   for (int i = 0; i < ns; i++) {
     const int l = (rr == 15) ? i : (rr + 1 + i) % ns;
     const int si = first + l;
-    const int c = S.si_comp[si];
-    const int kind = runnable_kind(S, x, si, c);
+    const int kind = runnable_kind(S, x, si, S.si.comp[si]);
     if (kind >= 0) {
-      start_iter(S, x, l, si, c, kind);
+      bool lazy = false;
+      const uint8_t fl = S.si.flags[si];
+      if (kind == IT_DECODE && !(fl & (SF_THINKER | SF_GATED)) &&
+          (S.si.qn[si] == 0 || S.si.rn[si] >= (int)S.si.beff[si])) {
+        lazy = true;  // ... unless a stage checked after this one has work
+        for (int i2 = i + 1; i2 < ns && lazy; i2++) {
+          const int l2 = (rr == 15) ? i2 : (rr + 1 + i2) % ns;
+          if (runnable_kind(S, x, first + l2, S.si.comp[first + l2]) >= 0) lazy = false;
+        }
+      }
+      start_iter(S, x, l, si, S.si.comp[si], kind, lazy);
       return;
     }
   }
 }
 
-__device__ void thinker_tick(Sim &S) {
-  if (S.remote_gate) dl_push(S, S.now + S.A->m.comm, (DL_TICK << 3));
+// An input reached executor x, busy in a decode run: the run stops at the
+// first step that ends at or after now (the steps before it are unchanged).
+__device__ void cut_run(Sim &S, int x) {
+  WaveShared &sh = *S.sh;
+  const uint32_t st = sh.ex_st[x];
+  if (!(st & EX_RUN) || !(sh.ex_tend[x] > S.now)) return;
+  const int si = sh.ex_first[x] + ((st >> 8) & 15u);
+  const uint32_t it0 = S.si.iter[si];
+  const uint32_t itgt = sh.ex_itgt[x];
+  const double dur = sh.ex_dur[x];
+  double t = sh.ex_t0[x] + dur;
+  uint32_t j = it0 + 1u;
+  while (t < S.now && j < itgt) {
+    t = t + dur;
+    j++;
+  }
+  sh.ex_tend[x] = t;
+  sh.ex_itgt[x] = j;
+  if (j <= it0 + 1u) sh.ex_st[x] = st & ~EX_RUN;
 }
 
-// compact the running slots of stage si, dropping slots whose key equals drop
-// (compressed) or whose token count reached n_out (gated, fin flags).
-__device__ void run_compact(Sim &S, int si, bool gated, uint32_t drop_key, const bool *fin_lane) {
-  const int rn = S.si_rn[si];
-  uint32_t *rr = S.run_r + S.si_roff[si];
-  uint32_t *rk = S.run_k + S.si_roff[si];
+__device__ __forceinline__ void thinker_tick(Sim &S) {
+  if (S.remote_gate) dl_push1(S, S.now + S.A->m.comm, (DL_TICK << 3));
+}
+
+// compacts stage si's running slots, dropping the lanes flagged in drop[]
+__device__ void run_compact(Sim &S, int si, const bool *drop) {
+  const int rn = S.si.rn[si];
+  uint32_t *rr = S.run_r + S.si.roff[si];
+  uint32_t *rk = S.run_k + S.si.roff[si];
   uint32_t vr[CF_MAX_BATCH / 64], vk[CF_MAX_BATCH / 64];
   bool keep[CF_MAX_BATCH / 64];
 #pragma unroll
@@ -557,7 +785,7 @@ __device__ void run_compact(Sim &S, int si, bool gated, uint32_t drop_key, const
     if (j < rn) {
       vr[p] = rr[j];
       vk[p] = rk[j];
-      keep[p] = gated ? !fin_lane[p] : (vk[p] != drop_key);
+      keep[p] = !drop[p];
     }
   }
   __syncthreads();
@@ -574,92 +802,66 @@ __device__ void run_compact(Sim &S, int si, bool gated, uint32_t drop_key, const
     w += (uint32_t)__popcll(bal);
   }
   __syncthreads();
-  S.si_rn[si] = (int)ru(w);
-  if (!gated) S.si_minfin[si] = ru(wave_min_u(mn));
+  S.si.rn[si] = (int)w;
+  if (!(S.si.flags[si] & SF_GATED)) S.si.minfin[si] = ru(wave_min_u(mn));
+}
+
+// collects the running slots flagged in fin[] (slot order) into mem,
+// processes them as finishing members, and drops them from the running set
+__device__ void finish_slots(Sim &S, int x, int si, int c, const bool *fin) {
+  const int rn = S.si.rn[si];
+  const uint32_t *rr = S.run_r + S.si.roff[si];
+  uint32_t *mem = S.mem + (size_t)x * CF_MAX_BATCH;
+  uint32_t nf = 0;
+#pragma unroll
+  for (int p = 0; p < CF_MAX_BATCH / 64; p++) {
+    const int j = p * 64 + lane_id();
+    const bool f = j < rn && fin[p];
+    const uint64_t bal = __ballot(f);
+    if (f) mem[nf + lanes_below(bal)] = rr[j];
+    nf += (uint32_t)__popcll(bal);
+  }
+  __syncthreads();
+  members_done(S, x, si, c, IT_FINISH, (int)nf, mem);
+  run_compact(S, si, fin);
 }
 
 __device__ void complete_iter(Sim &S, int x) {
-  const KModel &m = S.A->m;
   WaveShared &sh = *S.sh;
   const uint32_t st = sh.ex_st[x];
   const int kind = (st >> 2) & 3u, l = (st >> 8) & 15u, nmem = (st >> 12) & 511u;
   const int si = sh.ex_first[x] + l;
-  const int c = S.si_comp[si];
-  sh.ex_st[x] = (st & ~1u) | 2u;  // idle, has run
+  const int c = S.si.comp[si];
+  const uint8_t fl = S.si.flags[si];
+  sh.ex_st[x] = (st & ~(1u | EX_RUN)) | 2u;  // idle, has run
   sh.ex_last[x] = S.now;
   S.dirty |= 1ull << x;
-  const bool is_th = (m.gate_src_mask >> c) & 1u;
-  if (kind == IT_BATCH) {
-    const uint32_t *mem = S.mem + (size_t)x * CF_MAX_BATCH;
-    for (int i = 0; i < nmem; i++) {
-      const uint32_t r = ru(mem[i]);
-      S.events++;
-      finish(S, r, c, x);
+  if (kind == IT_BATCH || kind == IT_PREFILL) {
+    S.events += (uint64_t)nmem;
+    members_done(S, x, si, c, kind, nmem, S.mem + (size_t)x * CF_MAX_BATCH);
+    if (fl & SF_THINKER) thinker_tick(S);
+    return;
+  }
+  const int rn = S.si.rn[si];
+  const uint32_t it0 = S.si.iter[si];
+  const uint32_t it = (fl & SF_GATED) ? it0 + 1u : sh.ex_itgt[x];
+  S.si.iter[si] = it;
+  if ((fl & SF_THINKER) && lane_id() == 0) S.hist[(size_t)S.si.hist[si] * kHist + (it & (kHist - 1))] = S.now;
+  const uint32_t *rr = S.run_r + S.si.roff[si];
+  uint32_t *rk = S.run_k + S.si.roff[si];
+  if (!(fl & SF_GATED)) {
+    S.events += (uint64_t)rn * (uint64_t)(it - it0);
+    if (it == S.si.minfin[si]) {
+      bool fin[CF_MAX_BATCH / 64];
+#pragma unroll
+      for (int p = 0; p < CF_MAX_BATCH / 64; p++) {
+        const int j = p * 64 + lane_id();
+        fin[p] = j < rn && rk[j] == it;
+      }
+      finish_slots(S, x, si, c, fin);
     }
-  } else if (kind == IT_PREFILL) {
-    const uint32_t *mem = S.mem + (size_t)x * CF_MAX_BATCH;
-    const bool gated = (m.gated_mask >> c) & 1u;
-    const uint32_t iter = S.si_iter[si];
-    int rn = S.si_rn[si];
-    uint32_t mn = S.si_minfin[si];
-    uint32_t *rr = S.run_r + S.si_roff[si];
-    uint32_t *rk = S.run_k + S.si_roff[si];
-    for (int i = 0; i < nmem; i++) {
-      const uint32_t r = ru(mem[i]);
-      const int t = type_of(S, r);
-      S.events++;
-      if (c == m.ttft_c[t]) {
-        S.rs_tfirst[r] = S.now;
-        S.rs_tlast[r] = S.now;
-      }
-      const uint32_t no = nout_of(S, r, t, c);
-      if (c == m.th_c[t]) {
-        S.rs_thjoin[r] = iter;
-        deliver(S, r, m.ta_c[t], x);  // token 1: the talker receives the request
-      }
-      if (no == 1) {
-        finish(S, r, c, x);
-      } else {
-        const uint32_t key = gated ? 1u : iter + no - 1u;
-        rr[rn] = r;
-        rk[rn] = key;
-        rn++;
-        if (!gated && key < mn) mn = key;
-      }
-    }
-    S.si_rn[si] = rn;
-    if (!gated) S.si_minfin[si] = mn;
-    if (is_th) thinker_tick(S);
-  } else if (!((m.gated_mask >> c) & 1u)) {
-    const uint32_t it = S.si_iter[si] + 1u;
-    S.si_iter[si] = it;
-    const int rn = S.si_rn[si];
-    S.events += (uint64_t)rn;
-    if (is_th) S.hist[(size_t)S.si_hist[si] * kHist + (it & (kHist - 1))] = S.now;
-    if (it == S.si_minfin[si]) {
-      const uint32_t *rr = S.run_r + S.si_roff[si];
-      const uint32_t *rk = S.run_k + S.si_roff[si];
-      for (int b = 0; b < rn; b += 64) {
-        const int j = b + lane_id();
-        uint64_t bal = __ballot(j < rn && rk[j] == it);
-        while (bal) {
-          const int jj = b + __ffsll((long long)bal) - 1;
-          bal &= bal - 1;
-          const uint32_t r = ru(rr[jj]);
-          const int t = type_of(S, r);
-          if (c == m.ttft_c[t]) S.rs_tlast[r] = S.now;
-          finish(S, r, c, x);
-        }
-      }
-      run_compact(S, si, false, it, nullptr);
-    }
-    if (is_th) thinker_tick(S);
   } else {
     // gated decode step: every marked slot gains one token
-    const int rn = S.si_rn[si];
-    uint32_t *rr = S.run_r + S.si_roff[si];
-    uint32_t *rk = S.run_k + S.si_roff[si];
-    S.si_iter[si] = S.si_iter[si] + 1u;
     bool fin[CF_MAX_BATCH / 64];
     uint32_t part = 0;
 #pragma unroll
@@ -673,27 +875,18 @@ __device__ void complete_iter(Sim &S, int x) {
           const uint32_t tok = (v & 0xFFFFu) + 1u;
           rk[j] = tok;
           part++;
-          fin[p] = tok == nout_of(S, r, type_of(S, r), c);
+          fin[p] = tok == nout_of(S, r, rtype(S.rec[r].misc), c);
         }
       }
     }
     S.events += (uint64_t)ru(wave_sum_u(part));
     __syncthreads();
+    bool anyf = false;
 #pragma unroll
-    for (int p = 0; p < CF_MAX_BATCH / 64; p++) {
-      uint64_t bal = __ballot(fin[p]);
-      while (bal) {
-        const int jj = p * 64 + __ffsll((long long)bal) - 1;
-        bal &= bal - 1;
-        const uint32_t r = ru(rr[jj]);
-        const int t = type_of(S, r);
-        if (c == m.ttft_c[t]) S.rs_tlast[r] = S.now;
-        finish(S, r, c, x);
-      }
-    }
-    run_compact(S, si, true, 0, fin);
-    if (is_th) thinker_tick(S);
+    for (int p = 0; p < CF_MAX_BATCH / 64; p++) anyf |= __ballot(fin[p]) != 0;
+    if (anyf) finish_slots(S, x, si, c, fin);
   }
+  if (fl & SF_THINKER) thinker_tick(S);
 }
 
 // ------------------------------------------------------------------ setup
@@ -703,7 +896,7 @@ __device__ bool setup_plan(Sim &S, int p) {
   WaveShared &sh = *S.sh;
   const size_t P = (size_t)A.P;
   const int lane = lane_id();
-  const int nv = A.n_nodes[p];
+  const int nv = ri(A.n_nodes[p]);
   if (nv < 1 || nv > CF_MAX_NODES) return false;
   if (lane < CF_MAX_NODES) {
     sh.vcomp[lane] = lane < nv ? A.node_comp[lane * P + p] : 0;
@@ -714,13 +907,14 @@ __device__ bool setup_plan(Sim &S, int p) {
   if (lane < CF_MAX_TYPES) sh.nalt[lane] = lane < m.nt ? A.n_alt[lane * P + p] : 0;
   if (lane < 2 * CF_MAX_TYPES) (&sh.aw[0][0])[lane] = A.alt_w[lane * P + p];
   __syncthreads();
-  int base = 0;
+  int base = 0, nsi = 0;
   for (int v = 0; v < nv; v++) {
     const int cm = sh.vcomp[v], rep = sh.vrep[v], b = sh.vbatch[v];
     if (cm == 0 || (cm >> m.nc) || rep < 1 || b < 1 || b > CF_MAX_BATCH) return false;
     sh.vminc[v] = (uint8_t)(__ffs(cm) - 1);
     sh.vbase[v] = (uint8_t)(base < 255 ? base : 255);
     base += rep;
+    nsi += rep * __popc(cm);
   }
   if (base > CF_MAX_EXEC) return false;
   S.nx = base;
@@ -740,73 +934,144 @@ __device__ bool setup_plan(Sim &S, int p) {
       if (m.th_c[t] >= 0 && sh.route[t][a][m.th_c[t]] != sh.route[t][a][m.ta_c[t]]) S.remote_gate = true;
     }
   }
-  // executors and stage instances
-  int si = 0, roff = 0, hs = 0;
-  S.ta_exec_mask = 0;
-  for (int v = 0; v < nv; v++) {
-    const int cm = sh.vcomp[v];
-    for (int j = 0; j < sh.vrep[v]; j++) {
-      const int x = sh.vbase[v] + j;
-      sh.ex_node[x] = (uint8_t)v;
-      sh.ex_first[x] = (uint16_t)si;
-      sh.ex_ns[x] = (uint8_t)__popc(cm);
-      sh.ex_st[x] = 15u << 4;  // idle, never ran, no stage run yet
-      sh.ex_tend[x] = __builtin_inf();
-      sh.ex_last[x] = 0.0;
-      if (cm & m.gated_mask) S.ta_exec_mask |= 1ull << x;
-      uint32_t cc = (uint32_t)cm;
-      while (cc) {
-        const int c = __ffs(cc) - 1;
-        cc &= cc - 1;
-        if (si >= kMaxSI) return false;
-        const int beff = sh.vbatch[v] < m.cap[c] ? sh.vbatch[v] : m.cap[c];
-        S.si_comp[si] = (uint8_t)c;
-        S.si_exec[si] = (uint8_t)x;
-        S.si_beff[si] = (uint16_t)beff;
-        S.si_qn[si] = 0;
-        S.si_qhc[si] = -1;
-        S.si_qtc[si] = -1;
-        S.si_qhp[si] = 0;
-        S.si_qtp[si] = 0;
-        S.si_rn[si] = 0;
-        S.si_iter[si] = 0;
-        S.si_minfin[si] = kNone;
-        S.si_roff[si] = roff;
-        S.si_hist[si] = -1;
-        if (m.kind[c] == CF_LLM) roff += beff;
-        if ((m.gate_src_mask >> c) & 1u) S.si_hist[si] = hs++;
-        si++;
-      }
-    }
-  }
-  if (roff > A.L.run_cap || hs > A.L.hist_slots) {
+  if (nsi > A.nsi_cap) {
     S.status |= CF_ST_OVERFLOW;
     return true;
   }
+  // capacities of the running slots and thinker rings
+  int run_need = 0, ring_need = 0;
+  uint64_t ta_mask = 0;
+  for (int v = 0; v < nv; v++) {
+    const uint32_t cm = sh.vcomp[v];
+    if (cm & m.gated_mask)
+      for (int j = 0; j < sh.vrep[v]; j++) ta_mask |= 1ull << (sh.vbase[v] + j);
+    for (uint32_t cc = cm; cc;) {
+      const int c = __ffs(cc) - 1;
+      cc &= cc - 1;
+      if (m.kind[c] == CF_LLM) run_need += sh.vrep[v] * (sh.vbatch[v] < m.cap[c] ? sh.vbatch[v] : m.cap[c]);
+      if ((m.gate_src_mask >> c) & 1u) ring_need += sh.vrep[v];
+    }
+  }
+  S.ta_exec_mask = ta_mask;
+  if (run_need > A.L.run_cap || ring_need > A.L.hist_slots) {
+    S.status |= CF_ST_OVERFLOW;
+    return true;
+  }
+  // executors, one lane each
+  if (lane < S.nx) {
+    int v = 0;
+    while (v + 1 < nv && sh.vbase[v + 1] <= lane) v++;
+    int first = 0;
+    for (int u = 0; u < v; u++) first += sh.vrep[u] * __popc(sh.vcomp[u]);
+    first += (lane - sh.vbase[v]) * __popc(sh.vcomp[v]);
+    sh.ex_node[lane] = (uint8_t)v;
+    sh.ex_first[lane] = (uint16_t)first;
+    sh.ex_ns[lane] = (uint8_t)__popc(sh.vcomp[v]);
+    sh.ex_st[lane] = 15u << 4;  // idle, never ran, no stage run yet
+    sh.ex_tend[lane] = __builtin_inf();
+    sh.ex_last[lane] = 0.0;
+    sh.ex_t0[lane] = 0.0;
+    sh.ex_dur[lane] = 0.0;
+    sh.ex_itgt[lane] = 0;
+  }
+  // stage instances, one lane each (prefix sums give run-slot and ring offsets)
+  int roff_carry = 0, hs_carry = 0;
+  for (int s0 = 0; s0 < nsi; s0 += 64) {
+    const int s = s0 + lane;
+    int c = 0, beff = 0;
+    bool llm = false, thk = false;
+    if (s < nsi) {
+      int v = 0, acc = 0;
+      while (acc + sh.vrep[v] * __popc(sh.vcomp[v]) <= s) {
+        acc += sh.vrep[v] * __popc(sh.vcomp[v]);
+        v++;
+      }
+      const int per = __popc(sh.vcomp[v]);
+      const int k = (s - acc) % per;
+      uint32_t cc = sh.vcomp[v];
+      for (int q = 0; q < k; q++) cc &= cc - 1;
+      c = __ffs(cc) - 1;
+      beff = sh.vbatch[v] < m.cap[c] ? sh.vbatch[v] : m.cap[c];
+      llm = m.kind[c] == CF_LLM;
+      thk = (m.gate_src_mask >> c) & 1u;
+    }
+    uint32_t tot_r, tot_h;
+    const uint32_t ro = wave_excl_scan(llm ? (uint32_t)beff : 0u, tot_r);
+    const uint32_t ho = wave_excl_scan(thk ? 1u : 0u, tot_h);
+    if (s < nsi) {
+      S.si.comp[s] = (uint8_t)c;
+      S.si.flags[s] = (uint8_t)((llm ? SF_LLM : 0) | (((m.gated_mask >> c) & 1u) ? SF_GATED : 0) |
+                                (thk ? SF_THINKER : 0) | (m.kind[c] == CF_ENC ? SF_ENC : 0) |
+                                (m.kind[c] == CF_GEN ? SF_GEN : 0));
+      S.si.beff[s] = (uint16_t)beff;
+      S.si.qn[s] = 0;
+      S.si.qhc[s] = -1;
+      S.si.qtc[s] = -1;
+      S.si.qhp[s] = 0;
+      S.si.qtp[s] = 0;
+      S.si.rn[s] = 0;
+      S.si.iter[s] = 0;
+      S.si.minfin[s] = kNone;
+      S.si.roff[s] = roff_carry + (int)ro;
+      S.si.hist[s] = thk ? (int16_t)(hs_carry + (int)ho) : (int16_t)-1;
+    }
+    roff_carry += (int)tot_r;
+    hs_carry += (int)tot_h;
+  }
+  __syncthreads();
   return true;
 }
+
+extern __shared__ char dyn_lds[];
 
 __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
   __shared__ WaveShared sh;
   const FineArgs &A = *Ap;
+  const KModel &m = A.m;
+  const int lane = lane_id();
   Sim S;
   S.A = Ap;
   S.sh = &sh;
+  {
+    const int cap = A.nsi_cap;
+    char *p = dyn_lds;
+    S.si.qhc = (int *)p; p += 4 * cap;
+    S.si.qtc = (int *)p; p += 4 * cap;
+    S.si.qn = (int *)p; p += 4 * cap;
+    S.si.roff = (int *)p; p += 4 * cap;
+    S.si.rn = (int *)p; p += 4 * cap;
+    S.si.iter = (uint32_t *)p; p += 4 * cap;
+    S.si.minfin = (uint32_t *)p; p += 4 * cap;
+    S.si.beff = (uint16_t *)p; p += 2 * cap;
+    S.si.hist = (int16_t *)p; p += 2 * cap;
+    S.si.comp = (uint8_t *)p; p += cap;
+    S.si.flags = (uint8_t *)p; p += cap;
+    S.si.qhp = (uint8_t *)p; p += cap;
+    S.si.qtp = (uint8_t *)p; p += cap;
+  }
+  // model tables for per-lane indexing
+  for (int j = lane; j < CF_MAX_TYPES * CF_MAX_COMP; j += 64) {
+    (&sh.ml.child[0][0])[j] = (&m.child[0][0])[j];
+    (&sh.ml.npar[0][0])[j] = (&m.npar[0][0])[j];
+  }
+  if (lane < CF_MAX_TYPES) {
+    sh.ml.ttft_c[lane] = m.ttft_c[lane];
+    sh.ml.th_c[lane] = m.th_c[lane];
+    sh.ml.ta_c[lane] = m.ta_c[lane];
+    sh.ml.outm[lane] = (uint8_t)m.outm[lane];
+    sh.ml.pfo[lane] = (uint8_t)m.pfo[lane];
+    sh.ml.gen_out[lane] = m.gen_out[lane];
+    sh.ml.kind[lane] = (uint8_t)m.kind[lane];
+    sh.ml.nout_attr[lane] = (uint8_t)m.nout_attr[lane];
+  }
+  if (lane < CF_MAX_TYPES * 4) (&sh.ml.slo[0][0])[lane] = (&m.slo[0][0])[lane];
   char *slab = A.slab + (size_t)blockIdx.x * A.L.bytes;
   const Layout &L = A.L;
-  S.si_comp = (uint8_t *)(slab + L.si_comp);
-  S.si_exec = (uint8_t *)(slab + L.si_exec);
-  S.si_beff = (uint16_t *)(slab + L.si_beff);
-  S.si_qhc = (int *)(slab + L.si_qhc);
-  S.si_qhp = (int *)(slab + L.si_qhp);
-  S.si_qtc = (int *)(slab + L.si_qtc);
-  S.si_qtp = (int *)(slab + L.si_qtp);
-  S.si_qn = (int *)(slab + L.si_qn);
-  S.si_roff = (int *)(slab + L.si_roff);
-  S.si_rn = (int *)(slab + L.si_rn);
-  S.si_iter = (uint32_t *)(slab + L.si_iter);
-  S.si_minfin = (uint32_t *)(slab + L.si_minfin);
-  S.si_hist = (int *)(slab + L.si_hist);
+  S.rec = (Rec *)(slab + L.rec);
+  S.tfirst = (double *)(slab + L.tfirst);
+  S.tlast = (double *)(slab + L.tlast);
+  S.tmedia = (double *)(slab + L.tmedia);
+  S.thjoin = (uint32_t *)(slab + L.thjoin);
   S.run_r = (uint32_t *)(slab + L.run_r);
   S.run_k = (uint32_t *)(slab + L.run_k);
   S.hist = (double *)(slab + L.hist);
@@ -816,15 +1081,7 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
   S.pool = (uint32_t *)(slab + L.pool);
   S.pool_next = (int *)(slab + L.pool_next);
   S.pool_free = (int *)(slab + L.pool_free);
-  S.rs_ex = (uint64_t *)(slab + L.rs_ex);
-  S.rs_join = (uint32_t *)(slab + L.rs_join);
-  S.rs_flags = (uint32_t *)(slab + L.rs_flags);
-  S.rs_tfirst = (double *)(slab + L.rs_tfirst);
-  S.rs_tlast = (double *)(slab + L.rs_tlast);
-  S.rs_tmedia = (double *)(slab + L.rs_tmedia);
-  S.rs_thjoin = (uint32_t *)(slab + L.rs_thjoin);
-  const int lane = lane_id();
-  const KModel &m = A.m;
+  __syncthreads();
   const unsigned int per_seed = (unsigned int)A.n_plans * (unsigned int)A.K;
   for (;;) {
     unsigned int tk = 0;
@@ -837,11 +1094,12 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
     const int p = ri(A.plan_ids[i]);
     const size_t oidx = ((size_t)i * A.K + k) * A.S + s;
     S.soff = (size_t)s * A.n;
-    S.lam = rd(A.rates[(size_t)i * A.K + k]);
+    S.lam = rdb(A.rates[(size_t)i * A.K + k]);
     S.events = 0;
     S.status = 0;
     S.dirty = 0;
     S.dl_head = S.dl_tail = 0;
+    S.dl_head_t = __builtin_inf();
     S.pool_top = 0;
     S.pool_fresh = 0;
     S.n_done = 0;
@@ -849,44 +1107,51 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
     S.lat_slot = -1;
     for (int j = 0; j < A.n_lat; j++)
       if (A.lat_triples[j] == (int32_t)oidx) S.lat_slot = j;
-    if (lane < CF_MAX_TYPES) { sh.met[lane] = 0; sh.cnt[lane] = 0; }
+    if (lane < CF_MAX_TYPES) {
+      sh.met[lane] = 0;
+      sh.cnt[lane] = 0;
+    }
     __syncthreads();
     const bool ok = (p >= 0 && p < A.P) && S.lam > 0.0 && S.lam < __builtin_inf() && setup_plan(S, p);
     if (!ok) S.status |= CF_ST_INVALID;
-    if (ok && !(S.status & CF_ST_OVERFLOW) && A.n > 0 && S.lam > 0.0) {
+    if (ok && !(S.status & CF_ST_OVERFLOW) && A.n > 0) {
       uint32_t next_arr = 0;
-      double t_arr = arrival_time(S, 0);
+      S.t_arr = rdb(arrival_time(S, 0));
       uint64_t instants = 0;
       for (;;) {
         // --- next pending time
         double te = __builtin_inf();
         if (lane < S.nx && (sh.ex_st[lane] & 1u)) te = sh.ex_tend[lane];
-        te = rd(wave_min(te));
-        const double tdl = (S.dl_head != S.dl_tail) ? S.dl_t[S.dl_head & L.dl_mask] : __builtin_inf();
-        double t = te < tdl ? te : tdl;
-        t = t_arr < t ? t_arr : t;
+        te = rdb(wave_min(te));
+        double t = te < S.dl_head_t ? te : S.dl_head_t;
+        t = S.t_arr < t ? S.t_arr : t;
         if (t == __builtin_inf()) break;
         S.now = t;
-        if (++instants > 2 * S.events + 16ull * (uint64_t)A.n + 4096ull) { S.status |= CF_ST_DEADLOCK; break; }
+        if (++instants > 2 * S.events + 16ull * (uint64_t)A.n + 4096ull) {
+          S.status |= CF_ST_DEADLOCK;
+          break;
+        }
         // --- step 1: iterations ending at t, ascending executor
-        uint64_t done = __ballot(lane < S.nx && (sh.ex_st[lane] & 1u) && sh.ex_tend[lane] == t);
-        __syncthreads();
-        while (done) {
-          const int x = __ffsll((long long)done) - 1;
-          done &= done - 1;
-          complete_iter(S, x);
+        if (te == t) {
+          uint64_t done = __ballot(lane < S.nx && (sh.ex_st[lane] & 1u) && sh.ex_tend[lane] == t);
+          while (done) {
+            const int x = __ffsll((long long)done) - 1;
+            done &= done - 1;
+            complete_iter(S, x);
+          }
         }
         // --- step 2: delayed deliveries due at t (production order), then arrivals at t
-        while (S.dl_head != S.dl_tail && S.dl_t[S.dl_head & L.dl_mask] == t) {
-          const uint32_t v = S.dl_v[S.dl_head & L.dl_mask];
+        while (S.dl_head != S.dl_tail && S.dl_head_t == t) {
+          const uint32_t v = ru(S.dl_v[S.dl_head & L.dl_mask]);
           S.dl_head++;
+          S.dl_head_t = S.dl_head != S.dl_tail ? rdb(S.dl_t[S.dl_head & L.dl_mask]) : __builtin_inf();
           if (((v >> 3) & 1u) == DL_TICK) S.dirty |= S.ta_exec_mask;
-          else join(S, v >> 4, (int)(v & 7u));
+          else dl_deliver(S, v >> 4, (int)(v & 7u));
         }
-        while (next_arr < (uint32_t)A.n && t_arr == t) {
+        while (next_arr < (uint32_t)A.n && S.t_arr == t) {
           arrive(S, next_arr);
           next_arr++;
-          t_arr = next_arr < (uint32_t)A.n ? arrival_time(S, next_arr) : __builtin_inf();
+          S.t_arr = next_arr < (uint32_t)A.n ? rdb(arrival_time(S, next_arr)) : __builtin_inf();
         }
         // --- step 3: idle executors whose state changed may start an iteration
         uint64_t cand = S.dirty;
@@ -896,8 +1161,8 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
           const int x = __ffsll((long long)cand) - 1;
           cand &= cand - 1;
           if (!(sh.ex_st[x] & 1u)) try_start(S, x);
+          else cut_run(S, x);
         }
-        __syncthreads();
         if (S.status & (CF_ST_OVERFLOW | CF_ST_INVALID)) break;
       }
       if (S.n_done < A.n && !(S.status & (CF_ST_OVERFLOW | CF_ST_INVALID))) S.status |= CF_ST_DEADLOCK;
@@ -916,6 +1181,21 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
 
 __global__ void k_fine_reset(unsigned int *ticket) { *ticket = 0u; }
 
+// stage instances of the largest selected plan (malformed plans are skipped)
+__global__ void k_max_si(const uint8_t *n_nodes, const uint8_t *node_comp, const uint8_t *node_rep, int P,
+                         const int32_t *ids, int n, unsigned int *out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int p = ids[i];
+  if (p < 0 || p >= P) return;
+  const int nv = n_nodes[p];
+  if (nv < 1 || nv > CF_MAX_NODES) return;
+  unsigned int nsi = 0;
+  for (int v = 0; v < nv; v++)
+    nsi += (unsigned int)node_rep[(size_t)v * P + p] * (unsigned int)__popc(node_comp[(size_t)v * P + p]);
+  atomicMax(out, nsi < (unsigned)kMaxSI ? nsi : (unsigned)kMaxSI);
+}
+
 Layout make_layout(const KModel &m, int n) {
   Layout L{};
   size_t off = 0;
@@ -924,19 +1204,6 @@ Layout make_layout(const KModel &m, int n) {
     off += (bytes + 255) & ~(size_t)255;
     return o;
   };
-  L.si_comp = take(kMaxSI);
-  L.si_exec = take(kMaxSI);
-  L.si_beff = take(2 * kMaxSI);
-  L.si_qhc = take(4 * kMaxSI);
-  L.si_qhp = take(4 * kMaxSI);
-  L.si_qtc = take(4 * kMaxSI);
-  L.si_qtp = take(4 * kMaxSI);
-  L.si_qn = take(4 * kMaxSI);
-  L.si_roff = take(4 * kMaxSI);
-  L.si_rn = take(4 * kMaxSI);
-  L.si_iter = take(4 * kMaxSI);
-  L.si_minfin = take(4 * kMaxSI);
-  L.si_hist = take(4 * kMaxSI);
   int per_exec_run = 0, n_th = 0;
   for (int c = 0; c < m.nc; c++) {
     if (m.kind[c] == CF_LLM) per_exec_run += m.cap[c] < CF_MAX_BATCH ? m.cap[c] : CF_MAX_BATCH;
@@ -944,9 +1211,14 @@ Layout make_layout(const KModel &m, int n) {
   }
   L.run_cap = CF_MAX_EXEC * per_exec_run;
   L.hist_slots = CF_MAX_EXEC * n_th;
+  L.rec = take(sizeof(Rec) * (size_t)n);
+  L.tfirst = take(8 * (size_t)n);
+  L.tlast = take(8 * (size_t)n);
+  L.tmedia = take(8 * (size_t)n);
+  L.thjoin = take(4 * (size_t)n);
   L.run_r = take(4 * (size_t)L.run_cap);
   L.run_k = take(4 * (size_t)L.run_cap);
-  L.hist = take(8 * (size_t)L.hist_slots * kHist);
+  L.hist = take(8 * (size_t)L.hist_slots * kHist + 8);
   L.mem = take(4 * (size_t)CF_MAX_EXEC * CF_MAX_BATCH);
   size_t dl = 4096;
   while (dl < 2 * (size_t)n + 8192) dl <<= 1;
@@ -958,13 +1230,6 @@ Layout make_layout(const KModel &m, int n) {
   L.pool = take(4 * (size_t)L.n_chunks * kChunk);
   L.pool_next = take(4 * (size_t)L.n_chunks);
   L.pool_free = take(4 * (size_t)L.n_chunks);
-  L.rs_ex = take(8 * (size_t)n);
-  L.rs_join = take(4 * (size_t)n);
-  L.rs_flags = take(4 * (size_t)n);
-  L.rs_tfirst = take(8 * (size_t)n);
-  L.rs_tlast = take(8 * (size_t)n);
-  L.rs_tmedia = take(8 * (size_t)n);
-  L.rs_thjoin = take(4 * (size_t)n);
   L.bytes = (off + 4095) & ~(size_t)4095;
   return L;
 }
@@ -993,7 +1258,6 @@ extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_tabl
   if (trace->n_req > (1 << 26)) return set_error(CF_ECAPACITY, "n_req above 2^26");
   const unsigned long long total = (unsigned long long)n_plans * K * trace->n_seeds;
   if (total >= 0xFFFFFFFFull - 65536ull) return set_error(CF_ECAPACITY, "too many triples in one call");
-  if (total == 0) return CF_OK;
   a.P = plans->P;
   a.n_nodes = plans->n_nodes_dev;
   a.node_comp = plans->node_comp_dev;
@@ -1027,31 +1291,42 @@ extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_tabl
   a.n_lat = out->lat_dev ? out->n_lat : 0;
   a.L = make_layout(a.m, trace->n_req);
   a.total = (unsigned int)total;
-  long long waves = 4096;
+  long long waves = 8192;
   if (const char *e = getenv("CF_FINE_WAVES")) waves = atoll(e);
   if (waves < 1) waves = 1;
   if ((unsigned long long)waves > total) waves = (long long)total;
-  // keep the per-wave state within a fixed share of device memory
   size_t free_b = 0, tot_b = 0;
   if (hipMemGetInfo(&free_b, &tot_b) == hipSuccess && free_b > 0) {
     const size_t budget = free_b / 2;
     while (waves > 64 && (size_t)waves * a.L.bytes > budget) waves /= 2;
   }
-  const size_t hdr = 4096;
+  const size_t hdr = 8192;
+  static_assert(sizeof(FineArgs) + 512 <= 8192, "FineArgs must fit the scratch header");
   char *scr = (char *)scratch_get(SCR_FINE, hdr + (size_t)waves * a.L.bytes, &st);
   if (!scr) return st;
   a.ticket = (unsigned int *)scr;
-  FineArgs *args_dev = (FineArgs *)(scr + 256);
-  static_assert(sizeof(FineArgs) + 256 <= 4096, "FineArgs must fit the scratch header");
+  unsigned int *max_si = (unsigned int *)(scr + 64);
+  FineArgs *args_dev = (FineArgs *)(scr + 512);
   a.slab = scr + hdr;
   hipStream_t s = as_stream(stream);
+  // size the LDS stage table from the largest selected plan
+  hipLaunchKernelGGL(k_fine_reset, dim3(1), dim3(1), 0, s, max_si);
+  hipLaunchKernelGGL(k_max_si, dim3((unsigned)((n_plans + 255) / 256)), dim3(256), 0, s, a.n_nodes, a.node_comp,
+                     a.node_rep, a.P, plan_ids_dev, n_plans, max_si);
+  unsigned int nsi = 0;
+  st = hip_check(hipMemcpyAsync(&nsi, max_si, sizeof nsi, hipMemcpyDeviceToHost, s), "copy stage count");
+  if (st != CF_OK) return st;
+  st = hip_check(hipStreamSynchronize(s), "stage count sync");
+  if (st != CF_OK) return st;
+  a.nsi_cap = (int)((nsi + 63u) & ~63u);
+  if (a.nsi_cap < 64) a.nsi_cap = 64;
+  const size_t lds = kSiBytes * (size_t)a.nsi_cap;
   st = hip_check(hipMemcpyAsync(args_dev, &a, sizeof a, hipMemcpyHostToDevice, s), "copy fine args");
   if (st != CF_OK) return st;
   hipLaunchKernelGGL(k_fine_reset, dim3(1), dim3(1), 0, s, a.ticket);
-  hipLaunchKernelGGL(k_fine, dim3((unsigned)waves), dim3(64), 0, s, (const FineArgs *)args_dev);
+  hipLaunchKernelGGL(k_fine, dim3((unsigned)waves), dim3(64), lds, s, (const FineArgs *)args_dev);
   st = hip_check(hipGetLastError(), "cf_eval_fine launch");
   if (st != CF_OK) return st;
-  // the argument block is read by the kernel: the host copy must stay valid
-  // until the copy has happened
+  // the argument block is copied from host memory on the stream: wait for it
   return hip_check(hipStreamSynchronize(s), "cf_eval_fine sync");
 }
