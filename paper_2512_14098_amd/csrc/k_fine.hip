@@ -166,6 +166,28 @@ __device__ __forceinline__ uint32_t wave_or_u(uint32_t v) {
 __device__ __forceinline__ uint32_t lanes_below(uint64_t bal) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
 }
+// wavefront minimum of a u32 through DPP row shifts and row broadcasts
+// (identity ~0 for lanes whose source is out of range); result in lane 63
+__device__ __forceinline__ uint32_t dpp_min_u32(uint32_t v) {
+  v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)~0u, (int)v, 0x111, 0xf, 0xf, false));  // row_shr:1
+  v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)~0u, (int)v, 0x112, 0xf, 0xf, false));  // row_shr:2
+  v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)~0u, (int)v, 0x113, 0xf, 0xf, false));  // row_shr:3
+  v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)~0u, (int)v, 0x114, 0xf, 0xe, false));  // row_shr:4
+  v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)~0u, (int)v, 0x118, 0xf, 0xc, false));  // row_shr:8
+  v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)~0u, (int)v, 0x142, 0xa, 0xf, false));  // row_bcast:15
+  v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)~0u, (int)v, 0x143, 0xc, 0xf, false));  // row_bcast:31
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+// minimum of non-negative doubles (or +inf) over the wavefront: the bit
+// patterns of such doubles order like the values, so the high words are
+// reduced first and the low words among the lanes holding that high word
+__device__ __forceinline__ double wave_min_time(double t) {
+  const uint64_t b = (uint64_t)__double_as_longlong(t);
+  const uint32_t hi = dpp_min_u32((uint32_t)(b >> 32));
+  const uint32_t lo = dpp_min_u32((uint32_t)(b >> 32) == hi ? (uint32_t)b : ~0u);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
 // exclusive prefix sum of v over the lanes, and the total
 __device__ __forceinline__ uint32_t wave_excl_scan(uint32_t v, uint32_t &total) {
   uint32_t x = v;
@@ -503,8 +525,15 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, cons
     }
     const bool stream_remote = stream && ex_byte(R.ex, ta) != x;
     if (stream && !stream_remote) lc |= 1u << ta;
-    uint32_t dl_total;
-    const uint32_t dl_off = wave_excl_scan((stream_remote ? 1u : 0u) + (uint32_t)__popc(rc), dl_total);
+    const uint32_t ndl = (stream_remote ? 1u : 0u) + (uint32_t)__popc(rc);
+    uint32_t dl_total, dl_off;
+    const uint64_t dl_any = __ballot(ndl > 0);
+    if (__ballot(ndl > 1) == 0) {
+      dl_off = lanes_below(dl_any);
+      dl_total = (uint32_t)__popcll(dl_any);
+    } else {
+      dl_off = wave_excl_scan(ndl, dl_total);
+    }
     if (dl_total) {
       if (S.dl_tail - S.dl_head + dl_total > S.A->L.dl_mask + 1u) {
         S.status |= CF_ST_OVERFLOW;
@@ -566,14 +595,14 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, cons
       }
     }
     // queue appends per ready component, in member order
-    const uint32_t any_ready = ru(wave_or_u(ready));
-    for (uint32_t cc = any_ready; cc;) {
-      const int c2 = __ffs(cc) - 1;
-      cc &= cc - 1;
-      const uint64_t bal = __ballot((ready >> c2) & 1u);
-      S.events += (uint64_t)__popcll(bal);
-      q_push_lanes(S, stage_of(S, x, c2), bal, r);
-      S.dirty |= 1ull << x;
+    if (__ballot(ready != 0)) {
+      for (int c2 = 0; c2 < m.nc; c2++) {
+        const uint64_t bal = __ballot((ready >> c2) & 1u);
+        if (!bal) continue;
+        S.events += (uint64_t)__popcll(bal);
+        q_push_lanes(S, stage_of(S, x, c2), bal, r);
+        S.dirty |= 1ull << x;
+      }
     }
     // completed requests: latencies, SLO check, per-type counts
     const uint64_t dbal = __ballot(done);
@@ -600,13 +629,9 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, cons
           Lp[3] = media;
         }
       }
-      for (int tt = 0; tt < m.nt; tt++) {
-        const uint64_t bc = __ballot(done && t == tt);
-        if (bc) {
-          const uint64_t bm = __ballot(done && ok && t == tt);
-          S.sh->cnt[tt] += (uint32_t)__popcll(bc);
-          S.sh->met[tt] += (uint32_t)__popcll(bm);
-        }
+      if (done) {
+        atomicAdd(&S.sh->cnt[t], 1u);
+        if (ok) atomicAdd(&S.sh->met[t], 1u);
       }
       S.events += (uint64_t)__popcll(dbal);
       S.n_done += __popcll(dbal);
@@ -648,16 +673,14 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     nmem = rn;
     // Decode run: while no input reaches this executor, its next steps are
     // decode steps of this stage with the same members, so the end of every
-    // step follows by repeated addition.  Run to the first finishing step or
-    // to the first step ending at or after the next pending input, whichever
-    // comes first; an input arriving earlier cuts the run (cut_run).
+    // step follows by repeated addition.  Run to the first finishing step; an
+    // input reaching the executor earlier cuts the run (cut_run).
     const uint32_t it0 = S.si.iter[si];
     uint32_t itgt = it0 + 1u;
     double tend = S.now + dur;
     if (lazy && dur > 0.0) {
       const uint32_t fin = S.si.minfin[si];
-      const double horizon = S.dl_head_t < S.t_arr ? S.dl_head_t : S.t_arr;
-      while (itgt < fin && tend < horizon && itgt - it0 < 65536u) {
+      while (itgt < fin && itgt - it0 < 65536u) {
         tend = tend + dur;
         itgt++;
       }
@@ -1122,7 +1145,7 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
         // --- next pending time
         double te = __builtin_inf();
         if (lane < S.nx && (sh.ex_st[lane] & 1u)) te = sh.ex_tend[lane];
-        te = rdb(wave_min(te));
+        te = wave_min_time(te);
         double t = te < S.dl_head_t ? te : S.dl_head_t;
         t = S.t_arr < t ? S.t_arr : t;
         if (t == __builtin_inf()) break;
