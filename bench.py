@@ -19,6 +19,20 @@ sys.path.insert(0, ROOT)
 METRIC = "simulated request-events/sec and candidate plans fully evaluated/sec, 1 GPU"
 PEAK_LANE_OPS = 256 * 4 * 16 * 2.4e9 / 1e12  # T lane-ops/s: CUs x SIMDs x lanes x clock
 OPS_PER_EVENT = 4.0  # algorithmic lane-ops per request-event
+KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_fine.hip", "paper_2512_14098_amd/csrc/cf_internal.h")
+# HBM bytes per k_fine launch from rocprofv3 counters (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0,
+# the scale factors a plain 1 GiB device copy gives), keyed by the kernel source the counters
+# were taken on and the workload; any other source or workload reports null
+MEASURED_TRAFFIC = {("83b7a0ab926c84c5", "c1"): 9.355e11}
+
+
+def kernel_source_id():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def cpu_baseline(w, ids, rates, budget_s):
@@ -60,6 +74,9 @@ def main():
     ap.add_argument("--config", default="c1")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB three times (the reference "
+                         "reading for the HBM byte counters), then exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -67,6 +84,16 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.copy_probe > 0:
+        n = args.copy_probe << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n, "launches": 3}), flush=True)
+        return
 
     from paper_2512_14098_amd import cf, pipeline
 
@@ -118,7 +145,8 @@ def main():
                    "triples": n_sel * w.K * len(w.seeds), "request_events_per_step": ev_step,
                    "status_counts": st, "fine_ms": fine_ms},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_LANE_OPS, "unit": "TOP/s",
-                     "frac": achieved / PEAK_LANE_OPS, "traffic": None,
+                     "frac": achieved / PEAK_LANE_OPS,
+                     "traffic": MEASURED_TRAFFIC.get((kernel_source_id(), args.config)),
                      "kernel": "k_fine", "ops_per_event": OPS_PER_EVENT,
                      "kernel_ms": sum(fine_ms) / len(fine_ms)},
     }

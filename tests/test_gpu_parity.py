@@ -229,6 +229,51 @@ def test_fine_c2_gating_latencies(cf):
         assert np.array_equal(g["lat"][j], o["lat"])
 
 
+def _gate_placement(tab, p, th, ta):
+    """'sep' if every gated route puts thinker and talker on different nodes,
+    'col' if on the same node, 'mixed' otherwise."""
+    sep = set()
+    for rt in tab.plan(p)["routes"]:
+        for alt in rt:
+            nd = alt["node"]
+            if nd[ta] != 255:
+                sep.add(nd[th] != nd[ta])
+    return "sep" if sep == {True} else "col" if sep == {False} else "mixed"
+
+
+def test_fine_c2_thinker_talker_placements(cf):
+    """Omni plans kept by phase 1, eight per thinker/talker placement (different
+    nodes, same node, both), every other rate of the grid: counts, events and
+    status of every triple, latencies of every request of twelve triples."""
+    _say("fine c2 placements")
+    cfg = load_config("c2")
+    tab = make_plans(cfg)
+    m = O.make_model(cfg["model"])
+    names = [c["name"] for c in cfg["model"]["components"]]
+    th, ta = names.index("L_th"), names.index("L_ta")
+    mtr = O.trace_gen(m, [0], 2000)
+    rd, bn, fl = O.eval_coarse(m, tab, mtr["moments"][0], cfg["gpus"])
+    kept = O.select_topk(rd, fl, tab.P)
+    by = {"sep": [], "col": [], "mixed": []}
+    for p in kept:
+        c = _gate_placement(tab, int(p), th, ta)
+        if len(by[c]) < 8:
+            by[c].append(int(p))
+    ids = sorted(by["sep"] + by["col"] + by["mixed"])
+    assert len(ids) == 24
+    rates = O.rate_grid(rd, np.asarray(ids, np.int32), cfg["rates"]["grid"])[:, 1::2]
+    rates = np.ascontiguousarray(rates)
+    K = rates.shape[1]
+    lat_tr = [(i * K + k) for i in range(0, 24, 2) for k in (K - 1,)]
+    g, want, m, otr = _fine_pair(cf, cfg, tab, ids, rates, [5], 4000, lat_triples=lat_tr)
+    _assert_fine_equal(g, want)
+    assert np.all(g["status"] == 0)
+    for j, tid in enumerate(lat_tr):
+        i, k = divmod(tid, K)
+        o = O.sim_triple(m, tab, ids[i], rates[i, k], otr, 0, want_lat=True)
+        assert np.array_equal(g["lat"][j], o["lat"])
+
+
 # ------------------------------------------------------------------ micro-scenarios on the GPU
 
 def _run_both(cf, mcfg, plan, reqs, rate=1.0):
