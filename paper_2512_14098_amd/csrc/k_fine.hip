@@ -27,9 +27,25 @@
 // token count is (decode steps of its stage since it joined) + 1, so each
 // running slot stores the step index at which it finishes and only the
 // finishing slots are touched.  The gated stage (talker) keeps per-request
-// token counts; visibility of thinker tokens comes from the request's join
-// step in the thinker's stage and a ring of that stage's recent step end
-// times.
+// token counts; the time of a thinker token comes from the request's join
+// step in the thinker's stage and a ring of that stage's step end times.
+//
+// Two instantiations of the kernel: k_fine<false> simulates thinker steps
+// one at a time and wakes the talker executors after every remote thinker
+// step; it serves models without a gated stage, where none of that is
+// reached.  k_fine<true>, used for models with a gated stage, also runs
+// thinker stages in decode runs and replaces the per-step wake-ups by exact
+// wake times: a talker request becomes eligible at the visibility time of
+// the thinker token it waits for, the only state change not caused by an
+// event of its own executor.  An executor hosting a talker stage that is
+// idle (or in a decode run) keeps the earliest such time among its blocked
+// requests whose thinker runs elsewhere; the thinker's ring holds the last
+// completed steps and the predicted ends of the steps of its running decode
+// run.  Requests whose token is not scheduled yet register the executor
+// with the thinker's stage, and every start or cut of that stage's decode
+// steps makes the registered executors recompute their wake time.  A
+// thinker run on an executor that also hosts the talker stops at the first
+// step whose token a local blocked talker request waits for.
 #include <stdlib.h>
 #include <string.h>
 
@@ -40,7 +56,10 @@ namespace {
 
 constexpr int kMaxSI = CF_MAX_EXEC * CF_MAX_COMP;  // stage instances
 constexpr int kChunk = 64;                          // queue chunk entries
-constexpr int kHist = 64;                           // thinker step-time ring
+constexpr int kHist = 64;                           // k_fine<false>: ring of the last thinker step ends
+constexpr int kRing = 256;                          // k_fine<true>: thinker step-time ring
+constexpr int kKeep = 64;                           // k_fine<true>: completed steps kept in the ring
+constexpr uint32_t kThRun = kRing - kKeep;          // k_fine<true>: longest thinker decode run
 constexpr uint32_t kNone = 0xFFFFFFFFu;
 
 enum { IT_BATCH = 0, IT_PREFILL = 1, IT_DECODE = 2, IT_FINISH = 3 };
@@ -125,8 +144,12 @@ struct SiLds {
   int16_t *hist;
   int *qhc, *qtc, *qn, *roff, *rn;
   uint32_t *iter, *minfin;
+  uint64_t *watch;  // k_fine<true>, thinker stages: executors to notify when its decode steps are (re)scheduled
+  uint32_t *sched;  // k_fine<true>, thinker stages: last step whose end is known (completed or in the running run)
 };
 constexpr size_t kSiBytes = 1 + 1 + 1 + 1 + 2 + 2 + 4 * 7;
+constexpr size_t kSiBytesGated = kSiBytes + 8 + 4;
+static_assert(sizeof(WaveShared) % 8 == 0, "the dynamic LDS table after WaveShared holds 8-byte words");
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x; }
 __device__ __forceinline__ uint32_t ru(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -214,6 +237,9 @@ struct Sim {
   uint32_t status, dl_head, dl_tail;
   int pool_top, pool_fresh, n_done, nx, lat_slot;
   bool remote_gate;
+  // k_fine<true>
+  double *wake;        // per executor with a gated stage: next visibility time of a blocked request
+  uint64_t rewake;     // executors whose wake time is to be recomputed in this instant
 };
 
 // ------------------------------------------------------------------ trace
@@ -415,6 +441,83 @@ __device__ __forceinline__ bool slot_eligible(const Sim &S, uint32_t r, uint32_t
   const uint32_t nth = nout_of(S, r, t, th);
   const uint32_t k = tok + 1u < nth ? tok + 1u : nth;
   return token_visible(S, r, R.misc, th, ex_byte(R.ex, th), x, k, nth, undecided);
+}
+
+// k_fine<true>: time at which token k of request r, emitted by its gate
+// source (component th on executor xth), is visible at executor x: e_k +
+// delta (+inf while the step emitting it is not scheduled).  wsi receives
+// the thinker's stage instance while that time may still change (step not
+// completed), else -1.
+__device__ __forceinline__ double token_vis(const Sim &S, uint32_t r, uint32_t misc, int th, int xth, int x,
+                                            uint32_t k, uint32_t nth, int &wsi, bool &undecided) {
+  const double delta = (xth == x) ? 0.0 : S.A->m.comm;
+  wsi = -1;
+  double e;
+  if (k <= 1) {
+    e = S.tfirst[r];
+  } else if ((misc & MISC_TH_DONE) && k == nth) {
+    e = S.tlast[r];
+  } else {
+    const int si = stage_of(S, xth, th);
+    const uint32_t q = S.thjoin[r] + k - 1u;
+    if (q > S.si.sched[si]) {
+      wsi = si;
+      return __builtin_inf();
+    }
+    const uint32_t it = S.si.iter[si];
+    const double *h = S.hist + (size_t)S.si.hist[si] * kRing;
+    if (q > it) {
+      wsi = si;  // predicted end of a step of the running decode run
+      e = h[q & (kRing - 1)];
+    } else if (it - q < (uint32_t)kKeep) {
+      e = h[q & (kRing - 1)];
+    } else {
+      e = h[(it - (kKeep - 1)) & (kRing - 1)];  // oldest kept step: token k is no later
+      if (!(e + delta <= S.now)) {
+        undecided = true;
+        return __builtin_inf();
+      }
+    }
+  }
+  return e + delta;
+}
+
+// k_fine<true>: visibility time of the thinker token that the running slot
+// (request r, tok tokens) of gated stage component c on executor x waits for
+// (-inf for requests whose type is not gated at c); xth receives the
+// thinker's executor
+__device__ __forceinline__ double slot_vis(const Sim &S, uint32_t r, uint32_t tok, int c, int x, int &xth, int &wsi,
+                                           bool &undecided) {
+  const Rec R = S.rec[r];
+  const int t = rtype(R.misc);
+  xth = x;
+  wsi = -1;
+  if (S.sh->ml.ta_c[t] != c) return -__builtin_inf();
+  const int th = S.sh->ml.th_c[t];
+  const uint32_t nth = nout_of(S, r, t, th);
+  const uint32_t k = tok + 1u < nth ? tok + 1u : nth;
+  xth = ex_byte(R.ex, th);
+  return token_vis(S, r, R.misc, th, xth, x, k, nth, wsi, undecided);
+}
+
+template <bool G>
+__device__ __forceinline__ bool eligible(const Sim &S, uint32_t r, uint32_t tok, int c, int x, bool &undecided) {
+  if constexpr (G) {
+    int xth, wsi;
+    return slot_vis(S, r, tok, c, x, xth, wsi, undecided) <= S.now;
+  } else {
+    return slot_eligible(S, r, tok, c, x, undecided);
+  }
+}
+
+// k_fine<true>: the decode steps of thinker stage si were (re)scheduled; the
+// registered executors recompute their wake time
+__device__ __forceinline__ void notify(Sim &S, int si) {
+  const uint64_t w = S.si.watch[si];
+  if (w) {
+    S.rewake |= w;
+    S.si.watch[si] = 0;
+  }
 }
 
 // ------------------------------------------------------------------ requests
@@ -641,7 +744,8 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, cons
 }
 
 // ------------------------------------------------------------------ iterations
-__device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool lazy) {
+template <bool G>
+__device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool lazy, uint32_t bound) {
   const KModel &m = S.A->m;
   WaveShared &sh = *S.sh;
   double dur;
@@ -678,11 +782,28 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     const uint32_t it0 = S.si.iter[si];
     uint32_t itgt = it0 + 1u;
     double tend = S.now + dur;
-    if (lazy && dur > 0.0) {
-      const uint32_t fin = S.si.minfin[si];
-      while (itgt < fin && itgt - it0 < 65536u) {
-        tend = tend + dur;
-        itgt++;
+    if constexpr (G) {
+      // k_fine<true>: runs also stop at bound; a thinker stage records the
+      // predicted end of every step of the run in its ring
+      const bool thk = S.si.flags[si] & SF_THINKER;
+      double *h = S.hist + (size_t)(thk ? S.si.hist[si] : 0) * kRing;
+      if (thk && lane_id() == 0) h[itgt & (kRing - 1)] = tend;
+      if (lazy && dur > 0.0) {
+        const uint32_t fin = S.si.minfin[si] < bound ? S.si.minfin[si] : bound;
+        while (itgt < fin && itgt - it0 < 65536u) {
+          tend = tend + dur;
+          itgt++;
+          if (thk && lane_id() == 0) h[itgt & (kRing - 1)] = tend;
+        }
+      }
+      if (thk) S.si.sched[si] = itgt;
+    } else {
+      if (lazy && dur > 0.0) {
+        const uint32_t fin = S.si.minfin[si];
+        while (itgt < fin && itgt - it0 < 65536u) {
+          tend = tend + dur;
+          itgt++;
+        }
       }
     }
     sh.ex_t0[x] = S.now;
@@ -703,7 +824,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
       const int j = b + lane_id();
       if (j < rn) {
         const uint32_t tok = rk[j] & 0xFFFFu;
-        const bool el = slot_eligible(S, rr[j], tok, c, x, undecided);
+        const bool el = eligible<G>(S, rr[j], tok, c, x, undecided);
         rk[j] = el ? (tok | MARK) : tok;
         cntm += el ? 1u : 0u;
       }
@@ -713,6 +834,13 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     __syncthreads();
     dur = m.d0[c] + m.d1[c] * (double)cntm;
     nmem = (int)cntm;
+    if constexpr (G) {
+      if (S.si.flags[si] & SF_THINKER) {  // a gated stage that is also a gate source
+        const uint32_t it1 = S.si.iter[si] + 1u;
+        if (lane_id() == 0) S.hist[(size_t)S.si.hist[si] * kRing + (it1 & (kRing - 1))] = S.now + dur;
+        S.si.sched[si] = it1;
+      }
+    }
   }
   sh.ex_tend[x] = S.now + dur;
   sh.ex_itgt[x] = S.si.iter[si] + 1u;
@@ -720,6 +848,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
                 ((uint32_t)nmem << 12);
 }
 
+template <bool G>
 __device__ int runnable_kind(Sim &S, int x, int si, int c) {
   const uint8_t fl = S.si.flags[si];
   const int qn = S.si.qn[si];
@@ -734,13 +863,47 @@ __device__ int runnable_kind(Sim &S, int x, int si, int c) {
   for (int b = 0; b < rn && !any; b += 64) {
     const int j = b + lane_id();
     bool el = false;
-    if (j < rn) el = slot_eligible(S, rr[j], rk[j] & 0xFFFFu, c, x, undecided);
+    if (j < rn) el = eligible<G>(S, rr[j], rk[j] & 0xFFFFu, c, x, undecided);
     any = __ballot(el) != 0;
   }
   if (__ballot(undecided)) S.status |= CF_ST_OVERFLOW;
   return any ? IT_DECODE : -1;
 }
 
+// k_fine<true>: first step, after the thinker stage si's current one, whose
+// token a blocked request of a gated stage on the same executor x waits for
+// (the gated stages of x have no eligible request when this is called)
+__device__ __forceinline__ uint32_t local_gate_bound(const Sim &S, int x, int si) {
+  const int ns = S.sh->ex_ns[x], first = S.sh->ex_first[x];
+  const int cth = S.si.comp[si];
+  uint32_t qmin = kNone;
+  for (int g = first; g < first + ns; g++) {
+    if (!(S.si.flags[g] & SF_GATED)) continue;
+    const int c = S.si.comp[g], rn = S.si.rn[g];
+    const uint32_t *rr = S.run_r + S.si.roff[g];
+    const uint32_t *rk = S.run_k + S.si.roff[g];
+    for (int b = 0; b < rn; b += 64) {
+      const int j = b + lane_id();
+      if (j < rn) {
+        const uint32_t r = rr[j];
+        const Rec R = S.rec[r];
+        const int t = rtype(R.misc);
+        if (S.sh->ml.ta_c[t] == c && S.sh->ml.th_c[t] == cth && ex_byte(R.ex, cth) == x) {
+          const uint32_t nth = nout_of(S, r, t, cth);
+          const uint32_t tok = rk[j] & 0xFFFFu;
+          const uint32_t k = tok + 1u < nth ? tok + 1u : nth;
+          if (k > 1u && !((R.misc & MISC_TH_DONE) && k == nth)) {
+            const uint32_t q = S.thjoin[r] + k - 1u;
+            qmin = q < qmin ? q : qmin;
+          }
+        }
+      }
+    }
+  }
+  return ru(wave_min_u(qmin));
+}
+
+template <bool G>
 __device__ void try_start(Sim &S, int x) {
   WaveShared &sh = *S.sh;
   const uint32_t st = sh.ex_st[x];
@@ -749,19 +912,32 @@ __device__ void try_start(Sim &S, int x) {
   for (int i = 0; i < ns; i++) {
     const int l = (rr == 15) ? i : (rr + 1 + i) % ns;
     const int si = first + l;
-    const int kind = runnable_kind(S, x, si, S.si.comp[si]);
+    const int kind = runnable_kind<G>(S, x, si, S.si.comp[si]);
     if (kind >= 0) {
       bool lazy = false;
+      uint32_t bound = kNone;
       const uint8_t fl = S.si.flags[si];
-      if (kind == IT_DECODE && !(fl & (SF_THINKER | SF_GATED)) &&
-          (S.si.qn[si] == 0 || S.si.rn[si] >= (int)S.si.beff[si])) {
+      const uint8_t no_run = G ? SF_GATED : (SF_THINKER | SF_GATED);
+      if (kind == IT_DECODE && !(fl & no_run) && (S.si.qn[si] == 0 || S.si.rn[si] >= (int)S.si.beff[si])) {
         lazy = true;  // ... unless a stage checked after this one has work
         for (int i2 = i + 1; i2 < ns && lazy; i2++) {
           const int l2 = (rr == 15) ? i2 : (rr + 1 + i2) % ns;
-          if (runnable_kind(S, x, first + l2, S.si.comp[first + l2]) >= 0) lazy = false;
+          if (runnable_kind<G>(S, x, first + l2, S.si.comp[first + l2]) >= 0) lazy = false;
+        }
+        if constexpr (G) {
+          if (lazy && (fl & SF_THINKER)) {
+            bound = S.si.iter[si] + kThRun;
+            if ((S.ta_exec_mask >> x) & 1ull) {
+              const uint32_t q = local_gate_bound(S, x, si);
+              bound = q < bound ? q : bound;
+            }
+          }
         }
       }
-      start_iter(S, x, l, si, S.si.comp[si], kind, lazy);
+      start_iter<G>(S, x, l, si, S.si.comp[si], kind, lazy, bound);
+      if constexpr (G) {
+        if ((fl & SF_THINKER) && kind == IT_DECODE) notify(S, si);
+      }
       return;
     }
   }
@@ -769,6 +945,7 @@ __device__ void try_start(Sim &S, int x) {
 
 // An input reached executor x, busy in a decode run: the run stops at the
 // first step that ends at or after now (the steps before it are unchanged).
+template <bool G>
 __device__ void cut_run(Sim &S, int x) {
   WaveShared &sh = *S.sh;
   const uint32_t st = sh.ex_st[x];
@@ -786,6 +963,12 @@ __device__ void cut_run(Sim &S, int x) {
   sh.ex_tend[x] = t;
   sh.ex_itgt[x] = j;
   if (j <= it0 + 1u) sh.ex_st[x] = st & ~EX_RUN;
+  if constexpr (G) {
+    if ((S.si.flags[si] & SF_THINKER) && j < itgt) {
+      S.si.sched[si] = j;
+      notify(S, si);
+    }
+  }
 }
 
 __device__ __forceinline__ void thinker_tick(Sim &S) {
@@ -849,6 +1032,7 @@ __device__ void finish_slots(Sim &S, int x, int si, int c, const bool *fin) {
   run_compact(S, si, fin);
 }
 
+template <bool G>
 __device__ void complete_iter(Sim &S, int x) {
   WaveShared &sh = *S.sh;
   const uint32_t st = sh.ex_st[x];
@@ -862,14 +1046,18 @@ __device__ void complete_iter(Sim &S, int x) {
   if (kind == IT_BATCH || kind == IT_PREFILL) {
     S.events += (uint64_t)nmem;
     members_done(S, x, si, c, kind, nmem, S.mem + (size_t)x * CF_MAX_BATCH);
-    if (fl & SF_THINKER) thinker_tick(S);
+    if constexpr (!G) {
+      if (fl & SF_THINKER) thinker_tick(S);
+    }
     return;
   }
   const int rn = S.si.rn[si];
   const uint32_t it0 = S.si.iter[si];
   const uint32_t it = (fl & SF_GATED) ? it0 + 1u : sh.ex_itgt[x];
-  S.si.iter[si] = it;
-  if ((fl & SF_THINKER) && lane_id() == 0) S.hist[(size_t)S.si.hist[si] * kHist + (it & (kHist - 1))] = S.now;
+  S.si.iter[si] = it;  // k_fine<true>: a thinker's ring already holds the end of these steps
+  if constexpr (!G) {
+    if ((fl & SF_THINKER) && lane_id() == 0) S.hist[(size_t)S.si.hist[si] * kHist + (it & (kHist - 1))] = S.now;
+  }
   const uint32_t *rr = S.run_r + S.si.roff[si];
   uint32_t *rk = S.run_k + S.si.roff[si];
   if (!(fl & SF_GATED)) {
@@ -909,10 +1097,53 @@ __device__ void complete_iter(Sim &S, int x) {
     for (int p = 0; p < CF_MAX_BATCH / 64; p++) anyf |= __ballot(fin[p]) != 0;
     if (anyf) finish_slots(S, x, si, c, fin);
   }
-  if (fl & SF_THINKER) thinker_tick(S);
+  if constexpr (!G) {
+    if (fl & SF_THINKER) thinker_tick(S);
+  }
+}
+
+// k_fine<true>: recomputes the wake time of executor y, which hosts a gated
+// stage: the earliest visibility time, after now, of the token that a
+// blocked request of its gated stages waits for from a thinker on another
+// executor (a local thinker's steps end on y itself).  Only kept while y is
+// idle or in a decode run; y registers with the thinker stages whose steps
+// are not final.  Returns whether some such request is eligible already.
+__device__ __forceinline__ bool gate_wake(Sim &S, int y) {
+  WaveShared &sh = *S.sh;
+  const uint32_t st = sh.ex_st[y];
+  double w = __builtin_inf();
+  bool now_el = false;
+  if (!(st & 1u) || (st & EX_RUN)) {
+    const int ns = sh.ex_ns[y], first = sh.ex_first[y];
+    bool undecided = false;
+    for (int g = first; g < first + ns; g++) {
+      if (!(S.si.flags[g] & SF_GATED)) continue;
+      const int c = S.si.comp[g], rn = S.si.rn[g];
+      const uint32_t *rr = S.run_r + S.si.roff[g];
+      const uint32_t *rk = S.run_k + S.si.roff[g];
+      for (int b = 0; b < rn; b += 64) {
+        const int j = b + lane_id();
+        if (j < rn) {
+          int xth, wsi;
+          const double tv = slot_vis(S, rr[j], rk[j] & 0xFFFFu, c, y, xth, wsi, undecided);
+          if (xth != y) {
+            if (wsi >= 0) atomicOr((unsigned long long *)&S.si.watch[wsi], 1ull << y);
+            if (tv <= S.now) now_el = true;
+            else w = tv < w ? tv : w;
+          }
+        }
+      }
+    }
+    if (__ballot(undecided)) S.status |= CF_ST_OVERFLOW;
+    w = wave_min_time(w);
+    now_el = __ballot(now_el) != 0;
+  }
+  if (lane_id() == 0) S.wake[y] = w;
+  return now_el;
 }
 
 // ------------------------------------------------------------------ setup
+template <bool G>
 __device__ bool setup_plan(Sim &S, int p) {
   const FineArgs &A = *S.A;
   const KModel &m = A.m;
@@ -996,7 +1227,9 @@ __device__ bool setup_plan(Sim &S, int p) {
     sh.ex_t0[lane] = 0.0;
     sh.ex_dur[lane] = 0.0;
     sh.ex_itgt[lane] = 0;
+    if constexpr (G) S.wake[lane] = __builtin_inf();
   }
+  if constexpr (G) S.rewake = 0;
   // stage instances, one lane each (prefix sums give run-slot and ring offsets)
   int roff_carry = 0, hs_carry = 0;
   for (int s0 = 0; s0 < nsi; s0 += 64) {
@@ -1037,6 +1270,10 @@ __device__ bool setup_plan(Sim &S, int p) {
       S.si.minfin[s] = kNone;
       S.si.roff[s] = roff_carry + (int)ro;
       S.si.hist[s] = thk ? (int16_t)(hs_carry + (int)ho) : (int16_t)-1;
+      if constexpr (G) {
+        S.si.sched[s] = 0;
+        S.si.watch[s] = 0;
+      }
     }
     roff_carry += (int)tot_r;
     hs_carry += (int)tot_h;
@@ -1047,6 +1284,7 @@ __device__ bool setup_plan(Sim &S, int p) {
 
 extern __shared__ char dyn_lds[];
 
+template <bool G>
 __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
   __shared__ WaveShared sh;
   const FineArgs &A = *Ap;
@@ -1071,6 +1309,15 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
     S.si.flags = (uint8_t *)p; p += cap;
     S.si.qhp = (uint8_t *)p; p += cap;
     S.si.qtp = (uint8_t *)p; p += cap;
+    if constexpr (G) {
+      // cap is a multiple of 64 and the static LDS a multiple of 8 bytes: 8-byte aligned
+      S.si.sched = (uint32_t *)p; p += 4 * cap;
+      S.si.watch = (uint64_t *)p;
+    }
+  }
+  if constexpr (G) {
+    __shared__ double wake_lds[CF_MAX_EXEC];
+    S.wake = wake_lds;
   }
   // model tables for per-lane indexing
   for (int j = lane; j < CF_MAX_TYPES * CF_MAX_COMP; j += 64) {
@@ -1135,7 +1382,7 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
       sh.cnt[lane] = 0;
     }
     __syncthreads();
-    const bool ok = (p >= 0 && p < A.P) && S.lam > 0.0 && S.lam < __builtin_inf() && setup_plan(S, p);
+    const bool ok = (p >= 0 && p < A.P) && S.lam > 0.0 && S.lam < __builtin_inf() && setup_plan<G>(S, p);
     if (!ok) S.status |= CF_ST_INVALID;
     if (ok && !(S.status & CF_ST_OVERFLOW) && A.n > 0) {
       uint32_t next_arr = 0;
@@ -1145,6 +1392,12 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
         // --- next pending time
         double te = __builtin_inf();
         if (lane < S.nx && (sh.ex_st[lane] & 1u)) te = sh.ex_tend[lane];
+        if constexpr (G) {
+          if (lane < S.nx) {
+            const double wk = S.wake[lane];
+            te = wk < te ? wk : te;
+          }
+        }
         te = wave_min_time(te);
         double t = te < S.dl_head_t ? te : S.dl_head_t;
         t = S.t_arr < t ? S.t_arr : t;
@@ -1157,10 +1410,16 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
         // --- step 1: iterations ending at t, ascending executor
         if (te == t) {
           uint64_t done = __ballot(lane < S.nx && (sh.ex_st[lane] & 1u) && sh.ex_tend[lane] == t);
+          if constexpr (G) {
+            // wake times due: the executor examines its stages in step 3
+            const bool wk = lane < S.nx && S.wake[lane] == t;
+            if (wk) S.wake[lane] = __builtin_inf();
+            S.dirty |= __ballot(wk);
+          }
           while (done) {
             const int x = __ffsll((long long)done) - 1;
             done &= done - 1;
-            complete_iter(S, x);
+            complete_iter<G>(S, x);
           }
         }
         // --- step 2: delayed deliveries due at t (production order), then arrivals at t
@@ -1180,11 +1439,34 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
         uint64_t cand = S.dirty;
         S.dirty = 0;
         __syncthreads();
-        while (cand) {
-          const int x = __ffsll((long long)cand) - 1;
-          cand &= cand - 1;
-          if (!(sh.ex_st[x] & 1u)) try_start(S, x);
-          else cut_run(S, x);
+        if constexpr (G) {
+          // Examine the dirty executors; then recompute the wake times of the
+          // executors examined or notified.  An executor found with a request
+          // eligible now is examined once more (at most once per instant).
+          uint64_t extra = 0;
+          for (;;) {
+            S.rewake |= cand & S.ta_exec_mask;
+            while (cand) {
+              const int x = __ffsll((long long)cand) - 1;
+              cand &= cand - 1;
+              if (!(sh.ex_st[x] & 1u)) try_start<G>(S, x);
+              else cut_run<G>(S, x);
+            }
+            while (S.rewake) {
+              const int y = __ffsll((long long)S.rewake) - 1;
+              S.rewake &= S.rewake - 1;
+              if (gate_wake(S, y) && !((extra >> y) & 1ull)) cand |= 1ull << y;
+            }
+            if (!cand || (S.status & CF_ST_OVERFLOW)) break;
+            extra |= cand;
+          }
+        } else {
+          while (cand) {
+            const int x = __ffsll((long long)cand) - 1;
+            cand &= cand - 1;
+            if (!(sh.ex_st[x] & 1u)) try_start<G>(S, x);
+            else cut_run<G>(S, x);
+          }
         }
         if (S.status & (CF_ST_OVERFLOW | CF_ST_INVALID)) break;
       }
@@ -1241,7 +1523,7 @@ Layout make_layout(const KModel &m, int n) {
   L.thjoin = take(4 * (size_t)n);
   L.run_r = take(4 * (size_t)L.run_cap);
   L.run_k = take(4 * (size_t)L.run_cap);
-  L.hist = take(8 * (size_t)L.hist_slots * kHist + 8);
+  L.hist = take(8 * (size_t)L.hist_slots * (m.gated_mask ? kRing : kHist) + 8);
   L.mem = take(4 * (size_t)CF_MAX_EXEC * CF_MAX_BATCH);
   size_t dl = 4096;
   while (dl < 2 * (size_t)n + 8192) dl <<= 1;
@@ -1343,11 +1625,14 @@ extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_tabl
   if (st != CF_OK) return st;
   a.nsi_cap = (int)((nsi + 63u) & ~63u);
   if (a.nsi_cap < 64) a.nsi_cap = 64;
-  const size_t lds = kSiBytes * (size_t)a.nsi_cap;
+  const size_t lds = (a.m.gated_mask ? kSiBytesGated : kSiBytes) * (size_t)a.nsi_cap;
   st = hip_check(hipMemcpyAsync(args_dev, &a, sizeof a, hipMemcpyHostToDevice, s), "copy fine args");
   if (st != CF_OK) return st;
   hipLaunchKernelGGL(k_fine_reset, dim3(1), dim3(1), 0, s, a.ticket);
-  hipLaunchKernelGGL(k_fine, dim3((unsigned)waves), dim3(64), lds, s, (const FineArgs *)args_dev);
+  if (a.m.gated_mask)
+    hipLaunchKernelGGL(k_fine<true>, dim3((unsigned)waves), dim3(64), lds, s, (const FineArgs *)args_dev);
+  else
+    hipLaunchKernelGGL(k_fine<false>, dim3((unsigned)waves), dim3(64), lds, s, (const FineArgs *)args_dev);
   st = hip_check(hipGetLastError(), "cf_eval_fine launch");
   if (st != CF_OK) return st;
   // the argument block is copied from host memory on the stream: wait for it
