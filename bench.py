@@ -72,6 +72,9 @@ def main():
     ap.add_argument("--steps", type=int, default=2)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", default="c1")
+    ap.add_argument("--seeds", type=int, default=0, metavar="N",
+                    help="simulate only the first N seeds of the workload (a sample of a workload "
+                         "too large to run whole; stated in the output)")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -99,7 +102,11 @@ def main():
 
     torch.cuda.set_device(0)
     print("bench: loading workload %s" % args.config, file=sys.stderr, flush=True)
-    w = pipeline.Workload(args.config)
+    from paper_2512_14098_amd.inputs import load_config, seeds_of
+    cfg = load_config(args.config)
+    all_seeds = seeds_of(cfg)
+    seeds = all_seeds[: args.seeds] if args.seeds > 0 else all_seeds
+    w = pipeline.Workload(cfg, seeds=seeds)
     for i in range(args.warmup):
         out = pipeline.run_step(w)
         torch.cuda.synchronize()
@@ -114,9 +121,12 @@ def main():
         timers_all.append(timers)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    stage_ms = {}
     for i, timers in enumerate(timers_all):
         s, e = timers["fine"]
         fine_ms.append(s.elapsed_time(e))
+        for k, (s, e) in timers.items():
+            stage_ms.setdefault(k, []).append(s.elapsed_time(e))
     events = pipeline.events_total(out) * args.steps
     plans = int(out["ids"].numel()) * args.steps
     st = pipeline.status_summary(out)
@@ -126,6 +136,9 @@ def main():
     fine_avg_s = sum(fine_ms) / len(fine_ms) / 1e3
     achieved = OPS_PER_EVENT * ev_step / fine_avg_s / 1e12
     n_sel = int(out["ids"].numel())
+    workload = "%s: %s" % (args.config, w.cfg["summary"])
+    if len(seeds) < len(all_seeds):
+        workload += " (sample: first %d of its %d seeds)" % (len(seeds), len(all_seeds))
     res = {
         "metric": METRIC,
         "value": events / elapsed,
@@ -140,10 +153,11 @@ def main():
         "dtype": "f64",
         "data": "synthetic",
         "plans_per_s": plans / elapsed,
-        "config": {"workload": "%s: %s" % (args.config, w.cfg["summary"]), "plans_screened": w.tab.P,
+        "config": {"workload": workload, "plans_screened": w.tab.P,
                    "plans_simulated": n_sel, "rates": w.K, "seeds": len(w.seeds), "requests": w.n_req,
                    "triples": n_sel * w.K * len(w.seeds), "request_events_per_step": ev_step,
-                   "status_counts": st, "fine_ms": fine_ms},
+                   "status_counts": st, "fine_ms": fine_ms,
+                   "stage_ms": {k: sum(v) / len(v) for k, v in stage_ms.items()}},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_LANE_OPS, "unit": "TOP/s",
                      "frac": achieved / PEAK_LANE_OPS,
                      "traffic": MEASURED_TRAFFIC.get((kernel_source_id(), args.config)),

@@ -109,6 +109,7 @@ struct FineArgs {
   unsigned int *ticket;
   unsigned int total;
   int nsi_cap;  // stage instances provided in LDS
+  int nl_cap, nt_cap;  // k_fine<true>: LLM stage instances and thinker ring slots provided in LDS
 };
 
 // model tables read with per-lane (divergent) indices
@@ -138,9 +139,14 @@ struct WaveShared {
 };
 
 // stage-instance descriptors, structure of arrays in dynamic LDS
+// k_fine<false> indexes every field by stage instance.  k_fine<true> keeps
+// the LLM-only fields (rn, roff, iter, minfin, hist) for its LLM stage
+// instances only, at index lsi[si], and the thinker-only fields (sched,
+// watch) per thinker ring slot hist[lsi[si]].
 struct SiLds {
   uint8_t *comp, *flags, *qhp, *qtp;
   uint16_t *beff;
+  uint16_t *lsi;    // k_fine<true>: index of an LLM stage instance in the LLM-only fields
   int16_t *hist;
   int *qhc, *qtc, *qn, *roff, *rn;
   uint32_t *iter, *minfin;
@@ -148,8 +154,15 @@ struct SiLds {
   uint32_t *sched;  // k_fine<true>, thinker stages: last step whose end is known (completed or in the running run)
 };
 constexpr size_t kSiBytes = 1 + 1 + 1 + 1 + 2 + 2 + 4 * 7;
-constexpr size_t kSiBytesGated = kSiBytes + 8 + 4;
+// k_fine<true>: bytes per stage instance, per LLM stage instance, per thinker slot
+constexpr size_t kSiBytesG = 4 * 3 + 2 * 2 + 4, kLlmBytesG = 4 * 4 + 2, kThBytesG = 8 + 4;
 static_assert(sizeof(WaveShared) % 8 == 0, "the dynamic LDS table after WaveShared holds 8-byte words");
+
+template <bool G>
+__device__ __forceinline__ int lx_of(const SiLds &si, int s) {
+  if constexpr (G) return si.lsi[s];
+  else return s;
+}
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x; }
 __device__ __forceinline__ uint32_t ru(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -446,7 +459,7 @@ __device__ __forceinline__ bool slot_eligible(const Sim &S, uint32_t r, uint32_t
 // k_fine<true>: time at which token k of request r, emitted by its gate
 // source (component th on executor xth), is visible at executor x: e_k +
 // delta (+inf while the step emitting it is not scheduled).  wsi receives
-// the thinker's stage instance while that time may still change (step not
+// the thinker's ring slot while that time may still change (step not
 // completed), else -1.
 __device__ __forceinline__ double token_vis(const Sim &S, uint32_t r, uint32_t misc, int th, int xth, int x,
                                             uint32_t k, uint32_t nth, int &wsi, bool &undecided) {
@@ -458,16 +471,17 @@ __device__ __forceinline__ double token_vis(const Sim &S, uint32_t r, uint32_t m
   } else if ((misc & MISC_TH_DONE) && k == nth) {
     e = S.tlast[r];
   } else {
-    const int si = stage_of(S, xth, th);
+    const int lx = S.si.lsi[stage_of(S, xth, th)];
+    const int slot = S.si.hist[lx];
     const uint32_t q = S.thjoin[r] + k - 1u;
-    if (q > S.si.sched[si]) {
-      wsi = si;
+    if (q > S.si.sched[slot]) {
+      wsi = slot;
       return __builtin_inf();
     }
-    const uint32_t it = S.si.iter[si];
-    const double *h = S.hist + (size_t)S.si.hist[si] * kRing;
+    const uint32_t it = S.si.iter[lx];
+    const double *h = S.hist + (size_t)slot * kRing;
     if (q > it) {
-      wsi = si;  // predicted end of a step of the running decode run
+      wsi = slot;  // predicted end of a step of the running decode run
       e = h[q & (kRing - 1)];
     } else if (it - q < (uint32_t)kKeep) {
       e = h[q & (kRing - 1)];
@@ -510,13 +524,13 @@ __device__ __forceinline__ bool eligible(const Sim &S, uint32_t r, uint32_t tok,
   }
 }
 
-// k_fine<true>: the decode steps of thinker stage si were (re)scheduled; the
-// registered executors recompute their wake time
-__device__ __forceinline__ void notify(Sim &S, int si) {
-  const uint64_t w = S.si.watch[si];
+// k_fine<true>: the decode steps of the thinker stage with ring slot `slot`
+// were (re)scheduled; the registered executors recompute their wake time
+__device__ __forceinline__ void notify(Sim &S, int slot) {
+  const uint64_t w = S.si.watch[slot];
   if (w) {
     S.rewake |= w;
-    S.si.watch[si] = 0;
+    S.si.watch[slot] = 0;
   }
 }
 
@@ -580,11 +594,13 @@ __device__ void dl_deliver(Sim &S, uint32_t r, int c2) {
 //   IT_PREFILL: members get their first token (TTFT stamps, thinker's
 //               streaming delivery to the talker) and finish or join Run;
 //   IT_FINISH:  decode members that produced their last token finish c.
+template <bool G>
 __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, const uint32_t *mem) {
   const KModel &m = S.A->m;
   const ModelLds &ml = S.sh->ml;
   const bool gated = S.si.flags[si] & SF_GATED;
-  const uint32_t iter_s = S.si.iter[si];
+  const int lx = (G && kind != IT_PREFILL) ? 0 : lx_of<G>(S.si, si);  // LLM fields: prefill only
+  const uint32_t iter_s = S.si.iter[lx];
   const double now = S.now;
   for (int b = 0; b < n; b += 64) {
     const int j = b + lane_id();
@@ -685,16 +701,16 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, cons
     // running-set appends (prefill), in member order
     const uint64_t abal = __ballot(append);
     if (abal) {
-      const int rn = S.si.rn[si];
+      const int rn = S.si.rn[lx];
       if (append) {
         const int pos = rn + (int)lanes_below(abal);
-        S.run_r[S.si.roff[si] + pos] = r;
-        S.run_k[S.si.roff[si] + pos] = key;
+        S.run_r[S.si.roff[lx] + pos] = r;
+        S.run_k[S.si.roff[lx] + pos] = key;
       }
-      S.si.rn[si] = rn + __popcll(abal);
+      S.si.rn[lx] = rn + __popcll(abal);
       if (!gated) {
         const uint32_t mn = ru(wave_min_u(append ? key : kNone));
-        if (mn < S.si.minfin[si]) S.si.minfin[si] = mn;
+        if (mn < S.si.minfin[lx]) S.si.minfin[lx] = mn;
       }
     }
     // queue appends per ready component, in member order
@@ -750,10 +766,11 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
   WaveShared &sh = *S.sh;
   double dur;
   int nmem = 0;
+  const int lx = (G && !(S.si.flags[si] & SF_LLM)) ? 0 : lx_of<G>(S.si, si);
   if (kind != IT_DECODE) {
     const int qn = S.si.qn[si];
     const int beff = S.si.beff[si];
-    const int room = kind == IT_PREFILL ? beff - S.si.rn[si] : beff;
+    const int room = kind == IT_PREFILL ? beff - S.si.rn[lx] : beff;
     const int n = qn < room ? qn : room;
     uint32_t *dst = S.mem + (size_t)x * CF_MAX_BATCH;
     q_pop(S, si, n, dst);
@@ -772,34 +789,35 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     }
     nmem = n;
   } else if (!(S.si.flags[si] & SF_GATED)) {
-    const int rn = S.si.rn[si];
+    const int rn = S.si.rn[lx];
     dur = m.d0[c] + m.d1[c] * (double)rn;
     nmem = rn;
     // Decode run: while no input reaches this executor, its next steps are
     // decode steps of this stage with the same members, so the end of every
     // step follows by repeated addition.  Run to the first finishing step; an
     // input reaching the executor earlier cuts the run (cut_run).
-    const uint32_t it0 = S.si.iter[si];
+    const uint32_t it0 = S.si.iter[lx];
     uint32_t itgt = it0 + 1u;
     double tend = S.now + dur;
     if constexpr (G) {
       // k_fine<true>: runs also stop at bound; a thinker stage records the
       // predicted end of every step of the run in its ring
       const bool thk = S.si.flags[si] & SF_THINKER;
-      double *h = S.hist + (size_t)(thk ? S.si.hist[si] : 0) * kRing;
+      const int slot = thk ? S.si.hist[lx] : 0;
+      double *h = S.hist + (size_t)slot * kRing;
       if (thk && lane_id() == 0) h[itgt & (kRing - 1)] = tend;
       if (lazy && dur > 0.0) {
-        const uint32_t fin = S.si.minfin[si] < bound ? S.si.minfin[si] : bound;
+        const uint32_t fin = S.si.minfin[lx] < bound ? S.si.minfin[lx] : bound;
         while (itgt < fin && itgt - it0 < 65536u) {
           tend = tend + dur;
           itgt++;
           if (thk && lane_id() == 0) h[itgt & (kRing - 1)] = tend;
         }
       }
-      if (thk) S.si.sched[si] = itgt;
+      if (thk) S.si.sched[slot] = itgt;
     } else {
       if (lazy && dur > 0.0) {
-        const uint32_t fin = S.si.minfin[si];
+        const uint32_t fin = S.si.minfin[lx];
         while (itgt < fin && itgt - it0 < 65536u) {
           tend = tend + dur;
           itgt++;
@@ -815,9 +833,9 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     return;
   } else {
     // gated stage: mark the eligible running requests
-    const int rn = S.si.rn[si];
-    uint32_t *rr = S.run_r + S.si.roff[si];
-    uint32_t *rk = S.run_k + S.si.roff[si];
+    const int rn = S.si.rn[lx];
+    uint32_t *rr = S.run_r + S.si.roff[lx];
+    uint32_t *rk = S.run_k + S.si.roff[lx];
     uint32_t cntm = 0;
     bool undecided = false;
     for (int b = 0; b < rn; b += 64) {
@@ -836,14 +854,15 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     nmem = (int)cntm;
     if constexpr (G) {
       if (S.si.flags[si] & SF_THINKER) {  // a gated stage that is also a gate source
-        const uint32_t it1 = S.si.iter[si] + 1u;
-        if (lane_id() == 0) S.hist[(size_t)S.si.hist[si] * kRing + (it1 & (kRing - 1))] = S.now + dur;
-        S.si.sched[si] = it1;
+        const uint32_t it1 = S.si.iter[lx] + 1u;
+        const int slot = S.si.hist[lx];
+        if (lane_id() == 0) S.hist[(size_t)slot * kRing + (it1 & (kRing - 1))] = S.now + dur;
+        S.si.sched[slot] = it1;
       }
     }
   }
   sh.ex_tend[x] = S.now + dur;
-  sh.ex_itgt[x] = S.si.iter[si] + 1u;
+  sh.ex_itgt[x] = S.si.iter[lx] + 1u;
   sh.ex_st[x] = (sh.ex_st[x] & 2u) | 1u | ((uint32_t)kind << 2) | ((uint32_t)l << 4) | ((uint32_t)l << 8) |
                 ((uint32_t)nmem << 12);
 }
@@ -853,12 +872,13 @@ __device__ int runnable_kind(Sim &S, int x, int si, int c) {
   const uint8_t fl = S.si.flags[si];
   const int qn = S.si.qn[si];
   if (!(fl & SF_LLM)) return qn > 0 ? IT_BATCH : -1;
-  const int rn = S.si.rn[si];
+  const int lx = lx_of<G>(S.si, si);
+  const int rn = S.si.rn[lx];
   if (qn > 0 && rn < (int)S.si.beff[si]) return IT_PREFILL;
   if (rn == 0) return -1;
   if (!(fl & SF_GATED)) return IT_DECODE;
-  const uint32_t *rr = S.run_r + S.si.roff[si];
-  const uint32_t *rk = S.run_k + S.si.roff[si];
+  const uint32_t *rr = S.run_r + S.si.roff[lx];
+  const uint32_t *rk = S.run_k + S.si.roff[lx];
   bool any = false, undecided = false;
   for (int b = 0; b < rn && !any; b += 64) {
     const int j = b + lane_id();
@@ -879,9 +899,10 @@ __device__ __forceinline__ uint32_t local_gate_bound(const Sim &S, int x, int si
   uint32_t qmin = kNone;
   for (int g = first; g < first + ns; g++) {
     if (!(S.si.flags[g] & SF_GATED)) continue;
-    const int c = S.si.comp[g], rn = S.si.rn[g];
-    const uint32_t *rr = S.run_r + S.si.roff[g];
-    const uint32_t *rk = S.run_k + S.si.roff[g];
+    const int lg = S.si.lsi[g];
+    const int c = S.si.comp[g], rn = S.si.rn[lg];
+    const uint32_t *rr = S.run_r + S.si.roff[lg];
+    const uint32_t *rk = S.run_k + S.si.roff[lg];
     for (int b = 0; b < rn; b += 64) {
       const int j = b + lane_id();
       if (j < rn) {
@@ -918,7 +939,8 @@ __device__ void try_start(Sim &S, int x) {
       uint32_t bound = kNone;
       const uint8_t fl = S.si.flags[si];
       const uint8_t no_run = G ? SF_GATED : (SF_THINKER | SF_GATED);
-      if (kind == IT_DECODE && !(fl & no_run) && (S.si.qn[si] == 0 || S.si.rn[si] >= (int)S.si.beff[si])) {
+      if (kind == IT_DECODE && !(fl & no_run) &&
+          (S.si.qn[si] == 0 || S.si.rn[lx_of<G>(S.si, si)] >= (int)S.si.beff[si])) {
         lazy = true;  // ... unless a stage checked after this one has work
         for (int i2 = i + 1; i2 < ns && lazy; i2++) {
           const int l2 = (rr == 15) ? i2 : (rr + 1 + i2) % ns;
@@ -926,7 +948,7 @@ __device__ void try_start(Sim &S, int x) {
         }
         if constexpr (G) {
           if (lazy && (fl & SF_THINKER)) {
-            bound = S.si.iter[si] + kThRun;
+            bound = S.si.iter[S.si.lsi[si]] + kThRun;
             if ((S.ta_exec_mask >> x) & 1ull) {
               const uint32_t q = local_gate_bound(S, x, si);
               bound = q < bound ? q : bound;
@@ -936,7 +958,7 @@ __device__ void try_start(Sim &S, int x) {
       }
       start_iter<G>(S, x, l, si, S.si.comp[si], kind, lazy, bound);
       if constexpr (G) {
-        if ((fl & SF_THINKER) && kind == IT_DECODE) notify(S, si);
+        if ((fl & SF_THINKER) && kind == IT_DECODE) notify(S, S.si.hist[S.si.lsi[si]]);
       }
       return;
     }
@@ -951,7 +973,8 @@ __device__ void cut_run(Sim &S, int x) {
   const uint32_t st = sh.ex_st[x];
   if (!(st & EX_RUN) || !(sh.ex_tend[x] > S.now)) return;
   const int si = sh.ex_first[x] + ((st >> 8) & 15u);
-  const uint32_t it0 = S.si.iter[si];
+  const int lx = lx_of<G>(S.si, si);
+  const uint32_t it0 = S.si.iter[lx];
   const uint32_t itgt = sh.ex_itgt[x];
   const double dur = sh.ex_dur[x];
   double t = sh.ex_t0[x] + dur;
@@ -965,8 +988,9 @@ __device__ void cut_run(Sim &S, int x) {
   if (j <= it0 + 1u) sh.ex_st[x] = st & ~EX_RUN;
   if constexpr (G) {
     if ((S.si.flags[si] & SF_THINKER) && j < itgt) {
-      S.si.sched[si] = j;
-      notify(S, si);
+      const int slot = S.si.hist[lx];
+      S.si.sched[slot] = j;
+      notify(S, slot);
     }
   }
 }
@@ -976,10 +1000,12 @@ __device__ __forceinline__ void thinker_tick(Sim &S) {
 }
 
 // compacts stage si's running slots, dropping the lanes flagged in drop[]
+template <bool G>
 __device__ void run_compact(Sim &S, int si, const bool *drop) {
-  const int rn = S.si.rn[si];
-  uint32_t *rr = S.run_r + S.si.roff[si];
-  uint32_t *rk = S.run_k + S.si.roff[si];
+  const int lx = lx_of<G>(S.si, si);
+  const int rn = S.si.rn[lx];
+  uint32_t *rr = S.run_r + S.si.roff[lx];
+  uint32_t *rk = S.run_k + S.si.roff[lx];
   uint32_t vr[CF_MAX_BATCH / 64], vk[CF_MAX_BATCH / 64];
   bool keep[CF_MAX_BATCH / 64];
 #pragma unroll
@@ -1008,15 +1034,17 @@ __device__ void run_compact(Sim &S, int si, const bool *drop) {
     w += (uint32_t)__popcll(bal);
   }
   __syncthreads();
-  S.si.rn[si] = (int)w;
-  if (!(S.si.flags[si] & SF_GATED)) S.si.minfin[si] = ru(wave_min_u(mn));
+  S.si.rn[lx] = (int)w;
+  if (!(S.si.flags[si] & SF_GATED)) S.si.minfin[lx] = ru(wave_min_u(mn));
 }
 
 // collects the running slots flagged in fin[] (slot order) into mem,
 // processes them as finishing members, and drops them from the running set
+template <bool G>
 __device__ void finish_slots(Sim &S, int x, int si, int c, const bool *fin) {
-  const int rn = S.si.rn[si];
-  const uint32_t *rr = S.run_r + S.si.roff[si];
+  const int lx = lx_of<G>(S.si, si);
+  const int rn = S.si.rn[lx];
+  const uint32_t *rr = S.run_r + S.si.roff[lx];
   uint32_t *mem = S.mem + (size_t)x * CF_MAX_BATCH;
   uint32_t nf = 0;
 #pragma unroll
@@ -1028,8 +1056,8 @@ __device__ void finish_slots(Sim &S, int x, int si, int c, const bool *fin) {
     nf += (uint32_t)__popcll(bal);
   }
   __syncthreads();
-  members_done(S, x, si, c, IT_FINISH, (int)nf, mem);
-  run_compact(S, si, fin);
+  members_done<G>(S, x, si, c, IT_FINISH, (int)nf, mem);
+  run_compact<G>(S, si, fin);
 }
 
 template <bool G>
@@ -1045,31 +1073,32 @@ __device__ void complete_iter(Sim &S, int x) {
   S.dirty |= 1ull << x;
   if (kind == IT_BATCH || kind == IT_PREFILL) {
     S.events += (uint64_t)nmem;
-    members_done(S, x, si, c, kind, nmem, S.mem + (size_t)x * CF_MAX_BATCH);
+    members_done<G>(S, x, si, c, kind, nmem, S.mem + (size_t)x * CF_MAX_BATCH);
     if constexpr (!G) {
       if (fl & SF_THINKER) thinker_tick(S);
     }
     return;
   }
-  const int rn = S.si.rn[si];
-  const uint32_t it0 = S.si.iter[si];
+  const int lx = lx_of<G>(S.si, si);
+  const int rn = S.si.rn[lx];
+  const uint32_t it0 = S.si.iter[lx];
   const uint32_t it = (fl & SF_GATED) ? it0 + 1u : sh.ex_itgt[x];
-  S.si.iter[si] = it;  // k_fine<true>: a thinker's ring already holds the end of these steps
+  S.si.iter[lx] = it;  // k_fine<true>: a thinker's ring already holds the end of these steps
   if constexpr (!G) {
     if ((fl & SF_THINKER) && lane_id() == 0) S.hist[(size_t)S.si.hist[si] * kHist + (it & (kHist - 1))] = S.now;
   }
-  const uint32_t *rr = S.run_r + S.si.roff[si];
-  uint32_t *rk = S.run_k + S.si.roff[si];
+  const uint32_t *rr = S.run_r + S.si.roff[lx];
+  uint32_t *rk = S.run_k + S.si.roff[lx];
   if (!(fl & SF_GATED)) {
     S.events += (uint64_t)rn * (uint64_t)(it - it0);
-    if (it == S.si.minfin[si]) {
+    if (it == S.si.minfin[lx]) {
       bool fin[CF_MAX_BATCH / 64];
 #pragma unroll
       for (int p = 0; p < CF_MAX_BATCH / 64; p++) {
         const int j = p * 64 + lane_id();
         fin[p] = j < rn && rk[j] == it;
       }
-      finish_slots(S, x, si, c, fin);
+      finish_slots<G>(S, x, si, c, fin);
     }
   } else {
     // gated decode step: every marked slot gains one token
@@ -1095,7 +1124,7 @@ __device__ void complete_iter(Sim &S, int x) {
     bool anyf = false;
 #pragma unroll
     for (int p = 0; p < CF_MAX_BATCH / 64; p++) anyf |= __ballot(fin[p]) != 0;
-    if (anyf) finish_slots(S, x, si, c, fin);
+    if (anyf) finish_slots<G>(S, x, si, c, fin);
   }
   if constexpr (!G) {
     if (fl & SF_THINKER) thinker_tick(S);
@@ -1118,9 +1147,10 @@ __device__ __forceinline__ bool gate_wake(Sim &S, int y) {
     bool undecided = false;
     for (int g = first; g < first + ns; g++) {
       if (!(S.si.flags[g] & SF_GATED)) continue;
-      const int c = S.si.comp[g], rn = S.si.rn[g];
-      const uint32_t *rr = S.run_r + S.si.roff[g];
-      const uint32_t *rk = S.run_k + S.si.roff[g];
+      const int lg = S.si.lsi[g];
+      const int c = S.si.comp[g], rn = S.si.rn[lg];
+      const uint32_t *rr = S.run_r + S.si.roff[lg];
+      const uint32_t *rk = S.run_k + S.si.roff[lg];
       for (int b = 0; b < rn; b += 64) {
         const int j = b + lane_id();
         if (j < rn) {
@@ -1193,7 +1223,7 @@ __device__ bool setup_plan(Sim &S, int p) {
     return true;
   }
   // capacities of the running slots and thinker rings
-  int run_need = 0, ring_need = 0;
+  int run_need = 0, ring_need = 0, llm_need = 0;
   uint64_t ta_mask = 0;
   for (int v = 0; v < nv; v++) {
     const uint32_t cm = sh.vcomp[v];
@@ -1204,12 +1234,21 @@ __device__ bool setup_plan(Sim &S, int p) {
       cc &= cc - 1;
       if (m.kind[c] == CF_LLM) run_need += sh.vrep[v] * (sh.vbatch[v] < m.cap[c] ? sh.vbatch[v] : m.cap[c]);
       if ((m.gate_src_mask >> c) & 1u) ring_need += sh.vrep[v];
+      if constexpr (G) {
+        if (m.kind[c] == CF_LLM) llm_need += sh.vrep[v];
+      }
     }
   }
   S.ta_exec_mask = ta_mask;
   if (run_need > A.L.run_cap || ring_need > A.L.hist_slots) {
     S.status |= CF_ST_OVERFLOW;
     return true;
+  }
+  if constexpr (G) {
+    if (llm_need > A.nl_cap || ring_need > A.nt_cap) {
+      S.status |= CF_ST_OVERFLOW;
+      return true;
+    }
   }
   // executors, one lane each
   if (lane < S.nx) {
@@ -1231,7 +1270,7 @@ __device__ bool setup_plan(Sim &S, int p) {
   }
   if constexpr (G) S.rewake = 0;
   // stage instances, one lane each (prefix sums give run-slot and ring offsets)
-  int roff_carry = 0, hs_carry = 0;
+  int roff_carry = 0, hs_carry = 0, l_carry = 0;
   for (int s0 = 0; s0 < nsi; s0 += 64) {
     const int s = s0 + lane;
     int c = 0, beff = 0;
@@ -1251,9 +1290,10 @@ __device__ bool setup_plan(Sim &S, int p) {
       llm = m.kind[c] == CF_LLM;
       thk = (m.gate_src_mask >> c) & 1u;
     }
-    uint32_t tot_r, tot_h;
+    uint32_t tot_r, tot_h, tot_l = 0, lo = 0;
     const uint32_t ro = wave_excl_scan(llm ? (uint32_t)beff : 0u, tot_r);
     const uint32_t ho = wave_excl_scan(thk ? 1u : 0u, tot_h);
+    if constexpr (G) lo = wave_excl_scan(llm ? 1u : 0u, tot_l);
     if (s < nsi) {
       S.si.comp[s] = (uint8_t)c;
       S.si.flags[s] = (uint8_t)((llm ? SF_LLM : 0) | (((m.gated_mask >> c) & 1u) ? SF_GATED : 0) |
@@ -1265,18 +1305,31 @@ __device__ bool setup_plan(Sim &S, int p) {
       S.si.qtc[s] = -1;
       S.si.qhp[s] = 0;
       S.si.qtp[s] = 0;
-      S.si.rn[s] = 0;
-      S.si.iter[s] = 0;
-      S.si.minfin[s] = kNone;
-      S.si.roff[s] = roff_carry + (int)ro;
-      S.si.hist[s] = thk ? (int16_t)(hs_carry + (int)ho) : (int16_t)-1;
       if constexpr (G) {
-        S.si.sched[s] = 0;
-        S.si.watch[s] = 0;
+        const int ls = l_carry + (int)lo, slot = hs_carry + (int)ho;
+        S.si.lsi[s] = llm ? (uint16_t)ls : (uint16_t)0xFFFFu;
+        if (llm) {
+          S.si.rn[ls] = 0;
+          S.si.iter[ls] = 0;
+          S.si.minfin[ls] = kNone;
+          S.si.roff[ls] = roff_carry + (int)ro;
+          S.si.hist[ls] = thk ? (int16_t)slot : (int16_t)-1;
+        }
+        if (thk) {
+          S.si.sched[slot] = 0;
+          S.si.watch[slot] = 0;
+        }
+      } else {
+        S.si.rn[s] = 0;
+        S.si.iter[s] = 0;
+        S.si.minfin[s] = kNone;
+        S.si.roff[s] = roff_carry + (int)ro;
+        S.si.hist[s] = thk ? (int16_t)(hs_carry + (int)ho) : (int16_t)-1;
       }
     }
     roff_carry += (int)tot_r;
     hs_carry += (int)tot_h;
+    if constexpr (G) l_carry += (int)tot_l;
   }
   __syncthreads();
   return true;
@@ -1296,23 +1349,40 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
   {
     const int cap = A.nsi_cap;
     char *p = dyn_lds;
-    S.si.qhc = (int *)p; p += 4 * cap;
-    S.si.qtc = (int *)p; p += 4 * cap;
-    S.si.qn = (int *)p; p += 4 * cap;
-    S.si.roff = (int *)p; p += 4 * cap;
-    S.si.rn = (int *)p; p += 4 * cap;
-    S.si.iter = (uint32_t *)p; p += 4 * cap;
-    S.si.minfin = (uint32_t *)p; p += 4 * cap;
-    S.si.beff = (uint16_t *)p; p += 2 * cap;
-    S.si.hist = (int16_t *)p; p += 2 * cap;
-    S.si.comp = (uint8_t *)p; p += cap;
-    S.si.flags = (uint8_t *)p; p += cap;
-    S.si.qhp = (uint8_t *)p; p += cap;
-    S.si.qtp = (uint8_t *)p; p += cap;
     if constexpr (G) {
-      // cap is a multiple of 64 and the static LDS a multiple of 8 bytes: 8-byte aligned
-      S.si.sched = (uint32_t *)p; p += 4 * cap;
-      S.si.watch = (uint64_t *)p;
+      // 8-byte words first: cap, nl_cap and nt_cap are multiples of 64 and the
+      // static LDS a multiple of 8 bytes, so every array is aligned
+      const int lcap = A.nl_cap, tcap = A.nt_cap;
+      S.si.watch = (uint64_t *)p; p += 8 * tcap;
+      S.si.qhc = (int *)p; p += 4 * cap;
+      S.si.qtc = (int *)p; p += 4 * cap;
+      S.si.qn = (int *)p; p += 4 * cap;
+      S.si.roff = (int *)p; p += 4 * lcap;
+      S.si.rn = (int *)p; p += 4 * lcap;
+      S.si.iter = (uint32_t *)p; p += 4 * lcap;
+      S.si.minfin = (uint32_t *)p; p += 4 * lcap;
+      S.si.sched = (uint32_t *)p; p += 4 * tcap;
+      S.si.beff = (uint16_t *)p; p += 2 * cap;
+      S.si.lsi = (uint16_t *)p; p += 2 * cap;
+      S.si.hist = (int16_t *)p; p += 2 * lcap;
+      S.si.comp = (uint8_t *)p; p += cap;
+      S.si.flags = (uint8_t *)p; p += cap;
+      S.si.qhp = (uint8_t *)p; p += cap;
+      S.si.qtp = (uint8_t *)p; p += cap;
+    } else {
+      S.si.qhc = (int *)p; p += 4 * cap;
+      S.si.qtc = (int *)p; p += 4 * cap;
+      S.si.qn = (int *)p; p += 4 * cap;
+      S.si.roff = (int *)p; p += 4 * cap;
+      S.si.rn = (int *)p; p += 4 * cap;
+      S.si.iter = (uint32_t *)p; p += 4 * cap;
+      S.si.minfin = (uint32_t *)p; p += 4 * cap;
+      S.si.beff = (uint16_t *)p; p += 2 * cap;
+      S.si.hist = (int16_t *)p; p += 2 * cap;
+      S.si.comp = (uint8_t *)p; p += cap;
+      S.si.flags = (uint8_t *)p; p += cap;
+      S.si.qhp = (uint8_t *)p; p += cap;
+      S.si.qtp = (uint8_t *)p; p += cap;
     }
   }
   if constexpr (G) {
@@ -1485,20 +1555,32 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
 }
 
 __global__ void k_fine_reset(unsigned int *ticket) { *ticket = 0u; }
+__global__ void k_fine_reset3(unsigned int *v) {
+  v[0] = 0u;
+  v[1] = 0u;
+  v[2] = 0u;
+}
 
-// stage instances of the largest selected plan (malformed plans are skipped)
+// stage instances, LLM stage instances and gate-source stage instances of
+// the largest selected plans (out[0..2]; malformed plans are skipped)
 __global__ void k_max_si(const uint8_t *n_nodes, const uint8_t *node_comp, const uint8_t *node_rep, int P,
-                         const int32_t *ids, int n, unsigned int *out) {
+                         const int32_t *ids, int n, uint32_t llm_mask, uint32_t src_mask, unsigned int *out) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const int p = ids[i];
   if (p < 0 || p >= P) return;
   const int nv = n_nodes[p];
   if (nv < 1 || nv > CF_MAX_NODES) return;
-  unsigned int nsi = 0;
-  for (int v = 0; v < nv; v++)
-    nsi += (unsigned int)node_rep[(size_t)v * P + p] * (unsigned int)__popc(node_comp[(size_t)v * P + p]);
+  unsigned int nsi = 0, nl = 0, nt = 0;
+  for (int v = 0; v < nv; v++) {
+    const unsigned int rep = node_rep[(size_t)v * P + p], cm = node_comp[(size_t)v * P + p];
+    nsi += rep * (unsigned int)__popc(cm);
+    nl += rep * (unsigned int)__popc(cm & llm_mask);
+    nt += rep * (unsigned int)__popc(cm & src_mask);
+  }
   atomicMax(out, nsi < (unsigned)kMaxSI ? nsi : (unsigned)kMaxSI);
+  atomicMax(out + 1, nl < (unsigned)kMaxSI ? nl : (unsigned)kMaxSI);
+  atomicMax(out + 2, nt < (unsigned)kMaxSI ? nt : (unsigned)kMaxSI);
 }
 
 Layout make_layout(const KModel &m, int n) {
@@ -1615,17 +1697,24 @@ extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_tabl
   a.slab = scr + hdr;
   hipStream_t s = as_stream(stream);
   // size the LDS stage table from the largest selected plan
-  hipLaunchKernelGGL(k_fine_reset, dim3(1), dim3(1), 0, s, max_si);
+  uint32_t llm_mask = 0;
+  for (int c = 0; c < a.m.nc; c++)
+    if (a.m.kind[c] == CF_LLM) llm_mask |= 1u << c;
+  hipLaunchKernelGGL(k_fine_reset3, dim3(1), dim3(1), 0, s, max_si);
   hipLaunchKernelGGL(k_max_si, dim3((unsigned)((n_plans + 255) / 256)), dim3(256), 0, s, a.n_nodes, a.node_comp,
-                     a.node_rep, a.P, plan_ids_dev, n_plans, max_si);
-  unsigned int nsi = 0;
-  st = hip_check(hipMemcpyAsync(&nsi, max_si, sizeof nsi, hipMemcpyDeviceToHost, s), "copy stage count");
+                     a.node_rep, a.P, plan_ids_dev, n_plans, llm_mask, (uint32_t)a.m.gate_src_mask, max_si);
+  unsigned int caps[3] = {0, 0, 0};
+  st = hip_check(hipMemcpyAsync(caps, max_si, sizeof caps, hipMemcpyDeviceToHost, s), "copy stage count");
   if (st != CF_OK) return st;
   st = hip_check(hipStreamSynchronize(s), "stage count sync");
   if (st != CF_OK) return st;
-  a.nsi_cap = (int)((nsi + 63u) & ~63u);
-  if (a.nsi_cap < 64) a.nsi_cap = 64;
-  const size_t lds = (a.m.gated_mask ? kSiBytesGated : kSiBytes) * (size_t)a.nsi_cap;
+  auto round64 = [](unsigned int v) { return v < 64u ? 64 : (int)((v + 63u) & ~63u); };
+  a.nsi_cap = round64(caps[0]);
+  a.nl_cap = round64(caps[1]);
+  a.nt_cap = round64(caps[2]);
+  const size_t lds = a.m.gated_mask ? kSiBytesG * (size_t)a.nsi_cap + kLlmBytesG * (size_t)a.nl_cap +
+                                          kThBytesG * (size_t)a.nt_cap
+                                    : kSiBytes * (size_t)a.nsi_cap;
   st = hip_check(hipMemcpyAsync(args_dev, &a, sizeof a, hipMemcpyHostToDevice, s), "copy fine args");
   if (st != CF_OK) return st;
   hipLaunchKernelGGL(k_fine_reset, dim3(1), dim3(1), 0, s, a.ticket);

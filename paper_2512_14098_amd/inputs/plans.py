@@ -33,6 +33,7 @@ GPU budget, batches from the knob set, routing weights in tenths.
 import hashlib
 import itertools
 import os
+import sys
 
 import numpy as np
 
@@ -148,7 +149,7 @@ def _canon(pl):
     return (tuple(parts), routes)
 
 
-def _sample(model, spec, gpus, have, total):
+def _sample(model, spec, gpus, have, total, progress=True):
     """Seeded mixed / compound plans until ``total`` distinct plans exist."""
     names, idx, paths, edges = _model_index(model)
     T, C = len(paths), len(names)
@@ -160,7 +161,10 @@ def _sample(model, spec, gpus, have, total):
     out = []
     seen = set(_canon(p) for p in have)
     tries = 0
+    step = max(total // 10, 1)
     while len(have) + len(out) < total:
+        if total >= 200000 and (len(have) + len(out)) % step == 0 and len(out) and tries and progress:
+            print("plans: %d of %d sampled" % (len(have) + len(out), total), file=sys.stderr, flush=True)
         tries += 1
         if tries > 50 * total + 1000:
             raise RuntimeError("plan sampler could not reach the requested count")
@@ -220,8 +224,9 @@ def _sample(model, spec, gpus, have, total):
         reps = [1] * V
         extra = gpus - V
         k = int(rng.integers(0, extra + 1))
-        for _ in range(k):
-            reps[int(rng.integers(0, V))] += 1
+        if k:  # k draws of the node that gets one more replica (one vector draw: same stream)
+            for v, more in enumerate(np.bincount(rng.integers(0, V, size=k), minlength=V).tolist()):
+                reps[v] += more
         batch = []
         for mask in nodes:
             first = (mask & -mask).bit_length() - 1
