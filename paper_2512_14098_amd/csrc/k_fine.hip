@@ -68,6 +68,9 @@ constexpr uint32_t MISC_OUTS = 15u;     // outputs still to finish
 constexpr uint32_t MISC_TH_DONE = 16u;  // thinker finished
 constexpr uint32_t MARK = 0x80000000u;  // gated running slot: in the current decode step
 constexpr uint32_t EX_RUN = 1u << 21;   // executor state: busy with a multi-step decode run
+// k_fine<true>: executor state kind of a joint thinker/talker run (IT_FINISH
+// is a member kind only); the talker's stage index is in bits 22..25
+constexpr uint32_t IT_JOINT = 3;
 // stage flags
 constexpr uint8_t SF_LLM = 1, SF_GATED = 2, SF_THINKER = 4, SF_ENC = 8, SF_GEN = 16;
 
@@ -252,6 +255,7 @@ struct Sim {
   bool remote_gate;
   // k_fine<true>
   double *wake;        // per executor with a gated stage: next visibility time of a blocked request
+  double *dur2;        // per executor in a joint run: duration of its talker steps
   uint64_t rewake;     // executors whose wake time is to be recomputed in this instant
 };
 
@@ -890,17 +894,31 @@ __device__ int runnable_kind(Sim &S, int x, int si, int c) {
   return any ? IT_DECODE : -1;
 }
 
-// k_fine<true>: first step, after the thinker stage si's current one, whose
-// token a blocked request of a gated stage on the same executor x waits for
-// (the gated stages of x have no eligible request when this is called)
-__device__ __forceinline__ uint32_t local_gate_bound(const Sim &S, int x, int si) {
+// k_fine<true>: what the gated stages on executor x wait for, seen from the
+// thinker stage si on x, called when none of their running requests is
+// eligible.  qmin: the first step of si whose token a request whose thinker
+// is si waits for.  joint: exactly one gated stage (gsi) has running
+// requests, all of them wait for the next step of si; kta then receives the
+// talker steps before its first request finishes.
+struct GateView {
+  uint32_t qmin, kta;
+  int gsi;
+  bool joint;
+};
+__device__ __forceinline__ GateView local_gate_view(const Sim &S, int x, int si) {
   const int ns = S.sh->ex_ns[x], first = S.sh->ex_first[x];
   const int cth = S.si.comp[si];
-  uint32_t qmin = kNone;
+  const uint32_t next = S.si.iter[S.si.lsi[si]] + 1u;
+  uint32_t qmin = kNone, kta = kNone;
+  int gsi = -1, nbusy = 0;
+  bool other = false;  // a running request that does not wait for the next step of si
   for (int g = first; g < first + ns; g++) {
     if (!(S.si.flags[g] & SF_GATED)) continue;
     const int lg = S.si.lsi[g];
     const int c = S.si.comp[g], rn = S.si.rn[lg];
+    if (rn == 0) continue;
+    nbusy++;
+    gsi = g;
     const uint32_t *rr = S.run_r + S.si.roff[lg];
     const uint32_t *rk = S.run_k + S.si.roff[lg];
     for (int b = 0; b < rn; b += 64) {
@@ -909,23 +927,72 @@ __device__ __forceinline__ uint32_t local_gate_bound(const Sim &S, int x, int si
         const uint32_t r = rr[j];
         const Rec R = S.rec[r];
         const int t = rtype(R.misc);
+        const uint32_t tok = rk[j] & 0xFFFFu;
+        bool waits_next = false;
         if (S.sh->ml.ta_c[t] == c && S.sh->ml.th_c[t] == cth && ex_byte(R.ex, cth) == x) {
           const uint32_t nth = nout_of(S, r, t, cth);
-          const uint32_t tok = rk[j] & 0xFFFFu;
           const uint32_t k = tok + 1u < nth ? tok + 1u : nth;
           if (k > 1u && !((R.misc & MISC_TH_DONE) && k == nth)) {
             const uint32_t q = S.thjoin[r] + k - 1u;
             qmin = q < qmin ? q : qmin;
+            waits_next = q == next;
           }
         }
+        other |= !waits_next;
+        const uint32_t left = nout_of(S, r, t, c) - tok;
+        kta = left < kta ? left : kta;
       }
     }
   }
-  return ru(wave_min_u(qmin));
+  GateView v;
+  v.qmin = ru(wave_min_u(qmin));
+  v.kta = ru(wave_min_u(kta));
+  v.gsi = gsi;
+  v.joint = nbusy == 1 && __ballot(other) == 0;
+  return v;
+}
+
+// k_fine<true>: joint run of thinker stage sth (index lth on x) and gated
+// stage sta.  With no other stage runnable and every talker request waiting
+// for the thinker's next token on this executor, the executor alternates a
+// thinker decode step and a talker decode step over all its running
+// requests, so every step end follows by alternately adding the two step
+// durations.  The run stops at the first step with a finishing request of
+// either stage; an input cuts it (cut_run).  Returns false (nothing started)
+// for steps of zero duration.
+__device__ __forceinline__ bool start_joint(Sim &S, int x, int lth, int sth, int sta, uint32_t kta) {
+  const KModel &m = S.A->m;
+  WaveShared &sh = *S.sh;
+  const int cth = S.si.comp[sth], cta = S.si.comp[sta];
+  const int lx = S.si.lsi[sth], lg = S.si.lsi[sta];
+  const double d1 = m.d0[cth] + m.d1[cth] * (double)S.si.rn[lx];
+  const double d2 = m.d0[cta] + m.d1[cta] * (double)S.si.rn[lg];
+  if (!(d1 > 0.0) || !(d2 > 0.0)) return false;
+  const uint32_t it0 = S.si.iter[lx];
+  const uint32_t kth = S.si.minfin[lx] - it0;  // thinker steps up to its first finisher
+  uint32_t n = 2u * (kth < kThRun ? kth : kThRun) - 1u;
+  if (2u * kta < n) n = 2u * kta;
+  const int slot = S.si.hist[lx];
+  double *h = S.hist + (size_t)slot * kRing;
+  double t = S.now;
+  for (uint32_t i = 1; i <= n; i++) {
+    t = t + ((i & 1u) ? d1 : d2);
+    if ((i & 1u) && lane_id() == 0) h[(it0 + ((i + 1u) >> 1)) & (kRing - 1)] = t;
+  }
+  S.si.sched[slot] = it0 + ((n + 1u) >> 1);
+  sh.ex_t0[x] = S.now;
+  sh.ex_dur[x] = d1;
+  S.dur2[x] = d2;
+  sh.ex_itgt[x] = n;  // steps of the run, thinker first
+  sh.ex_tend[x] = t;
+  const uint32_t lta = (uint32_t)(sta - sh.ex_first[x]);
+  sh.ex_st[x] = (sh.ex_st[x] & 2u) | 1u | (IT_JOINT << 2) | ((uint32_t)lth << 4) | ((uint32_t)lth << 8) | EX_RUN |
+                (lta << 22);
+  return true;
 }
 
 template <bool G>
-__device__ void try_start(Sim &S, int x) {
+__device__ __forceinline__ void try_start(Sim &S, int x) {
   WaveShared &sh = *S.sh;
   const uint32_t st = sh.ex_st[x];
   const int ns = sh.ex_ns[x], first = sh.ex_first[x];
@@ -950,8 +1017,12 @@ __device__ void try_start(Sim &S, int x) {
           if (lazy && (fl & SF_THINKER)) {
             bound = S.si.iter[S.si.lsi[si]] + kThRun;
             if ((S.ta_exec_mask >> x) & 1ull) {
-              const uint32_t q = local_gate_bound(S, x, si);
-              bound = q < bound ? q : bound;
+              const GateView gv = local_gate_view(S, x, si);
+              if (gv.joint && start_joint(S, x, l, si, gv.gsi, gv.kta)) {
+                notify(S, S.si.hist[S.si.lsi[si]]);
+                return;
+              }
+              bound = gv.qmin < bound ? gv.qmin : bound;
             }
           }
         }
@@ -973,6 +1044,27 @@ __device__ void cut_run(Sim &S, int x) {
   const uint32_t st = sh.ex_st[x];
   if (!(st & EX_RUN) || !(sh.ex_tend[x] > S.now)) return;
   const int si = sh.ex_first[x] + ((st >> 8) & 15u);
+  if constexpr (G) {
+    if (((st >> 2) & 3u) == IT_JOINT) {
+      const uint32_t n = sh.ex_itgt[x];
+      const double d1 = sh.ex_dur[x], d2 = S.dur2[x];
+      double t = sh.ex_t0[x] + d1;
+      uint32_t j = 1;
+      while (t < S.now && j < n) {
+        j++;
+        t = t + ((j & 1u) ? d1 : d2);
+      }
+      sh.ex_tend[x] = t;
+      sh.ex_itgt[x] = j;
+      if (j < n) {
+        const int lx = S.si.lsi[si];
+        const int slot = S.si.hist[lx];
+        S.si.sched[slot] = S.si.iter[lx] + ((j + 1u) >> 1);
+        notify(S, slot);
+      }
+      return;
+    }
+  }
   const int lx = lx_of<G>(S.si, si);
   const uint32_t it0 = S.si.iter[lx];
   const uint32_t itgt = sh.ex_itgt[x];
@@ -1060,11 +1152,77 @@ __device__ void finish_slots(Sim &S, int x, int si, int c, const bool *fin) {
   run_compact<G>(S, si, fin);
 }
 
+// k_fine<true>: end of a joint run of n steps (thinker first): the thinker
+// stage advanced (n + 1) / 2 steps and every running talker request gained
+// n / 2 tokens; the stage of the last step resumes the round robin and its
+// finishing requests finish.
+__device__ __forceinline__ void complete_joint(Sim &S, int x, uint32_t st) {
+  WaveShared &sh = *S.sh;
+  const int first = sh.ex_first[x];
+  const int lth = (st >> 8) & 15u, lta = (st >> 22) & 15u;
+  const int sth = first + lth, sta = first + lta;
+  const uint32_t n = sh.ex_itgt[x];
+  const uint32_t nth_s = (n + 1u) >> 1, nta_s = n >> 1;
+  const uint32_t llast = (n & 1u) ? (uint32_t)lth : (uint32_t)lta;
+  sh.ex_st[x] = (st & ~(1u | EX_RUN | (15u << 4) | (15u << 22))) | 2u | (llast << 4);
+  sh.ex_last[x] = S.now;
+  S.dirty |= 1ull << x;
+  // thinker
+  const int lx = S.si.lsi[sth];
+  const int cth = S.si.comp[sth];
+  const int rn = S.si.rn[lx];
+  const uint32_t it = S.si.iter[lx] + nth_s;
+  S.si.iter[lx] = it;
+  S.events += (uint64_t)rn * (uint64_t)nth_s;
+  // talker
+  const int lg = S.si.lsi[sta];
+  const int cta = S.si.comp[sta];
+  const int rng = S.si.rn[lg];
+  const uint32_t *rrg = S.run_r + S.si.roff[lg];
+  uint32_t *rkg = S.run_k + S.si.roff[lg];
+  bool fin[CF_MAX_BATCH / 64];
+#pragma unroll
+  for (int p = 0; p < CF_MAX_BATCH / 64; p++) {
+    const int j = p * 64 + lane_id();
+    fin[p] = false;
+    if (j < rng) {
+      const uint32_t r = rrg[j];
+      const uint32_t tok = (rkg[j] & 0xFFFFu) + nta_s;
+      rkg[j] = tok;
+      fin[p] = !(n & 1u) && tok == nout_of(S, r, rtype(S.rec[r].misc), cta);
+    }
+  }
+  S.events += (uint64_t)rng * (uint64_t)nta_s;
+  __syncthreads();
+  if (n & 1u) {
+    if (it == S.si.minfin[lx]) {
+      const uint32_t *rk = S.run_k + S.si.roff[lx];
+#pragma unroll
+      for (int p = 0; p < CF_MAX_BATCH / 64; p++) {
+        const int j = p * 64 + lane_id();
+        fin[p] = j < rn && rk[j] == it;
+      }
+      finish_slots<true>(S, x, sth, cth, fin);
+    }
+  } else {
+    bool anyf = false;
+#pragma unroll
+    for (int p = 0; p < CF_MAX_BATCH / 64; p++) anyf |= __ballot(fin[p]) != 0;
+    if (anyf) finish_slots<true>(S, x, sta, cta, fin);
+  }
+}
+
 template <bool G>
-__device__ void complete_iter(Sim &S, int x) {
+__device__ __forceinline__ void complete_iter(Sim &S, int x) {
   WaveShared &sh = *S.sh;
   const uint32_t st = sh.ex_st[x];
   const int kind = (st >> 2) & 3u, l = (st >> 8) & 15u, nmem = (st >> 12) & 511u;
+  if constexpr (G) {
+    if (kind == (int)IT_JOINT) {
+      complete_joint(S, x, st);
+      return;
+    }
+  }
   const int si = sh.ex_first[x] + l;
   const int c = S.si.comp[si];
   const uint8_t fl = S.si.flags[si];
@@ -1386,8 +1544,9 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
     }
   }
   if constexpr (G) {
-    __shared__ double wake_lds[CF_MAX_EXEC];
+    __shared__ double wake_lds[CF_MAX_EXEC], dur2_lds[CF_MAX_EXEC];
     S.wake = wake_lds;
+    S.dur2 = dur2_lds;
   }
   // model tables for per-lane indexing
   for (int j = lane; j < CF_MAX_TYPES * CF_MAX_COMP; j += 64) {
