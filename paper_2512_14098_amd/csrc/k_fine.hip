@@ -50,6 +50,7 @@
 #include <string.h>
 
 #include "cf_internal.h"
+#include "cf_run.h"
 
 namespace cf {
 namespace {
@@ -176,32 +177,6 @@ __device__ __forceinline__ uint64_t ru64(uint64_t v) {
 __device__ __forceinline__ double rdb(double v) {
   return __longlong_as_double((long long)ru64((uint64_t)__double_as_longlong(v)));
 }
-__device__ __forceinline__ double wave_min(double v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const double w = __shfl_xor(v, o, 64);
-    v = w < v ? w : v;
-  }
-  return v;
-}
-__device__ __forceinline__ uint32_t wave_min_u(uint32_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const uint32_t w = __shfl_xor(v, o, 64);
-    v = w < v ? w : v;
-  }
-  return v;
-}
-__device__ __forceinline__ uint32_t wave_sum_u(uint32_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-__device__ __forceinline__ uint32_t wave_or_u(uint32_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v |= __shfl_xor(v, o, 64);
-  return v;
-}
 __device__ __forceinline__ uint32_t lanes_below(uint64_t bal) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
 }
@@ -227,15 +202,27 @@ __device__ __forceinline__ double wave_min_time(double t) {
   return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
+// inclusive prefix sum over the lanes through DPP: row_shr 1, 2, 4, 8 scan
+// each row of 16 lanes (identity 0 where the source is out of range), then
+// row_bcast 15 and row_bcast 31 carry the row totals into the later rows.
+// Needs every lane active.
+__device__ __forceinline__ uint32_t dpp_scan_add(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return v;
+}
+// wavefront sum (uniform result)
+__device__ __forceinline__ uint32_t dpp_sum_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)dpp_scan_add(v), 63);
+}
 // exclusive prefix sum of v over the lanes, and the total
 __device__ __forceinline__ uint32_t wave_excl_scan(uint32_t v, uint32_t &total) {
-  uint32_t x = v;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t o = __shfl_up(x, d, 64);
-    if (lane_id() >= d) x += o;
-  }
-  total = ru(__shfl(x, 63, 64));
+  const uint32_t x = dpp_scan_add(v);
+  total = (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
   return x - v;
 }
 
@@ -713,7 +700,7 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, cons
       }
       S.si.rn[lx] = rn + __popcll(abal);
       if (!gated) {
-        const uint32_t mn = ru(wave_min_u(append ? key : kNone));
+        const uint32_t mn = dpp_min_u32(append ? key : kNone);
         if (mn < S.si.minfin[lx]) S.si.minfin[lx] = mn;
       }
     }
@@ -785,7 +772,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
       const int j = b + lane_id();
       xs += (j < n) ? x_of(S, dst[j], sel) : 0u;
     }
-    xs = ru(wave_sum_u(xs));
+    xs = dpp_sum_u32(xs);
     dur = (m.k0[c] + m.k1[c] * (double)xs) + m.k2[c] * (double)n;
     if (S.si.flags[si] & SF_ENC) {
       const bool ran = (sh.ex_st[x] >> 1) & 1u;
@@ -798,34 +785,32 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     nmem = rn;
     // Decode run: while no input reaches this executor, its next steps are
     // decode steps of this stage with the same members, so the end of every
-    // step follows by repeated addition.  Run to the first finishing step; an
-    // input reaching the executor earlier cuts the run (cut_run).
+    // step follows by repeated addition (run_walk).  Run to the first
+    // finishing step; an input reaching the executor earlier cuts the run
+    // (cut_run).
     const uint32_t it0 = S.si.iter[lx];
     uint32_t itgt = it0 + 1u;
-    double tend = S.now + dur;
+    const double t1 = S.now + dur;
+    double tend = t1;
+    uint32_t fin = S.si.minfin[lx];
+    if constexpr (G) fin = fin < bound ? fin : bound;  // k_fine<true>: runs also stop at bound
+    if (lazy && dur > 0.0 && fin > itgt) {
+      const uint32_t more = fin - itgt < 65535u ? fin - itgt : 65535u;
+      uint32_t taken = 0;
+      tend = run_walk(t1, dur, more, __builtin_inf(), &taken);
+      itgt += taken;
+    }
     if constexpr (G) {
-      // k_fine<true>: runs also stop at bound; a thinker stage records the
-      // predicted end of every step of the run in its ring
-      const bool thk = S.si.flags[si] & SF_THINKER;
-      const int slot = thk ? S.si.hist[lx] : 0;
-      double *h = S.hist + (size_t)slot * kRing;
-      if (thk && lane_id() == 0) h[itgt & (kRing - 1)] = tend;
-      if (lazy && dur > 0.0) {
-        const uint32_t fin = S.si.minfin[lx] < bound ? S.si.minfin[lx] : bound;
-        while (itgt < fin && itgt - it0 < 65536u) {
-          tend = tend + dur;
-          itgt++;
-          if (thk && lane_id() == 0) h[itgt & (kRing - 1)] = tend;
+      // k_fine<true>: a thinker stage records the predicted end of every
+      // step of the run in its ring, one step per lane
+      if (S.si.flags[si] & SF_THINKER) {
+        const int slot = S.si.hist[lx];
+        double *h = S.hist + (size_t)slot * kRing;
+        for (uint32_t i = (uint32_t)lane_id(); i <= itgt - (it0 + 1u); i += 64u) {
+          uint32_t taken = 0;
+          h[(it0 + 1u + i) & (kRing - 1)] = run_walk(t1, dur, i, __builtin_inf(), &taken);
         }
-      }
-      if (thk) S.si.sched[slot] = itgt;
-    } else {
-      if (lazy && dur > 0.0) {
-        const uint32_t fin = S.si.minfin[lx];
-        while (itgt < fin && itgt - it0 < 65536u) {
-          tend = tend + dur;
-          itgt++;
-        }
+        S.si.sched[slot] = itgt;
       }
     }
     sh.ex_t0[x] = S.now;
@@ -852,7 +837,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
       }
     }
     if (__ballot(undecided)) S.status |= CF_ST_OVERFLOW;
-    cntm = ru(wave_sum_u(cntm));
+    cntm = dpp_sum_u32(cntm);
     __syncthreads();
     dur = m.d0[c] + m.d1[c] * (double)cntm;
     nmem = (int)cntm;
@@ -945,8 +930,8 @@ __device__ __forceinline__ GateView local_gate_view(const Sim &S, int x, int si)
     }
   }
   GateView v;
-  v.qmin = ru(wave_min_u(qmin));
-  v.kta = ru(wave_min_u(kta));
+  v.qmin = dpp_min_u32(qmin);
+  v.kta = dpp_min_u32(kta);
   v.gsi = gsi;
   v.joint = nbusy == 1 && __ballot(other) == 0;
   return v;
@@ -1069,12 +1054,9 @@ __device__ void cut_run(Sim &S, int x) {
   const uint32_t it0 = S.si.iter[lx];
   const uint32_t itgt = sh.ex_itgt[x];
   const double dur = sh.ex_dur[x];
-  double t = sh.ex_t0[x] + dur;
-  uint32_t j = it0 + 1u;
-  while (t < S.now && j < itgt) {
-    t = t + dur;
-    j++;
-  }
+  uint32_t taken = 0;
+  const double t = run_walk(sh.ex_t0[x] + dur, dur, itgt - (it0 + 1u), S.now, &taken);
+  const uint32_t j = it0 + 1u + taken;
   sh.ex_tend[x] = t;
   sh.ex_itgt[x] = j;
   if (j <= it0 + 1u) sh.ex_st[x] = st & ~EX_RUN;
@@ -1127,7 +1109,7 @@ __device__ void run_compact(Sim &S, int si, const bool *drop) {
   }
   __syncthreads();
   S.si.rn[lx] = (int)w;
-  if (!(S.si.flags[si] & SF_GATED)) S.si.minfin[lx] = ru(wave_min_u(mn));
+  if (!(S.si.flags[si] & SF_GATED)) S.si.minfin[lx] = dpp_min_u32(mn);
 }
 
 // collects the running slots flagged in fin[] (slot order) into mem,
@@ -1277,7 +1259,7 @@ __device__ __forceinline__ void complete_iter(Sim &S, int x) {
         }
       }
     }
-    S.events += (uint64_t)ru(wave_sum_u(part));
+    S.events += (uint64_t)dpp_sum_u32(part);
     __syncthreads();
     bool anyf = false;
 #pragma unroll
@@ -1585,7 +1567,7 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
   for (;;) {
     unsigned int tk = 0;
     if (lane == 0) tk = atomicAdd(A.ticket, 1u);
-    tk = ru(__shfl(tk, 0, 64));
+    tk = ru(tk);
     if (tk >= A.total) break;
     const int s = (int)(tk / per_seed);
     const unsigned int rem = tk % per_seed;
