@@ -226,14 +226,37 @@ __device__ __forceinline__ uint32_t wave_excl_scan(uint32_t v, uint32_t &total) 
   return x - v;
 }
 
+// Device memory (global address space) addressed by a 32-bit byte offset
+// from a base held in scalar registers: loads and stores take the
+// scalar-base + vector-offset form, with no 64-bit address arithmetic per
+// lane.  Every array the kernel indexes is far below 4 GiB.
+#define CF_GLOBAL __attribute__((address_space(1)))
+template <typename T>
+struct GPtr {
+  CF_GLOBAL T *p;
+  __device__ __forceinline__ CF_GLOBAL T &operator[](uint32_t i) const {
+    return *(CF_GLOBAL T *)((CF_GLOBAL char *)p + i * (uint32_t)sizeof(T));
+  }
+  __device__ __forceinline__ GPtr operator+(uint32_t i) const { return GPtr{&(*this)[i]}; }
+};
+template <typename T>
+__device__ __forceinline__ GPtr<T> gptr_at(char *base, size_t off) {
+  return GPtr<T>{(CF_GLOBAL T *)(base + off)};
+}
+// element o of a read-only input array
+template <typename T>
+__device__ __forceinline__ T gload(const T *p, size_t o) {
+  return *(const CF_GLOBAL T *)((const CF_GLOBAL char *)p + (uint32_t)o * (uint32_t)sizeof(T));
+}
+
 struct Sim {
   const FineArgs *A;
   WaveShared *sh;
   SiLds si;
-  Rec *rec;
-  double *tfirst, *tlast, *tmedia, *hist, *dl_t;
-  uint32_t *thjoin, *run_r, *run_k, *mem, *dl_v, *pool;
-  int *pool_next, *pool_free;
+  GPtr<Rec> rec;
+  GPtr<double> tfirst, tlast, tmedia, hist, dl_t;
+  GPtr<uint32_t> thjoin, run_r, run_k, mem, dl_v, pool;
+  GPtr<int> pool_next, pool_free;
   size_t soff;
   double lam, now, dl_head_t, t_arr;
   uint64_t events, dirty, ta_exec_mask;
@@ -246,18 +269,33 @@ struct Sim {
   uint64_t rewake;     // executors whose wake time is to be recomputed in this instant
 };
 
+__device__ __forceinline__ Rec rec_get(const Sim &S, uint32_t r) {
+  CF_GLOBAL Rec &q = S.rec[r];
+  Rec R;
+  R.ex = q.ex;
+  R.join = q.join;
+  R.misc = q.misc;
+  return R;
+}
+__device__ __forceinline__ void rec_put(const Sim &S, uint32_t r, const Rec &R) {
+  CF_GLOBAL Rec &q = S.rec[r];
+  q.ex = R.ex;
+  q.join = R.join;
+  q.misc = R.misc;
+}
+
 // ------------------------------------------------------------------ trace
 __device__ __forceinline__ uint32_t attr(const Sim &S, uint32_t r, int a) {
   const size_t o = S.soff + r;
   const FineArgs &A = *S.A;
   switch (a) {
-    case CF_ATTR_PROMPT: return A.prompt[o];
-    case CF_ATTR_OUT: return A.out[o];
-    case CF_ATTR_PATCHES: return A.patches[o];
-    case CF_ATTR_AUDIN_MS: return A.aud_in[o];
-    case CF_ATTR_AUDOUT_MS: return A.aud_out[o];
-    case CF_ATTR_AUDIN_TOK: return (A.aud_in[o] + 79u) / 80u;
-    case CF_ATTR_AUDOUT_TOK: return (A.aud_out[o] + 79u) / 80u;
+    case CF_ATTR_PROMPT: return gload(A.prompt, o);
+    case CF_ATTR_OUT: return gload(A.out, o);
+    case CF_ATTR_PATCHES: return gload(A.patches, o);
+    case CF_ATTR_AUDIN_MS: return gload(A.aud_in, o);
+    case CF_ATTR_AUDOUT_MS: return gload(A.aud_out, o);
+    case CF_ATTR_AUDIN_TOK: return (gload(A.aud_in, o) + 79u) / 80u;
+    case CF_ATTR_AUDOUT_TOK: return (gload(A.aud_out, o) + 79u) / 80u;
     default: return 0;
   }
 }
@@ -276,7 +314,7 @@ __device__ __forceinline__ uint32_t nout_of(const Sim &S, uint32_t r, int t, int
   return v < 1 ? 1 : v;
 }
 __device__ __forceinline__ double arrival_time(const Sim &S, uint32_t r) {
-  return ((double)S.A->ticks[S.soff + r] * 0x1p-32) / S.lam;
+  return ((double)gload(S.A->ticks, S.soff + r) * 0x1p-32) / S.lam;
 }
 __device__ __forceinline__ int ex_byte(uint64_t ex, int c) { return (int)((ex >> (8 * c)) & 0xFFu); }
 __device__ __forceinline__ int rtype(uint32_t misc) { return (int)((misc >> 8) & 7u); }
@@ -330,7 +368,7 @@ __device__ void q_push_lanes(Sim &S, int si, uint64_t bal, uint32_t r) {
     const int k = (int)lanes_below(bal);
     const int ch = k < room ? tc : c1;
     const int pos = k < room ? tp + k : k - room;
-    S.pool[(size_t)ch * kChunk + pos] = r;
+    S.pool[(uint32_t)(ch * kChunk + pos)] = r;
   }
   if (cnt <= room) {
     S.si.qtc[si] = tc;
@@ -343,7 +381,7 @@ __device__ void q_push_lanes(Sim &S, int si, uint64_t bal, uint32_t r) {
 }
 
 // pops the first k entries of stage si's queue into dst[0..k)
-__device__ void q_pop(Sim &S, int si, int k, uint32_t *dst) {
+__device__ void q_pop(Sim &S, int si, int k, GPtr<uint32_t> dst) {
   int hc = S.si.qhc[si], hp = S.si.qhp[si];
   const int tc = S.si.qtc[si], tp = S.si.qtp[si];
   if (k <= 0) return;
@@ -360,7 +398,7 @@ __device__ void q_pop(Sim &S, int si, int k, uint32_t *dst) {
       S.status |= CF_ST_OVERFLOW;
       break;
     }
-    if (lane_id() < take) dst[got + lane_id()] = S.pool[(size_t)hc * kChunk + hp + lane_id()];
+    if (lane_id() < take) dst[got + lane_id()] = S.pool[(uint32_t)(hc * kChunk + hp + lane_id())];
     got += take;
     hp += take;
     if (hp == kChunk && got < k) {
@@ -423,7 +461,7 @@ __device__ __forceinline__ bool token_visible(const Sim &S, uint32_t r, uint32_t
     const uint32_t q = S.thjoin[r] + k - 1u;
     const uint32_t it = S.si.iter[si];
     if (q > it) return false;
-    const double *h = S.hist + (size_t)S.si.hist[si] * kHist;
+    const GPtr<double> h = S.hist + (uint32_t)(S.si.hist[si] * kHist);
     if (it - q < (uint32_t)kHist) {
       e = h[q & (kHist - 1)];
     } else {
@@ -438,7 +476,7 @@ __device__ __forceinline__ bool token_visible(const Sim &S, uint32_t r, uint32_t
 }
 
 __device__ __forceinline__ bool slot_eligible(const Sim &S, uint32_t r, uint32_t tok, int c, int x, bool &undecided) {
-  const Rec R = S.rec[r];
+  const Rec R = rec_get(S, r);
   const int t = rtype(R.misc);
   if (S.sh->ml.ta_c[t] != c) return true;
   const int th = S.sh->ml.th_c[t];
@@ -470,7 +508,7 @@ __device__ __forceinline__ double token_vis(const Sim &S, uint32_t r, uint32_t m
       return __builtin_inf();
     }
     const uint32_t it = S.si.iter[lx];
-    const double *h = S.hist + (size_t)slot * kRing;
+    const GPtr<double> h = S.hist + (uint32_t)(slot * kRing);
     if (q > it) {
       wsi = slot;  // predicted end of a step of the running decode run
       e = h[q & (kRing - 1)];
@@ -493,7 +531,7 @@ __device__ __forceinline__ double token_vis(const Sim &S, uint32_t r, uint32_t m
 // thinker's executor
 __device__ __forceinline__ double slot_vis(const Sim &S, uint32_t r, uint32_t tok, int c, int x, int &xth, int &wsi,
                                            bool &undecided) {
-  const Rec R = S.rec[r];
+  const Rec R = rec_get(S, r);
   const int t = rtype(R.misc);
   xth = x;
   wsi = -1;
@@ -532,13 +570,13 @@ __device__ void arrive(Sim &S, uint32_t r) {
   const WaveShared &sh = *S.sh;
   S.events++;
   const size_t o = S.soff + r;
-  const int t = ri(A.type[o]);
+  const int t = ri(gload(A.type, o));
   if (t >= m.nt) {
     S.status |= CF_ST_INVALID;
     return;
   }
-  const uint64_t k0 = ru64(A.rkey0[o]), k1 = ru64(A.rkey1[o]);
-  const uint32_t ak = ru(A.akey[o]);
+  const uint64_t k0 = ru64(gload(A.rkey0, o)), k1 = ru64(gload(A.rkey1, o));
+  const uint32_t ak = ru(gload(A.akey, o));
   int alt = 0;
   if (sh.nalt[t] == 2) {
     const uint64_t w0 = sh.aw[t][0], w1 = sh.aw[t][1];
@@ -559,7 +597,7 @@ __device__ void arrive(Sim &S, uint32_t r) {
   R.ex = ex;
   R.join = 0;
   R.misc = (uint32_t)__popc(m.outm[t]) | ((uint32_t)t << 8);
-  if (lane_id() == 0) S.rec[r] = R;
+  if (lane_id() == 0) rec_put(S, r, R);
   uint32_t src = m.srcm[t];
   while (src) {
     const int c = __ffs(src) - 1;
@@ -570,7 +608,7 @@ __device__ void arrive(Sim &S, uint32_t r) {
 
 // step 2: a delayed delivery of request r to component c2
 __device__ void dl_deliver(Sim &S, uint32_t r, int c2) {
-  const Rec R = S.rec[r];
+  const Rec R = rec_get(S, r);
   const uint64_t ex = ru64(R.ex);
   const uint32_t join = ru(R.join) + (1u << (4 * c2));
   const uint32_t misc = ru(R.misc);
@@ -586,7 +624,7 @@ __device__ void dl_deliver(Sim &S, uint32_t r, int c2) {
 //               streaming delivery to the talker) and finish or join Run;
 //   IT_FINISH:  decode members that produced their last token finish c.
 template <bool G>
-__device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, const uint32_t *mem) {
+__device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr<uint32_t> mem) {
   const KModel &m = S.A->m;
   const ModelLds &ml = S.sh->ml;
   const bool gated = S.si.flags[si] & SF_GATED;
@@ -600,7 +638,7 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, cons
     Rec R = {0, 0, 0};
     if (valid) {
       r = mem[j];
-      R = S.rec[r];
+      R = rec_get(S, r);
     }
     const int t = rtype(R.misc);
     bool fin = valid;
@@ -763,7 +801,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     const int beff = S.si.beff[si];
     const int room = kind == IT_PREFILL ? beff - S.si.rn[lx] : beff;
     const int n = qn < room ? qn : room;
-    uint32_t *dst = S.mem + (size_t)x * CF_MAX_BATCH;
+    const GPtr<uint32_t> dst = S.mem + (uint32_t)(x * CF_MAX_BATCH);
     q_pop(S, si, n, dst);
     if (S.status & CF_ST_OVERFLOW) return;  // the triple is abandoned at the end of this instant
     uint32_t xs = 0;
@@ -805,7 +843,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
       // step of the run in its ring, one step per lane
       if (S.si.flags[si] & SF_THINKER) {
         const int slot = S.si.hist[lx];
-        double *h = S.hist + (size_t)slot * kRing;
+        const GPtr<double> h = S.hist + (uint32_t)(slot * kRing);
         for (uint32_t i = (uint32_t)lane_id(); i <= itgt - (it0 + 1u); i += 64u) {
           uint32_t taken = 0;
           h[(it0 + 1u + i) & (kRing - 1)] = run_walk(t1, dur, i, __builtin_inf(), &taken);
@@ -823,8 +861,8 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
   } else {
     // gated stage: mark the eligible running requests
     const int rn = S.si.rn[lx];
-    uint32_t *rr = S.run_r + S.si.roff[lx];
-    uint32_t *rk = S.run_k + S.si.roff[lx];
+    const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lx];
+    const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
     uint32_t cntm = 0;
     bool undecided = false;
     for (int b = 0; b < rn; b += 64) {
@@ -845,7 +883,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
       if (S.si.flags[si] & SF_THINKER) {  // a gated stage that is also a gate source
         const uint32_t it1 = S.si.iter[lx] + 1u;
         const int slot = S.si.hist[lx];
-        if (lane_id() == 0) S.hist[(size_t)slot * kRing + (it1 & (kRing - 1))] = S.now + dur;
+        if (lane_id() == 0) S.hist[(uint32_t)(slot * kRing) + (it1 & (kRing - 1))] = S.now + dur;
         S.si.sched[slot] = it1;
       }
     }
@@ -866,8 +904,8 @@ __device__ int runnable_kind(Sim &S, int x, int si, int c) {
   if (qn > 0 && rn < (int)S.si.beff[si]) return IT_PREFILL;
   if (rn == 0) return -1;
   if (!(fl & SF_GATED)) return IT_DECODE;
-  const uint32_t *rr = S.run_r + S.si.roff[lx];
-  const uint32_t *rk = S.run_k + S.si.roff[lx];
+  const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lx];
+  const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
   bool any = false, undecided = false;
   for (int b = 0; b < rn && !any; b += 64) {
     const int j = b + lane_id();
@@ -904,13 +942,13 @@ __device__ __forceinline__ GateView local_gate_view(const Sim &S, int x, int si)
     if (rn == 0) continue;
     nbusy++;
     gsi = g;
-    const uint32_t *rr = S.run_r + S.si.roff[lg];
-    const uint32_t *rk = S.run_k + S.si.roff[lg];
+    const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lg];
+    const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lg];
     for (int b = 0; b < rn; b += 64) {
       const int j = b + lane_id();
       if (j < rn) {
         const uint32_t r = rr[j];
-        const Rec R = S.rec[r];
+        const Rec R = rec_get(S, r);
         const int t = rtype(R.misc);
         const uint32_t tok = rk[j] & 0xFFFFu;
         bool waits_next = false;
@@ -958,7 +996,7 @@ __device__ __forceinline__ bool start_joint(Sim &S, int x, int lth, int sth, int
   uint32_t n = 2u * (kth < kThRun ? kth : kThRun) - 1u;
   if (2u * kta < n) n = 2u * kta;
   const int slot = S.si.hist[lx];
-  double *h = S.hist + (size_t)slot * kRing;
+  const GPtr<double> h = S.hist + (uint32_t)(slot * kRing);
   double t = S.now;
   for (uint32_t i = 1; i <= n; i++) {
     t = t + ((i & 1u) ? d1 : d2);
@@ -1078,8 +1116,8 @@ template <bool G>
 __device__ void run_compact(Sim &S, int si, const bool *drop) {
   const int lx = lx_of<G>(S.si, si);
   const int rn = S.si.rn[lx];
-  uint32_t *rr = S.run_r + S.si.roff[lx];
-  uint32_t *rk = S.run_k + S.si.roff[lx];
+  const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lx];
+  const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
   uint32_t vr[CF_MAX_BATCH / 64], vk[CF_MAX_BATCH / 64];
   bool keep[CF_MAX_BATCH / 64];
 #pragma unroll
@@ -1118,8 +1156,8 @@ template <bool G>
 __device__ void finish_slots(Sim &S, int x, int si, int c, const bool *fin) {
   const int lx = lx_of<G>(S.si, si);
   const int rn = S.si.rn[lx];
-  const uint32_t *rr = S.run_r + S.si.roff[lx];
-  uint32_t *mem = S.mem + (size_t)x * CF_MAX_BATCH;
+  const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lx];
+  const GPtr<uint32_t> mem = S.mem + (uint32_t)(x * CF_MAX_BATCH);
   uint32_t nf = 0;
 #pragma unroll
   for (int p = 0; p < CF_MAX_BATCH / 64; p++) {
@@ -1160,8 +1198,8 @@ __device__ __forceinline__ void complete_joint(Sim &S, int x, uint32_t st) {
   const int lg = S.si.lsi[sta];
   const int cta = S.si.comp[sta];
   const int rng = S.si.rn[lg];
-  const uint32_t *rrg = S.run_r + S.si.roff[lg];
-  uint32_t *rkg = S.run_k + S.si.roff[lg];
+  const GPtr<uint32_t> rrg = S.run_r + (uint32_t)S.si.roff[lg];
+  const GPtr<uint32_t> rkg = S.run_k + (uint32_t)S.si.roff[lg];
   bool fin[CF_MAX_BATCH / 64];
 #pragma unroll
   for (int p = 0; p < CF_MAX_BATCH / 64; p++) {
@@ -1178,7 +1216,7 @@ __device__ __forceinline__ void complete_joint(Sim &S, int x, uint32_t st) {
   __syncthreads();
   if (n & 1u) {
     if (it == S.si.minfin[lx]) {
-      const uint32_t *rk = S.run_k + S.si.roff[lx];
+      const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
 #pragma unroll
       for (int p = 0; p < CF_MAX_BATCH / 64; p++) {
         const int j = p * 64 + lane_id();
@@ -1213,7 +1251,7 @@ __device__ __forceinline__ void complete_iter(Sim &S, int x) {
   S.dirty |= 1ull << x;
   if (kind == IT_BATCH || kind == IT_PREFILL) {
     S.events += (uint64_t)nmem;
-    members_done<G>(S, x, si, c, kind, nmem, S.mem + (size_t)x * CF_MAX_BATCH);
+    members_done<G>(S, x, si, c, kind, nmem, S.mem + (uint32_t)(x * CF_MAX_BATCH));
     if constexpr (!G) {
       if (fl & SF_THINKER) thinker_tick(S);
     }
@@ -1225,10 +1263,10 @@ __device__ __forceinline__ void complete_iter(Sim &S, int x) {
   const uint32_t it = (fl & SF_GATED) ? it0 + 1u : sh.ex_itgt[x];
   S.si.iter[lx] = it;  // k_fine<true>: a thinker's ring already holds the end of these steps
   if constexpr (!G) {
-    if ((fl & SF_THINKER) && lane_id() == 0) S.hist[(size_t)S.si.hist[si] * kHist + (it & (kHist - 1))] = S.now;
+    if ((fl & SF_THINKER) && lane_id() == 0) S.hist[(uint32_t)(S.si.hist[si] * kHist) + (it & (kHist - 1))] = S.now;
   }
-  const uint32_t *rr = S.run_r + S.si.roff[lx];
-  uint32_t *rk = S.run_k + S.si.roff[lx];
+  const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lx];
+  const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
   if (!(fl & SF_GATED)) {
     S.events += (uint64_t)rn * (uint64_t)(it - it0);
     if (it == S.si.minfin[lx]) {
@@ -1289,8 +1327,8 @@ __device__ __forceinline__ bool gate_wake(Sim &S, int y) {
       if (!(S.si.flags[g] & SF_GATED)) continue;
       const int lg = S.si.lsi[g];
       const int c = S.si.comp[g], rn = S.si.rn[lg];
-      const uint32_t *rr = S.run_r + S.si.roff[lg];
-      const uint32_t *rk = S.run_k + S.si.roff[lg];
+      const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lg];
+      const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lg];
       for (int b = 0; b < rn; b += 64) {
         const int j = b + lane_id();
         if (j < rn) {
@@ -1548,20 +1586,20 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
   if (lane < CF_MAX_TYPES * 4) (&sh.ml.slo[0][0])[lane] = (&m.slo[0][0])[lane];
   char *slab = A.slab + (size_t)blockIdx.x * A.L.bytes;
   const Layout &L = A.L;
-  S.rec = (Rec *)(slab + L.rec);
-  S.tfirst = (double *)(slab + L.tfirst);
-  S.tlast = (double *)(slab + L.tlast);
-  S.tmedia = (double *)(slab + L.tmedia);
-  S.thjoin = (uint32_t *)(slab + L.thjoin);
-  S.run_r = (uint32_t *)(slab + L.run_r);
-  S.run_k = (uint32_t *)(slab + L.run_k);
-  S.hist = (double *)(slab + L.hist);
-  S.mem = (uint32_t *)(slab + L.mem);
-  S.dl_t = (double *)(slab + L.dl_t);
-  S.dl_v = (uint32_t *)(slab + L.dl_v);
-  S.pool = (uint32_t *)(slab + L.pool);
-  S.pool_next = (int *)(slab + L.pool_next);
-  S.pool_free = (int *)(slab + L.pool_free);
+  S.rec = gptr_at<Rec>(slab, L.rec);
+  S.tfirst = gptr_at<double>(slab, L.tfirst);
+  S.tlast = gptr_at<double>(slab, L.tlast);
+  S.tmedia = gptr_at<double>(slab, L.tmedia);
+  S.thjoin = gptr_at<uint32_t>(slab, L.thjoin);
+  S.run_r = gptr_at<uint32_t>(slab, L.run_r);
+  S.run_k = gptr_at<uint32_t>(slab, L.run_k);
+  S.hist = gptr_at<double>(slab, L.hist);
+  S.mem = gptr_at<uint32_t>(slab, L.mem);
+  S.dl_t = gptr_at<double>(slab, L.dl_t);
+  S.dl_v = gptr_at<uint32_t>(slab, L.dl_v);
+  S.pool = gptr_at<uint32_t>(slab, L.pool);
+  S.pool_next = gptr_at<int>(slab, L.pool_next);
+  S.pool_free = gptr_at<int>(slab, L.pool_free);
   __syncthreads();
   const unsigned int per_seed = (unsigned int)A.n_plans * (unsigned int)A.K;
   for (;;) {
