@@ -58,8 +58,9 @@ constexpr double run_walk(double e, double d, uint32_t n, double stop, uint32_t 
     const uint64_t m2 = b2 & kMant, D = m2 - (b1 & kMant);
     uint64_t j = n - k;
     if (D > 0) {
-      const uint64_t jb = floor_div53(kMant - m2, D);  // steps that stay in the binade
-      j = jb < j ? jb : j;
+      // the steps that stay in the binade (no division when all of them do)
+      uint64_t span = 0;
+      if (__builtin_mul_overflow(j, D, &span) || span > kMant - m2) j = floor_div53(kMant - m2, D);
       const uint64_t bs = __builtin_bit_cast(uint64_t, stop);
       if ((bs >> 52) == ex) {
         // stop lies in this binade above e: the ends m2 + i D reach it from

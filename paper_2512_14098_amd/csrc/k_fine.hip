@@ -81,8 +81,14 @@ struct __attribute__((aligned(16))) Rec {
   uint32_t misc;  // outputs left (4 bits), thinker done (bit 4), type (bits 8..10)
 };
 
+// token and media times of a request, and its join step in the thinker's stage
+struct __attribute__((aligned(32))) Tim {
+  double tfirst, tlast, tmedia;
+  uint32_t thjoin, pad;
+};
+
 struct Layout {
-  size_t rec, tfirst, tlast, tmedia, thjoin;
+  size_t rec, tim;
   size_t run_r, run_k, hist, mem, dl_t, dl_v, pool, pool_next, pool_free;
   size_t bytes;
   int run_cap, hist_slots, n_chunks;
@@ -254,8 +260,9 @@ struct Sim {
   WaveShared *sh;
   SiLds si;
   GPtr<Rec> rec;
-  GPtr<double> tfirst, tlast, tmedia, hist, dl_t;
-  GPtr<uint32_t> thjoin, run_r, run_k, mem, dl_v, pool;
+  GPtr<Tim> tim;
+  GPtr<double> hist, dl_t;
+  GPtr<uint32_t> run_r, run_k, mem, dl_v, pool;
   GPtr<int> pool_next, pool_free;
   size_t soff;
   double lam, now, dl_head_t, t_arr;
@@ -453,12 +460,12 @@ __device__ __forceinline__ bool token_visible(const Sim &S, uint32_t r, uint32_t
   const double delta = (xth == x) ? 0.0 : S.A->m.comm;
   double e;
   if (k <= 1) {
-    e = S.tfirst[r];
+    e = S.tim[r].tfirst;
   } else if ((misc & MISC_TH_DONE) && k == nth) {
-    e = S.tlast[r];
+    e = S.tim[r].tlast;
   } else {
     const int si = stage_of(S, xth, th);
-    const uint32_t q = S.thjoin[r] + k - 1u;
+    const uint32_t q = S.tim[r].thjoin + k - 1u;
     const uint32_t it = S.si.iter[si];
     if (q > it) return false;
     const GPtr<double> h = S.hist + (uint32_t)(S.si.hist[si] * kHist);
@@ -496,13 +503,13 @@ __device__ __forceinline__ double token_vis(const Sim &S, uint32_t r, uint32_t m
   wsi = -1;
   double e;
   if (k <= 1) {
-    e = S.tfirst[r];
+    e = S.tim[r].tfirst;
   } else if ((misc & MISC_TH_DONE) && k == nth) {
-    e = S.tlast[r];
+    e = S.tim[r].tlast;
   } else {
     const int lx = S.si.lsi[stage_of(S, xth, th)];
     const int slot = S.si.hist[lx];
-    const uint32_t q = S.thjoin[r] + k - 1u;
+    const uint32_t q = S.tim[r].thjoin + k - 1u;
     if (q > S.si.sched[slot]) {
       wsi = slot;
       return __builtin_inf();
@@ -648,18 +655,18 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
     if (valid && kind == IT_PREFILL) {
       const uint32_t no = nout_of(S, r, t, c);
       if (c == ml.ttft_c[t]) {
-        S.tfirst[r] = now;
-        S.tlast[r] = now;
+        S.tim[r].tfirst = now;
+        S.tim[r].tlast = now;
       }
       if (c == ml.th_c[t]) {
-        S.thjoin[r] = iter_s;
+        S.tim[r].thjoin = iter_s;
         stream = true;
         ta = ml.ta_c[t];
       }
       fin = no == 1;
       key = gated ? 1u : iter_s + no - 1u;
     } else if (valid && kind == IT_FINISH) {
-      if (c == ml.ttft_c[t]) S.tlast[r] = now;
+      if (c == ml.ttft_c[t]) S.tim[r].tlast = now;
     }
     const bool append = valid && kind == IT_PREFILL && !fin;
     // delayed deliveries: the streaming one first, then remote children
@@ -718,7 +725,7 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
     if (fin && valid) {
       if (c == ml.th_c[t]) misc |= MISC_TH_DONE;
       if ((ml.outm[t] >> c) & 1u) {
-        if (ml.kind[c] == CF_GEN) S.tmedia[r] = now;
+        if (ml.kind[c] == CF_GEN) S.tim[r].tmedia = now;
         misc -= 1u;
         done = (misc & MISC_OUTS) == 0;
       }
@@ -761,13 +768,13 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
         double ttft = 0.0, tpot = 0.0, media = 0.0;
         const int tc = ml.ttft_c[t];
         if (tc >= 0) {
-          const double tf = S.tfirst[r];
+          const double tf = S.tim[r].tfirst;
           ttft = tf - a;
           const uint32_t n1 = nout_of(S, r, t, tc);
-          if (n1 > 1) tpot = (S.tlast[r] - tf) / (double)(n1 - 1);
+          if (n1 > 1) tpot = (S.tim[r].tlast - tf) / (double)(n1 - 1);
         }
         const double e2e = now - a;
-        if (ml.gen_out[t]) media = S.tmedia[r] - a;
+        if (ml.gen_out[t]) media = S.tim[r].tmedia - a;
         ok = ttft <= ml.slo[t][0] && tpot <= ml.slo[t][1] && e2e <= ml.slo[t][2] && media <= ml.slo[t][3];
         if (S.lat_slot >= 0) {
           double *Lp = S.A->lat + ((size_t)S.lat_slot * S.A->n + r) * 4;
@@ -956,7 +963,7 @@ __device__ __forceinline__ GateView local_gate_view(const Sim &S, int x, int si)
           const uint32_t nth = nout_of(S, r, t, cth);
           const uint32_t k = tok + 1u < nth ? tok + 1u : nth;
           if (k > 1u && !((R.misc & MISC_TH_DONE) && k == nth)) {
-            const uint32_t q = S.thjoin[r] + k - 1u;
+            const uint32_t q = S.tim[r].thjoin + k - 1u;
             qmin = q < qmin ? q : qmin;
             waits_next = q == next;
           }
@@ -1021,7 +1028,8 @@ __device__ __forceinline__ void try_start(Sim &S, int x) {
   const int ns = sh.ex_ns[x], first = sh.ex_first[x];
   const int rr = (st >> 4) & 15u;
   for (int i = 0; i < ns; i++) {
-    const int l = (rr == 15) ? i : (rr + 1 + i) % ns;
+    int l = (rr == 15) ? i : rr + 1 + i;  // rr < ns, i < ns
+    if (l >= ns) l -= ns;
     const int si = first + l;
     const int kind = runnable_kind<G>(S, x, si, S.si.comp[si]);
     if (kind >= 0) {
@@ -1033,7 +1041,8 @@ __device__ __forceinline__ void try_start(Sim &S, int x) {
           (S.si.qn[si] == 0 || S.si.rn[lx_of<G>(S.si, si)] >= (int)S.si.beff[si])) {
         lazy = true;  // ... unless a stage checked after this one has work
         for (int i2 = i + 1; i2 < ns && lazy; i2++) {
-          const int l2 = (rr == 15) ? i2 : (rr + 1 + i2) % ns;
+          int l2 = (rr == 15) ? i2 : rr + 1 + i2;
+          if (l2 >= ns) l2 -= ns;
           if (runnable_kind<G>(S, x, first + l2, S.si.comp[first + l2]) >= 0) lazy = false;
         }
         if constexpr (G) {
@@ -1587,10 +1596,7 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
   char *slab = A.slab + (size_t)blockIdx.x * A.L.bytes;
   const Layout &L = A.L;
   S.rec = gptr_at<Rec>(slab, L.rec);
-  S.tfirst = gptr_at<double>(slab, L.tfirst);
-  S.tlast = gptr_at<double>(slab, L.tlast);
-  S.tmedia = gptr_at<double>(slab, L.tmedia);
-  S.thjoin = gptr_at<uint32_t>(slab, L.thjoin);
+  S.tim = gptr_at<Tim>(slab, L.tim);
   S.run_r = gptr_at<uint32_t>(slab, L.run_r);
   S.run_k = gptr_at<uint32_t>(slab, L.run_k);
   S.hist = gptr_at<double>(slab, L.hist);
@@ -1778,10 +1784,7 @@ Layout make_layout(const KModel &m, int n) {
   L.run_cap = CF_MAX_EXEC * per_exec_run;
   L.hist_slots = CF_MAX_EXEC * n_th;
   L.rec = take(sizeof(Rec) * (size_t)n);
-  L.tfirst = take(8 * (size_t)n);
-  L.tlast = take(8 * (size_t)n);
-  L.tmedia = take(8 * (size_t)n);
-  L.thjoin = take(4 * (size_t)n);
+  L.tim = take(sizeof(Tim) * (size_t)n);
   L.run_r = take(4 * (size_t)L.run_cap);
   L.run_k = take(4 * (size_t)L.run_cap);
   L.hist = take(8 * (size_t)L.hist_slots * (m.gated_mask ? kRing : kHist) + 8);
