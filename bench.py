@@ -66,6 +66,64 @@ def cpu_baseline(w, ids, rates, budget_s):
                       "(%d request-events in %.1f s, single thread)" % (n, ev, dt)}
 
 
+def stress(reps, steps):
+    """HBM-bound steps at full size on the c4 inputs, each timed with HIP events on the stream it
+    runs on: trace generation of all 64 seeds x 10^5 requests (write-bound), and phase-1
+    screening of the 10^6 c4 plans tiled reps times (read-bound).  Algorithmic bytes: the trace
+    fields written (44 B per request); per plan, the table bytes the screening must read (plan
+    node count, 5 B per node, per type its alternative count and, per alternative, the weight and
+    one node byte per path component) plus the 13 B written (R_d, bottleneck, flags)."""
+    import numpy as np
+    import torch
+
+    from paper_2512_14098_amd import cf
+    from paper_2512_14098_amd.inputs import load_config, make_plans, seeds_of
+    cfg = load_config("c4")
+    desc = cf.model_desc(cfg["model"])
+    seeds, n = seeds_of(cfg), int(cfg["n_req"])
+    peak = 8.0e12
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            out = fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / steps / 1e3, out
+
+    t_tr, (tr, mom) = timed(lambda: cf.cf_trace_gen(desc, seeds, n))
+    tr_bytes = 44.0 * len(seeds) * n
+    print(json.dumps({"stress": "cf_trace_gen", "workload": "c4 trace: %d seeds x %d requests" % (len(seeds), n),
+                      "ms": t_tr * 1e3, "requests_per_s": len(seeds) * n / t_tr,
+                      "roofline": {"bound": "hbm", "achieved": tr_bytes / t_tr / 1e9, "peak": peak / 1e9,
+                                   "unit": "GB/s", "frac": tr_bytes / t_tr / peak,
+                                   "alg_bytes_per_request": 44}}), flush=True)
+    tab = make_plans(cfg)
+    base = cf.DevicePlans(tab)
+    big = cf.DevicePlans.__new__(cf.DevicePlans)
+    big.P, big.t, big.c = base.P * reps, {}, cf.cf_plan_table()
+    big.c.P = big.P
+    for f, t in base.t.items():
+        big.t[f] = t.repeat(reps) if t.dim() == 1 else t.repeat(1, reps)
+        setattr(big.c, f + "_dev", big.t[f].data_ptr())
+    del base
+    nt = desc.n_types
+    path_len = np.array([bin(int(desc.path_mask[t])).count("1") for t in range(nt)])
+    na = tab.n_alt[:nt].astype(np.int64)
+    per_plan = 1 + 5 * tab.n_nodes.astype(np.int64) + (na * (1 + path_len[:, None])).sum(axis=0) + nt + 13
+    plan_bytes = float(per_plan.sum()) * reps
+    t_co, _ = timed(lambda: cf.cf_eval_coarse(desc, big, mom[0], int(cfg["gpus"])))
+    print(json.dumps({"stress": "cf_eval_coarse", "workload": "c4 plans: %d sampled plans tiled %d times" % (tab.P, reps),
+                      "plans": big.P, "ms": t_co * 1e3, "plans_per_s": big.P / t_co,
+                      "roofline": {"bound": "hbm", "achieved": plan_bytes / t_co / 1e9, "peak": peak / 1e9,
+                                   "unit": "GB/s", "frac": plan_bytes / t_co / peak,
+                                   "alg_bytes_per_plan": plan_bytes / big.P,
+                                   "table_bytes_per_plan": 233 + 13}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -80,6 +138,9 @@ def main():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (the reference "
                          "reading for the HBM byte counters), then exit")
+    ap.add_argument("--stress", type=int, default=0, metavar="REPS",
+                    help="only time the HBM-bound steps at full size: trace generation of the c4 trace "
+                         "and screening of the c4 plans tiled REPS times, then exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -96,6 +157,11 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": n, "launches": 3}), flush=True)
+        return
+
+    if args.stress > 0:
+        torch.cuda.set_device(0)
+        stress(args.stress, max(1, args.steps))
         return
 
     from paper_2512_14098_amd import cf, pipeline

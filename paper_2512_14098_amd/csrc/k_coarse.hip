@@ -2,10 +2,11 @@
 // (Sec. 4.3, Alg. 2): flow-based throughput estimation with redundancy
 // pruning and the GPU budget of Eq. (1).
 //
-// One thread per plan streams the plan's structure-of-arrays record
-// (coalesced across the wave), accumulates the per-node demand u_v in LDS in
-// the fixed order (type, alternative, component), and writes R_d, the
-// bottleneck node and the flag bits.  Per-type means of X and of the output
+// One thread per plan loads the fields of the plan's structure-of-arrays
+// record it needs (coalesced across the wave, all loads independent),
+// accumulates the per-node demand u_v in LDS in the fixed order (type,
+// alternative, component), and writes R_d, the bottleneck node and the flag
+// bits.  Per-type means of X and of the output
 // length are computed once per block from the moments.
 #include "cf_internal.h"
 
@@ -25,6 +26,8 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
   __shared__ double ex_s[CF_MAX_TYPES][CF_MAX_COMP];
   __shared__ double en_s[CF_MAX_TYPES][CF_MAX_COMP];
   __shared__ double u_s[CF_MAX_NODES][kBlock];
+  __shared__ uint16_t b_s[CF_MAX_NODES][kBlock];  // node batch
+  __shared__ uint8_t c_s[CF_MAX_NODES][kBlock];   // node component set
   const int tid = threadIdx.x;
   if (tid < m.nt * m.nc) {
     const int t = tid / m.nc, c = tid % m.nc;
@@ -48,32 +51,84 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
   if (p >= pv.P) return;
   const size_t P = (size_t)pv.P;
 #define AT(arr, slot) (arr)[(size_t)(slot) * P + (size_t)p]
+  // Every field the plan's evaluation needs is loaded first, with no load
+  // depending on another (one memory latency per plan instead of one per
+  // field); slots past the plan's node count and alternatives past its
+  // count are not fetched.
   const int nv = pv.n_nodes[p];
+  uint32_t rep[CF_MAX_NODES], gp[CF_MAX_NODES];
+#pragma unroll
+  for (int v = 0; v < CF_MAX_NODES; v++) {
+    uint32_t cm = 0, b = 0;
+    rep[v] = 0;
+    gp[v] = 0;
+    if (v < nv) {
+      cm = AT(pv.node_comp, v);
+      rep[v] = AT(pv.node_rep, v);
+      b = AT(pv.node_batch, v);
+      gp[v] = AT(pv.node_gpus, v);
+    }
+    c_s[v][tid] = (uint8_t)cm;
+    b_s[v][tid] = (uint16_t)b;
+  }
   bool valid = nv >= 1 && nv <= CF_MAX_NODES;
   int execs = 0;
-  uint32_t cm[CF_MAX_NODES];
+#pragma unroll
   for (int v = 0; v < CF_MAX_NODES; v++) {
-    cm[v] = 0;
     if (v < nv) {
-      cm[v] = AT(pv.node_comp, v);
-      const int rep = AT(pv.node_rep, v), b = AT(pv.node_batch, v);
-      if (cm[v] == 0 || (cm[v] >> m.nc) || rep < 1 || b < 1 || b > CF_MAX_BATCH || AT(pv.node_gpus, v) < 1)
-        valid = false;
-      execs += rep;
+      const uint32_t cm = c_s[v][tid], b = b_s[v][tid];
+      if (cm == 0 || (cm >> m.nc) || rep[v] < 1 || b < 1 || b > CF_MAX_BATCH || gp[v] < 1) valid = false;
+      execs += (int)rep[v];
     }
   }
   if (execs > CF_MAX_EXEC) valid = false;
-  for (int t = 0; t < m.nt && valid; t++) {
-    const int na = AT(pv.n_alt, t);
-    if (na < 1 || na > 2) { valid = false; break; }
-    for (int a = 0; a < na && valid; a++) {
-      if (na > 1 && AT(pv.alt_w, 2 * t + a) < 1) valid = false;
-      uint32_t path = m.path[t];
-      while (path) {
-        const int c = __ffs(path) - 1;
-        path &= path - 1;
-        const int v = AT(pv.alt_node, (2 * t + a) * 8 + c);
-        if (v >= nv || !((cm[v] >> c) & 1u)) { valid = false; break; }
+  if (!valid) {
+    rd[p] = 0.0;
+    bott[p] = -1;
+    flags[p] = CF_FLAG_INVALID;
+    return;
+  }
+  // per type: the routes of both alternatives are loaded together, then
+  // checked and accumulated: u_v += (pi_t q_a) w in the order t, a, c
+  for (int v = 0; v < nv; v++) u_s[v][tid] = 0.0;
+  const double wsum = (double)m.wsum;
+  for (int t = 0; t < m.nt; t++) {
+    const uint32_t path = m.path[t];
+    const uint32_t na = AT(pv.n_alt, t);
+    uint32_t wl[2], nd[2][CF_MAX_COMP];
+#pragma unroll
+    for (int a = 0; a < 2; a++) {
+      wl[a] = AT(pv.alt_w, 2 * t + a);
+#pragma unroll
+      for (int c = 0; c < CF_MAX_COMP; c++) nd[a][c] = ((path >> c) & 1u) ? AT(pv.alt_node, (2 * t + a) * 8 + c) : 0u;
+    }
+    if (na < 1 || na > 2) {
+      valid = false;
+      break;
+    }
+    const double pi = (double)m.weight[t] / wsum;
+    const uint32_t wtot = na > 1 ? wl[0] + wl[1] : 1u;
+#pragma unroll
+    for (int a = 0; a < 2; a++) {
+      if (a < (int)na) {
+        if (na > 1 && wl[a] < 1) valid = false;
+        const uint32_t wa = na > 1 ? wl[a] : 1u;
+        const double q = (double)wa / (double)wtot;
+        const double pq = pi * q;
+#pragma unroll
+        for (int c = 0; c < CF_MAX_COMP; c++) {
+          if (!((path >> c) & 1u)) continue;
+          const int v = (int)nd[a][c];
+          if (v >= nv || !((c_s[v][tid] >> c) & 1u)) {
+            valid = false;
+            continue;
+          }
+          const int bn = b_s[v][tid];
+          const double B = (double)(bn < m.cap[c] ? bn : m.cap[c]);
+          double w = ((m.k0[c] / B) + m.k1[c] * ex_s[t][c]) + m.k2[c];
+          if (m.kind[c] == CF_LLM) w = w + (en_s[t][c] - 1.0) * ((m.d0[c] / B) + m.d1[c]);
+          u_s[v][tid] = u_s[v][tid] + pq * w;
+        }
       }
     }
   }
@@ -83,47 +138,28 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
     flags[p] = CF_FLAG_INVALID;
     return;
   }
-  for (int v = 0; v < nv; v++) u_s[v][tid] = 0.0;
-  const double wsum = (double)m.wsum;
-  for (int t = 0; t < m.nt; t++) {
-    const double pi = (double)m.weight[t] / wsum;
-    const int na = AT(pv.n_alt, t);
-    uint32_t wtot = 0;
-    for (int a = 0; a < na; a++) wtot += na > 1 ? AT(pv.alt_w, 2 * t + a) : 1u;
-    for (int a = 0; a < na; a++) {
-      const uint32_t wa = na > 1 ? AT(pv.alt_w, 2 * t + a) : 1u;
-      const double q = (double)wa / (double)wtot;
-      const double pq = pi * q;
-      uint32_t path = m.path[t];
-      while (path) {
-        const int c = __ffs(path) - 1;
-        path &= path - 1;
-        const int v = AT(pv.alt_node, (2 * t + a) * 8 + c);
-        const int bn = AT(pv.node_batch, v);
-        const double B = (double)(bn < m.cap[c] ? bn : m.cap[c]);
-        double w = ((m.k0[c] / B) + m.k1[c] * ex_s[t][c]) + m.k2[c];
-        if (m.kind[c] == CF_LLM) w = w + (en_s[t][c] - 1.0) * ((m.d0[c] / B) + m.d1[c]);
-        u_s[v][tid] = u_s[v][tid] + pq * w;
+  double best = __builtin_inf();
+  int bn = -1;
+  bool redundant = false;
+  uint64_t gpus = 0;
+#pragma unroll
+  for (int v = 0; v < CF_MAX_NODES; v++) {
+    if (v < nv) {
+      const double u = u_s[v][tid];
+      if (u > 0.0) {
+        const double r = (double)rep[v] / u;
+        if (r < best) { best = r; bn = v; }
       }
     }
   }
-  double best = __builtin_inf();
-  int bn = -1;
-  for (int v = 0; v < nv; v++) {
-    const double u = u_s[v][tid];
-    if (u > 0.0) {
-      const double r = (double)AT(pv.node_rep, v) / u;
-      if (r < best) { best = r; bn = v; }
+#pragma unroll
+  for (int v = 0; v < CF_MAX_NODES; v++) {
+    if (v < nv) {
+      const double u = u_s[v][tid];
+      gpus += (uint64_t)rep[v] * gp[v];
+      if (u == 0.0) redundant = true;
+      else if (rep[v] >= 2 && (double)(rep[v] - 1) / u >= best) redundant = true;
     }
-  }
-  bool redundant = false;
-  uint64_t gpus = 0;
-  for (int v = 0; v < nv; v++) {
-    const int rep = AT(pv.node_rep, v);
-    const double u = u_s[v][tid];
-    gpus += (uint64_t)rep * AT(pv.node_gpus, v);
-    if (u == 0.0) redundant = true;
-    else if (rep >= 2 && (double)(rep - 1) / u >= best) redundant = true;
   }
   const bool over = gpus > (uint64_t)n_gpus;
   rd[p] = best;
