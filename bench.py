@@ -133,6 +133,9 @@ def main():
     ap.add_argument("--seeds", type=int, default=0, metavar="N",
                     help="simulate only the first N seeds of the workload (a sample of a workload "
                          "too large to run whole; stated in the output)")
+    ap.add_argument("--plans", type=int, default=0, metavar="N",
+                    help="simulate only the first N plans phase 1 selects (a sample of a workload too "
+                         "large to run whole; stated in the output)")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -173,6 +176,9 @@ def main():
     all_seeds = seeds_of(cfg)
     seeds = all_seeds[: args.seeds] if args.seeds > 0 else all_seeds
     w = pipeline.Workload(cfg, seeds=seeds)
+    full_top = w.top_k
+    if args.plans > 0:
+        w.top_k = min(w.top_k, args.plans)
     for i in range(args.warmup):
         out = pipeline.run_step(w)
         torch.cuda.synchronize()
@@ -203,8 +209,13 @@ def main():
     achieved = OPS_PER_EVENT * ev_step / fine_avg_s / 1e12
     n_sel = int(out["ids"].numel())
     workload = "%s: %s" % (args.config, w.cfg["summary"])
+    sample = []
+    if args.plans > 0 and w.top_k < full_top:
+        sample.append("first %d of its %d selected plans" % (w.top_k, full_top))
     if len(seeds) < len(all_seeds):
-        workload += " (sample: first %d of its %d seeds)" % (len(seeds), len(all_seeds))
+        sample.append("first %d of its %d seeds" % (len(seeds), len(all_seeds)))
+    if sample:
+        workload += " (sample: %s)" % ", ".join(sample)
     res = {
         "metric": METRIC,
         "value": events / elapsed,

@@ -68,6 +68,16 @@ enum { DL_DELIVER = 0, DL_TICK = 1 };
 constexpr uint32_t MISC_OUTS = 15u;     // outputs still to finish
 constexpr uint32_t MISC_TH_DONE = 16u;  // thinker finished
 constexpr uint32_t MARK = 0x80000000u;  // gated running slot: in the current decode step
+// A gated stage's running slot word: tokens so far (bits 0..15), the
+// request's own token count at the stage (bits 16..30), MARK (bit 31).
+constexpr uint32_t RK_TOK = 0xFFFFu;
+__device__ __forceinline__ uint32_t rk_own(uint32_t v) { return (v >> 16) & 0x7FFFu; }
+// k_fine<true>: gate word of a gated stage's running slot, fixed when the
+// request joined: the request's type is gated at the stage (bit 31), its
+// thinker component (bits 24..26), the thinker's executor (bits 16..21) and
+// the thinker's token count (bits 0..15); run_q holds the request's join
+// step in the thinker's stage.
+constexpr uint32_t RG_GATED = 0x80000000u;
 constexpr uint32_t EX_RUN = 1u << 21;   // executor state: busy with a multi-step decode run
 // k_fine<true>: executor state kind of a joint thinker/talker run (IT_FINISH
 // is a member kind only); the talker's stage index is in bits 22..25
@@ -89,7 +99,7 @@ struct __attribute__((aligned(32))) Tim {
 
 struct Layout {
   size_t rec, tim;
-  size_t run_r, run_k, hist, mem, dl_t, dl_v, pool, pool_next, pool_free;
+  size_t run_r, run_k, run_g, run_q, hist, mem, dl_t, dl_v, pool, pool_next, pool_free;
   size_t bytes;
   int run_cap, hist_slots, n_chunks;
   uint32_t dl_mask;
@@ -262,7 +272,7 @@ struct Sim {
   GPtr<Rec> rec;
   GPtr<Tim> tim;
   GPtr<double> hist, dl_t;
-  GPtr<uint32_t> run_r, run_k, mem, dl_v, pool;
+  GPtr<uint32_t> run_r, run_k, run_g, run_q, mem, dl_v, pool;
   GPtr<int> pool_next, pool_free;
   size_t soff;
   double lam, now, dl_head_t, t_arr;
@@ -550,6 +560,51 @@ __device__ __forceinline__ double slot_vis(const Sim &S, uint32_t r, uint32_t to
   return token_vis(S, r, R.misc, th, xth, x, k, nth, wsi, undecided);
 }
 
+// k_fine<true>: slot_vis from the slot's gate word g and thinker join step
+// q0, without reading the request's record or trace: the step's ring entry
+// is the time of its token (for a finished thinker's last token too, while
+// that step is kept in the ring).
+__device__ __forceinline__ double slot_vis_g(const Sim &S, uint32_t r, uint32_t g, uint32_t q0, uint32_t tok, int x,
+                                             int &xth, int &wsi, bool &undecided) {
+  xth = x;
+  wsi = -1;
+  if (!(g & RG_GATED)) return -__builtin_inf();
+  const int th = (int)((g >> 24) & 7u);
+  xth = (int)((g >> 16) & 63u);
+  const uint32_t nth = g & 0xFFFFu;
+  const uint32_t k = tok + 1u < nth ? tok + 1u : nth;
+  const double delta = (xth == x) ? 0.0 : S.A->m.comm;
+  double e;
+  if (k <= 1) {
+    e = S.tim[r].tfirst;
+  } else {
+    const int lx = S.si.lsi[stage_of(S, xth, th)];
+    const int slot = S.si.hist[lx];
+    const uint32_t q = q0 + k - 1u;
+    if (q > S.si.sched[slot]) {
+      wsi = slot;
+      return __builtin_inf();
+    }
+    const uint32_t it = S.si.iter[lx];
+    const GPtr<double> h = S.hist + (uint32_t)(slot * kRing);
+    if (q > it) {
+      wsi = slot;  // predicted end of a step of the running decode run
+      e = h[q & (kRing - 1)];
+    } else if (it - q < (uint32_t)kKeep) {
+      e = h[q & (kRing - 1)];
+    } else if (k == nth && (S.rec[r].misc & MISC_TH_DONE)) {
+      e = S.tim[r].tlast;
+    } else {
+      e = h[(it - (kKeep - 1)) & (kRing - 1)];  // oldest kept step: token k is no later
+      if (!(e + delta <= S.now)) {
+        undecided = true;
+        return __builtin_inf();
+      }
+    }
+  }
+  return e + delta;
+}
+
 template <bool G>
 __device__ __forceinline__ bool eligible(const Sim &S, uint32_t r, uint32_t tok, int c, int x, bool &undecided) {
   if constexpr (G) {
@@ -651,7 +706,7 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
     bool fin = valid;
     bool stream = false;  // thinker: deliver to the talker now
     int ta = 0;
-    uint32_t key = 0;
+    uint32_t key = 0, gw = 0, gq = 0;
     if (valid && kind == IT_PREFILL) {
       const uint32_t no = nout_of(S, r, t, c);
       if (c == ml.ttft_c[t]) {
@@ -664,7 +719,12 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
         ta = ml.ta_c[t];
       }
       fin = no == 1;
-      key = gated ? 1u : iter_s + no - 1u;
+      key = gated ? (1u | (no << 16)) : iter_s + no - 1u;
+      if (gated && ml.ta_c[t] == c) {
+        const int th = ml.th_c[t];
+        gw = RG_GATED | ((uint32_t)th << 24) | ((uint32_t)ex_byte(R.ex, th) << 16) | nout_of(S, r, t, th);
+        gq = S.tim[r].thjoin;
+      }
     } else if (valid && kind == IT_FINISH) {
       if (c == ml.ttft_c[t]) S.tim[r].tlast = now;
     }
@@ -742,6 +802,10 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
         const int pos = rn + (int)lanes_below(abal);
         S.run_r[S.si.roff[lx] + pos] = r;
         S.run_k[S.si.roff[lx] + pos] = key;
+        if (gated) {
+          S.run_g[S.si.roff[lx] + pos] = gw;
+          S.run_q[S.si.roff[lx] + pos] = gq;
+        }
       }
       S.si.rn[lx] = rn + __popcll(abal);
       if (!gated) {
@@ -870,14 +934,22 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     const int rn = S.si.rn[lx];
     const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lx];
     const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
+    const GPtr<uint32_t> rg = S.run_g + (uint32_t)S.si.roff[lx];
+    const GPtr<uint32_t> rq = S.run_q + (uint32_t)S.si.roff[lx];
     uint32_t cntm = 0;
     bool undecided = false;
     for (int b = 0; b < rn; b += 64) {
       const int j = b + lane_id();
       if (j < rn) {
-        const uint32_t tok = rk[j] & 0xFFFFu;
-        const bool el = eligible<G>(S, rr[j], tok, c, x, undecided);
-        rk[j] = el ? (tok | MARK) : tok;
+        const uint32_t v = rk[j];
+        bool el;
+        if constexpr (G) {
+          int xth, wsi;
+          el = slot_vis_g(S, rr[j], rg[j], rq[j], v & RK_TOK, x, xth, wsi, undecided) <= S.now;
+        } else {
+          el = eligible<G>(S, rr[j], v & RK_TOK, c, x, undecided);
+        }
+        rk[j] = el ? (v | MARK) : (v & ~MARK);
         cntm += el ? 1u : 0u;
       }
     }
@@ -913,11 +985,20 @@ __device__ int runnable_kind(Sim &S, int x, int si, int c) {
   if (!(fl & SF_GATED)) return IT_DECODE;
   const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lx];
   const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
+  const GPtr<uint32_t> rg = S.run_g + (uint32_t)S.si.roff[lx];
+  const GPtr<uint32_t> rq = S.run_q + (uint32_t)S.si.roff[lx];
   bool any = false, undecided = false;
   for (int b = 0; b < rn && !any; b += 64) {
     const int j = b + lane_id();
     bool el = false;
-    if (j < rn) el = eligible<G>(S, rr[j], rk[j] & 0xFFFFu, c, x, undecided);
+    if (j < rn) {
+      if constexpr (G) {
+        int xth, wsi;
+        el = slot_vis_g(S, rr[j], rg[j], rq[j], rk[j] & RK_TOK, x, xth, wsi, undecided) <= S.now;
+      } else {
+        el = eligible<G>(S, rr[j], rk[j] & RK_TOK, c, x, undecided);
+      }
+    }
     any = __ballot(el) != 0;
   }
   if (__ballot(undecided)) S.status |= CF_ST_OVERFLOW;
@@ -949,27 +1030,27 @@ __device__ __forceinline__ GateView local_gate_view(const Sim &S, int x, int si)
     if (rn == 0) continue;
     nbusy++;
     gsi = g;
-    const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lg];
     const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lg];
+    const GPtr<uint32_t> rg = S.run_g + (uint32_t)S.si.roff[lg];
+    const GPtr<uint32_t> rq = S.run_q + (uint32_t)S.si.roff[lg];
     for (int b = 0; b < rn; b += 64) {
       const int j = b + lane_id();
       if (j < rn) {
-        const uint32_t r = rr[j];
-        const Rec R = rec_get(S, r);
-        const int t = rtype(R.misc);
-        const uint32_t tok = rk[j] & 0xFFFFu;
+        const uint32_t v = rk[j], g = rg[j];
+        const uint32_t tok = v & RK_TOK;
         bool waits_next = false;
-        if (S.sh->ml.ta_c[t] == c && S.sh->ml.th_c[t] == cth && ex_byte(R.ex, cth) == x) {
-          const uint32_t nth = nout_of(S, r, t, cth);
+        if ((g & RG_GATED) && (int)((g >> 24) & 7u) == cth && (int)((g >> 16) & 63u) == x) {
+          const uint32_t nth = g & 0xFFFFu;
           const uint32_t k = tok + 1u < nth ? tok + 1u : nth;
-          if (k > 1u && !((R.misc & MISC_TH_DONE) && k == nth)) {
-            const uint32_t q = S.tim[r].thjoin + k - 1u;
+          const uint32_t q = rq[j] + k - 1u;
+          // a thinker on this executor has finished once its last step is completed
+          if (k > 1u && !(k == nth && q < next)) {
             qmin = q < qmin ? q : qmin;
             waits_next = q == next;
           }
         }
         other |= !waits_next;
-        const uint32_t left = nout_of(S, r, t, c) - tok;
+        const uint32_t left = rk_own(v) - tok;
         kta = left < kta ? left : kta;
       }
     }
@@ -1127,7 +1208,10 @@ __device__ void run_compact(Sim &S, int si, const bool *drop) {
   const int rn = S.si.rn[lx];
   const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lx];
   const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
-  uint32_t vr[CF_MAX_BATCH / 64], vk[CF_MAX_BATCH / 64];
+  const GPtr<uint32_t> rg = S.run_g + (uint32_t)S.si.roff[lx];
+  const GPtr<uint32_t> rq = S.run_q + (uint32_t)S.si.roff[lx];
+  const bool gated = G && (S.si.flags[si] & SF_GATED);  // k_fine<true>: gate words move with their slots
+  uint32_t vr[CF_MAX_BATCH / 64], vk[CF_MAX_BATCH / 64], vg[CF_MAX_BATCH / 64], vq[CF_MAX_BATCH / 64];
   bool keep[CF_MAX_BATCH / 64];
 #pragma unroll
   for (int p = 0; p < CF_MAX_BATCH / 64; p++) {
@@ -1135,9 +1219,15 @@ __device__ void run_compact(Sim &S, int si, const bool *drop) {
     keep[p] = false;
     vr[p] = 0;
     vk[p] = 0;
+    vg[p] = 0;
+    vq[p] = 0;
     if (j < rn) {
       vr[p] = rr[j];
       vk[p] = rk[j];
+      if (gated) {
+        vg[p] = rg[j];
+        vq[p] = rq[j];
+      }
       keep[p] = !drop[p];
     }
   }
@@ -1150,6 +1240,10 @@ __device__ void run_compact(Sim &S, int si, const bool *drop) {
       const uint32_t d = w + lanes_below(bal);
       rr[d] = vr[p];
       rk[d] = vk[p];
+      if (gated) {
+        rg[d] = vg[p];
+        rq[d] = vq[p];
+      }
       mn = vk[p] < mn ? vk[p] : mn;
     }
     w += (uint32_t)__popcll(bal);
@@ -1215,10 +1309,10 @@ __device__ __forceinline__ void complete_joint(Sim &S, int x, uint32_t st) {
     const int j = p * 64 + lane_id();
     fin[p] = false;
     if (j < rng) {
-      const uint32_t r = rrg[j];
-      const uint32_t tok = (rkg[j] & 0xFFFFu) + nta_s;
-      rkg[j] = tok;
-      fin[p] = !(n & 1u) && tok == nout_of(S, r, rtype(S.rec[r].misc), cta);
+      const uint32_t v = rkg[j];
+      const uint32_t tok = (v & RK_TOK) + nta_s;
+      rkg[j] = (v & (0x7FFFu << 16)) | tok;
+      fin[p] = !(n & 1u) && tok == rk_own(v);
     }
   }
   S.events += (uint64_t)rng * (uint64_t)nta_s;
@@ -1298,11 +1392,10 @@ __device__ __forceinline__ void complete_iter(Sim &S, int x) {
       if (j < rn) {
         const uint32_t v = rk[j];
         if (v & MARK) {
-          const uint32_t r = rr[j];
-          const uint32_t tok = (v & 0xFFFFu) + 1u;
-          rk[j] = tok;
+          const uint32_t tok = (v & RK_TOK) + 1u;
+          rk[j] = (v & (0x7FFFu << 16)) | tok;
           part++;
-          fin[p] = tok == nout_of(S, r, rtype(S.rec[r].misc), c);
+          fin[p] = tok == rk_own(v);
         }
       }
     }
@@ -1338,11 +1431,13 @@ __device__ __forceinline__ bool gate_wake(Sim &S, int y) {
       const int c = S.si.comp[g], rn = S.si.rn[lg];
       const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lg];
       const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lg];
+      const GPtr<uint32_t> rg = S.run_g + (uint32_t)S.si.roff[lg];
+      const GPtr<uint32_t> rq = S.run_q + (uint32_t)S.si.roff[lg];
       for (int b = 0; b < rn; b += 64) {
         const int j = b + lane_id();
         if (j < rn) {
           int xth, wsi;
-          const double tv = slot_vis(S, rr[j], rk[j] & 0xFFFFu, c, y, xth, wsi, undecided);
+          const double tv = slot_vis_g(S, rr[j], rg[j], rq[j], rk[j] & RK_TOK, y, xth, wsi, undecided);
           if (xth != y) {
             if (wsi >= 0) atomicOr((unsigned long long *)&S.si.watch[wsi], 1ull << y);
             if (tv <= S.now) now_el = true;
@@ -1599,6 +1694,8 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
   S.tim = gptr_at<Tim>(slab, L.tim);
   S.run_r = gptr_at<uint32_t>(slab, L.run_r);
   S.run_k = gptr_at<uint32_t>(slab, L.run_k);
+  S.run_g = gptr_at<uint32_t>(slab, L.run_g);
+  S.run_q = gptr_at<uint32_t>(slab, L.run_q);
   S.hist = gptr_at<double>(slab, L.hist);
   S.mem = gptr_at<uint32_t>(slab, L.mem);
   S.dl_t = gptr_at<double>(slab, L.dl_t);
@@ -1787,6 +1884,8 @@ Layout make_layout(const KModel &m, int n) {
   L.tim = take(sizeof(Tim) * (size_t)n);
   L.run_r = take(4 * (size_t)L.run_cap);
   L.run_k = take(4 * (size_t)L.run_cap);
+  L.run_g = take(4 * (size_t)L.run_cap);
+  L.run_q = take(4 * (size_t)L.run_cap);
   L.hist = take(8 * (size_t)L.hist_slots * (m.gated_mask ? kRing : kHist) + 8);
   L.mem = take(4 * (size_t)CF_MAX_EXEC * CF_MAX_BATCH);
   size_t dl = 4096;
