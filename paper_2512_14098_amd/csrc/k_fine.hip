@@ -284,6 +284,8 @@ struct Sim {
   double *wake;        // per executor with a gated stage: next visibility time of a blocked request
   double *dur2;        // per executor in a joint run: duration of its talker steps
   uint64_t rewake;     // executors whose wake time is to be recomputed in this instant
+  int gmark_si;        // gated stage whose running slots runnable_kind has just marked (-1: none)
+  uint32_t gmark_n;    // the number of slots it marked eligible
 };
 
 __device__ __forceinline__ Rec rec_get(const Sim &S, uint32_t r) {
@@ -937,25 +939,30 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     const GPtr<uint32_t> rg = S.run_g + (uint32_t)S.si.roff[lx];
     const GPtr<uint32_t> rq = S.run_q + (uint32_t)S.si.roff[lx];
     uint32_t cntm = 0;
-    bool undecided = false;
-    for (int b = 0; b < rn; b += 64) {
-      const int j = b + lane_id();
-      if (j < rn) {
-        const uint32_t v = rk[j];
-        bool el;
-        if constexpr (G) {
-          int xth, wsi;
-          el = slot_vis_g(S, rr[j], rg[j], rq[j], v & RK_TOK, x, xth, wsi, undecided) <= S.now;
-        } else {
-          el = eligible<G>(S, rr[j], v & RK_TOK, c, x, undecided);
+    if (G && S.gmark_si == si) {
+      cntm = S.gmark_n;  // marked by runnable_kind in this instant
+    } else {
+      bool undecided = false;
+      for (int b = 0; b < rn; b += 64) {
+        const int j = b + lane_id();
+        if (j < rn) {
+          const uint32_t v = rk[j];
+          bool el;
+          if constexpr (G) {
+            int xth, wsi;
+            el = slot_vis_g(S, rr[j], rg[j], rq[j], v & RK_TOK, x, xth, wsi, undecided) <= S.now;
+          } else {
+            el = eligible<G>(S, rr[j], v & RK_TOK, c, x, undecided);
+          }
+          rk[j] = el ? (v | MARK) : (v & ~MARK);
+          cntm += el ? 1u : 0u;
         }
-        rk[j] = el ? (v | MARK) : (v & ~MARK);
-        cntm += el ? 1u : 0u;
       }
+      if (__ballot(undecided)) S.status |= CF_ST_OVERFLOW;
+      cntm = dpp_sum_u32(cntm);
+      __syncthreads();
     }
-    if (__ballot(undecided)) S.status |= CF_ST_OVERFLOW;
-    cntm = dpp_sum_u32(cntm);
-    __syncthreads();
+    S.gmark_si = -1;
     dur = m.d0[c] + m.d1[c] * (double)cntm;
     nmem = (int)cntm;
     if constexpr (G) {
@@ -988,18 +995,32 @@ __device__ int runnable_kind(Sim &S, int x, int si, int c) {
   const GPtr<uint32_t> rg = S.run_g + (uint32_t)S.si.roff[lx];
   const GPtr<uint32_t> rq = S.run_q + (uint32_t)S.si.roff[lx];
   bool any = false, undecided = false;
-  for (int b = 0; b < rn && !any; b += 64) {
-    const int j = b + lane_id();
-    bool el = false;
-    if (j < rn) {
-      if constexpr (G) {
+  if constexpr (G) {
+    // k_fine<true>: mark every eligible slot now; a decode step started on
+    // this stage in the same instant takes the marks as they are
+    uint32_t cnt = 0;
+    for (int b = 0; b < rn; b += 64) {
+      const int j = b + lane_id();
+      if (j < rn) {
+        const uint32_t v = rk[j];
         int xth, wsi;
-        el = slot_vis_g(S, rr[j], rg[j], rq[j], rk[j] & RK_TOK, x, xth, wsi, undecided) <= S.now;
-      } else {
-        el = eligible<G>(S, rr[j], rk[j] & RK_TOK, c, x, undecided);
+        const bool el = slot_vis_g(S, rr[j], rg[j], rq[j], v & RK_TOK, x, xth, wsi, undecided) <= S.now;
+        rk[j] = el ? (v | MARK) : (v & ~MARK);
+        cnt += el ? 1u : 0u;
       }
     }
-    any = __ballot(el) != 0;
+    cnt = dpp_sum_u32(cnt);
+    __syncthreads();
+    S.gmark_si = si;
+    S.gmark_n = cnt;
+    any = cnt > 0;
+  } else {
+    for (int b = 0; b < rn && !any; b += 64) {
+      const int j = b + lane_id();
+      bool el = false;
+      if (j < rn) el = eligible<G>(S, rr[j], rk[j] & RK_TOK, c, x, undecided);
+      any = __ballot(el) != 0;
+    }
   }
   if (__ballot(undecided)) S.status |= CF_ST_OVERFLOW;
   return any ? IT_DECODE : -1;
@@ -1720,6 +1741,7 @@ __global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
     S.events = 0;
     S.status = 0;
     S.dirty = 0;
+    S.gmark_si = -1;
     S.dl_head = S.dl_tail = 0;
     S.dl_head_t = __builtin_inf();
     S.pool_top = 0;
