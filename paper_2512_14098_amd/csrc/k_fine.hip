@@ -1641,7 +1641,9 @@ __device__ bool setup_plan(Sim &S, int p) {
 extern __shared__ char dyn_lds[];
 
 template <bool G>
-__global__ void __launch_bounds__(64) k_fine(const FineArgs *__restrict__ Ap) {
+// k_fine<false> is held to 72 VGPRs (7 wavefronts per SIMD); k_fine<true>,
+// whose LDS table allows fewer wavefronts per CU, to 128.
+__global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restrict__ Ap) {
   __shared__ WaveShared sh;
   const FineArgs &A = *Ap;
   const KModel &m = A.m;
@@ -2012,7 +2014,9 @@ extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_tabl
   st = hip_check(hipStreamSynchronize(s), "stage count sync");
   if (st != CF_OK) return st;
   auto round64 = [](unsigned int v) { return v < 64u ? 64 : (int)((v + 63u) & ~63u); };
-  a.nsi_cap = round64(caps[0]);
+  // k_fine<false>'s table needs 8-entry alignment only; a small table leaves room for more wavefronts per CU
+  auto round16 = [](unsigned int v) { return v < 16u ? 16 : (int)((v + 15u) & ~15u); };
+  a.nsi_cap = a.m.gated_mask ? round64(caps[0]) : round16(caps[0]);
   a.nl_cap = round64(caps[1]);
   a.nt_cap = round64(caps[2]);
   const size_t lds = a.m.gated_mask ? kSiBytesG * (size_t)a.nsi_cap + kLlmBytesG * (size_t)a.nl_cap +
