@@ -19,11 +19,12 @@ sys.path.insert(0, ROOT)
 METRIC = "simulated request-events/sec and candidate plans fully evaluated/sec, 1 GPU"
 PEAK_LANE_OPS = 256 * 4 * 16 * 2.4e9 / 1e12  # T lane-ops/s: CUs x SIMDs x lanes x clock
 OPS_PER_EVENT = 4.0  # algorithmic lane-ops per request-event
-KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_fine.hip", "paper_2512_14098_amd/csrc/cf_internal.h")
+KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_fine.hip", "paper_2512_14098_amd/csrc/cf_internal.h",
+                  "paper_2512_14098_amd/csrc/cf_run.h")
 # HBM bytes per k_fine launch from rocprofv3 counters (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0,
 # the scale factors a plain 1 GiB device copy gives), keyed by the kernel source the counters
-# were taken on and the workload; any other source or workload reports null
-MEASURED_TRAFFIC = {("83b7a0ab926c84c5", "c1"): 9.355e11}
+# were taken on and the workload (with its sample); any other source or workload reports null
+MEASURED_TRAFFIC = {}
 
 
 def kernel_source_id():
@@ -237,7 +238,7 @@ def main():
                    "stage_ms": {k: sum(v) / len(v) for k, v in stage_ms.items()}},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_LANE_OPS, "unit": "TOP/s",
                      "frac": achieved / PEAK_LANE_OPS,
-                     "traffic": MEASURED_TRAFFIC.get((kernel_source_id(), args.config)),
+                     "traffic": MEASURED_TRAFFIC.get((kernel_source_id(), workload)),
                      "kernel": "k_fine", "ops_per_event": OPS_PER_EVENT,
                      "kernel_ms": sum(fine_ms) / len(fine_ms)},
     }
