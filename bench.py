@@ -24,7 +24,13 @@ KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_fine.hip", "paper_2512_14098_amd/
 # HBM bytes per k_fine launch from rocprofv3 counters (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0,
 # the scale factors a plain 1 GiB device copy gives), keyed by the kernel source the counters
 # were taken on and the workload (with its sample); any other source or workload reports null
-MEASURED_TRAFFIC = {}
+MEASURED_TRAFFIC = {
+    ("89c98c7ebdbec7d6", "c1: MLLM graph E->L on 8 simulated GPUs (7B LLM, 600M ViT); ~1000 plans; "
+     "16-point rate grid; 32 seeds x 10000 requests"): 2.0785e12,
+    ("89c98c7ebdbec7d6", "c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse "
+     "screening of 10^6 sampled plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 "
+     "requests (sample: first 250 of its 1000 selected plans, first 1 of its 64 seeds)"): 4.293e12,
+}
 
 
 def kernel_source_id():
