@@ -3,7 +3,8 @@
 //
 // One wavefront simulates one triple; a persistent grid of wavefronts takes
 // triples from an atomic ticket, seed-major so that concurrent wavefronts
-// read the same seed's trace (L2 / MALL reuse).
+// read the same seed's trace (L2 / MALL reuse), and within a seed from the
+// lowest rate up (the costliest triples first).
 //
 // The event structure needs no heap.  Pending times are
 //   - the end of the running iteration of each executor (lane x holds
@@ -1733,9 +1734,12 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
     if (lane == 0) tk = atomicAdd(A.ticket, 1u);
     tk = ru(tk);
     if (tk >= A.total) break;
+    // seed-major, then rate, then plan: a triple costs more the lower its
+    // rate (less batching, more instants per request), so the costliest
+    // triples of a seed are taken first and the launch ends on cheap ones
     const int s = (int)(tk / per_seed);
     const unsigned int rem = tk % per_seed;
-    const int i = (int)(rem / (unsigned)A.K), k = (int)(rem % (unsigned)A.K);
+    const int k = (int)(rem / (unsigned)A.n_plans), i = (int)(rem % (unsigned)A.n_plans);
     const int p = ri(A.plan_ids[i]);
     const size_t oidx = ((size_t)i * A.K + k) * A.S + s;
     S.soff = (size_t)s * A.n;
