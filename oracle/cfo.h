@@ -13,6 +13,8 @@
  *   - request traces (workload with per-type fractions pi_t, Sec. 3.1);
  *   - phase 1 flow-based throughput R_d, bottleneck and redundancy pruning
  *     (Sec. 4.3, Alg. 2 phase 1);
+ *   - phase 2 Monte Carlo latency with occupancy-aware latency scaling and
+ *     Pareto pruning (Sec. 4.3, Alg. 2 phase 2; Sec. 5.2);
  *   - phase 3 request-level simulation of a physical plan at a given rate
  *     (Sec. 4.3, Alg. 2 phase 3; Sec. 5.2 CPU-GPU overlap and communication
  *     overhead);
@@ -114,6 +116,26 @@ int cfo_trace_gen(const cfo_model *m, const uint64_t *seeds, int32_t n_seeds, in
 
 int cfo_eval_coarse(const cfo_model *m, const cfo_plans *pl, const uint64_t *moments /* [T][8] */,
                     int32_t n_gpus, double *rd, int32_t *bottleneck, uint8_t *flags);
+
+/* phase-1 helpers shared inside the oracle: structural validity of plan p,
+ * and the per-node demand u_v (seconds of executor time per request). */
+int cfo_plan_valid(const cfo_model *m, const cfo_plans *pl, int p);
+void cfo_node_demand(const cfo_model *m, const cfo_plans *pl, int p, const uint64_t *moments,
+                     double u[CFO_MAXV]);
+
+/* Phase 2 (Monte Carlo latency with occupancy-aware scaling) for plans
+ * ids[0..n): the first n_sample requests of trace seed seed_idx, routed
+ * through each plan without queueing.  met/cnt are [n][T], gt [n][T] the
+ * per-type goodput alpha R_d pi_t F_t; lat (optional) [n][n_sample][4] =
+ * ttft, tpot, e2e, media of every sampled request. */
+int cfo_eval_mc(const cfo_model *m, const cfo_plans *pl, const int32_t *ids, int32_t n,
+                const double *rd, const uint64_t *moments, double alpha, const cfo_trace *tr,
+                int32_t seed_idx, int32_t n_sample, uint32_t *met, uint32_t *cnt, double *gt,
+                double *lat);
+
+/* Pareto pruning: keep[i] = 0 iff some other vector of g[n][T] is >= in
+ * every component and > in one. */
+int cfo_pareto(const double *g, int32_t n, int32_t T, uint8_t *keep);
 
 int cfo_select_topk(const double *rd, const uint8_t *flags, int32_t P, int32_t k,
                     int32_t *ids, int32_t *n_selected);

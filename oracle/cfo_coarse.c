@@ -24,7 +24,7 @@
 
 /* structural validity of plan p against model m (Eq. 1's ">= 1 executor
  * per node", routes that name a node hosting the component). */
-static int plan_valid(const cfo_model *m, const cfo_plans *pl, int p) {
+int cfo_plan_valid(const cfo_model *m, const cfo_plans *pl, int p) {
   int P = pl->P;
   int nv = pl->n_nodes[p];
   if (nv < 1 || nv > CFO_MAXV) return 0;
@@ -54,56 +54,63 @@ static int plan_valid(const cfo_model *m, const cfo_plans *pl, int p) {
   return 1;
 }
 
+/* u_v: seconds of executor time that one request of the workload mix puts
+ * on node v (summed over its replicas) at the node's configured batch:
+ * u_v += (pi_t * q_a) * w(c, t, B) in the order t, a, c ascending. */
+void cfo_node_demand(const cfo_model *m, const cfo_plans *pl, int p, const uint64_t *moments,
+                     double u[CFO_MAXV]) {
+  int P = pl->P;
+  uint64_t wsum_i = 0;
+  for (int t = 0; t < m->n_types; t++) wsum_i += m->weight[t];
+  double wsum = (double)wsum_i;
+  for (int v = 0; v < CFO_MAXV; v++) u[v] = 0.0;
+  for (int t = 0; t < m->n_types; t++) {
+    const uint64_t *mo = moments + (size_t)t * 8;
+    double pi = (double)m->weight[t] / wsum;
+    int na = P_AT(pl->n_alt, t, P, p);
+    uint64_t wa_sum = 0;
+    for (int a = 0; a < na; a++) wa_sum += (na > 1) ? P_AT(pl->alt_w, t * 2 + a, P, p) : 1u;
+    for (int a = 0; a < na; a++) {
+      uint64_t wa = (na > 1) ? P_AT(pl->alt_w, t * 2 + a, P, p) : 1u;
+      double q = (double)wa / (double)wa_sum;
+      for (int c = 0; c < m->n_comp; c++) {
+        if (!((m->path_mask[t] >> c) & 1u)) continue;
+        int v = P_AT(pl->alt_node, (t * 2 + a) * 8 + c, P, p);
+        int bnode = P_AT(pl->node_batch, v, P, p);
+        int beff = bnode < m->batch_cap[c] ? bnode : m->batch_cap[c];
+        double B = (double)beff;
+        /* per-type mean of X and of the output length */
+        double ex = 0.0, en = 1.0;
+        if (mo[0] > 0) {
+          uint64_t xs = 0;
+          for (int at = 0; at < CFO_NATTR; at++)
+            if ((m->x_sel[c] >> at) & 1u) xs += mo[1 + at];
+          ex = (double)xs / (double)mo[0];
+          if (m->kind[c] == CFO_LLM && !((m->prefill_only[t] >> c) & 1u)) {
+            en = (double)mo[1 + m->nout_attr[c]] / (double)mo[0];
+            if (en < 1.0) en = 1.0;
+          }
+        }
+        /* seconds of executor time per request at batch B */
+        double w = ((m->k0[c] / B) + m->k1[c] * ex) + m->k2[c];
+        if (m->kind[c] == CFO_LLM) w = w + (en - 1.0) * ((m->d0[c] / B) + m->d1[c]);
+        u[v] = u[v] + (pi * q) * w;
+      }
+    }
+  }
+}
+
 int cfo_eval_coarse(const cfo_model *m, const cfo_plans *pl, const uint64_t *moments,
                     int32_t n_gpus, double *rd, int32_t *bottleneck, uint8_t *flags) {
   int P = pl->P;
-  /* workload fractions pi_t = W_t / sum W */
-  double wsum = 0.0;
-  uint64_t wsum_i = 0;
-  for (int t = 0; t < m->n_types; t++) wsum_i += m->weight[t];
-  wsum = (double)wsum_i;
   for (int p = 0; p < P; p++) {
-    if (!plan_valid(m, pl, p)) {
+    if (!cfo_plan_valid(m, pl, p)) {
       rd[p] = 0.0; bottleneck[p] = -1; flags[p] = 4;
       continue;
     }
     int nv = pl->n_nodes[p];
     double u[CFO_MAXV];
-    for (int v = 0; v < CFO_MAXV; v++) u[v] = 0.0;
-    for (int t = 0; t < m->n_types; t++) {
-      const uint64_t *mo = moments + (size_t)t * 8;
-      double pi = (double)m->weight[t] / wsum;
-      int na = P_AT(pl->n_alt, t, P, p);
-      uint64_t wa_sum = 0;
-      for (int a = 0; a < na; a++) wa_sum += (na > 1) ? P_AT(pl->alt_w, t * 2 + a, P, p) : 1u;
-      for (int a = 0; a < na; a++) {
-        uint64_t wa = (na > 1) ? P_AT(pl->alt_w, t * 2 + a, P, p) : 1u;
-        double q = (double)wa / (double)wa_sum;
-        for (int c = 0; c < m->n_comp; c++) {
-          if (!((m->path_mask[t] >> c) & 1u)) continue;
-          int v = P_AT(pl->alt_node, (t * 2 + a) * 8 + c, P, p);
-          int bnode = P_AT(pl->node_batch, v, P, p);
-          int beff = bnode < m->batch_cap[c] ? bnode : m->batch_cap[c];
-          double B = (double)beff;
-          /* per-type mean of X and of the output length */
-          double ex = 0.0, en = 1.0;
-          if (mo[0] > 0) {
-            uint64_t xs = 0;
-            for (int at = 0; at < CFO_NATTR; at++)
-              if ((m->x_sel[c] >> at) & 1u) xs += mo[1 + at];
-            ex = (double)xs / (double)mo[0];
-            if (m->kind[c] == CFO_LLM && !((m->prefill_only[t] >> c) & 1u)) {
-              en = (double)mo[1 + m->nout_attr[c]] / (double)mo[0];
-              if (en < 1.0) en = 1.0;
-            }
-          }
-          /* seconds of executor time per request at batch B */
-          double w = ((m->k0[c] / B) + m->k1[c] * ex) + m->k2[c];
-          if (m->kind[c] == CFO_LLM) w = w + (en - 1.0) * ((m->d0[c] / B) + m->d1[c]);
-          u[v] = u[v] + (pi * q) * w;
-        }
-      }
-    }
+    cfo_node_demand(m, pl, p, moments, u);
     double best = INFINITY;
     int bn = -1;
     for (int v = 0; v < nv; v++) {

@@ -297,6 +297,38 @@ def eval_fine(model, tab, plan_ids, rates, tr, triples=None):
     return met, cnt, events, status
 
 
+def eval_mc(model, tab, plan_ids, rd, moments0, alpha, tr, seed_idx, n_sample, want_lat=False):
+    """Phase 2 (Monte Carlo latency) of plans plan_ids: met, cnt [n, T] u32, goodput G [n, T]
+    and, with want_lat, the latencies [n, n_sample, 4] of every sampled request."""
+    ids = np.ascontiguousarray(plan_ids, np.int32)
+    n, T = len(ids), model.n_types
+    met = np.zeros((n, T), np.uint32)
+    cnt = np.zeros((n, T), np.uint32)
+    gt = np.zeros((n, T), np.float64)
+    lat = np.zeros((n, n_sample, 4), np.float64) if want_lat else None
+    L = lib()
+    L.cfo_eval_mc.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
+                              C.c_double, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
+                              C.c_void_p, C.c_void_p]
+    pst, tst = plans_struct(tab), trace_struct(tr)
+    L.cfo_eval_mc(C.byref(model), C.byref(pst), _ptr(ids), n, _ptr(np.ascontiguousarray(rd, np.float64)),
+                  _ptr(np.ascontiguousarray(moments0, np.uint64)), float(alpha), C.byref(tst),
+                  int(seed_idx), int(n_sample), _ptr(met), _ptr(cnt), _ptr(gt),
+                  _ptr(lat) if lat is not None else None)
+    return (met, cnt, gt, lat) if want_lat else (met, cnt, gt)
+
+
+def pareto(g):
+    """keep[i] = 0 iff another row of g is >= everywhere and > somewhere."""
+    g = np.ascontiguousarray(g, np.float64)
+    n, T = g.shape
+    keep = np.zeros(n, np.uint8)
+    L = lib()
+    L.cfo_pareto.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p]
+    L.cfo_pareto(_ptr(g), n, T, _ptr(keep))
+    return keep
+
+
 def goodput_reduce(met, cnt, rates, theta, n_req):
     n_plans, K, S, T = met.shape
     kstar = np.zeros(n_plans, np.int32)
