@@ -208,6 +208,37 @@ cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_table *plans,
                        int32_t K, const cf_trace *trace, uint32_t flags, const cf_fine_out *out,
                        void *stream);
 
+/* Phase 2 (Sec. 4.3, Alg. 2 phase 2) with occupancy-aware latency scaling
+ * (Sec. 5.2): plan plan_ids_dev[i], i < n_plans, is evaluated on the first
+ * n_sample requests of trace seed seed_idx, each routed through the plan
+ * alone (no queueing).  Every component a request visits costs one
+ * iteration at its effective batch b = clamp(ceil(B * (R_d / R_v)), 1, B)
+ * (B = min(node batch, cap), R_v = m_v / u_v the node's phase-1 capacity):
+ * an encoder or generator a static batch of b such requests, an LLM the
+ * request's own prefill then decode steps d0 + d1 b; a component starts
+ * when its last input arrives (comm later across executors; a gated LLM
+ * after its gate source's first token, each further token after the gate
+ * source's matching token).
+ * rd_dev: phase 1's R_d indexed by plan id ([P]); moments_dev: the [T][8]
+ * moments phase 1 used; alpha in (0, 1].  Outputs (device, caller-owned):
+ * met_dev, cnt_dev [n_plans][T] (sampled requests of each type meeting every
+ * target / in all), goodput_t_dev [n_plans][T] = (alpha R_d) pi_t met/cnt
+ * (0 when cnt = 0), lat_dev optional [n_plans][n_sample][4] = TTFT, TPOT,
+ * E2E, MEDIA of every sampled request (NULL = off).  An invalid plan gets
+ * zeros.  Asynchronous on stream.
+ * Errors: CF_EINVAL (descriptor, sizes, seed_idx or n_sample outside the
+ * trace, alpha). */
+cf_status cf_eval_mc(const cf_model_desc *model, const cf_plan_table *plans, const int32_t *plan_ids_dev,
+                     int32_t n_plans, const double *rd_dev, const uint64_t *moments_dev, double alpha,
+                     const cf_trace *trace, int32_t seed_idx, int32_t n_sample, uint32_t *met_dev,
+                     uint32_t *cnt_dev, double *goodput_t_dev, double *lat_dev, void *stream);
+
+/* Pareto pruning (Alg. 2, after phases 2 and 3): keep_dev[i] = 0 iff some
+ * other row of goodput_t_dev [n][T] (device) is >= in every component and >
+ * in at least one, else 1.  1 <= T <= 8.  Asynchronous on stream.
+ * Errors: CF_EINVAL (sizes, NULL arrays). */
+cf_status cf_pareto(const double *goodput_t_dev, int32_t n, int32_t T, uint8_t *keep_dev, void *stream);
+
 /* Goodput (Sec. 3.2) at the highest feasible rate (Sec. 6.1): M_t, N_t
  * pooled over seeds; rate k feasible iff theta_den*M_t >= theta_num*N_t for
  * every type with N_t > 0; kstar = first infeasible - 1; goodput_t =

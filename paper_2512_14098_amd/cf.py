@@ -83,6 +83,8 @@ def _load():
         "cf_rate_grid": ([vp, vp, i32, i32, dbl, vp, vp], i32),
         "cf_eval_fine": ([vp, vp, vp, i32, vp, i32, vp, u32, vp, vp], i32),
         "cf_goodput_reduce": ([vp, vp, i32, i32, i32, i32, vp, u32, u32, i32, vp, vp, vp, vp], i32),
+        "cf_eval_mc": ([vp, vp, vp, i32, vp, vp, dbl, vp, i32, i32, vp, vp, vp, vp, vp], i32),
+        "cf_pareto": ([vp, i32, i32, vp, vp], i32),
         "cf_select_best": ([vp, i32, vp, vp], i32),
         "cf_math_eval": ([i32, vp, vp, vp, i64, vp], i32),
         "cf_philox_eval": ([vp, vp, vp, i64, vp], i32),
@@ -97,8 +99,8 @@ def _load():
 
 _lib = _load()
 EXPORTED = ("cf_last_error", "cf_status_str", "cf_version", "cf_trace_gen", "cf_eval_coarse",
-            "cf_select_topk", "cf_rate_grid", "cf_eval_fine", "cf_goodput_reduce", "cf_select_best",
-            "cf_math_eval", "cf_philox_eval", "cf_release_scratch")
+            "cf_select_topk", "cf_rate_grid", "cf_eval_fine", "cf_eval_mc", "cf_pareto",
+            "cf_goodput_reduce", "cf_select_best", "cf_math_eval", "cf_philox_eval", "cf_release_scratch")
 
 
 def lib():
@@ -297,6 +299,27 @@ def cf_eval_fine(desc, plans, plan_ids, rates, trace, lat_triples=None):
                              _p(rates.contiguous()), int(K), C.byref(trace.c), 0, C.byref(out),
                              _stream()), "cf_eval_fine")
     return dict(met=met, cnt=cnt, events=events, status=status, lat=lat)
+
+
+def cf_eval_mc(desc, plans, plan_ids, rd, moments_seed, alpha, trace, seed_idx, n_sample,
+               want_lat=False):
+    n = int(plan_ids.numel())
+    T, dev = desc.n_types, rd.device
+    met = torch.empty((n, T), dtype=torch.int32, device=dev)
+    cnt = torch.empty((n, T), dtype=torch.int32, device=dev)
+    gt = torch.empty((n, T), dtype=torch.float64, device=dev)
+    lat = torch.empty((n, int(n_sample), 4), dtype=torch.float64, device=dev) if want_lat else None
+    _check(_lib.cf_eval_mc(C.byref(desc), C.byref(plans.c), _p(plan_ids.contiguous()), n, _p(rd.contiguous()),
+                           _p(moments_seed.contiguous()), float(alpha), C.byref(trace.c), int(seed_idx),
+                           int(n_sample), _p(met), _p(cnt), _p(gt), _p(lat), _stream()), "cf_eval_mc")
+    return dict(met=met, cnt=cnt, goodput_t=gt, lat=lat)
+
+
+def cf_pareto(goodput_t):
+    n, T = goodput_t.shape
+    keep = torch.empty(n, dtype=torch.uint8, device=goodput_t.device)
+    _check(_lib.cf_pareto(_p(goodput_t.contiguous()), int(n), int(T), _p(keep), _stream()), "cf_pareto")
+    return keep
 
 
 def cf_goodput_reduce(met, cnt, rates, theta, n_req):

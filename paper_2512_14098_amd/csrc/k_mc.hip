@@ -1,0 +1,403 @@
+// k_mc.hip -- cf_eval_mc and cf_pareto: phase 2 of the plan evaluation
+// (Sec. 4.3, Alg. 2 phase 2) with occupancy-aware latency scaling
+// (Sec. 5.2), and Pareto pruning of per-type goodput vectors (Alg. 2).
+//
+// Phase 2 draws K requests from the workload and routes each through a plan
+// alone, without queueing; every component it visits costs one iteration of
+// its latency model at the component's effective batch on its node.  The
+// fraction of sampled requests of type t meeting the targets is F_t and the
+// goodput estimate G_t = alpha R_d pi_t F_t.
+//   - effective batch: node v, whose phase-1 capacity is R_v = m_v / u_v,
+//     runs at b = clamp(ceil(B (R_d / R_v)), 1, B), B = min(node batch, cap)
+//     (the bottleneck at its configured batch);
+//   - encoder / generator iteration: a static batch of b requests like this
+//     one, (k0 + k1 (b x)) + k2 b; LLM: the request's own prefill,
+//     (k0 + k1 x) + k2, then decode steps d0 + d1 b shared with the running set;
+//   - a component starts at the last arrival of its inputs (a parent's finish,
+//     a gate source's first token for a gated LLM, plus comm across
+//     executors); token k+1 of a gated LLM waits for the gate source's token
+//     min(k+1, n_src) (comm later across executors) and for its own token k.
+//
+// One wavefront per plan: the plan's nodes, routes and effective batches are
+// set up in LDS (the per-node demand u_v is summed by one lane in the order
+// phase 1 uses), then the lanes take the sampled requests, 64 at a time;
+// each lane walks its request's path in component order with the whole
+// timeline in registers (a decode run in closed form, a gated decode one
+// token at a time), and SLO counts are LDS atomics per type.
+#include "cf_internal.h"
+#include "cf_run.h"
+
+namespace cf {
+namespace {
+
+struct McView {
+  int P;
+  const uint8_t *n_nodes, *node_comp, *node_rep, *node_gpus, *n_alt, *alt_w, *alt_node;
+  const uint16_t *node_batch;
+  const int32_t *ids;
+  const double *rd;
+  const uint64_t *moments;
+  double alpha;
+  const uint64_t *ticks, *rkey0, *rkey1;
+  const uint8_t *type;
+  const uint16_t *patches, *prompt, *out;
+  const uint32_t *aud_in, *aud_out, *akey;
+  size_t toff;  // first sampled request: seed_idx * n_req
+  int n_sample;
+  uint32_t *met, *cnt;
+  double *gt, *lat;
+};
+
+__device__ __forceinline__ uint32_t mc_attr(const McView &V, size_t o, int a) {
+  switch (a) {
+    case CF_ATTR_PROMPT: return V.prompt[o];
+    case CF_ATTR_OUT: return V.out[o];
+    case CF_ATTR_PATCHES: return V.patches[o];
+    case CF_ATTR_AUDIN_MS: return V.aud_in[o];
+    case CF_ATTR_AUDOUT_MS: return V.aud_out[o];
+    case CF_ATTR_AUDIN_TOK: return (V.aud_in[o] + 79u) / 80u;
+    case CF_ATTR_AUDOUT_TOK: return (V.aud_out[o] + 79u) / 80u;
+    default: return 0;
+  }
+}
+
+__global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
+  __shared__ uint8_t vcomp[CF_MAX_NODES], vrep[CF_MAX_NODES], vminc[CF_MAX_NODES], vbase[CF_MAX_NODES];
+  __shared__ uint16_t vbatch[CF_MAX_NODES];
+  __shared__ uint16_t beff[CF_MAX_NODES][CF_MAX_COMP];
+  __shared__ uint8_t route[CF_MAX_TYPES][2][CF_MAX_COMP];
+  __shared__ uint8_t nalt[CF_MAX_TYPES], aw[CF_MAX_TYPES][2];
+  __shared__ double ex_s[CF_MAX_TYPES][CF_MAX_COMP], en_s[CF_MAX_TYPES][CF_MAX_COMP];
+  __shared__ double u_s[CF_MAX_NODES];
+  __shared__ uint32_t met_s[CF_MAX_TYPES], cnt_s[CF_MAX_TYPES];
+  __shared__ int valid_s;
+  const int i = blockIdx.x, lane = threadIdx.x;
+  const int p = V.ids[i];
+  const size_t P = (size_t)V.P;
+  if (lane < CF_MAX_TYPES) {
+    met_s[lane] = 0;
+    cnt_s[lane] = 0;
+  }
+  if (lane == 0) valid_s = 0;
+  // per-type means of X and of the output length (phase 1's work per request)
+  if (lane < m.nt * m.nc) {
+    const int t = lane / m.nc, c = lane % m.nc;
+    const uint64_t *mo = V.moments + (size_t)t * 8;
+    double ex = 0.0, en = 1.0;
+    if (mo[0] > 0) {
+      uint64_t xs = 0;
+      for (int a = 0; a < 7; a++)
+        if ((m.xsel[c] >> a) & 1u) xs += mo[1 + a];
+      ex = (double)xs / (double)mo[0];
+      if (m.kind[c] == CF_LLM && !((m.pfo[t] >> c) & 1u)) {
+        en = (double)mo[1 + m.nout_attr[c]] / (double)mo[0];
+        if (en < 1.0) en = 1.0;
+      }
+    }
+    ex_s[t][c] = ex;
+    en_s[t][c] = en;
+  }
+  const bool in_range = p >= 0 && p < V.P;
+  const int nv = in_range ? V.n_nodes[p] : 0;
+  if (in_range && lane < CF_MAX_NODES) {
+    vcomp[lane] = lane < nv ? V.node_comp[lane * P + p] : 0;
+    vrep[lane] = lane < nv ? V.node_rep[lane * P + p] : 0;
+    vbatch[lane] = lane < nv ? V.node_batch[lane * P + p] : 0;
+  }
+  if (in_range) {
+    for (int j = lane; j < CF_MAX_TYPES * 2 * CF_MAX_COMP; j += 64) (&route[0][0][0])[j] = V.alt_node[j * P + p];
+    if (lane < CF_MAX_TYPES) nalt[lane] = lane < m.nt ? V.n_alt[lane * P + p] : 0;
+    if (lane < 2 * CF_MAX_TYPES) (&aw[0][0])[lane] = V.alt_w[lane * P + p];
+  }
+  __syncthreads();
+  // validity (phase 1's), capacities, effective batches: one lane, phase 1's order
+  if (lane == 0 && in_range) {
+    bool ok = nv >= 1 && nv <= CF_MAX_NODES;
+    int execs = 0;
+    for (int v = 0; v < nv && ok; v++) {
+      const int cm = vcomp[v], rep = vrep[v], b = vbatch[v];
+      if (cm == 0 || (cm >> m.nc) || rep < 1 || b < 1 || b > CF_MAX_BATCH || V.node_gpus[v * P + p] < 1) ok = false;
+      vminc[v] = (uint8_t)(cm ? __ffs(cm) - 1 : 0);
+      vbase[v] = (uint8_t)(execs < 255 ? execs : 255);
+      execs += rep;
+    }
+    if (execs > CF_MAX_EXEC) ok = false;
+    for (int t = 0; t < m.nt && ok; t++) {
+      const int na = nalt[t];
+      if (na < 1 || na > 2) { ok = false; break; }
+      for (int a = 0; a < na && ok; a++) {
+        if (na > 1 && aw[t][a] < 1) ok = false;
+        for (int c = 0; c < m.nc; c++) {
+          if (!((m.path[t] >> c) & 1u)) continue;
+          const int v = route[t][a][c];
+          if (v >= nv || !((vcomp[v] >> c) & 1u)) { ok = false; break; }
+        }
+      }
+    }
+    if (ok) {
+      for (int v = 0; v < CF_MAX_NODES; v++) u_s[v] = 0.0;
+      const double wsum = (double)m.wsum;
+      for (int t = 0; t < m.nt; t++) {
+        const double pi = (double)m.weight[t] / wsum;
+        const int na = nalt[t];
+        uint32_t wtot = 0;
+        for (int a = 0; a < na; a++) wtot += na > 1 ? aw[t][a] : 1u;
+        for (int a = 0; a < na; a++) {
+          const uint32_t wa = na > 1 ? aw[t][a] : 1u;
+          const double q = (double)wa / (double)wtot;
+          const double pq = pi * q;
+          for (int c = 0; c < m.nc; c++) {
+            if (!((m.path[t] >> c) & 1u)) continue;
+            const int v = route[t][a][c];
+            const int bn = vbatch[v];
+            const double B = (double)(bn < m.cap[c] ? bn : m.cap[c]);
+            double w = ((m.k0[c] / B) + m.k1[c] * ex_s[t][c]) + m.k2[c];
+            if (m.kind[c] == CF_LLM) w = w + (en_s[t][c] - 1.0) * ((m.d0[c] / B) + m.d1[c]);
+            u_s[v] = u_s[v] + pq * w;
+          }
+        }
+      }
+      const double R_d = V.rd[p];
+      for (int v = 0; v < nv; v++) {
+        const double Rv = u_s[v] > 0.0 ? (double)vrep[v] / u_s[v] : __builtin_inf();
+        const double q = R_d / Rv;
+        for (int c = 0; c < m.nc; c++) {
+          const int bn = vbatch[v];
+          const int B = bn < m.cap[c] ? bn : m.cap[c];
+          const double bb = ceil((double)B * q);
+          beff[v][c] = (uint16_t)(bb < 1.0 ? 1 : (bb > (double)B ? B : (int)bb));
+        }
+      }
+      valid_s = 1;
+    }
+  }
+  __syncthreads();
+  if (valid_s) {
+    const double comm = m.comm;
+    for (int r = lane; r < V.n_sample; r += 64) {
+      const size_t o = V.toff + (size_t)r;
+      const int t = V.type[o];
+      if (t >= m.nt) continue;
+      int alt = 0;
+      if (nalt[t] == 2) {
+        const uint64_t w0 = aw[t][0], w1 = aw[t][1];
+        alt = ((((uint64_t)V.akey[o]) * (w0 + w1)) >> 32) < w0 ? 0 : 1;
+      }
+      const uint64_t k0 = V.rkey0[o], k1 = V.rkey1[o];
+      const int ta = m.ta_c[t], th = m.th_c[t];
+      int ex[CF_MAX_COMP], nout[CF_MAX_COMP];
+      double fin[CF_MAX_COMP], first[CF_MAX_COMP], dstep[CF_MAX_COMP];
+      int ttft_c = -1;
+      double completion = 0.0, media = 0.0;
+#pragma unroll
+      for (int c = 0; c < CF_MAX_COMP; c++) {
+        ex[c] = 0;
+        nout[c] = 1;
+        fin[c] = 0.0;
+        first[c] = 0.0;
+        dstep[c] = 0.0;
+      }
+#pragma unroll
+      for (int c = 0; c < CF_MAX_COMP; c++) {
+        if (c >= m.nc || !((m.path[t] >> c) & 1u)) continue;
+        const int v = route[t][alt][c];
+        const int mc = vminc[v];
+        const uint64_t key = ((mc < 4 ? k0 : k1) >> (16 * (mc & 3))) & 0xFFFFull;
+        ex[c] = vbase[v] + (int)((key * vrep[v]) >> 16);
+        // the last input to arrive
+        double start = 0.0;
+#pragma unroll
+        for (int pc = 0; pc < c; pc++) {
+          const bool gate_edge = c == ta && pc == th;
+          if (!(((m.child[t][pc] >> c) & 1u) || gate_edge)) continue;
+          const double hop = ex[pc] == ex[c] ? 0.0 : comm;
+          const double ready = gate_edge ? first[pc] + hop : fin[pc] + hop;
+          start = ready > start ? ready : start;
+        }
+        const int b = beff[v][c];
+        uint32_t x = 0;
+        for (uint32_t sel = m.xsel[c]; sel; sel &= sel - 1) x += mc_attr(V, o, __ffs(sel) - 1);
+        if (m.kind[c] != CF_LLM) {
+          const double dur = (m.k0[c] + m.k1[c] * (double)((uint64_t)b * x)) + m.k2[c] * (double)b;
+          fin[c] = start + dur;
+          first[c] = fin[c];
+        } else {
+          const double dur = (m.k0[c] + m.k1[c] * (double)x) + m.k2[c] * 1.0;
+          uint32_t no = ((m.pfo[t] >> c) & 1u) ? 1u : mc_attr(V, o, m.nout_attr[c]);
+          no = no < 1 ? 1u : no;
+          nout[c] = (int)no;
+          const double D = m.d0[c] + m.d1[c] * (double)b;
+          dstep[c] = D;
+          first[c] = start + dur;
+          double e = first[c];
+          if (c != ta) {
+            uint32_t taken = 0;
+            e = run_walk(e, D, no - 1u, __builtin_inf(), &taken);
+          } else {
+            // the gate source's tokens: its first token, then one step of dstep each
+            double eg = 0.0, dg = 0.0, hop = 0.0;
+            int ng = 1;
+#pragma unroll
+            for (int s2 = 0; s2 < c; s2++) {
+              if (s2 == th) {
+                eg = first[s2];
+                dg = dstep[s2];
+                ng = nout[s2];
+                hop = ex[s2] == ex[c] ? 0.0 : comm;
+              }
+            }
+            int jg = 1;
+            for (int k = 1; k < (int)no; k++) {
+              const int need = k + 1 < ng ? k + 1 : ng;
+              if (jg < need) {
+                eg = eg + dg;
+                jg++;
+              }
+              const double vis = eg + hop;
+              const double s = e < vis ? vis : e;
+              e = s + D;
+            }
+          }
+          fin[c] = e;
+          if (ttft_c < 0) ttft_c = c;
+        }
+        if ((m.outm[t] >> c) & 1u) {
+          completion = fin[c] > completion ? fin[c] : completion;
+          if (m.kind[c] == CF_GEN) media = fin[c] > media ? fin[c] : media;
+        }
+      }
+      double ttft = 0.0, tpot = 0.0;
+#pragma unroll
+      for (int c = 0; c < CF_MAX_COMP; c++) {
+        if (c == ttft_c) {
+          ttft = first[c];
+          if (nout[c] > 1) tpot = (fin[c] - first[c]) / (double)(nout[c] - 1);
+        }
+      }
+      const double md = m.gen_out[t] ? media : 0.0;
+      const bool ok = ttft <= m.slo[t][0] && tpot <= m.slo[t][1] && completion <= m.slo[t][2] && md <= m.slo[t][3];
+      atomicAdd(&cnt_s[t], 1u);
+      if (ok) atomicAdd(&met_s[t], 1u);
+      if (V.lat) {
+        double *L = V.lat + ((size_t)i * V.n_sample + r) * 4;
+        L[0] = ttft;
+        L[1] = tpot;
+        L[2] = completion;
+        L[3] = md;
+      }
+    }
+  }
+  __syncthreads();
+  if (lane < m.nt) {
+    const size_t oi = (size_t)i * m.nt + lane;
+    const uint32_t mt = met_s[lane], ct = cnt_s[lane];
+    V.met[oi] = mt;
+    V.cnt[oi] = ct;
+    double g = 0.0;
+    if (valid_s && ct > 0) {
+      const double pi = (double)m.weight[lane] / (double)m.wsum;
+      g = ((V.alpha * V.rd[p]) * pi) * ((double)mt / (double)ct);
+    }
+    V.gt[oi] = g;
+  }
+}
+
+// keep[i] = 0 iff another row j of g[n][T] is >= in every component and >
+// in one; the rows are streamed through LDS 256 at a time
+constexpr int kParBlock = 256;
+__global__ void __launch_bounds__(kParBlock) k_pareto(const double *g, int n, int T, uint8_t *keep) {
+  __shared__ double tile[kParBlock * CF_MAX_TYPES];
+  const int i = blockIdx.x * kParBlock + threadIdx.x;
+  double mine[CF_MAX_TYPES];
+#pragma unroll
+  for (int t = 0; t < CF_MAX_TYPES; t++) mine[t] = (i < n && t < T) ? g[(size_t)i * T + t] : 0.0;
+  bool dominated = false;
+  for (int j0 = 0; j0 < n; j0 += kParBlock) {
+    __syncthreads();
+    const int cnt = n - j0 < kParBlock ? n - j0 : kParBlock;
+    for (int q = threadIdx.x; q < cnt * T; q += kParBlock) tile[q] = g[(size_t)j0 * T + q];
+    __syncthreads();
+    if (i < n && !dominated) {
+      for (int jj = 0; jj < cnt; jj++) {
+        if (j0 + jj == i) continue;
+        bool ge = true, gt = false;
+#pragma unroll
+        for (int t = 0; t < CF_MAX_TYPES; t++) {
+          if (t < T) {
+            const double a = tile[jj * T + t], b = mine[t];
+            ge = ge && !(a < b);
+            gt = gt || a > b;
+          }
+        }
+        if (ge && gt) {
+          dominated = true;
+          break;
+        }
+      }
+    }
+  }
+  if (i < n) keep[i] = dominated ? 0 : 1;
+}
+
+}  // namespace
+}  // namespace cf
+
+extern "C" cf_status cf_eval_mc(const cf_model_desc *model, const cf_plan_table *plans, const int32_t *plan_ids_dev,
+                                int32_t n_plans, const double *rd_dev, const uint64_t *moments_dev, double alpha,
+                                const cf_trace *trace, int32_t seed_idx, int32_t n_sample, uint32_t *met_dev,
+                                uint32_t *cnt_dev, double *goodput_t_dev, double *lat_dev, void *stream) {
+  using namespace cf;
+  KModel m;
+  cf_status st = lower_model(model, &m);
+  if (st != CF_OK) return st;
+  if (!plans || !trace) return set_error(CF_EINVAL, "NULL argument");
+  if (n_plans < 0 || n_sample < 0 || plans->P < 0) return set_error(CF_EINVAL, "sizes");
+  if (n_plans == 0) return CF_OK;
+  if (!plan_ids_dev || !rd_dev || !moments_dev || !met_dev || !cnt_dev || !goodput_t_dev)
+    return set_error(CF_EINVAL, "NULL device array");
+  if (!(alpha > 0.0) || !(alpha <= 1.0)) return set_error(CF_EINVAL, "alpha must be in (0, 1]");
+  if (seed_idx < 0 || seed_idx >= trace->n_seeds || n_sample > trace->n_req)
+    return set_error(CF_EINVAL, "seed_idx or n_sample outside the trace");
+  McView V;
+  V.P = plans->P;
+  V.n_nodes = plans->n_nodes_dev;
+  V.node_comp = plans->node_comp_dev;
+  V.node_rep = plans->node_rep_dev;
+  V.node_gpus = plans->node_gpus_dev;
+  V.n_alt = plans->n_alt_dev;
+  V.alt_w = plans->alt_w_dev;
+  V.alt_node = plans->alt_node_dev;
+  V.node_batch = plans->node_batch_dev;
+  V.ids = plan_ids_dev;
+  V.rd = rd_dev;
+  V.moments = moments_dev;
+  V.alpha = alpha;
+  V.ticks = trace->arr_ticks_dev;
+  V.rkey0 = trace->rkey0_dev;
+  V.rkey1 = trace->rkey1_dev;
+  V.type = trace->type_dev;
+  V.patches = trace->patches_dev;
+  V.prompt = trace->prompt_dev;
+  V.out = trace->out_dev;
+  V.aud_in = trace->aud_in_ms_dev;
+  V.aud_out = trace->aud_out_ms_dev;
+  V.akey = trace->akey_dev;
+  V.toff = (size_t)seed_idx * (size_t)trace->n_req;
+  V.n_sample = n_sample;
+  V.met = met_dev;
+  V.cnt = cnt_dev;
+  V.gt = goodput_t_dev;
+  V.lat = lat_dev;
+  hipLaunchKernelGGL(k_mc, dim3((unsigned)n_plans), dim3(64), 0, as_stream(stream), m, V);
+  return hip_check(hipGetLastError(), "cf_eval_mc launch");
+}
+
+extern "C" cf_status cf_pareto(const double *goodput_t_dev, int32_t n, int32_t T, uint8_t *keep_dev, void *stream) {
+  using namespace cf;
+  if (n < 0 || T < 1 || T > CF_MAX_TYPES) return set_error(CF_EINVAL, "sizes");
+  if (n == 0) return CF_OK;
+  if (!goodput_t_dev || !keep_dev) return set_error(CF_EINVAL, "NULL device array");
+  hipLaunchKernelGGL(k_pareto, dim3((unsigned)((n + kParBlock - 1) / kParBlock)), dim3(kParBlock), 0,
+                     as_stream(stream), goodput_t_dev, n, T, keep_dev);
+  return hip_check(hipGetLastError(), "cf_pareto launch");
+}

@@ -20,7 +20,7 @@ def declared_functions():
 
 def test_header_declares_the_path():
     names = declared_functions()
-    for f in ("cf_trace_gen", "cf_eval_coarse", "cf_select_topk", "cf_rate_grid", "cf_eval_fine",
+    for f in ("cf_trace_gen", "cf_eval_coarse", "cf_select_topk", "cf_rate_grid", "cf_eval_fine", "cf_eval_mc", "cf_pareto",
               "cf_goodput_reduce", "cf_select_best"):
         assert f in names
 

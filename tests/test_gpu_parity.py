@@ -398,3 +398,73 @@ def test_full_size_c1_sampled(cf):
         o = O.sim_triple(m, w.tab, int(ids[i]), float(rates[i, k]), otr, seeds_needed.index(s))
         assert np.array_equal(met[i, k, s], o["met"]) and np.array_equal(cnt[i, k, s], o["cnt"])
         assert int(ev[i, k, s]) == o["events"]
+
+
+# ------------------------------------------------------------------ phase 2 (Monte Carlo) and Pareto
+@pytest.mark.parametrize("name,n_plans,n_sample,seed", [
+    ("c0", 6, 1000, 0),
+    ("c1", 64, 1024, 3),
+    ("c2", 64, 1024, 1),
+    ("c3", 48, 1024, 2),
+    ("c4", 48, 1024, 0),
+])
+def test_mc_parity(cf, name, n_plans, n_sample, seed):
+    """Phase 2 on each side's own trace and phase 1: counts, goodput and every
+    sampled request's latencies bit-identical; the Pareto flags identical."""
+    _say(f"mc {name} plans={n_plans} K={n_sample}")
+    cfg = load_config(name)
+    if name == "c4":
+        cfg["plans"]["sampled"]["total"] = 20000  # the c4 sampler, first 2e4 plans
+    tab = make_plans(cfg)
+    m = O.make_model(cfg["model"])
+    otr = O.trace_gen(m, [seed], n_sample)
+    rd, _, fl = O.eval_coarse(m, tab, otr["moments"][0], cfg["gpus"])
+    ids = O.select_topk(rd, fl, n_plans)
+    alpha = 0.8
+    met, cnt, gt, lat = O.eval_mc(m, tab, ids, rd, otr["moments"][0], alpha, otr, 0, n_sample, want_lat=True)
+    keep = O.pareto(gt)
+    desc = cf.model_desc(cfg["model"])
+    tr, mom = cf.cf_trace_gen(desc, [seed], n_sample)
+    plans = cf.DevicePlans(tab)
+    grd, _, _ = cf.cf_eval_coarse(desc, plans, mom[0], cfg["gpus"])
+    out = cf.cf_eval_mc(desc, plans, torch.as_tensor(ids).cuda(), grd, mom[0], alpha, tr, 0, n_sample,
+                        want_lat=True)
+    gkeep = cf.cf_pareto(out["goodput_t"])
+    torch.cuda.synchronize()
+    assert np.array_equal(out["met"].cpu().numpy().view(np.uint32), met)
+    assert np.array_equal(out["cnt"].cpu().numpy().view(np.uint32), cnt)
+    ggt = out["goodput_t"].cpu().numpy()
+    np.testing.assert_allclose(ggt, gt, rtol=1e-12, atol=0)
+    assert np.array_equal(ggt.view(np.int64), gt.view(np.int64))  # same operations, same order
+    glat = out["lat"].cpu().numpy()
+    np.testing.assert_allclose(glat, lat, rtol=1e-9, atol=0)
+    assert np.array_equal(glat.view(np.int64), lat.view(np.int64))
+    assert np.array_equal(gkeep.cpu().numpy(), keep)
+
+
+def test_mc_edges_and_pareto_sizes(cf):
+    _say("mc edges")
+    cfg = load_config("c1")
+    tab = make_plans(cfg)
+    desc = cf.model_desc(cfg["model"])
+    plans = cf.DevicePlans(tab)
+    tr, mom = cf.cf_trace_gen(desc, [0], 64)
+    rd, _, _ = cf.cf_eval_coarse(desc, plans, mom[0], cfg["gpus"])
+    # an invalid plan id and a route that does not fit give zeros
+    bad = plan_table_from_list([dict(nodes=[(1, 1, 8, 1)], routes=[[(10, {1: 0})], [(10, {0: 0, 1: 0})]])])
+    out = cf.cf_eval_mc(desc, cf.DevicePlans(bad), torch.tensor([0, 5], dtype=torch.int32).cuda(),
+                        torch.ones(1, dtype=torch.float64).cuda(), mom[0], 0.8, tr, 0, 64)
+    assert int(out["cnt"].sum().item()) == 0 and float(out["goodput_t"].abs().sum().item()) == 0.0
+    # no sampled requests
+    out = cf.cf_eval_mc(desc, plans, torch.tensor([0, 1], dtype=torch.int32).cuda(), rd, mom[0], 0.8, tr, 0, 0)
+    assert int(out["cnt"].sum().item()) == 0
+    # bad arguments are rejected before any launch
+    with pytest.raises(cf.CfError):
+        cf.cf_eval_mc(desc, plans, torch.tensor([0], dtype=torch.int32).cuda(), rd, mom[0], 1.5, tr, 0, 8)
+    with pytest.raises(cf.CfError):
+        cf.cf_eval_mc(desc, plans, torch.tensor([0], dtype=torch.int32).cuda(), rd, mom[0], 0.5, tr, 0, 65)
+    # Pareto over many vectors with ties, across several 256-row tiles
+    rng = np.random.default_rng(5)
+    g = rng.integers(0, 6, size=(1000, 3)).astype(np.float64)
+    keep = cf.cf_pareto(torch.from_numpy(g).cuda()).cpu().numpy()
+    assert np.array_equal(keep, O.pareto(g))
