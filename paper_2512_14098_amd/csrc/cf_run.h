@@ -9,17 +9,21 @@
 // the binade is rounded to the grid of spacing u = 2^(E-52).  Write q = d/u.
 //   - If q is not an odd multiple of 1/2, a step from significand m gives
 //     m + round(q), whatever m is.
-//   - If it is (a rounding tie), the sum goes to the even neighbour: from an
-//     even m the increment is whichever of floor(q), floor(q) + 1 is even,
-//     and the result is even again.
-// So from a point with an even significand the increment D (in units of u)
-// is the same for every later step of the binade, and a step from m lands
-// on m + D as long as m + D is still inside the binade (the exact sum is
-// then below 2^(E+1), so the grid does not change).  The steps of a segment
-// inside a binade are therefore computed in integer units of u; the step
-// that measures D, odd significands, binade crossings and non-normal values
-// are taken one addition at a time.
-//
+//   - If it is (a rounding tie), the sum goes to the even neighbour, so a
+//     step from any grid point lands on an even significand, and from an
+//     even significand the increment is whichever of floor(q), floor(q) + 1
+//     is even.
+// So once a step has been taken from a point of the binade's grid (or from
+// a point with an even significand), the increment D (in units of u) is the
+// same for every later step of the binade, and a step from m lands on
+// m + D as long as m + D is still inside the binade (the exact sum is then
+// below 2^(E+1), so the grid does not change).  The first step into a
+// binade starts from the finer grid below it, so it may leave an odd
+// significand with a tie: one more step inside the binade settles that.
+// The steps of a segment inside a binade are therefore computed in integer
+// units of u: at most three single additions per binade (entering it,
+// settling the parity, measuring D), then one jump.  Non-normal values are
+// taken one addition at a time.
 // The functions are constexpr (usable from device code and from host-side
 // tests) and use only IEEE binary64 addition, division and conversions.
 #pragma once
@@ -47,9 +51,18 @@ constexpr double run_walk(double e, double d, uint32_t n, double stop, uint32_t 
     e = e + d;
     k++;
     if (k >= n || !(e < stop)) break;
-    const uint64_t b1 = __builtin_bit_cast(uint64_t, e);
+    uint64_t b1 = __builtin_bit_cast(uint64_t, e);
     const uint64_t ex = b1 >> 52;  // e >= 0: the sign bit is clear
-    if ((b1 & 1u) || ex == 0 || ex >= 0x7FF) continue;
+    if (ex == 0 || ex >= 0x7FF) continue;
+    if (b1 & 1u) {
+      // an odd significand may have come from the finer grid below: one
+      // step from this grid point fixes the increment
+      e = e + d;
+      k++;
+      if (k >= n || !(e < stop)) break;
+      b1 = __builtin_bit_cast(uint64_t, e);
+      if ((b1 >> 52) != ex) continue;
+    }
     e = e + d;
     k++;
     if (k >= n || !(e < stop)) break;

@@ -44,21 +44,85 @@ struct McView {
   const uint32_t *aud_in, *aud_out, *akey;
   size_t toff;  // first sampled request: seed_idx * n_req
   int n_sample;
+  const uint32_t *order;  // the sampled requests in walking order (a permutation of 0..n_sample-1)
   uint32_t *met, *cnt;
   double *gt, *lat;
 };
 
-__device__ __forceinline__ uint32_t mc_attr(const McView &V, size_t o, int a) {
+// the request's attributes, loaded together once per request
+struct McReq {
+  uint32_t prompt, out, patches, aud_in, aud_out;
+};
+
+__device__ __forceinline__ uint32_t mc_attr(const McReq &q, int a) {
   switch (a) {
-    case CF_ATTR_PROMPT: return V.prompt[o];
-    case CF_ATTR_OUT: return V.out[o];
-    case CF_ATTR_PATCHES: return V.patches[o];
-    case CF_ATTR_AUDIN_MS: return V.aud_in[o];
-    case CF_ATTR_AUDOUT_MS: return V.aud_out[o];
-    case CF_ATTR_AUDIN_TOK: return (V.aud_in[o] + 79u) / 80u;
-    case CF_ATTR_AUDOUT_TOK: return (V.aud_out[o] + 79u) / 80u;
+    case CF_ATTR_PROMPT: return q.prompt;
+    case CF_ATTR_OUT: return q.out;
+    case CF_ATTR_PATCHES: return q.patches;
+    case CF_ATTR_AUDIN_MS: return q.aud_in;
+    case CF_ATTR_AUDOUT_MS: return q.aud_out;
+    case CF_ATTR_AUDIN_TOK: return (q.aud_in + 79u) / 80u;
+    case CF_ATTR_AUDOUT_TOK: return (q.aud_out + 79u) / 80u;
     default: return 0;
   }
+}
+
+// The order the lanes take the sampled requests in.  Every request's walk
+// is independent of the others and the counts are sums, so any order gives
+// the same results; this one groups requests by type and then by the token
+// count of the type's gated decode, so that a wavefront mostly walks one
+// path and its gated decode loops have nearly equal lengths.  One workgroup:
+// a histogram over (type, min(tokens, 255)), an exclusive scan, a scatter.
+constexpr int kOrdThreads = 1024, kOrdBuckets = CF_MAX_TYPES * 256;
+__global__ void __launch_bounds__(kOrdThreads) k_mc_order(KModel m, McView V, uint32_t *order) {
+  __shared__ uint32_t hist[kOrdBuckets];
+  __shared__ uint32_t part[kOrdThreads];
+  __shared__ int8_t tok_attr[CF_MAX_TYPES];
+  const int tid = threadIdx.x;
+  for (int b = tid; b < kOrdBuckets; b += kOrdThreads) hist[b] = 0;
+  if (tid < CF_MAX_TYPES) {
+    const int ta = tid < m.nt ? m.ta_c[tid] : -1;
+    tok_attr[tid] = (int8_t)(ta >= 0 && !((m.pfo[tid] >> ta) & 1u) ? m.nout_attr[ta] : -1);
+  }
+  __syncthreads();
+  auto bucket = [&](int r) -> uint32_t {
+    const size_t o = V.toff + (size_t)r;
+    const uint32_t t = V.type[o] < CF_MAX_TYPES ? V.type[o] : CF_MAX_TYPES - 1;
+    uint32_t tok = 0;
+    if (tok_attr[t] >= 0) {
+      McReq q;
+      q.prompt = V.prompt[o];
+      q.out = V.out[o];
+      q.patches = V.patches[o];
+      q.aud_in = V.aud_in[o];
+      q.aud_out = V.aud_out[o];
+      tok = mc_attr(q, tok_attr[t]);
+      tok = tok < 255u ? tok : 255u;
+    }
+    return t * 256u + tok;
+  };
+  for (int r = tid; r < V.n_sample; r += kOrdThreads) atomicAdd(&hist[bucket(r)], 1u);
+  __syncthreads();
+  // exclusive scan: each thread owns kOrdBuckets / kOrdThreads consecutive buckets
+  constexpr int per = kOrdBuckets / kOrdThreads;
+  uint32_t mine = 0;
+  for (int k = 0; k < per; k++) mine += hist[tid * per + k];
+  part[tid] = mine;
+  __syncthreads();
+  for (int d = 1; d < kOrdThreads; d <<= 1) {
+    const uint32_t add = tid >= d ? part[tid - d] : 0u;
+    __syncthreads();
+    part[tid] += add;
+    __syncthreads();
+  }
+  uint32_t run = part[tid] - mine;
+  for (int k = 0; k < per; k++) {
+    const uint32_t h = hist[tid * per + k];
+    hist[tid * per + k] = run;
+    run += h;
+  }
+  __syncthreads();
+  for (int r = tid; r < V.n_sample; r += kOrdThreads) order[atomicAdd(&hist[bucket(r)], 1u)] = (uint32_t)r;
 }
 
 __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
@@ -71,6 +135,12 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
   __shared__ double u_s[CF_MAX_NODES];
   __shared__ uint32_t met_s[CF_MAX_TYPES], cnt_s[CF_MAX_TYPES];
   __shared__ int valid_s;
+  // per-type model fields indexed by a lane's request type (kernel arguments
+  // indexed per lane would be one memory round trip each)
+  __shared__ uint64_t child_s[CF_MAX_TYPES];  // byte c: the non-streaming children of c
+  __shared__ uint32_t tinfo_s[CF_MAX_TYPES];  // path | outm << 8 | pfo << 16 | gen_out << 24
+  __shared__ int8_t ta_s[CF_MAX_TYPES], th_s[CF_MAX_TYPES];
+  __shared__ double slo_s[CF_MAX_TYPES][4];
   const int i = blockIdx.x, lane = threadIdx.x;
   const int p = V.ids[i];
   const size_t P = (size_t)V.P;
@@ -79,6 +149,17 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
     cnt_s[lane] = 0;
   }
   if (lane == 0) valid_s = 0;
+  if (lane < CF_MAX_TYPES) {
+    uint64_t ch = 0;
+#pragma unroll
+    for (int c = 0; c < CF_MAX_COMP; c++) ch |= (uint64_t)m.child[lane][c] << (8 * c);
+    child_s[lane] = ch;
+    tinfo_s[lane] = (m.path[lane] & 0xFFu) | ((m.outm[lane] & 0xFFu) << 8) | ((m.pfo[lane] & 0xFFu) << 16) |
+                    ((uint32_t)(m.gen_out[lane] ? 1 : 0) << 24);
+    ta_s[lane] = m.ta_c[lane];
+    th_s[lane] = m.th_c[lane];
+  }
+  if (lane < CF_MAX_TYPES * 4) (&slo_s[0][0])[lane] = (&m.slo[0][0])[lane];
   // per-type means of X and of the output length (phase 1's work per request)
   if (lane < m.nt * m.nc) {
     const int t = lane / m.nc, c = lane % m.nc;
@@ -174,7 +255,8 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
   __syncthreads();
   if (valid_s) {
     const double comm = m.comm;
-    for (int r = lane; r < V.n_sample; r += 64) {
+    for (int j = lane; j < V.n_sample; j += 64) {
+      const int r = (int)V.order[j];
       const size_t o = V.toff + (size_t)r;
       const int t = V.type[o];
       if (t >= m.nt) continue;
@@ -184,7 +266,16 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
         alt = ((((uint64_t)V.akey[o]) * (w0 + w1)) >> 32) < w0 ? 0 : 1;
       }
       const uint64_t k0 = V.rkey0[o], k1 = V.rkey1[o];
-      const int ta = m.ta_c[t], th = m.th_c[t];
+      McReq q;
+      q.prompt = V.prompt[o];
+      q.out = V.out[o];
+      q.patches = V.patches[o];
+      q.aud_in = V.aud_in[o];
+      q.aud_out = V.aud_out[o];
+      const int ta = ta_s[t], th = th_s[t];
+      const uint64_t child = child_s[t];
+      const uint32_t tinfo = tinfo_s[t];
+      const uint32_t path = tinfo & 0xFFu, outm = (tinfo >> 8) & 0xFFu, pfo = (tinfo >> 16) & 0xFFu;
       int ex[CF_MAX_COMP], nout[CF_MAX_COMP];
       double fin[CF_MAX_COMP], first[CF_MAX_COMP], dstep[CF_MAX_COMP];
       int ttft_c = -1;
@@ -199,7 +290,7 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
       }
 #pragma unroll
       for (int c = 0; c < CF_MAX_COMP; c++) {
-        if (c >= m.nc || !((m.path[t] >> c) & 1u)) continue;
+        if (c >= m.nc || !((path >> c) & 1u)) continue;
         const int v = route[t][alt][c];
         const int mc = vminc[v];
         const uint64_t key = ((mc < 4 ? k0 : k1) >> (16 * (mc & 3))) & 0xFFFFull;
@@ -209,21 +300,21 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
 #pragma unroll
         for (int pc = 0; pc < c; pc++) {
           const bool gate_edge = c == ta && pc == th;
-          if (!(((m.child[t][pc] >> c) & 1u) || gate_edge)) continue;
+          if (!(((child >> (8 * pc + c)) & 1u) || gate_edge)) continue;
           const double hop = ex[pc] == ex[c] ? 0.0 : comm;
           const double ready = gate_edge ? first[pc] + hop : fin[pc] + hop;
           start = ready > start ? ready : start;
         }
         const int b = beff[v][c];
         uint32_t x = 0;
-        for (uint32_t sel = m.xsel[c]; sel; sel &= sel - 1) x += mc_attr(V, o, __ffs(sel) - 1);
+        for (uint32_t sel = m.xsel[c]; sel; sel &= sel - 1) x += mc_attr(q, __ffs(sel) - 1);
         if (m.kind[c] != CF_LLM) {
           const double dur = (m.k0[c] + m.k1[c] * (double)((uint64_t)b * x)) + m.k2[c] * (double)b;
           fin[c] = start + dur;
           first[c] = fin[c];
         } else {
           const double dur = (m.k0[c] + m.k1[c] * (double)x) + m.k2[c] * 1.0;
-          uint32_t no = ((m.pfo[t] >> c) & 1u) ? 1u : mc_attr(V, o, m.nout_attr[c]);
+          uint32_t no = ((pfo >> c) & 1u) ? 1u : mc_attr(q, m.nout_attr[c]);
           no = no < 1 ? 1u : no;
           nout[c] = (int)no;
           const double D = m.d0[c] + m.d1[c] * (double)b;
@@ -261,7 +352,7 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
           fin[c] = e;
           if (ttft_c < 0) ttft_c = c;
         }
-        if ((m.outm[t] >> c) & 1u) {
+        if ((outm >> c) & 1u) {
           completion = fin[c] > completion ? fin[c] : completion;
           if (m.kind[c] == CF_GEN) media = fin[c] > media ? fin[c] : media;
         }
@@ -274,8 +365,8 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
           if (nout[c] > 1) tpot = (fin[c] - first[c]) / (double)(nout[c] - 1);
         }
       }
-      const double md = m.gen_out[t] ? media : 0.0;
-      const bool ok = ttft <= m.slo[t][0] && tpot <= m.slo[t][1] && completion <= m.slo[t][2] && md <= m.slo[t][3];
+      const double md = (tinfo >> 24) ? media : 0.0;
+      const bool ok = ttft <= slo_s[t][0] && tpot <= slo_s[t][1] && completion <= slo_s[t][2] && md <= slo_s[t][3];
       atomicAdd(&cnt_s[t], 1u);
       if (ok) atomicAdd(&met_s[t], 1u);
       if (V.lat) {
@@ -388,6 +479,15 @@ extern "C" cf_status cf_eval_mc(const cf_model_desc *model, const cf_plan_table 
   V.cnt = cnt_dev;
   V.gt = goodput_t_dev;
   V.lat = lat_dev;
+  V.order = nullptr;
+  if (n_sample > 0) {
+    uint32_t *order = (uint32_t *)scratch_get(SCR_MC, sizeof(uint32_t) * (size_t)n_sample, &st);
+    if (!order) return st;
+    hipLaunchKernelGGL(k_mc_order, dim3(1), dim3(kOrdThreads), 0, as_stream(stream), m, V, order);
+    st = hip_check(hipGetLastError(), "cf_eval_mc order launch");
+    if (st != CF_OK) return st;
+    V.order = order;
+  }
   hipLaunchKernelGGL(k_mc, dim3((unsigned)n_plans), dim3(64), 0, as_stream(stream), m, V);
   return hip_check(hipGetLastError(), "cf_eval_mc launch");
 }

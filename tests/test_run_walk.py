@@ -3,7 +3,8 @@
 run_walk must return exactly what one IEEE binary64 addition per step
 returns.  The header is compiled with g++ (-O2 -ffp-contract=off) into a
 small driver that compares it with the plain loop on seeded random cases:
-realistic times and durations, durations that make every step a rounding tie,
+realistic times and durations, durations that make every step a rounding tie (from even and from odd
+significands, and entering a binade from the finer grid below it),
 runs that cross binades, durations below half an ulp, and stop times inside
 and outside the run.
 """
@@ -65,7 +66,7 @@ int main() {
     if (cf::floor_div53(a, b) != a / b) { if (bad < 10) std::printf("DIV %llu %llu\n", (unsigned long long)a, (unsigned long long)b); bad++; }
   }
   for (int i = 0; i < 300000; i++) {
-    const int kind = i % 6;
+    const int kind = i % 8;
     double e = 0, d = 0, stop = INFINITY;
     uint32_t n = (uint32_t)(next64() % 400);
     if (kind == 0) {  // decode runs of the workloads: times up to 1e4 s, steps of ms
@@ -86,9 +87,21 @@ int main() {
       e = unif() * 100;
       d = 1e-3 + unif() * 1e-2;
       n = (uint32_t)(next64() % 20000);
-    } else {  // arbitrary significands
+    } else if (kind == 5) {  // arbitrary significands
       e = std::ldexp(unif(), (int)(next64() % 60) - 30);
       d = std::ldexp(unif(), (int)(next64() % 60) - 40);
+    } else if (kind == 6) {  // ties from an odd significand inside a binade
+      const int E = (int)(next64() % 40) - 20;
+      e = std::ldexp(1.0 + std::ldexp((double)((next64() >> 12) | 1u), -52), E);
+      const double u = std::ldexp(1.0, E - 52);
+      d = ((double)(next64() % 1000) + 0.5) * u * (double)(1u << (next64() % 4));
+      n = (uint32_t)(next64() % 3000);
+    } else {  // ties relative to the binade above, from just below it (odd landing)
+      const int E = (int)(next64() % 40) - 20;
+      e = std::ldexp(1.0 - std::ldexp((double)((next64() % 4000) + 1), -52), E);
+      const double u = std::ldexp(1.0, E - 52);
+      d = ((double)(next64() % 1000) + 0.5) * u;
+      n = (uint32_t)(next64() % 3000);
     }
     const int sk = (int)(next64() % 4);
     if (sk == 1) stop = e + d * (double)n * unif() * 1.2;
