@@ -6,6 +6,11 @@ grid, phase-3 simulation of every (plan, rate, seed) triple, goodput
 reduction and selection.  Default workload: c1 (E->L on 8 simulated GPUs,
 1000 plans screened, the kept ones simulated at 16 rates x 32 seeds x 10^4
 requests).  Prints one JSON line.
+
+Other modes (each prints its own JSON line and exits): --phase2 times phase 2
+(Monte Carlo latency of every plan phase 1 keeps, default workload c4) and
+Pareto pruning; --stress times the HBM-bound steps at full c4 size;
+--copy-probe runs the plain copy the HBM byte counters are calibrated on.
 """
 import argparse
 import json
@@ -131,6 +136,117 @@ def stress(reps, steps):
                                    "table_bytes_per_plan": 233 + 13}}), flush=True)
 
 
+PHASE2_OPS = {"component": 6.0, "llm_component": 8.0, "gated_token": 4.0, "slo": 5.0}
+
+
+def phase2_ops_per_plan(cfg, tr_np, K):
+    """Algorithmic lane-ops of one plan's phase 2 over the first K requests of seed 0: per
+    request, 6 per encoder/generator visited (latest input, (k0 + k1 (b x)) + k2 b, finish),
+    8 per LLM visited (latest input, prefill, decode step time, closed-form end of the decode
+    run), 4 per gated decode token after the first (source token, its arrival, wait, step),
+    5 for the SLO test and count.  The same for every plan (paths depend on the type only)."""
+    import numpy as np
+    mc = cfg["model"]
+    comps = mc["components"]
+    ttype = tr_np["type"][:K].astype(np.int64)
+    attrs = {"prompt": tr_np["prompt"][:K].astype(np.int64), "out": tr_np["out"][:K].astype(np.int64),
+             "patches": tr_np["patches"][:K].astype(np.int64),
+             "aud_in_ms": tr_np["aud_in_ms"][:K].astype(np.int64),
+             "aud_out_ms": tr_np["aud_out_ms"][:K].astype(np.int64)}
+    attrs["aud_in_tok"] = (attrs["aud_in_ms"] + 79) // 80
+    attrs["aud_out_tok"] = (attrs["aud_out_ms"] + 79) // 80
+    total = 0.0
+    for t, ty in enumerate(mc["types"]):
+        sel = ttype == t
+        nreq = int(sel.sum())
+        if nreq == 0:
+            continue
+        ops = PHASE2_OPS["slo"]
+        for cn in ty["comps"]:
+            c = next(x for x in comps if x["name"] == cn)
+            ops += PHASE2_OPS["llm_component"] if c["kind"] == "LLM" else PHASE2_OPS["component"]
+        total += ops * nreq
+        for cn in ty["comps"]:
+            c = next(x for x in comps if x["name"] == cn)
+            if c.get("gate") in ty["comps"] and [c["gate"], cn] in [list(e) for e in ty.get("edges", [])]:
+                tok = np.maximum(attrs[c.get("n_out", "out")][sel], 1)
+                total += PHASE2_OPS["gated_token"] * float((tok - 1).sum())
+    return total
+
+
+def phase2_bench(args):
+    """Phase 2 (Monte Carlo latency with occupancy-aware batches) of every plan phase 1 keeps,
+    then Pareto pruning, timed with HIP events on the stream they run on."""
+    import numpy as np
+    import torch
+
+    from paper_2512_14098_amd import cf
+    from paper_2512_14098_amd.inputs import load_config, make_plans, seeds_of
+    cfg = load_config(args.config)
+    K, alpha = int(args.mc_samples), float(args.mc_alpha)
+    desc = cf.model_desc(cfg["model"])
+    seed = seeds_of(cfg)[0]
+    print("bench: phase 2 on %s, plans" % args.config, file=sys.stderr, flush=True)
+    tab = make_plans(cfg)
+    plans = cf.DevicePlans(tab)
+    tr, mom = cf.cf_trace_gen(desc, [seed], max(K, 1))
+    rd, _, flags = cf.cf_eval_coarse(desc, plans, mom[0], int(cfg["gpus"]))
+    cand = cf.cf_select_topk(rd, flags, 65536)
+    n = int(cand.numel())
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+
+    def step():
+        ev[0].record()
+        out = cf.cf_eval_mc(desc, plans, cand, rd, mom[0], alpha, tr, 0, K)
+        ev[1].record()
+        keep = cf.cf_pareto(out["goodput_t"], cand, flags)
+        ev[2].record()
+        return out, keep
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    mc_ms, par_ms = [], []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        out, keep = step()
+        torch.cuda.synchronize()
+        mc_ms.append(ev[0].elapsed_time(ev[1]))
+        par_ms.append(ev[1].elapsed_time(ev[2]))
+    elapsed = time.perf_counter() - t0
+    kept = int(keep.sum().item())
+    ops = phase2_ops_per_plan(cfg, tr.to_numpy(), K) * n
+    mc_s = sum(mc_ms) / len(mc_ms) / 1e3
+    achieved = ops / mc_s / 1e12
+    workload = ("%s phase 2: the %d plans phase 1 keeps of %d, %d sampled requests (seed %d), alpha %g, "
+                "then Pareto pruning" % (args.config, n, tab.P, K, seed, alpha))
+    res = {"metric": "candidate plans through phase 2 (Monte Carlo latency + Pareto pruning)/sec, 1 GPU",
+           "value": n * args.steps / elapsed, "unit": "plans/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": elapsed * 1e3 / args.steps, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+           "config": {"workload": workload, "plans": n, "kept_after_pareto": kept, "mc_ms": mc_ms,
+                      "pareto_ms": par_ms},
+           "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_LANE_OPS, "unit": "TOP/s",
+                        "frac": achieved / PEAK_LANE_OPS, "traffic": None, "kernel": "k_mc",
+                        "ops_per_plan": ops / max(n, 1), "kernel_ms": sum(mc_ms) / len(mc_ms)}}
+    if not args.no_cpu_baseline and n > 0:
+        from oracle import oracle as O
+        m = O.make_model(cfg["model"])
+        otr = O.trace_gen(m, [seed], max(K, 1))
+        ids = cand.cpu().numpy()
+        rd_h = rd.cpu().numpy()
+        done, t0 = 0, time.perf_counter()
+        while done < n and time.perf_counter() - t0 < args.cpu_budget:
+            chunk = ids[done:done + 16]
+            O.eval_mc(m, tab, chunk, rd_h, otr["moments"][0], alpha, otr, 0, K)
+            done += len(chunk)
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": done / dt, "unit": "plans/s", "cores": 1, "kind": "oracle",
+                               "sample": "the first %d of the %d plans (highest R_d), %d requests each, "
+                                         "single thread, %.1f s" % (done, n, K, dt)}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -151,6 +267,11 @@ def main():
     ap.add_argument("--stress", type=int, default=0, metavar="REPS",
                     help="only time the HBM-bound steps at full size: trace generation of the c4 trace "
                          "and screening of the c4 plans tiled REPS times, then exit")
+    ap.add_argument("--phase2", action="store_true",
+                    help="only time phase 2 (Monte Carlo latency) and Pareto pruning over the plans "
+                         "phase 1 keeps (default workload c4), then exit")
+    ap.add_argument("--mc-samples", type=int, default=1024, metavar="K")
+    ap.add_argument("--mc-alpha", type=float, default=0.8)
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -167,6 +288,13 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": n, "launches": 3}), flush=True)
+        return
+
+    if args.phase2:
+        torch.cuda.set_device(0)
+        if args.config == "c1" and "--config" not in sys.argv:
+            args.config = "c4"
+        phase2_bench(args)
         return
 
     if args.stress > 0:

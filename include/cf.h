@@ -235,9 +235,16 @@ cf_status cf_eval_mc(const cf_model_desc *model, const cf_plan_table *plans, con
 
 /* Pareto pruning (Alg. 2, after phases 2 and 3): keep_dev[i] = 0 iff some
  * other row of goodput_t_dev [n][T] (device) is >= in every component and >
- * in at least one, else 1.  1 <= T <= 8.  Asynchronous on stream.
- * Errors: CF_EINVAL (sizes, NULL arrays). */
-cf_status cf_pareto(const double *goodput_t_dev, int32_t n, int32_t T, uint8_t *keep_dev, void *stream);
+ * in at least one, else 1.  1 <= T <= 8.  Rows given in decreasing R_d
+ * order (as cf_select_topk returns them) are the fast case.
+ * Optionally (plan_ids_dev and flags_dev both non-NULL, both device): row i
+ * is plan plan_ids_dev[i], and a dominated row clears CF_FLAG_KEEP in
+ * flags_dev[plan] (flags_dev has n_flags entries; ids outside [0, n_flags)
+ * are left alone), so that cf_select_topk then returns the survivors.
+ * Plan ids must be distinct.  Asynchronous on stream.
+ * Errors: CF_EINVAL (sizes, NULL arrays, only one of plan_ids_dev/flags_dev). */
+cf_status cf_pareto(const double *goodput_t_dev, int32_t n, int32_t T, uint8_t *keep_dev,
+                    const int32_t *plan_ids_dev, uint8_t *flags_dev, int32_t n_flags, void *stream);
 
 /* Goodput (Sec. 3.2) at the highest feasible rate (Sec. 6.1): M_t, N_t
  * pooled over seeds; rate k feasible iff theta_den*M_t >= theta_num*N_t for

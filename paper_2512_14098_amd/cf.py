@@ -84,7 +84,7 @@ def _load():
         "cf_eval_fine": ([vp, vp, vp, i32, vp, i32, vp, u32, vp, vp], i32),
         "cf_goodput_reduce": ([vp, vp, i32, i32, i32, i32, vp, u32, u32, i32, vp, vp, vp, vp], i32),
         "cf_eval_mc": ([vp, vp, vp, i32, vp, vp, dbl, vp, i32, i32, vp, vp, vp, vp, vp], i32),
-        "cf_pareto": ([vp, i32, i32, vp, vp], i32),
+        "cf_pareto": ([vp, i32, i32, vp, vp, vp, i32, vp], i32),
         "cf_select_best": ([vp, i32, vp, vp], i32),
         "cf_math_eval": ([i32, vp, vp, vp, i64, vp], i32),
         "cf_philox_eval": ([vp, vp, vp, i64, vp], i32),
@@ -315,10 +315,19 @@ def cf_eval_mc(desc, plans, plan_ids, rd, moments_seed, alpha, trace, seed_idx, 
     return dict(met=met, cnt=cnt, goodput_t=gt, lat=lat)
 
 
-def cf_pareto(goodput_t):
+def cf_pareto(goodput_t, plan_ids=None, flags=None):
+    """keep[i] (uint8) = row i not dominated; with plan_ids and flags, also clears
+    CF_FLAG_KEEP in flags for the plans of dominated rows (in place)."""
     n, T = goodput_t.shape
     keep = torch.empty(n, dtype=torch.uint8, device=goodput_t.device)
-    _check(_lib.cf_pareto(_p(goodput_t.contiguous()), int(n), int(T), _p(keep), _stream()), "cf_pareto")
+    if (plan_ids is None) != (flags is None):
+        raise CfError("cf_pareto: plan_ids and flags go together")
+    if flags is not None and (flags.dtype != torch.uint8 or not flags.is_contiguous()):
+        raise CfError("cf_pareto: flags must be a contiguous uint8 tensor (updated in place)")
+    nf = int(flags.numel()) if flags is not None else 0
+    _check(_lib.cf_pareto(_p(goodput_t.contiguous()), int(n), int(T), _p(keep),
+                          _p(plan_ids.contiguous()) if plan_ids is not None else None,
+                          _p(flags) if flags is not None else None, nf, _stream()), "cf_pareto")
     return keep
 
 

@@ -393,41 +393,103 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
   }
 }
 
-// keep[i] = 0 iff another row j of g[n][T] is >= in every component and >
-// in one; the rows are streamed through LDS 256 at a time
+// Pareto pruning, keep[i] = 0 iff another row j of g[n][T] is >= in every
+// component and > in one.  Dominance is a strict partial order on finitely
+// many rows, so a dominated row is dominated by some row that nothing
+// dominates, and such a row is never pruned.  Two passes use this:
+//   1. each block of kParBlock consecutive rows prunes the rows another row
+//      of the same block dominates and lists its survivors;
+//   2. each survivor is tested against the survivors of every block (which
+//      include every undominated row), a block stopping once all of its
+//      survivors are dominated.
+// The result is the plain all-pairs definition; the work is n * kParBlock
+// plus (survivors)^2 comparisons instead of n^2.
 constexpr int kParBlock = 256;
-__global__ void __launch_bounds__(kParBlock) k_pareto(const double *g, int n, int T, uint8_t *keep) {
+
+__device__ __forceinline__ bool dominates(const double *a, const double *b, int T) {
+  bool ge = true, gt = false;
+#pragma unroll
+  for (int t = 0; t < CF_MAX_TYPES; t++) {
+    if (t < T) {
+      ge = ge && !(a[t] < b[t]);
+      gt = gt || a[t] > b[t];
+    }
+  }
+  return ge && gt;
+}
+
+__device__ __forceinline__ void prune(int i, uint8_t *keep, const int32_t *plan_ids, uint8_t *flags, int n_flags,
+                                      bool dominated) {
+  keep[i] = dominated ? 0 : 1;
+  if (flags && dominated) {
+    const int p = plan_ids[i];
+    if (p >= 0 && p < n_flags) flags[p] = (uint8_t)(flags[p] & ~CF_FLAG_KEEP);
+  }
+}
+
+__global__ void __launch_bounds__(kParBlock) k_pareto_local(const double *g, int n, int T, uint8_t *keep,
+                                                            const int32_t *plan_ids, uint8_t *flags, int n_flags,
+                                                            int32_t *surv, int32_t *surv_n) {
   __shared__ double tile[kParBlock * CF_MAX_TYPES];
-  const int i = blockIdx.x * kParBlock + threadIdx.x;
+  __shared__ int cnt_s;
+  const int i0 = blockIdx.x * kParBlock, i = i0 + threadIdx.x;
+  const int cnt = n - i0 < kParBlock ? n - i0 : kParBlock;
+  if (threadIdx.x == 0) cnt_s = 0;
+  for (int q = threadIdx.x; q < cnt * T; q += kParBlock) tile[q] = g[(size_t)i0 * T + q];
+  __syncthreads();
+  if (i < n) {
+    double mine[CF_MAX_TYPES];
+#pragma unroll
+    for (int t = 0; t < CF_MAX_TYPES; t++) mine[t] = t < T ? tile[threadIdx.x * T + t] : 0.0;
+    bool dominated = false;
+    for (int jj = 0; jj < cnt && !dominated; jj++) {
+      double other[CF_MAX_TYPES];
+#pragma unroll
+      for (int t = 0; t < CF_MAX_TYPES; t++) other[t] = t < T ? tile[jj * T + t] : 0.0;
+      dominated = jj != (int)threadIdx.x && dominates(other, mine, T);
+    }
+    if (dominated)
+      prune(i, keep, plan_ids, flags, n_flags, true);
+    else
+      surv[i0 + atomicAdd(&cnt_s, 1)] = i;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) surv_n[blockIdx.x] = cnt_s;
+}
+
+__global__ void __launch_bounds__(kParBlock) k_pareto_global(const double *g, int n, int T, uint8_t *keep,
+                                                             const int32_t *plan_ids, uint8_t *flags, int n_flags,
+                                                             const int32_t *surv, const int32_t *surv_n) {
+  __shared__ double tile[kParBlock * CF_MAX_TYPES];
+  const int nb = (n + kParBlock - 1) / kParBlock;
+  const int b = blockIdx.x, ns = surv_n[b];
+  const int i = (int)threadIdx.x < ns ? surv[b * kParBlock + threadIdx.x] : -1;
   double mine[CF_MAX_TYPES];
 #pragma unroll
-  for (int t = 0; t < CF_MAX_TYPES; t++) mine[t] = (i < n && t < T) ? g[(size_t)i * T + t] : 0.0;
+  for (int t = 0; t < CF_MAX_TYPES; t++) mine[t] = (i >= 0 && t < T) ? g[(size_t)i * T + t] : 0.0;
   bool dominated = false;
-  for (int j0 = 0; j0 < n; j0 += kParBlock) {
+  for (int b2 = 0; b2 < nb; b2++) {
+    const int n2 = surv_n[b2];
+    for (int q = threadIdx.x; q < n2 * T; q += kParBlock) {
+      const int k = q / T, t = q - k * T;
+      tile[q] = g[(size_t)surv[b2 * kParBlock + k] * T + t];
+    }
     __syncthreads();
-    const int cnt = n - j0 < kParBlock ? n - j0 : kParBlock;
-    for (int q = threadIdx.x; q < cnt * T; q += kParBlock) tile[q] = g[(size_t)j0 * T + q];
-    __syncthreads();
-    if (i < n && !dominated) {
-      for (int jj = 0; jj < cnt; jj++) {
-        if (j0 + jj == i) continue;
-        bool ge = true, gt = false;
+    if (i >= 0 && !dominated) {
+      for (int k = 0; k < n2; k++) {
+        double other[CF_MAX_TYPES];
 #pragma unroll
-        for (int t = 0; t < CF_MAX_TYPES; t++) {
-          if (t < T) {
-            const double a = tile[jj * T + t], b = mine[t];
-            ge = ge && !(a < b);
-            gt = gt || a > b;
-          }
-        }
-        if (ge && gt) {
+        for (int t = 0; t < CF_MAX_TYPES; t++) other[t] = t < T ? tile[k * T + t] : 0.0;
+        if (dominates(other, mine, T)) {
           dominated = true;
           break;
         }
       }
     }
+    // also the barrier before the next tile overwrites this one
+    if (!__syncthreads_or(i >= 0 && !dominated)) break;
   }
-  if (i < n) keep[i] = dominated ? 0 : 1;
+  if (i >= 0) prune(i, keep, plan_ids, flags, n_flags, dominated);
 }
 
 }  // namespace
@@ -492,12 +554,25 @@ extern "C" cf_status cf_eval_mc(const cf_model_desc *model, const cf_plan_table 
   return hip_check(hipGetLastError(), "cf_eval_mc launch");
 }
 
-extern "C" cf_status cf_pareto(const double *goodput_t_dev, int32_t n, int32_t T, uint8_t *keep_dev, void *stream) {
+extern "C" cf_status cf_pareto(const double *goodput_t_dev, int32_t n, int32_t T, uint8_t *keep_dev,
+                               const int32_t *plan_ids_dev, uint8_t *flags_dev, int32_t n_flags, void *stream) {
   using namespace cf;
   if (n < 0 || T < 1 || T > CF_MAX_TYPES) return set_error(CF_EINVAL, "sizes");
+  if ((plan_ids_dev == nullptr) != (flags_dev == nullptr))
+    return set_error(CF_EINVAL, "plan_ids_dev and flags_dev are given together or not at all");
+  if (flags_dev && n_flags < 0) return set_error(CF_EINVAL, "n_flags");
   if (n == 0) return CF_OK;
   if (!goodput_t_dev || !keep_dev) return set_error(CF_EINVAL, "NULL device array");
-  hipLaunchKernelGGL(k_pareto, dim3((unsigned)((n + kParBlock - 1) / kParBlock)), dim3(kParBlock), 0,
-                     as_stream(stream), goodput_t_dev, n, T, keep_dev);
+  const int nb = (n + kParBlock - 1) / kParBlock;
+  cf_status st = CF_OK;
+  int32_t *surv = (int32_t *)scratch_get(SCR_PARETO, sizeof(int32_t) * ((size_t)nb * kParBlock + nb), &st);
+  if (!surv) return st;
+  int32_t *surv_n = surv + (size_t)nb * kParBlock;
+  hipLaunchKernelGGL(k_pareto_local, dim3((unsigned)nb), dim3(kParBlock), 0, as_stream(stream), goodput_t_dev, n, T,
+                     keep_dev, plan_ids_dev, flags_dev, n_flags, surv, surv_n);
+  st = hip_check(hipGetLastError(), "cf_pareto launch");
+  if (st != CF_OK) return st;
+  hipLaunchKernelGGL(k_pareto_global, dim3((unsigned)nb), dim3(kParBlock), 0, as_stream(stream), goodput_t_dev, n, T,
+                     keep_dev, plan_ids_dev, flags_dev, n_flags, surv, surv_n);
   return hip_check(hipGetLastError(), "cf_pareto launch");
 }

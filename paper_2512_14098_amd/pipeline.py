@@ -1,6 +1,7 @@
 """One pass of the evaluated path on the GPU for a workload configuration.
 
-trace generation -> phase 1 screening (Alg. 2) -> top-K by R_d -> rate grid
+trace generation -> phase 1 screening (Alg. 2) -> [phase 2: Monte Carlo
+latency of every kept plan and Pareto pruning] -> top-K by R_d -> rate grid
 -> phase 3 simulation of every (plan, rate, seed) -> goodput reduction ->
 selection.  Every step is a libcf call on torch's current stream; this
 module only allocates device tensors and sequences the calls.
@@ -11,11 +12,13 @@ import torch
 from . import cf
 from .inputs import load_config, make_plans, seeds_of
 
+MAX_PHASE2 = 65536  # plans per phase-2 pass (the selection's capacity)
+
 
 class Workload:
     """Device-resident inputs of one configuration (plans, model, seeds)."""
 
-    def __init__(self, cfg, n_req=None, seeds=None, device="cuda"):
+    def __init__(self, cfg, n_req=None, seeds=None, device="cuda", phase2=None):
         if isinstance(cfg, str):
             cfg = load_config(cfg)
         self.cfg = cfg
@@ -33,6 +36,9 @@ class Workload:
         top = cfg.get("top_k")
         self.top_k = int(top) if top else self.tab.P
         self.device = device
+        # phase 2 (optional): dict(K=sampled requests, alpha=headroom), or None to go
+        # from phase 1 straight to phase 3 over the top_k plans
+        self.phase2 = phase2 if phase2 is not None else cfg.get("phase2")
 
 
 def run_step(w, timers=None):
@@ -56,6 +62,18 @@ def run_step(w, timers=None):
     mark("coarse")
     rd, bott, flags = cf.cf_eval_coarse(w.desc, w.plans, moments[0], w.n_gpus)
     mark("coarse")
+    mc = None
+    if w.phase2:
+        mark("phase2")
+        cand = cf.cf_select_topk(rd, flags, MAX_PHASE2)
+        if cand.numel() >= MAX_PHASE2:
+            # plans past the selection's capacity would keep their flag unevaluated
+            raise cf.CfError("phase 2 takes fewer than %d kept plans" % MAX_PHASE2)
+        K = min(int(w.phase2["K"]), w.n_req)
+        mc = cf.cf_eval_mc(w.desc, w.plans, cand, rd, moments[0], float(w.phase2["alpha"]), trace, 0, K)
+        mc["ids"] = cand
+        mc["keep"] = cf.cf_pareto(mc["goodput_t"], cand, flags)
+        mark("phase2")
     mark("select")
     ids = cf.cf_select_topk(rd, flags, w.top_k)
     if w.explicit_rates:
@@ -73,7 +91,7 @@ def run_step(w, timers=None):
     if timers is not None:
         timers.update(ev)
     return dict(trace=trace, moments=moments, rd=rd, bottleneck=bott, flags=flags, ids=ids,
-                rates=rates, fine=fine, kstar=kstar, goodput_t=gt, goodput=g, best=best)
+                rates=rates, fine=fine, kstar=kstar, goodput_t=gt, goodput=g, best=best, phase2=mc)
 
 
 def best_plan(out):

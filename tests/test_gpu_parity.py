@@ -468,3 +468,50 @@ def test_mc_edges_and_pareto_sizes(cf):
     g = rng.integers(0, 6, size=(1000, 3)).astype(np.float64)
     keep = cf.cf_pareto(torch.from_numpy(g).cuda()).cpu().numpy()
     assert np.array_equal(keep, O.pareto(g))
+    # with plan ids and flags: dominated rows clear the keep flag of their plan, other plans untouched
+    ids = rng.permutation(3000)[:1000].astype(np.int32)
+    fl0 = rng.integers(0, 16, size=3000).astype(np.uint8)
+    fl = torch.from_numpy(fl0.copy()).cuda()
+    keep = cf.cf_pareto(torch.from_numpy(g).cuda(), torch.from_numpy(ids).cuda(), fl).cpu().numpy()
+    want = fl0.copy()
+    want[ids[O.pareto(g) == 0]] &= ~np.uint8(1)
+    assert np.array_equal(keep, O.pareto(g)) and np.array_equal(fl.cpu().numpy(), want)
+    with pytest.raises(cf.CfError):
+        cf.cf_pareto(torch.from_numpy(g).cuda(), torch.from_numpy(ids).cuda(), None)
+    # one row, and rows that are all equal: nothing dominates
+    assert cf.cf_pareto(torch.ones((1, 2), dtype=torch.float64).cuda()).tolist() == [1]
+    assert cf.cf_pareto(torch.ones((300, 4), dtype=torch.float64).cuda()).sum().item() == 300
+    # every row on the front (no block prunes anything), and a front hidden in the last block
+    x = rng.permutation(2000).astype(np.float64)
+    g = np.stack([x, 2000.0 - x], axis=1)
+    assert cf.cf_pareto(torch.from_numpy(g).cuda()).sum().item() == 2000
+    g = rng.uniform(0, 1, size=(1500, 3))
+    g[1400:] += 1.0
+    keep = cf.cf_pareto(torch.from_numpy(g).cuda()).cpu().numpy()
+    assert np.array_equal(keep, O.pareto(g)) and keep[:1400].sum() == 0
+
+
+def test_pipeline_with_phase2(cf):
+    """Phase 1 -> phase 2 -> Pareto -> top-K selection through the pipeline, against the
+    oracle's steps on the same seeds."""
+    _say("pipeline phase 2 c2")
+    from paper_2512_14098_amd import pipeline
+    cfg = load_config("c2")
+    cfg["n_req"], cfg["top_k"] = 2000, 12
+    w = pipeline.Workload(cfg, seeds=[11, 12], phase2=dict(K=700, alpha=0.75))
+    out = pipeline.run_step(w)
+    torch.cuda.synchronize()
+    m = O.make_model(cfg["model"])
+    otr = O.trace_gen(m, [11, 12], 2000)
+    rd, _, fl = O.eval_coarse(m, w.tab, otr["moments"][0], cfg["gpus"])
+    cand = O.select_topk(rd, fl, 65536)
+    met, cnt, gt = O.eval_mc(m, w.tab, cand, rd, otr["moments"][0], 0.75, otr, 0, 700)
+    keep = O.pareto(gt)
+    fl2 = fl.copy()
+    fl2[cand[keep == 0]] &= ~np.uint8(1)
+    assert np.array_equal(out["phase2"]["ids"].cpu().numpy(), cand)
+    assert np.array_equal(out["phase2"]["goodput_t"].cpu().numpy(), gt)
+    assert np.array_equal(out["phase2"]["keep"].cpu().numpy(), keep)
+    assert np.array_equal(out["flags"].cpu().numpy(), fl2)
+    assert np.array_equal(out["ids"].cpu().numpy(), O.select_topk(rd, fl2, 12))
+    assert 0 < int(keep.sum()) < len(cand)
