@@ -26,22 +26,29 @@ PEAK_LANE_OPS = 256 * 4 * 16 * 2.4e9 / 1e12  # T lane-ops/s: CUs x SIMDs x lanes
 OPS_PER_EVENT = 4.0  # algorithmic lane-ops per request-event
 KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_fine.hip", "paper_2512_14098_amd/csrc/cf_internal.h",
                   "paper_2512_14098_amd/csrc/cf_run.h")
-# HBM bytes per k_fine launch from rocprofv3 counters (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0,
-# the scale factors a plain 1 GiB device copy gives), keyed by the kernel source the counters
-# were taken on and the workload (with its sample); any other source or workload reports null
+MC_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_mc.hip", "paper_2512_14098_amd/csrc/cf_internal.h",
+                     "paper_2512_14098_amd/csrc/cf_run.h")
+# HBM bytes per launch of the dominant kernel from rocprofv3 counters (FETCH_SIZE x 2.0 +
+# WRITE_SIZE x 1.0, the scale factors a plain 1 GiB device copy gives), keyed by the kernel
+# source the counters were taken on and the workload (with its sample); any other source or
+# workload reports null
 MEASURED_TRAFFIC = {
-    ("89c98c7ebdbec7d6", "c1: MLLM graph E->L on 8 simulated GPUs (7B LLM, 600M ViT); ~1000 plans; "
-     "16-point rate grid; 32 seeds x 10000 requests"): 2.0785e12,
-    ("89c98c7ebdbec7d6", "c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse "
+    ("34cd2a50a31fb944", "c1: MLLM graph E->L on 8 simulated GPUs (7B LLM, 600M ViT); ~1000 plans; "
+     "16-point rate grid; 32 seeds x 10000 requests"): 2.1129e12,
+    ("34cd2a50a31fb944", "c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse "
      "screening of 10^6 sampled plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 "
-     "requests (sample: first 250 of its 1000 selected plans, first 1 of its 64 seeds)"): 4.293e12,
+     "requests (sample: first 250 of its 1000 selected plans, first 1 of its 64 seeds)"): 4.2524e12,
+}
+MC_MEASURED_TRAFFIC = {
+    ("a9573cd69484e802", "c4 phase 2: the 17444 plans phase 1 keeps of 1000000, 1024 sampled requests (seed 0), "
+     "alpha 0.8, then Pareto pruning"): 3.706e8,
 }
 
 
-def kernel_source_id():
+def kernel_source_id(files=KERNEL_SOURCES):
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in files:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -227,7 +234,9 @@ def phase2_bench(args):
            "config": {"workload": workload, "plans": n, "kept_after_pareto": kept, "mc_ms": mc_ms,
                       "pareto_ms": par_ms},
            "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_LANE_OPS, "unit": "TOP/s",
-                        "frac": achieved / PEAK_LANE_OPS, "traffic": None, "kernel": "k_mc",
+                        "frac": achieved / PEAK_LANE_OPS,
+                        "traffic": MC_MEASURED_TRAFFIC.get((kernel_source_id(MC_KERNEL_SOURCES), workload)),
+                        "kernel": "k_mc",
                         "ops_per_plan": ops / max(n, 1), "kernel_ms": sum(mc_ms) / len(mc_ms)}}
     if not args.no_cpu_baseline and n > 0:
         from oracle import oracle as O
@@ -274,8 +283,9 @@ def main():
     ap.add_argument("--mc-alpha", type=float, default=0.8)
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(sharding by plan blocks is described in DESIGN.md)", file=sys.stderr)
+        print("bench.py runs on one GPU only: the library has no multi-GPU path (triples are "
+              "independent; they would shard by contiguous blocks of the selected plans)",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
