@@ -9,7 +9,7 @@ import subprocess
 import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-SOURCES = ["cfo_trace.c", "cfo_coarse.c", "cfo_des.c", "cfo_mc.c"]
+SOURCES = ["cfo_trace.c", "cfo_coarse.c", "cfo_des.c", "cfo_mc.c", "cfo_enum.c"]
 LIB = os.path.join(HERE, "liboracle.so")
 CFLAGS = ["-O2", "-std=gnu11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared",
           "-Wall", "-Wextra", "-Wno-unused-parameter"]

@@ -18,6 +18,9 @@
  *   - phase 3 request-level simulation of a physical plan at a given rate
  *     (Sec. 4.3, Alg. 2 phase 3; Sec. 5.2 CPU-GPU overlap and communication
  *     overhead);
+ *   - plan enumeration: logical plans from simple and compound subplans,
+ *     physical plans by the executor partitions of Eq. (1) and routing
+ *     weights (Sec. 4.2, Alg. 1);
  *   - per-type goodput = throughput of requests meeting their latency target
  *     (Sec. 3.2), maximum achievable goodput over a rate grid (Sec. 6.1),
  *     argmax selection (Alg. 2, final step).
@@ -136,6 +139,40 @@ int cfo_eval_mc(const cfo_model *m, const cfo_plans *pl, const int32_t *ids, int
 /* Pareto pruning: keep[i] = 0 iff some other vector of g[n][T] is >= in
  * every component and > in one. */
 int cfo_pareto(const double *g, int32_t n, int32_t T, uint8_t *keep);
+
+/* Plan enumeration (Sec. 4.2, Alg. 1; Eq. 1).  Options: GPU budget N,
+ * subplans per logical plan (1 or 2), node sharing between the two
+ * subplans, colocatable edges (colocatable[p] bit c: edge p -> c may be
+ * merged), and per component its batch knobs and GPUs-per-executor options
+ * (a node takes those of its lowest component). */
+typedef struct {
+  int32_t n_gpus, k_s, share;
+  uint32_t colocatable[CFO_MAXC];
+  int32_t n_batch[CFO_MAXC];
+  uint16_t batch[CFO_MAXC][8];
+  int32_t n_gpu_opt[CFO_MAXC];
+  uint8_t gpu_opt[CFO_MAXC][4];
+} cfo_enum_opts;
+
+/* a logical plan: nodes (component masks) and per type one or two
+ * alternatives mapping each path component to a node (255 = off the path) */
+typedef struct {
+  uint8_t n_nodes;
+  uint8_t node_comp[CFO_MAXV];
+  uint8_t n_alt[CFO_MAXT];
+  uint8_t alt_node[CFO_MAXT][2][CFO_MAXC];
+} cfo_logical;
+
+int cfo_enum_logical(const cfo_model *m, const cfo_enum_opts *o, cfo_logical *out, int32_t cap,
+                     int32_t *n_out);
+/* physical plans of one logical plan (UINT64_MAX if that overflows) */
+uint64_t cfo_enum_count(const cfo_model *m, const cfo_enum_opts *o, const cfo_logical *L);
+/* physical plans first .. first+count-1 of the concatenation over L[0..n),
+ * written as plan-table columns 0..count-1 ([slot][count] arrays) */
+int cfo_enum_plans(const cfo_model *m, const cfo_enum_opts *o, const cfo_logical *L, int32_t n_logical,
+                   uint64_t first, int32_t count, uint8_t *n_nodes, uint8_t *node_comp, uint8_t *node_rep,
+                   uint16_t *node_batch, uint8_t *node_gpus, uint8_t *n_alt, uint8_t *alt_w,
+                   uint8_t *alt_node);
 
 int cfo_select_topk(const double *rd, const uint8_t *flags, int32_t P, int32_t k,
                     int32_t *ids, int32_t *n_selected);

@@ -60,6 +60,18 @@ class Plans(C.Structure):
                 ("n_alt", C.c_void_p), ("alt_w", C.c_void_p), ("alt_node", C.c_void_p)]
 
 
+class EnumOpts(C.Structure):
+    _fields_ = [("n_gpus", C.c_int32), ("k_s", C.c_int32), ("share", C.c_int32),
+                ("colocatable", C.c_uint32 * 8), ("n_batch", C.c_int32 * 8),
+                ("batch", (C.c_uint16 * 8) * 8), ("n_gpu_opt", C.c_int32 * 8),
+                ("gpu_opt", (C.c_uint8 * 4) * 8)]
+
+
+class Logical(C.Structure):
+    _fields_ = [("n_nodes", C.c_uint8), ("node_comp", C.c_uint8 * 16), ("n_alt", C.c_uint8 * 8),
+                ("alt_node", ((C.c_uint8 * 8) * 2) * 8)]
+
+
 TRACE_FIELDS = [("arr_ticks", np.uint64), ("type", np.uint8), ("n_img", np.uint8),
                 ("patches", np.uint16), ("prompt", np.uint16), ("out", np.uint16),
                 ("aud_in_ms", np.uint32), ("aud_out_ms", np.uint32), ("rkey0", np.uint64),
@@ -88,6 +100,10 @@ def lib():
         L.cfo_sim_triple.argtypes = [vp, vp, i32, dbl, vp, i32, vp, vp, vp, vp, vp, vp]
         L.cfo_goodput_reduce.argtypes = [vp, vp, i32, i32, i32, i32, vp, C.c_uint32, C.c_uint32,
                                          i32, vp, vp, vp]
+        L.cfo_enum_logical.argtypes = [vp, vp, vp, i32, vp]
+        L.cfo_enum_count.argtypes = [vp, vp, vp]
+        L.cfo_enum_count.restype = C.c_uint64
+        L.cfo_enum_plans.argtypes = [vp, vp, vp, i32, C.c_uint64, i32] + [vp] * 8
         L.cfo_argmax.argtypes = [vp, i32]
         L.cfo_argmax.restype = i32
         _lib = L
@@ -363,3 +379,61 @@ def philox_n(ctr, key):
     out = np.zeros_like(ctr)
     L.cfo_philox_n(_ptr(ctr), _ptr(key), _ptr(out), ctr.shape[0])
     return out
+
+
+# ---------------------------------------------------------------- plan enumeration
+def enum_opts(mcfg, spec, n_gpus):
+    """Enumeration options from a model description and an ``enumerate`` spec:
+    k_s, share, colocatable edges (default: every edge of every type), per-component
+    batch knobs and GPUs-per-executor options (default [1])."""
+    o = EnumOpts()
+    names = {c["name"]: i for i, c in enumerate(mcfg["components"])}
+    o.n_gpus, o.k_s, o.share = int(n_gpus), int(spec.get("k_s", 2)), int(bool(spec.get("share", True)))
+    edges = spec.get("colocatable")
+    if edges is None:
+        edges = [e for t in mcfg["types"] for e in t.get("edges", [])]
+    for a, b in edges:
+        o.colocatable[names[a]] |= 1 << names[b]
+    for c in mcfg["components"]:
+        i = names[c["name"]]
+        knobs = spec["batch"][c["name"]]
+        o.n_batch[i] = len(knobs)
+        for k, v in enumerate(knobs):
+            o.batch[i][k] = int(v)
+        g = spec.get("gpus", {}).get(c["name"], [1])
+        o.n_gpu_opt[i] = len(g)
+        for k, v in enumerate(g):
+            o.gpu_opt[i][k] = int(v)
+    return o
+
+
+def enum_logical(model, opts, cap=200000):
+    out = (Logical * cap)()
+    n = C.c_int32(0)
+    rc = lib().cfo_enum_logical(C.byref(model), C.byref(opts), out, int(cap), C.byref(n))
+    if rc != 0:
+        raise RuntimeError("cfo_enum_logical failed (%d)" % rc)
+    return out[: n.value]
+
+
+def logical_array(logical):
+    arr = (Logical * max(len(logical), 1))()
+    for i, L in enumerate(logical):
+        arr[i] = L
+    return arr
+
+
+def enum_count(model, opts, L):
+    return int(lib().cfo_enum_count(C.byref(model), C.byref(opts), C.byref(L)))
+
+
+def enum_plans(model, opts, logical, first, count):
+    """Physical plans first..first+count-1 as a plan table (inputs.PlanTable layout)."""
+    from paper_2512_14098_amd.inputs.plans import PlanTable
+    tab = PlanTable(int(count))
+    arr = logical_array(logical)
+    rc = lib().cfo_enum_plans(C.byref(model), C.byref(opts), arr, len(logical), C.c_uint64(int(first)),
+                              int(count), *[_ptr(getattr(tab, f)) for f in PlanTable.FIELDS])
+    if rc != 0:
+        raise RuntimeError("cfo_enum_plans failed (%d)" % rc)
+    return tab
