@@ -246,6 +246,77 @@ cf_status cf_eval_mc(const cf_model_desc *model, const cf_plan_table *plans, con
 cf_status cf_pareto(const double *goodput_t_dev, int32_t n, int32_t T, uint8_t *keep_dev,
                     const int32_t *plan_ids_dev, uint8_t *flags_dev, int32_t n_flags, void *stream);
 
+/* ------------------------------------------------------------------ plan enumeration
+ * Plan enumeration (Sec. 4.2, Alg. 1) and the executor partitions of
+ * Eq. (1).  Options: GPU budget N (1..64), subplans per logical plan k_s (1
+ * or 2), node sharing between the two subplans (compound subplans), the
+ * colocatable edges (bit c of colocatable[p]: the edge p -> c may be
+ * merged), and per component its batch knobs (1..8 values in 1..256) and
+ * GPUs-per-executor options (1..4 values in 1..N); a node takes the options
+ * of its lowest component. */
+typedef struct cf_enum_opts {
+  int32_t n_gpus;
+  int32_t k_s;
+  int32_t share;
+  uint32_t colocatable[CF_MAX_COMP];
+  int32_t n_batch[CF_MAX_COMP];
+  uint16_t batch[CF_MAX_COMP][8];
+  int32_t n_gpu_opt[CF_MAX_COMP];
+  uint8_t gpu_opt[CF_MAX_COMP][4];
+} cf_enum_opts;
+
+/* A logical plan (Alg. 1): nodes as component masks, and per type one or
+ * two alternative paths mapping each component of the type's path to a
+ * node (255 off the path).  153 bytes, no padding. */
+typedef struct cf_logical {
+  uint8_t n_nodes;
+  uint8_t node_comp[CF_MAX_NODES];
+  uint8_t n_alt[CF_MAX_TYPES];
+  uint8_t alt_node[CF_MAX_TYPES][2][CF_MAX_COMP];
+} cf_logical;
+
+/* Logical plans (host only, no device work), in this order: subgraphs are
+ * the distinct unions of type paths, ascending as bitmasks, each covering
+ * the types whose paths it contains; the simple subplans of a subgraph come
+ * from the Keep/Merge vectors m = 0 .. 2^k - 1 over its covered types'
+ * colocatable edges in ascending (parent, child) order (bit i merges edge
+ * i), nodes = connected groups in ascending mask order, a repeated grouping
+ * skipped.  Logical plans: each simple subplan covering every type alone;
+ * then, if k_s = 2, each pair i <= j covering every type together, once per
+ * set of shared nodes (a node of j equal to a node of i; subsets in
+ * ascending bitmask order; none without sharing; never all of j's nodes);
+ * nodes = i's, then j's unshared; a type covered by both gets two
+ * alternatives (i's first) unless they map its path to the same nodes.
+ * Plans over 16 nodes and exact repeats are dropped.  Writes up to cap
+ * plans to out_host and their number to *n_out.
+ * Errors: CF_EINVAL (descriptor, options), CF_ECAPACITY (more than cap
+ * plans, or over 16 colocatable edges in one subgraph). */
+cf_status cf_enum_logical(const cf_model_desc *model, const cf_enum_opts *opts, cf_logical *out_host,
+                          int32_t cap, int32_t *n_out);
+
+/* Physical plans per logical plan (Eq. 1): node v takes a configuration k
+ * (GPU option major, batch knob minor) and n_v >= 1 executors with
+ * sum_v gpus_v n_v <= N; each type with two alternatives takes a weight w in
+ * 1..9 tenths for its first (10 - w for the second).  The plans of logical
+ * plan l are numbered offsets[l] .. offsets[l+1]-1: executor assignments
+ * lexicographically in ((k_0, n_0), (k_1, n_1), ...), routing weights
+ * lexicographically inside each (lowest type most significant).
+ * logical_dev: n_logical plans in device memory; writes offsets_dev[n_logical
+ * + 1] (device) and the total to *total_host (synchronises the stream).
+ * Errors: CF_EINVAL, CF_ECAPACITY (the total does not fit 64 bits). */
+cf_status cf_enum_count(const cf_model_desc *model, const cf_enum_opts *opts, const cf_logical *logical_dev,
+                        int32_t n_logical, uint64_t *offsets_dev, uint64_t *total_host, void *stream);
+
+/* Physical plans first .. first+count-1 (numbered as cf_enum_count numbers
+ * them; offsets_dev and total from it, with the same options and logical
+ * plans) into columns 0..count-1 of the device plan table *out (out->P >=
+ * count; its arrays are written, unused node slots 0, unused route entries
+ * 255).  One thread per plan, asynchronous on stream.
+ * Errors: CF_EINVAL (options, sizes, first + count > total). */
+cf_status cf_enum_plans(const cf_model_desc *model, const cf_enum_opts *opts, const cf_logical *logical_dev,
+                        int32_t n_logical, const uint64_t *offsets_dev, uint64_t total, uint64_t first,
+                        int32_t count, const cf_plan_table *out, void *stream);
+
 /* Goodput (Sec. 3.2) at the highest feasible rate (Sec. 6.1): M_t, N_t
  * pooled over seeds; rate k feasible iff theta_den*M_t >= theta_num*N_t for
  * every type with N_t > 0; kstar = first infeasible - 1; goodput_t =

@@ -62,6 +62,16 @@ class cf_plan_table(C.Structure):
                                            "node_gpus", "n_alt", "alt_w", "alt_node")]
 
 
+class cf_enum_opts(C.Structure):
+    _fields_ = [("n_gpus", C.c_int32), ("k_s", C.c_int32), ("share", C.c_int32),
+                ("colocatable", C.c_uint32 * MAX_COMP), ("n_batch", C.c_int32 * MAX_COMP),
+                ("batch", (C.c_uint16 * 8) * MAX_COMP), ("n_gpu_opt", C.c_int32 * MAX_COMP),
+                ("gpu_opt", (C.c_uint8 * 4) * MAX_COMP)]
+
+
+LOGICAL_BYTES = 1 + 16 + 8 + 8 * 2 * 8  # sizeof(cf_logical)
+
+
 class cf_fine_out(C.Structure):
     _fields_ = [("met_dev", C.c_void_p), ("cnt_dev", C.c_void_p), ("events_dev", C.c_void_p),
                 ("status_dev", C.c_void_p), ("lat_dev", C.c_void_p), ("lat_triples_dev", C.c_void_p),
@@ -85,6 +95,9 @@ def _load():
         "cf_goodput_reduce": ([vp, vp, i32, i32, i32, i32, vp, u32, u32, i32, vp, vp, vp, vp], i32),
         "cf_eval_mc": ([vp, vp, vp, i32, vp, vp, dbl, vp, i32, i32, vp, vp, vp, vp, vp], i32),
         "cf_pareto": ([vp, i32, i32, vp, vp, vp, i32, vp], i32),
+        "cf_enum_logical": ([vp, vp, vp, i32, vp], i32),
+        "cf_enum_count": ([vp, vp, vp, i32, vp, vp, vp], i32),
+        "cf_enum_plans": ([vp, vp, vp, i32, vp, C.c_uint64, C.c_uint64, i32, vp, vp], i32),
         "cf_select_best": ([vp, i32, vp, vp], i32),
         "cf_math_eval": ([i32, vp, vp, vp, i64, vp], i32),
         "cf_philox_eval": ([vp, vp, vp, i64, vp], i32),
@@ -100,6 +113,7 @@ def _load():
 _lib = _load()
 EXPORTED = ("cf_last_error", "cf_status_str", "cf_version", "cf_trace_gen", "cf_eval_coarse",
             "cf_select_topk", "cf_rate_grid", "cf_eval_fine", "cf_eval_mc", "cf_pareto",
+            "cf_enum_logical", "cf_enum_count", "cf_enum_plans",
             "cf_goodput_reduce", "cf_select_best", "cf_math_eval", "cf_philox_eval", "cf_release_scratch")
 
 
@@ -243,6 +257,32 @@ class DevicePlans:
             self.t[f] = torch.from_numpy(a).to(device)
             setattr(self.c, f + "_dev", self.t[f].data_ptr())
 
+    SHAPES = {"n_nodes": (None, torch.uint8), "node_comp": (16, torch.uint8), "node_rep": (16, torch.uint8),
+              "node_batch": (16, torch.int16), "node_gpus": (16, torch.uint8), "n_alt": (8, torch.uint8),
+              "alt_w": (16, torch.uint8), "alt_node": (128, torch.uint8)}
+
+    @classmethod
+    def empty(cls, P, device="cuda"):
+        """An unfilled device plan table of P columns (written by cf_enum_plans)."""
+        self = cls.__new__(cls)
+        self.P, self.t, self.c = int(P), {}, cf_plan_table()
+        self.c.P = self.P
+        for f in cls.FIELDS:
+            rows, dt = cls.SHAPES[f]
+            shape = (self.P,) if rows is None else (rows, self.P)
+            self.t[f] = torch.empty(shape, dtype=dt, device=device)
+            setattr(self.c, f + "_dev", self.t[f].data_ptr())
+        return self
+
+    def to_host(self):
+        """The table as an inputs.PlanTable (host copy)."""
+        from .inputs.plans import PlanTable
+        tab = PlanTable(self.P)
+        for f in self.FIELDS:
+            a = self.t[f].cpu().numpy()
+            setattr(tab, f, a.view(np.uint16) if f == "node_batch" else a)
+        return tab
+
 
 # ------------------------------------------------------------------ entry points
 def cf_trace_gen(desc, seeds, n_req, device="cuda"):
@@ -329,6 +369,61 @@ def cf_pareto(goodput_t, plan_ids=None, flags=None):
                           _p(plan_ids.contiguous()) if plan_ids is not None else None,
                           _p(flags) if flags is not None else None, nf, _stream()), "cf_pareto")
     return keep
+
+
+def enum_opts(mcfg, spec, n_gpus):
+    """cf_enum_opts from a model description and an enumeration spec (keys k_s,
+    share, colocatable (edge list; default every edge of every type), batch
+    {component: knobs}, gpus {component: options}, default [1])."""
+    o = cf_enum_opts()
+    idx = {c["name"]: i for i, c in enumerate(mcfg["components"])}
+    o.n_gpus = int(n_gpus)
+    o.k_s = int(spec.get("k_s", 2))
+    o.share = 1 if spec.get("share", True) else 0
+    edges = spec.get("colocatable")
+    if edges is None:
+        edges = [e for ty in mcfg["types"] for e in ty.get("edges", [])]
+    for a, b in edges:
+        o.colocatable[idx[a]] |= 1 << idx[b]
+    for name, i in idx.items():
+        knobs = list(spec["batch"][name])
+        o.n_batch[i] = len(knobs)
+        for k, v in enumerate(knobs):
+            o.batch[i][k] = int(v)
+        gl = list(spec.get("gpus", {}).get(name, [1]))
+        o.n_gpu_opt[i] = len(gl)
+        for k, v in enumerate(gl):
+            o.gpu_opt[i][k] = int(v)
+    return o
+
+
+def cf_enum_logical(desc, opts, cap=65536):
+    """Logical plans (host): uint8 array [n, LOGICAL_BYTES] in cf_logical layout."""
+    buf = np.zeros((cap, LOGICAL_BYTES), np.uint8)
+    n = C.c_int32(0)
+    _check(_lib.cf_enum_logical(C.byref(desc), C.byref(opts), buf.ctypes.data_as(C.c_void_p), int(cap),
+                                C.byref(n)), "cf_enum_logical")
+    return buf[: n.value].copy()
+
+
+def cf_enum_count(desc, opts, logical_dev):
+    """(offsets [n+1] uint64 on the device, total physical plans)."""
+    n = int(logical_dev.shape[0])
+    offsets = torch.empty(n + 1, dtype=torch.int64, device=logical_dev.device)
+    total = C.c_uint64(0)
+    _check(_lib.cf_enum_count(C.byref(desc), C.byref(opts), _p(logical_dev.contiguous()), n, _p(offsets),
+                              C.byref(total), _stream()), "cf_enum_count")
+    return offsets, int(total.value)
+
+
+def cf_enum_plans(desc, opts, logical_dev, offsets, total, first, count, out=None):
+    """Physical plans first..first+count-1 into a device plan table (new, or out)."""
+    if out is None:
+        out = DevicePlans.empty(count, logical_dev.device)
+    _check(_lib.cf_enum_plans(C.byref(desc), C.byref(opts), _p(logical_dev.contiguous()),
+                              int(logical_dev.shape[0]), _p(offsets), C.c_uint64(int(total)),
+                              C.c_uint64(int(first)), int(count), C.byref(out.c), _stream()), "cf_enum_plans")
+    return out
 
 
 def cf_goodput_reduce(met, cnt, rates, theta, n_req):

@@ -113,6 +113,6 @@ __device__ __forceinline__ double dev_exp(double x) {
 namespace cf {
 // Per-device scratch owned by the library, grown on demand, one region per
 // purpose.  Calls that use the same region must not overlap on one device.
-enum ScratchSlot { SCR_TRACE = 0, SCR_SELECT = 1, SCR_FINE = 2, SCR_MC = 3, SCR_PARETO = 4, SCR_NSLOTS = 5 };
+enum ScratchSlot { SCR_TRACE = 0, SCR_SELECT = 1, SCR_FINE = 2, SCR_MC = 3, SCR_PARETO = 4, SCR_ENUM = 5, SCR_NSLOTS = 6 };
 void *scratch_get(int slot, size_t bytes, cf_status *st);
 }  // namespace cf

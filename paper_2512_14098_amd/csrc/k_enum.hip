@@ -1,0 +1,479 @@
+// k_enum.hip -- cf_enum_logical, cf_enum_count, cf_enum_plans: plan
+// enumeration (Sec. 4.2, Alg. 1) and the executor partitions of Eq. (1).
+//
+// Logical plans are few (hundreds to thousands) and are built on the host.
+// Physical plans are many (a logical plan of five nodes on 64 GPUs has
+// billions), so they are numbered and produced on the device by unranking:
+//   - per logical plan, a table cnt[v][b] = number of executor assignments
+//     of nodes v.. within b GPUs (one block per logical plan, the budgets
+//     across threads, the nodes from the last to the first);
+//   - offsets = exclusive prefix sum of cnt[0][N] * 9^(types with two
+//     alternatives);
+//   - one thread per plan index: the logical plan by binary search in the
+//     offsets, the routing weights as base-9 digits of the index within it,
+//     the executor assignment by walking the table (at node v with budget
+//     b, the candidates (k, n) in order each own cnt[v+1][b - gpus_k n]
+//     consecutive numbers), then the plan-table columns are written
+//     slot-major, so a wavefront's 64 plans fill 64 consecutive bytes of
+//     each slot row.
+#include "cf_internal.h"
+
+#include <algorithm>
+#include <cstring>
+#include <map>
+#include <set>
+#include <string>
+#include <vector>
+
+namespace cf {
+namespace {
+
+constexpr int kEnumMaxN = 64;                       // GPU budget limit (executors per plan)
+constexpr int kTabStride = kEnumMaxN + 1;           // budgets 0..N
+constexpr int kTabSize = (CF_MAX_NODES + 1) * kTabStride;  // u64 entries per logical plan
+
+cf_status check_opts(const cf_model_desc *d, const cf_enum_opts *o) {
+  if (!d || !o) return set_error(CF_EINVAL, "NULL argument");
+  if (d->n_comp < 1 || d->n_comp > CF_MAX_COMP || d->n_types < 1 || d->n_types > CF_MAX_TYPES)
+    return set_error(CF_EINVAL, "model sizes");
+  if (o->n_gpus < 1 || o->n_gpus > kEnumMaxN) return set_error(CF_EINVAL, "n_gpus must be in 1..%d", kEnumMaxN);
+  if (o->k_s < 1 || o->k_s > 2) return set_error(CF_EINVAL, "k_s must be 1 or 2");
+  for (int c = 0; c < d->n_comp; c++) {
+    if (o->n_batch[c] < 1 || o->n_batch[c] > 8) return set_error(CF_EINVAL, "n_batch[%d]", c);
+    for (int k = 0; k < o->n_batch[c]; k++)
+      if (o->batch[c][k] < 1 || o->batch[c][k] > CF_MAX_BATCH) return set_error(CF_EINVAL, "batch[%d][%d]", c, k);
+    if (o->n_gpu_opt[c] < 1 || o->n_gpu_opt[c] > 4) return set_error(CF_EINVAL, "n_gpu_opt[%d]", c);
+    for (int k = 0; k < o->n_gpu_opt[c]; k++)
+      if (o->gpu_opt[c][k] < 1 || o->gpu_opt[c][k] > o->n_gpus) return set_error(CF_EINVAL, "gpu_opt[%d][%d]", c, k);
+  }
+  return CF_OK;
+}
+
+// ------------------------------------------------------------------ host: logical plans
+struct Subplan {
+  uint32_t cs, cov;
+  std::vector<uint8_t> nodes;  // ascending masks
+  int node_of(int c) const {
+    for (size_t k = 0; k < nodes.size(); k++)
+      if ((nodes[k] >> c) & 1u) return (int)k;
+    return -1;
+  }
+};
+
+int uf_find(int *par, int x) {
+  while (par[x] != x) {
+    par[x] = par[par[x]];
+    x = par[x];
+  }
+  return x;
+}
+
+std::string plan_key(const cf_logical &L, int T) {
+  std::string k;
+  k.push_back((char)L.n_nodes);
+  for (int v = 0; v < L.n_nodes; v++) k.push_back((char)L.node_comp[v]);
+  for (int t = 0; t < T; t++) {
+    k.push_back((char)L.n_alt[t]);
+    for (int a = 0; a < L.n_alt[t]; a++)
+      for (int c = 0; c < CF_MAX_COMP; c++) k.push_back((char)L.alt_node[t][a][c]);
+  }
+  return k;
+}
+
+void route_type(cf_logical &L, int t, int a, uint32_t path, const Subplan &s, const int *node_map) {
+  for (int c = 0; c < CF_MAX_COMP; c++)
+    if ((path >> c) & 1u) L.alt_node[t][a][c] = (uint8_t)node_map[s.node_of(c)];
+}
+
+// ------------------------------------------------------------------ device
+struct EnumView {
+  int N;
+  const cf_logical *logical;
+  int n_logical;
+  uint64_t *tab;      // [n_logical][kTabSize]
+  uint64_t *totals;   // [n_logical]
+};
+
+__device__ __forceinline__ uint64_t sat_add(uint64_t a, uint64_t b) { return a > ~0ull - b ? ~0ull : a + b; }
+__device__ __forceinline__ uint64_t sat_mul(uint64_t a, uint64_t b) { return (b && a > ~0ull / b) ? ~0ull : a * b; }
+
+// The option tables a node indexes by its lowest component, staged in LDS.
+struct OptsLds {
+  uint8_t n_batch[CF_MAX_COMP], n_gpu[CF_MAX_COMP];
+  uint8_t gpu[CF_MAX_COMP][4];
+  uint16_t batch[CF_MAX_COMP][8];
+};
+
+__device__ void stage_opts(OptsLds &s, const cf_enum_opts &o, int tid, int nthreads) {
+  for (int i = tid; i < CF_MAX_COMP; i += nthreads) {
+    s.n_batch[i] = (uint8_t)o.n_batch[i];
+    s.n_gpu[i] = (uint8_t)o.n_gpu_opt[i];
+    for (int k = 0; k < 4; k++) s.gpu[i][k] = o.gpu_opt[i][k];
+    for (int k = 0; k < 8; k++) s.batch[i][k] = o.batch[i][k];
+  }
+}
+
+// One block per logical plan: cnt[v][b], then the plan's total.
+__global__ void __launch_bounds__(128) k_enum_table(cf_enum_opts o, EnumView V) {
+  __shared__ OptsLds so;
+  __shared__ uint64_t cnt[CF_MAX_NODES + 1][kTabStride];
+  const int l = blockIdx.x, b = threadIdx.x;
+  stage_opts(so, o, threadIdx.x, blockDim.x);
+  const cf_logical &L = V.logical[l];
+  const int nv = L.n_nodes <= CF_MAX_NODES ? L.n_nodes : CF_MAX_NODES;
+  if (b <= V.N) cnt[nv][b] = 1;
+  __syncthreads();
+  for (int v = nv - 1; v >= 0; v--) {
+    if (b <= V.N) {
+      const int c0 = L.node_comp[v] ? __ffs(L.node_comp[v]) - 1 : 0;
+      uint64_t tot = 0;
+      for (int gi = 0; gi < so.n_gpu[c0]; gi++) {
+        const int g = so.gpu[c0][gi];
+        uint64_t per_cfg = 0;
+        for (int n = 1; g * n <= b; n++) per_cfg = sat_add(per_cfg, cnt[v + 1][b - g * n]);
+        for (int bi = 0; bi < so.n_batch[c0]; bi++) tot = sat_add(tot, per_cfg);
+      }
+      cnt[v][b] = tot;
+    }
+    __syncthreads();
+  }
+  uint64_t *out = V.tab + (size_t)l * kTabSize;
+  for (int i = threadIdx.x; i < (nv + 1) * kTabStride; i += blockDim.x) out[i] = (&cnt[0][0])[i];
+  if (threadIdx.x == 0) {
+    uint64_t tot = cnt[0][V.N];
+    for (int t = 0; t < CF_MAX_TYPES; t++)
+      if (L.n_alt[t] == 2) tot = sat_mul(tot, 9);
+    V.totals[l] = tot;
+  }
+}
+
+// offsets[0] = 0, offsets[l+1] = offsets[l] + totals[l] (saturating); one block.
+__global__ void __launch_bounds__(1024) k_enum_offsets(const uint64_t *totals, int n, uint64_t *offsets) {
+  __shared__ uint64_t part[1024];
+  __shared__ uint64_t carry_s;
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    carry_s = 0;
+    offsets[0] = 0;
+  }
+  __syncthreads();
+  for (int base = 0; base < n; base += 1024) {
+    const uint64_t x = base + tid < n ? totals[base + tid] : 0;
+    part[tid] = x;
+    __syncthreads();
+    for (int d = 1; d < 1024; d <<= 1) {
+      const uint64_t add = tid >= d ? part[tid - d] : 0;
+      __syncthreads();
+      part[tid] = sat_add(part[tid], add);
+      __syncthreads();
+    }
+    if (base + tid < n) offsets[base + tid + 1] = sat_add(carry_s, part[tid]);
+    __syncthreads();
+    if (tid == 1023) carry_s = sat_add(carry_s, part[1023]);
+    __syncthreads();
+  }
+}
+
+struct PlanOut {
+  int P;
+  uint8_t *n_nodes, *node_comp, *node_rep, *node_gpus, *n_alt, *alt_w, *alt_node;
+  uint16_t *node_batch;
+};
+
+__global__ void __launch_bounds__(256) k_enum_unrank(cf_enum_opts o, EnumView V, const uint64_t *offsets,
+                                                    uint64_t first, int count, PlanOut out) {
+  __shared__ OptsLds so;
+  stage_opts(so, o, threadIdx.x, blockDim.x);
+  __syncthreads();
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= count) return;
+  const uint64_t idx = first + (uint64_t)p;
+  const size_t P = (size_t)out.P;
+  // the logical plan: the last l with offsets[l] <= idx
+  int lo = 0, hi = V.n_logical;  // offsets[lo] <= idx < offsets[hi] when in range
+  const bool in_range = idx < offsets[V.n_logical];
+  if (in_range) {
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (offsets[mid] <= idx) lo = mid; else hi = mid;
+    }
+  }
+  const cf_logical &L = V.logical[lo];
+  const int nv = in_range ? L.n_nodes : 0;
+  uint64_t local = in_range ? idx - offsets[lo] : 0;
+  // routing digits: types with two alternatives, lowest type most significant
+  int na2 = 0;
+  for (int t = 0; t < CF_MAX_TYPES; t++) na2 += L.n_alt[t] == 2;
+  uint64_t R = 1;
+  for (int i = 0; i < na2; i++) R *= 9;
+  uint64_t r = local % R, q = local / R;
+  uint8_t wdig[CF_MAX_TYPES];
+  for (int i = na2 - 1; i >= 0; i--) {
+    wdig[i] = (uint8_t)(r % 9 + 1);
+    r /= 9;
+  }
+  // the executor assignment
+  const uint64_t *tab = V.tab + (size_t)lo * kTabSize;
+  int b = V.N;
+  for (int v = 0; v < CF_MAX_NODES; v++) {
+    uint8_t comp = 0, rep = 0, gpus = 0;
+    uint16_t batch = 0;
+    if (v < nv) {
+      comp = L.node_comp[v];
+      const int c0 = comp ? __ffs(comp) - 1 : 0;
+      const int nb = so.n_batch[c0];
+      bool done = false;
+      for (int gi = 0; gi < so.n_gpu[c0] && !done; gi++) {
+        const int g = so.gpu[c0][gi];
+        for (int bi = 0; bi < nb && !done; bi++) {
+          for (int n = 1; g * n <= b; n++) {
+            const uint64_t c = tab[(v + 1) * kTabStride + (b - g * n)];
+            if (q < c) {
+              rep = (uint8_t)n;
+              gpus = (uint8_t)g;
+              batch = so.batch[c0][bi];
+              b -= g * n;
+              done = true;
+              break;
+            }
+            q -= c;
+          }
+        }
+      }
+    }
+    out.node_comp[v * P + p] = comp;
+    out.node_rep[v * P + p] = rep;
+    out.node_gpus[v * P + p] = gpus;
+    out.node_batch[v * P + p] = batch;
+  }
+  out.n_nodes[p] = (uint8_t)nv;
+  int i2 = 0;
+  for (int t = 0; t < CF_MAX_TYPES; t++) {
+    const int na = in_range ? L.n_alt[t] : 0;
+    uint8_t w0 = 0, w1 = 0;
+    if (na == 1) w0 = 10;
+    if (na == 2) {
+      w0 = wdig[i2++];
+      w1 = (uint8_t)(10 - w0);
+    }
+    out.n_alt[t * P + p] = (uint8_t)na;
+    out.alt_w[(2 * t) * P + p] = w0;
+    out.alt_w[(2 * t + 1) * P + p] = w1;
+    for (int a = 0; a < 2; a++)
+      for (int c = 0; c < CF_MAX_COMP; c++)
+        out.alt_node[((2 * t + a) * CF_MAX_COMP + c) * P + p] = in_range ? L.alt_node[t][a][c] : (uint8_t)255;
+  }
+}
+
+cf_status run_tables(const cf_enum_opts *opts, const cf_logical *logical_dev, int n_logical, uint64_t **tab_out,
+                     uint64_t **totals_out, hipStream_t s) {
+  cf_status st = CF_OK;
+  const size_t bytes = sizeof(uint64_t) * ((size_t)n_logical * kTabSize + (size_t)n_logical);
+  uint64_t *scr = (uint64_t *)scratch_get(SCR_ENUM, bytes, &st);
+  if (!scr) return st;
+  EnumView V;
+  V.N = opts->n_gpus;
+  V.logical = logical_dev;
+  V.n_logical = n_logical;
+  V.tab = scr;
+  V.totals = scr + (size_t)n_logical * kTabSize;
+  hipLaunchKernelGGL(k_enum_table, dim3((unsigned)n_logical), dim3(128), 0, s, *opts, V);
+  st = hip_check(hipGetLastError(), "cf_enum table launch");
+  *tab_out = V.tab;
+  *totals_out = V.totals;
+  return st;
+}
+
+}  // namespace
+}  // namespace cf
+
+extern "C" cf_status cf_enum_logical(const cf_model_desc *model, const cf_enum_opts *opts, cf_logical *out_host,
+                                     int32_t cap, int32_t *n_out) {
+  using namespace cf;
+  cf_status st = check_opts(model, opts);
+  if (st != CF_OK) return st;
+  if (!out_host || !n_out || cap < 0) return set_error(CF_EINVAL, "NULL output or cap < 0");
+  *n_out = 0;
+  const int T = model->n_types, C = model->n_comp;
+  const uint32_t all_types = (1u << T) - 1u;
+  // subgraphs: distinct unions of type paths, ascending
+  std::set<uint32_t> subgraphs;
+  for (uint32_t u = 1; u <= all_types; u++) {
+    uint32_t cs = 0;
+    for (int t = 0; t < T; t++)
+      if ((u >> t) & 1u) cs |= model->path_mask[t];
+    subgraphs.insert(cs);
+  }
+  // simple subplans
+  std::vector<Subplan> S;
+  for (uint32_t cs : subgraphs) {
+    uint32_t cov = 0;
+    for (int t = 0; t < T; t++)
+      if (!(model->path_mask[t] & ~cs)) cov |= 1u << t;
+    std::vector<std::pair<int, int>> edges;
+    for (int p = 0; p < C; p++)
+      for (int c = 0; c < C; c++) {
+        if (!((opts->colocatable[p] >> c) & 1u)) continue;
+        bool on = false;
+        for (int t = 0; t < T && !on; t++) on = ((cov >> t) & 1u) && ((model->parents[t][c] >> p) & 1u);
+        if (on) edges.emplace_back(p, c);
+      }
+    if (edges.size() > 16) return set_error(CF_ECAPACITY, "more than 16 colocatable edges in a subgraph");
+    std::set<std::vector<uint8_t>> seen;
+    for (uint32_t m = 0; m < (1u << edges.size()); m++) {
+      int par[CF_MAX_COMP];
+      for (int c = 0; c < CF_MAX_COMP; c++) par[c] = c;
+      for (size_t i = 0; i < edges.size(); i++)
+        if ((m >> i) & 1u) {
+          const int ra = uf_find(par, edges[i].first), rb = uf_find(par, edges[i].second);
+          if (ra != rb) par[std::max(ra, rb)] = std::min(ra, rb);
+        }
+      std::map<int, uint8_t> groups;
+      for (int c = 0; c < CF_MAX_COMP; c++)
+        if ((cs >> c) & 1u) groups[uf_find(par, c)] |= (uint8_t)(1u << c);
+      std::vector<uint8_t> nodes;
+      for (auto &g : groups) nodes.push_back(g.second);
+      std::sort(nodes.begin(), nodes.end());
+      if (!seen.insert(nodes).second) continue;
+      S.push_back(Subplan{cs, cov, nodes});
+    }
+  }
+  // logical plans
+  std::set<std::string> emitted;
+  int n = 0;
+  auto emit = [&](const cf_logical &L) -> cf_status {
+    if (!emitted.insert(plan_key(L, T)).second) return CF_OK;
+    if (n >= cap) return set_error(CF_ECAPACITY, "more than %d logical plans", cap);
+    out_host[n++] = L;
+    return CF_OK;
+  };
+  auto blank = []() {
+    cf_logical L;
+    memset(&L, 0, sizeof L);
+    memset(L.alt_node, 255, sizeof L.alt_node);
+    return L;
+  };
+  for (const Subplan &s : S) {
+    if (s.cov != all_types) continue;
+    cf_logical L = blank();
+    L.n_nodes = (uint8_t)s.nodes.size();
+    int ident[CF_MAX_COMP];
+    for (size_t v = 0; v < s.nodes.size(); v++) {
+      L.node_comp[v] = s.nodes[v];
+      ident[v] = (int)v;
+    }
+    for (int t = 0; t < T; t++) {
+      L.n_alt[t] = 1;
+      route_type(L, t, 0, model->path_mask[t], s, ident);
+    }
+    if ((st = emit(L)) != CF_OK) return st;
+  }
+  if (opts->k_s == 2) {
+    for (size_t i = 0; i < S.size(); i++)
+      for (size_t j = i; j < S.size(); j++) {
+        const Subplan &A = S[i], &B = S[j];
+        if ((A.cov | B.cov) != all_types) continue;
+        std::vector<std::pair<int, int>> matchable;  // (node of B, equal node of A), in B's order
+        for (size_t v = 0; v < B.nodes.size(); v++)
+          for (size_t w = 0; w < A.nodes.size(); w++)
+            if (B.nodes[v] == A.nodes[w]) matchable.emplace_back((int)v, (int)w);
+        const uint32_t n_sets = opts->share ? (1u << matchable.size()) : 1u;
+        for (uint32_t sh = 0; sh < n_sets; sh++) {
+          if (opts->share && matchable.size() == B.nodes.size() && sh == n_sets - 1) continue;
+          int amap[CF_MAX_COMP], bmap[CF_MAX_COMP];
+          int nv = (int)A.nodes.size();
+          for (int v = 0; v < nv; v++) amap[v] = v;
+          for (size_t v = 0; v < B.nodes.size(); v++) bmap[v] = -1;
+          for (size_t k = 0; k < matchable.size(); k++)
+            if ((sh >> k) & 1u) bmap[matchable[k].first] = matchable[k].second;
+          for (size_t v = 0; v < B.nodes.size(); v++)
+            if (bmap[v] < 0) bmap[v] = nv++;
+          if (nv > CF_MAX_NODES) continue;
+          cf_logical L = blank();
+          L.n_nodes = (uint8_t)nv;
+          for (size_t v = 0; v < A.nodes.size(); v++) L.node_comp[v] = A.nodes[v];
+          for (size_t v = 0; v < B.nodes.size(); v++) L.node_comp[bmap[v]] = B.nodes[v];
+          for (int t = 0; t < T; t++) {
+            const bool inA = (A.cov >> t) & 1u, inB = (B.cov >> t) & 1u;
+            int na = 0;
+            if (inA) route_type(L, t, na++, model->path_mask[t], A, amap);
+            if (inB) {
+              route_type(L, t, na, model->path_mask[t], B, bmap);
+              if (na == 1 && !memcmp(L.alt_node[t][0], L.alt_node[t][1], CF_MAX_COMP))
+                memset(L.alt_node[t][1], 255, CF_MAX_COMP);
+              else
+                na++;
+            }
+            L.n_alt[t] = (uint8_t)na;
+          }
+          if ((st = emit(L)) != CF_OK) return st;
+        }
+      }
+  }
+  *n_out = n;
+  return CF_OK;
+}
+
+extern "C" cf_status cf_enum_count(const cf_model_desc *model, const cf_enum_opts *opts, const cf_logical *logical_dev,
+                                   int32_t n_logical, uint64_t *offsets_dev, uint64_t *total_host, void *stream) {
+  using namespace cf;
+  cf_status st = check_opts(model, opts);
+  if (st != CF_OK) return st;
+  if (n_logical < 0 || !offsets_dev || !total_host || (n_logical > 0 && !logical_dev))
+    return set_error(CF_EINVAL, "NULL array or n_logical < 0");
+  hipStream_t s = as_stream(stream);
+  *total_host = 0;
+  if (n_logical == 0) {
+    const uint64_t zero = 0;
+    st = hip_check(hipMemcpyAsync(offsets_dev, &zero, sizeof zero, hipMemcpyHostToDevice, s), "cf_enum_count copy");
+    if (st != CF_OK) return st;
+    return hip_check(hipStreamSynchronize(s), "cf_enum_count sync");
+  }
+  uint64_t *tab = nullptr, *totals = nullptr;
+  if ((st = run_tables(opts, logical_dev, n_logical, &tab, &totals, s)) != CF_OK) return st;
+  hipLaunchKernelGGL(k_enum_offsets, dim3(1), dim3(1024), 0, s, totals, n_logical, offsets_dev);
+  if ((st = hip_check(hipGetLastError(), "cf_enum offsets launch")) != CF_OK) return st;
+  st = hip_check(hipMemcpyAsync(total_host, offsets_dev + n_logical, sizeof(uint64_t), hipMemcpyDeviceToHost, s),
+                 "cf_enum_count copy");
+  if (st != CF_OK) return st;
+  if ((st = hip_check(hipStreamSynchronize(s), "cf_enum_count sync")) != CF_OK) return st;
+  if (*total_host == ~0ull) return set_error(CF_ECAPACITY, "the number of physical plans does not fit 64 bits");
+  return CF_OK;
+}
+
+extern "C" cf_status cf_enum_plans(const cf_model_desc *model, const cf_enum_opts *opts, const cf_logical *logical_dev,
+                                   int32_t n_logical, const uint64_t *offsets_dev, uint64_t total, uint64_t first,
+                                   int32_t count, const cf_plan_table *out, void *stream) {
+  using namespace cf;
+  cf_status st = check_opts(model, opts);
+  if (st != CF_OK) return st;
+  if (!out || count < 0 || out->P < count) return set_error(CF_EINVAL, "output table smaller than count");
+  if (count == 0) return CF_OK;
+  if (n_logical < 1 || !logical_dev || !offsets_dev) return set_error(CF_EINVAL, "no logical plans");
+  if (first > total || (uint64_t)count > total - first) return set_error(CF_EINVAL, "first + count > total");
+  if (!out->n_nodes_dev || !out->node_comp_dev || !out->node_rep_dev || !out->node_batch_dev ||
+      !out->node_gpus_dev || !out->n_alt_dev || !out->alt_w_dev || !out->alt_node_dev)
+    return set_error(CF_EINVAL, "NULL plan-table array");
+  hipStream_t s = as_stream(stream);
+  uint64_t *tab = nullptr, *totals = nullptr;
+  if ((st = run_tables(opts, logical_dev, n_logical, &tab, &totals, s)) != CF_OK) return st;
+  EnumView V;
+  V.N = opts->n_gpus;
+  V.logical = logical_dev;
+  V.n_logical = n_logical;
+  V.tab = tab;
+  V.totals = totals;
+  PlanOut o;
+  o.P = out->P;
+  o.n_nodes = const_cast<uint8_t *>(out->n_nodes_dev);
+  o.node_comp = const_cast<uint8_t *>(out->node_comp_dev);
+  o.node_rep = const_cast<uint8_t *>(out->node_rep_dev);
+  o.node_batch = const_cast<uint16_t *>(out->node_batch_dev);
+  o.node_gpus = const_cast<uint8_t *>(out->node_gpus_dev);
+  o.n_alt = const_cast<uint8_t *>(out->n_alt_dev);
+  o.alt_w = const_cast<uint8_t *>(out->alt_w_dev);
+  o.alt_node = const_cast<uint8_t *>(out->alt_node_dev);
+  hipLaunchKernelGGL(k_enum_unrank, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, *opts, V, offsets_dev,
+                     first, count, o);
+  return hip_check(hipGetLastError(), "cf_enum_plans launch");
+}
