@@ -7,7 +7,8 @@ reduction and selection.  Default workload: c1 (E->L on 8 simulated GPUs,
 1000 plans screened, the kept ones simulated at 16 rates x 32 seeds x 10^4
 requests).  Prints one JSON line.
 
-Other modes (each prints its own JSON line and exits): --phase2 times phase 2
+Other modes (each prints its own JSON line and exits): --enum times plan
+enumeration on the device and phase-1 screening of its output; --phase2 times phase 2
 (Monte Carlo latency of every plan phase 1 keeps, default workload c4) and
 Pareto pruning; --stress times the HBM-bound steps at full c4 size;
 --copy-probe runs the plain copy the HBM byte counters are calibrated on.
@@ -39,6 +40,9 @@ MEASURED_TRAFFIC = {
      "screening of 10^6 sampled plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 "
      "requests (sample: first 250 of its 1000 selected plans, first 1 of its 64 seeds)"): 4.2524e12,
 }
+ENUM_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_enum.hip", "paper_2512_14098_amd/csrc/cf_internal.h")
+# bytes per k_enum_unrank launch of 2^25 plans (the write counter reads exactly the table bytes)
+ENUM_MEASURED_TRAFFIC = {("8a66e58269296fa0", 1 << 25): 7.8189e9}
 MC_MEASURED_TRAFFIC = {
     ("a9573cd69484e802", "c4 phase 2: the 17444 plans phase 1 keeps of 1000000, 1024 sampled requests (seed 0), "
      "alpha 0.8, then Pareto pruning"): 3.706e8,
@@ -256,6 +260,81 @@ def phase2_bench(args):
     print(json.dumps(res), flush=True)
 
 
+ENUM_PLAN_BYTES = 233  # plan-table bytes written per plan: 1 + 16 x (1 + 1 + 2 + 1) + 8 + 16 + 128
+
+
+def enum_bench(args):
+    """Plan enumeration on the device: the omni graph's space on 16 GPUs (c2's model, two
+    subplans, shared nodes, batch knobs {16, 64, 256}), CHUNK plans per launch at evenly spaced
+    starting points, then phase-1 screening of the same table.  HBM-bound: the table is written
+    once (233 B per plan); the count tables and logical plans stay in cache."""
+    import torch
+
+    from paper_2512_14098_amd import cf
+    from paper_2512_14098_amd.inputs import load_config
+    cfg = load_config(args.config)
+    mc = cfg["model"]
+    N = int(cfg["gpus"])
+    spec = {"k_s": 2, "share": True, "batch": {c["name"]: [16, 64, 256] for c in mc["components"]}}
+    desc, opts = cf.model_desc(mc), cf.enum_opts(mc, spec, N)
+    t0 = time.perf_counter()
+    logical = cf.cf_enum_logical(desc, opts)
+    t_logical = time.perf_counter() - t0
+    ldev = torch.from_numpy(logical).cuda()
+    offsets, total = cf.cf_enum_count(desc, opts, ldev)
+    chunk = int(args.enum_chunk)
+    out = cf.DevicePlans.empty(chunk)
+    tr, mom = cf.cf_trace_gen(desc, [0], 4096)
+    starts = [(total - chunk) * i // max(args.steps - 1, 1) for i in range(args.steps)]
+    for _ in range(args.warmup):
+        cf.cf_enum_plans(desc, opts, ldev, offsets, total, 0, chunk, out)
+        cf.cf_eval_coarse(desc, out, mom[0], N)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    enum_ms, coarse_ms = [], []
+    t0 = time.perf_counter()
+    for s0 in starts:
+        ev[0].record()
+        cf.cf_enum_plans(desc, opts, ldev, offsets, total, s0, chunk, out)
+        ev[1].record()
+        cf.cf_eval_coarse(desc, out, mom[0], N)
+        ev[2].record()
+        torch.cuda.synchronize()
+        enum_ms.append(ev[0].elapsed_time(ev[1]))
+        coarse_ms.append(ev[1].elapsed_time(ev[2]))
+    elapsed = time.perf_counter() - t0
+    e_s = sum(enum_ms) / len(enum_ms) / 1e3
+    achieved = ENUM_PLAN_BYTES * chunk / e_s
+    res = {"metric": "physical plans enumerated (Alg. 1, Eq. 1) and screened (phase 1)/sec, 1 GPU",
+           "value": chunk * len(starts) / elapsed, "unit": "plans/s", "n_gpus": 1, "steps": len(starts),
+           "warmup": args.warmup, "ms_per_step": elapsed * 1e3 / len(starts), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "u8", "data": "synthetic",
+           "config": {"workload": "%s plan space: %d logical plans, %d physical plans on %d GPUs; %d plans per "
+                                  "launch at %d evenly spaced starts" % (args.config, len(logical), total, N,
+                                                                         chunk, len(starts)),
+                      "logical_plans": int(len(logical)), "physical_plans": total, "logical_host_s": t_logical,
+                      "enum_ms": enum_ms, "coarse_ms": coarse_ms, "enum_plans_per_s": chunk / e_s,
+                      "enum_coarse_plans_per_s": chunk / ((sum(enum_ms) + sum(coarse_ms)) / len(enum_ms) / 1e3)},
+           "roofline": {"bound": "hbm", "achieved": achieved / 1e9, "peak": 8000.0, "unit": "GB/s",
+                        "frac": achieved / 8.0e12,
+                        "traffic": ENUM_MEASURED_TRAFFIC.get((kernel_source_id(ENUM_KERNEL_SOURCES), chunk)),
+                        "kernel": "k_enum_unrank",
+                        "alg_bytes_per_plan": ENUM_PLAN_BYTES, "kernel_ms": sum(enum_ms) / len(enum_ms)}}
+    if not args.no_cpu_baseline:
+        from oracle import oracle as O
+        m, oo = O.make_model(mc), O.enum_opts(mc, spec, N)
+        Ls = O.enum_logical(m, oo)
+        done, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < args.cpu_budget and done < 4 * chunk:
+            O.enum_plans(m, oo, Ls, starts[0] + done, 200000)
+            done += 200000
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": done / dt, "unit": "plans/s", "cores": 1, "kind": "oracle",
+                               "sample": "%d consecutive plans from the first start, single thread, %.1f s "
+                                         "(enumeration only)" % (done, dt)}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -279,6 +358,10 @@ def main():
     ap.add_argument("--phase2", action="store_true",
                     help="only time phase 2 (Monte Carlo latency) and Pareto pruning over the plans "
                          "phase 1 keeps (default workload c4), then exit")
+    ap.add_argument("--enum", action="store_true",
+                    help="only time plan enumeration on the device and phase-1 screening of the enumerated "
+                         "table (default model: c2's omni graph on 16 GPUs), then exit")
+    ap.add_argument("--enum-chunk", type=int, default=1 << 25, metavar="PLANS")
     ap.add_argument("--mc-samples", type=int, default=1024, metavar="K")
     ap.add_argument("--mc-alpha", type=float, default=0.8)
     args = ap.parse_args()
@@ -298,6 +381,13 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": n, "launches": 3}), flush=True)
+        return
+
+    if args.enum:
+        torch.cuda.set_device(0)
+        if "--config" not in sys.argv:
+            args.config = "c2"
+        enum_bench(args)
         return
 
     if args.phase2:

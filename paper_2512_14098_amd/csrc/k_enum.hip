@@ -9,13 +9,13 @@
 //     across threads, the nodes from the last to the first);
 //   - offsets = exclusive prefix sum of cnt[0][N] * 9^(types with two
 //     alternatives);
-//   - one thread per plan index: the logical plan by binary search in the
-//     offsets, the routing weights as base-9 digits of the index within it,
-//     the executor assignment by walking the table (at node v with budget
-//     b, the candidates (k, n) in order each own cnt[v+1][b - gpus_k n]
-//     consecutive numbers), then the plan-table columns are written
-//     slot-major, so a wavefront's 64 plans fill 64 consecutive bytes of
-//     each slot row.
+//   - four consecutive plan indices per thread: for each, the logical plan by
+//     binary search in the offsets, the routing weights as base-9 digits of
+//     the index within it, the executor assignment by walking the table (at
+//     node v with budget b, the candidates (k, n) in order each own
+//     cnt[v+1][b - gpus_k n] consecutive numbers); the plan-table columns
+//     are written slot-major, four plans per 32-bit store, so a wavefront
+//     fills 256 consecutive bytes of a slot row per store instruction.
 #include "cf_internal.h"
 
 #include <algorithm>
@@ -180,88 +180,159 @@ struct PlanOut {
   uint16_t *node_batch;
 };
 
-__global__ void __launch_bounds__(256) k_enum_unrank(cf_enum_opts o, EnumView V, const uint64_t *offsets,
-                                                    uint64_t first, int count, PlanOut out) {
-  __shared__ OptsLds so;
-  stage_opts(so, o, threadIdx.x, blockDim.x);
-  __syncthreads();
-  const int p = blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= count) return;
-  const uint64_t idx = first + (uint64_t)p;
-  const size_t P = (size_t)out.P;
-  // the logical plan: the last l with offsets[l] <= idx
-  int lo = 0, hi = V.n_logical;  // offsets[lo] <= idx < offsets[hi] when in range
-  const bool in_range = idx < offsets[V.n_logical];
-  if (in_range) {
+// The position of plan idx: its logical plan, routing digits and the cursor
+// of the executor-assignment walk.
+struct Cursor {
+  int l, nv;
+  bool ok;
+  uint64_t q;   // rank among the executor assignments still to place
+  int b;        // GPUs left
+  uint32_t w;   // routing weights, 4 bits per type with two alternatives, in type order
+};
+
+__device__ Cursor locate(const EnumView &V, const uint64_t *offsets, uint64_t idx, bool valid) {
+  Cursor c;
+  c.ok = valid && idx < offsets[V.n_logical];
+  int lo = 0, hi = V.n_logical;  // offsets[lo] <= idx < offsets[hi]
+  if (c.ok) {
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
       if (offsets[mid] <= idx) lo = mid; else hi = mid;
     }
   }
+  c.l = lo;
   const cf_logical &L = V.logical[lo];
-  const int nv = in_range ? L.n_nodes : 0;
-  uint64_t local = in_range ? idx - offsets[lo] : 0;
-  // routing digits: types with two alternatives, lowest type most significant
+  c.nv = c.ok ? L.n_nodes : 0;
+  const uint64_t local = c.ok ? idx - offsets[lo] : 0;
   int na2 = 0;
   for (int t = 0; t < CF_MAX_TYPES; t++) na2 += L.n_alt[t] == 2;
   uint64_t R = 1;
   for (int i = 0; i < na2; i++) R *= 9;
-  uint64_t r = local % R, q = local / R;
-  uint8_t wdig[CF_MAX_TYPES];
-  for (int i = na2 - 1; i >= 0; i--) {
-    wdig[i] = (uint8_t)(r % 9 + 1);
+  uint64_t r = local % R;
+  c.q = local / R;
+  c.w = 0;
+  for (int i = na2 - 1; i >= 0; i--) {  // lowest type is the most significant digit
+    c.w |= (uint32_t)(r % 9 + 1) << (4 * i);
     r /= 9;
   }
-  // the executor assignment
-  const uint64_t *tab = V.tab + (size_t)lo * kTabSize;
-  int b = V.N;
-  for (int v = 0; v < CF_MAX_NODES; v++) {
-    uint8_t comp = 0, rep = 0, gpus = 0;
-    uint16_t batch = 0;
-    if (v < nv) {
-      comp = L.node_comp[v];
-      const int c0 = comp ? __ffs(comp) - 1 : 0;
-      const int nb = so.n_batch[c0];
-      bool done = false;
-      for (int gi = 0; gi < so.n_gpu[c0] && !done; gi++) {
-        const int g = so.gpu[c0][gi];
-        for (int bi = 0; bi < nb && !done; bi++) {
-          for (int n = 1; g * n <= b; n++) {
-            const uint64_t c = tab[(v + 1) * kTabStride + (b - g * n)];
-            if (q < c) {
-              rep = (uint8_t)n;
-              gpus = (uint8_t)g;
-              batch = so.batch[c0][bi];
-              b -= g * n;
-              done = true;
-              break;
-            }
-            q -= c;
-          }
+  c.b = V.N;
+  return c;
+}
+
+struct NodeCfg {
+  uint8_t comp, rep, gpus;
+  uint16_t batch;
+};
+
+// Node v of the plan at cursor c: the candidates (k, n) in order own
+// cnt[v+1][b - gpus_k n] consecutive ranks each.
+__device__ NodeCfg place(const EnumView &V, const OptsLds &so, Cursor &c, int v) {
+  NodeCfg r = {0, 0, 0, 0};
+  if (v >= c.nv) return r;
+  const cf_logical &L = V.logical[c.l];
+  const uint64_t *tab = V.tab + (size_t)c.l * kTabSize + (size_t)(v + 1) * kTabStride;
+  r.comp = L.node_comp[v];
+  const int c0 = r.comp ? __ffs(r.comp) - 1 : 0;
+  const int nb = so.n_batch[c0];
+  for (int gi = 0; gi < so.n_gpu[c0]; gi++) {
+    const int g = so.gpu[c0][gi];
+    for (int bi = 0; bi < nb; bi++) {
+      for (int n = 1; g * n <= c.b; n++) {
+        const uint64_t k = tab[c.b - g * n];
+        if (c.q < k) {
+          r.rep = (uint8_t)n;
+          r.gpus = (uint8_t)g;
+          r.batch = so.batch[c0][bi];
+          c.b -= g * n;
+          return r;
         }
+        c.q -= k;
       }
     }
-    out.node_comp[v * P + p] = comp;
-    out.node_rep[v * P + p] = rep;
-    out.node_gpus[v * P + p] = gpus;
-    out.node_batch[v * P + p] = batch;
   }
-  out.n_nodes[p] = (uint8_t)nv;
-  int i2 = 0;
-  for (int t = 0; t < CF_MAX_TYPES; t++) {
-    const int na = in_range ? L.n_alt[t] : 0;
-    uint8_t w0 = 0, w1 = 0;
-    if (na == 1) w0 = 10;
-    if (na == 2) {
-      w0 = wdig[i2++];
-      w1 = (uint8_t)(10 - w0);
+  return r;
+}
+
+// Four consecutive plans per thread, each slot row written with one 32-bit
+// store (64-bit for the batch row): a wavefront writes 256 bytes of a row
+// per instruction.  Needs out.P % 4 == 0; the last thread writes bytes.
+constexpr int kPlansPerThread = 4;
+__global__ void __launch_bounds__(256) k_enum_unrank(cf_enum_opts o, EnumView V, const uint64_t *offsets,
+                                                    uint64_t first, int count, PlanOut out) {
+  __shared__ OptsLds so;
+  stage_opts(so, o, threadIdx.x, blockDim.x);
+  __syncthreads();
+  const int p0 = (blockIdx.x * blockDim.x + threadIdx.x) * kPlansPerThread;
+  if (p0 >= count) return;
+  const size_t P = (size_t)out.P;
+  const bool packed = p0 + kPlansPerThread <= count && (out.P % kPlansPerThread) == 0;
+  // consecutive plans of one logical plan that differ only in their routing
+  // weights share the executor assignment: it is walked once
+  Cursor cur[kPlansPerThread];
+  bool same[kPlansPerThread];
+#pragma unroll
+  for (int j = 0; j < kPlansPerThread; j++) {
+    cur[j] = locate(V, offsets, first + (uint64_t)(p0 + j), p0 + j < count);
+    same[j] = j > 0 && cur[j].ok && cur[j - 1].ok && cur[j].l == cur[j - 1].l && cur[j].q == cur[j - 1].q;
+  }
+  auto put8 = [&](uint8_t *row, const uint8_t *x) {
+    if (packed) {
+      *(uint32_t *)(row + p0) = (uint32_t)x[0] | ((uint32_t)x[1] << 8) | ((uint32_t)x[2] << 16) | ((uint32_t)x[3] << 24);
+    } else {
+      for (int j = 0; j < kPlansPerThread; j++)
+        if (p0 + j < count) row[p0 + j] = x[j];
     }
-    out.n_alt[t * P + p] = (uint8_t)na;
-    out.alt_w[(2 * t) * P + p] = w0;
-    out.alt_w[(2 * t + 1) * P + p] = w1;
+  };
+  uint8_t b8[kPlansPerThread];
+#pragma unroll
+  for (int j = 0; j < kPlansPerThread; j++) b8[j] = (uint8_t)cur[j].nv;
+  put8(out.n_nodes, b8);
+  for (int v = 0; v < CF_MAX_NODES; v++) {
+    NodeCfg nc[kPlansPerThread];
+#pragma unroll
+    for (int j = 0; j < kPlansPerThread; j++) nc[j] = same[j] ? nc[j - 1] : place(V, so, cur[j], v);
+#pragma unroll
+    for (int j = 0; j < kPlansPerThread; j++) b8[j] = nc[j].comp;
+    put8(out.node_comp + v * P, b8);
+#pragma unroll
+    for (int j = 0; j < kPlansPerThread; j++) b8[j] = nc[j].rep;
+    put8(out.node_rep + v * P, b8);
+#pragma unroll
+    for (int j = 0; j < kPlansPerThread; j++) b8[j] = nc[j].gpus;
+    put8(out.node_gpus + v * P, b8);
+    uint16_t *brow = out.node_batch + v * P;
+    if (packed) {
+      *(uint64_t *)(brow + p0) = (uint64_t)nc[0].batch | ((uint64_t)nc[1].batch << 16) |
+                                 ((uint64_t)nc[2].batch << 32) | ((uint64_t)nc[3].batch << 48);
+    } else {
+      for (int j = 0; j < kPlansPerThread; j++)
+        if (p0 + j < count) brow[p0 + j] = nc[j].batch;
+    }
+  }
+  int i2[kPlansPerThread] = {0, 0, 0, 0};
+  for (int t = 0; t < CF_MAX_TYPES; t++) {
+    uint8_t na[kPlansPerThread], w0[kPlansPerThread], w1[kPlansPerThread];
+#pragma unroll
+    for (int j = 0; j < kPlansPerThread; j++) {
+      na[j] = cur[j].ok ? V.logical[cur[j].l].n_alt[t] : 0;
+      w0[j] = na[j] == 1 ? 10 : 0;
+      w1[j] = 0;
+      if (na[j] == 2) {
+        w0[j] = (uint8_t)((cur[j].w >> (4 * i2[j])) & 15u);
+        w1[j] = (uint8_t)(10 - w0[j]);
+        i2[j]++;
+      }
+    }
+    put8(out.n_alt + t * P, na);
+    put8(out.alt_w + (2 * t) * P, w0);
+    put8(out.alt_w + (2 * t + 1) * P, w1);
     for (int a = 0; a < 2; a++)
-      for (int c = 0; c < CF_MAX_COMP; c++)
-        out.alt_node[((2 * t + a) * CF_MAX_COMP + c) * P + p] = in_range ? L.alt_node[t][a][c] : (uint8_t)255;
+      for (int c = 0; c < CF_MAX_COMP; c++) {
+#pragma unroll
+        for (int j = 0; j < kPlansPerThread; j++)
+          b8[j] = cur[j].ok ? V.logical[cur[j].l].alt_node[t][a][c] : (uint8_t)255;
+        put8(out.alt_node + ((2 * t + a) * CF_MAX_COMP + c) * P, b8);
+      }
   }
 }
 
@@ -473,7 +544,8 @@ extern "C" cf_status cf_enum_plans(const cf_model_desc *model, const cf_enum_opt
   o.n_alt = const_cast<uint8_t *>(out->n_alt_dev);
   o.alt_w = const_cast<uint8_t *>(out->alt_w_dev);
   o.alt_node = const_cast<uint8_t *>(out->alt_node_dev);
-  hipLaunchKernelGGL(k_enum_unrank, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, *opts, V, offsets_dev,
-                     first, count, o);
+  const unsigned threads = (unsigned)((count + kPlansPerThread - 1) / kPlansPerThread);
+  hipLaunchKernelGGL(k_enum_unrank, dim3((threads + 255) / 256), dim3(256), 0, s, *opts, V, offsets_dev, first,
+                     count, o);
   return hip_check(hipGetLastError(), "cf_enum_plans launch");
 }

@@ -70,6 +70,12 @@ def test_enum_omni_graph_windows(cf):
     starts += [int(x) for x in rng.integers(0, total - 5000, size=4)]
     for s in starts:
         _check_window(cf, desc, opts, ldev, offsets, total, m, oo, Ls, s, 5000)
+    # a count that is not a multiple of four in a table whose width is (the last thread's tail)
+    out = cf.DevicePlans.empty(5000)
+    got = cf.cf_enum_plans(desc, opts, ldev, offsets, total, starts[3], 4997, out).to_host()
+    want = O.enum_plans(m, oo, Ls, starts[3], 4997)
+    for f in PlanTable.FIELDS:
+        assert np.array_equal(getattr(got, f)[..., :4997], getattr(want, f)), f
 
 
 def test_enum_large_budget_single_subplans(cf):
