@@ -136,6 +136,21 @@ int cfo_eval_mc(const cfo_model *m, const cfo_plans *pl, const int32_t *ids, int
                 int32_t seed_idx, int32_t n_sample, uint32_t *met, uint32_t *cnt, double *gt,
                 double *lat);
 
+/* Latency histogram over a target table targets[T][n_bins][4] (bounds on
+ * TTFT, TPOT, E2E, MEDIA): hist[T][n_bins + 1], request r of type type[r]
+ * in the first bin whose bounds its latencies lat[r][4] meet, n_bins if
+ * none. */
+int cfo_latency_hist(const double *lat, const uint8_t *type, int32_t n, int32_t T, int32_t n_bins,
+                     const double *targets, uint32_t *hist);
+
+/* Phase 2 with the CDF of the accumulated latencies over a target table
+ * (Alg. 2: F_{t,d}): cfo_eval_mc's outputs plus hist [n][T][n_bins + 1] and
+ * curve [n][n_bins][T] = ((alpha R_d) pi_t) (requests in bins 0..b / cnt_t). */
+int cfo_mc_curve(const cfo_model *m, const cfo_plans *pl, const int32_t *ids, int32_t n, const double *rd,
+                 const uint64_t *moments, double alpha, const cfo_trace *tr, int32_t seed_idx, int32_t n_sample,
+                 int32_t n_bins, const double *targets, uint32_t *met, uint32_t *cnt, double *gt, uint32_t *hist,
+                 double *curve);
+
 /* Pareto pruning: keep[i] = 0 iff some other vector of g[n][T] is >= in
  * every component and > in one. */
 int cfo_pareto(const double *g, int32_t n, int32_t T, uint8_t *keep);

@@ -203,3 +203,59 @@ int cfo_pareto(const double *g, int32_t n, int32_t T, uint8_t *keep) {
   }
   return 0;
 }
+
+/* The bin of one request: the first bin whose four bounds its latencies
+ * meet, by a scan from bin 0 (n_bins if none). */
+static int first_bin(const double *targets, int n_bins, int t, const double *lat) {
+  for (int b = 0; b < n_bins; b++) {
+    const double *g = targets + ((size_t)t * n_bins + b) * 4;
+    if (lat[0] <= g[0] && lat[1] <= g[1] && lat[2] <= g[2] && lat[3] <= g[3]) return b;
+  }
+  return n_bins;
+}
+
+int cfo_latency_hist(const double *lat, const uint8_t *type, int32_t n, int32_t T, int32_t n_bins,
+                     const double *targets, uint32_t *hist) {
+  for (int q = 0; q < T * (n_bins + 1); q++) hist[q] = 0;
+  for (int r = 0; r < n; r++) {
+    const int t = type[r];
+    if (t >= T) continue;
+    hist[t * (n_bins + 1) + first_bin(targets, n_bins, t, lat + (size_t)r * 4)]++;
+  }
+  return 0;
+}
+
+int cfo_mc_curve(const cfo_model *m, const cfo_plans *pl, const int32_t *ids, int32_t n, const double *rd,
+                 const uint64_t *moments, double alpha, const cfo_trace *tr, int32_t seed_idx, int32_t n_sample,
+                 int32_t n_bins, const double *targets, uint32_t *met, uint32_t *cnt, double *gt, uint32_t *hist,
+                 double *curve) {
+  const int T = m->n_types;
+  double *lat = (double *)malloc(sizeof(double) * 4 * (size_t)(n_sample > 0 ? n_sample : 1));
+  if (!lat) return -1;
+  uint64_t wsum_i = 0;
+  for (int t = 0; t < T; t++) wsum_i += m->weight[t];
+  const double wsum = (double)wsum_i;
+  for (int i = 0; i < n; i++) {
+    cfo_eval_mc(m, pl, ids + i, 1, rd, moments, alpha, tr, seed_idx, n_sample, met + (size_t)i * T,
+                cnt + (size_t)i * T, gt + (size_t)i * T, lat);
+    uint32_t *h = hist + (size_t)i * T * (n_bins + 1);
+    const int p = ids[i];
+    const int valid = p >= 0 && p < pl->P && cfo_plan_valid(m, pl, p);
+    if (valid)
+      cfo_latency_hist(lat, tr->type + (size_t)seed_idx * (size_t)tr->n_req, n_sample, T, n_bins, targets, h);
+    else
+      for (int q = 0; q < T * (n_bins + 1); q++) h[q] = 0;
+    /* F_t at bin b: the requests in bins 0..b over the type's count */
+    for (int b = 0; b < n_bins; b++)
+      for (int t = 0; t < T; t++) {
+        uint32_t below = 0;
+        for (int k = 0; k <= b; k++) below += h[t * (n_bins + 1) + k];
+        const uint32_t ct = cnt[(size_t)i * T + t];
+        const double pi = (double)m->weight[t] / wsum;
+        curve[((size_t)i * n_bins + b) * T + t] =
+            (valid && ct > 0) ? ((alpha * rd[p]) * pi) * ((double)below / (double)ct) : 0.0;
+      }
+  }
+  free(lat);
+  return 0;
+}

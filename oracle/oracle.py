@@ -100,6 +100,8 @@ def lib():
         L.cfo_sim_triple.argtypes = [vp, vp, i32, dbl, vp, i32, vp, vp, vp, vp, vp, vp]
         L.cfo_goodput_reduce.argtypes = [vp, vp, i32, i32, i32, i32, vp, C.c_uint32, C.c_uint32,
                                          i32, vp, vp, vp]
+        L.cfo_latency_hist.argtypes = [vp, vp, i32, i32, i32, vp, vp]
+        L.cfo_mc_curve.argtypes = [vp, vp, vp, i32, vp, vp, dbl, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp]
         L.cfo_enum_logical.argtypes = [vp, vp, vp, i32, vp]
         L.cfo_enum_count.argtypes = [vp, vp, vp]
         L.cfo_enum_count.restype = C.c_uint64
@@ -437,3 +439,45 @@ def enum_plans(model, opts, logical, first, count):
     if rc != 0:
         raise RuntimeError("cfo_enum_plans failed (%d)" % rc)
     return tab
+
+
+# ---------------------------------------------------------------- latency CDFs over target tables
+def latency_hist(lat, types, T, targets):
+    """hist[T][n_bins + 1] of requests by the first target bin they meet (targets [T][n_bins][4])."""
+    targets = np.ascontiguousarray(targets, np.float64)
+    nb = targets.shape[1]
+    lat = np.ascontiguousarray(lat, np.float64)
+    types = np.ascontiguousarray(types, np.uint8)
+    h = np.zeros((T, nb + 1), np.uint32)
+    lib().cfo_latency_hist(_ptr(lat), _ptr(types), len(types), int(T), int(nb), _ptr(targets), _ptr(h))
+    return h
+
+
+def mc_curve(model, tab, plan_ids, rd, moments0, alpha, tr, seed_idx, n_sample, targets):
+    """Phase 2 with its latency CDF over a target table: (met, cnt, gt, hist, curve)."""
+    ids = np.ascontiguousarray(plan_ids, np.int32)
+    n, T = len(ids), model.n_types
+    targets = np.ascontiguousarray(targets, np.float64)
+    nb = targets.shape[1]
+    met = np.zeros((n, T), np.uint32)
+    cnt = np.zeros((n, T), np.uint32)
+    gt = np.zeros((n, T), np.float64)
+    hist = np.zeros((n, T, nb + 1), np.uint32)
+    curve = np.zeros((n, nb, T), np.float64)
+    pst, tst = plans_struct(tab), trace_struct(tr)
+    lib().cfo_mc_curve(C.byref(model), C.byref(pst), _ptr(ids), n, _ptr(np.ascontiguousarray(rd, np.float64)),
+                       _ptr(np.ascontiguousarray(moments0, np.uint64)), float(alpha), C.byref(tst), int(seed_idx),
+                       int(n_sample), int(nb), _ptr(targets), _ptr(met), _ptr(cnt), _ptr(gt), _ptr(hist),
+                       _ptr(curve))
+    return met, cnt, gt, hist, curve
+
+
+def scaled_targets(model, scales):
+    """A target table: the type's own bounds times each scale (inf stays inf)."""
+    T = model.n_types
+    out = np.zeros((T, len(scales), 4), np.float64)
+    for t in range(T):
+        for b, sc in enumerate(scales):
+            for j in range(4):
+                out[t, b, j] = model.slo[t][j] * float(sc)
+    return out
