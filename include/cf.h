@@ -161,6 +161,15 @@ typedef struct cf_fine_out {
   double *lat_dev;        /* optional [n_lat][n_req][4]: TTFT, TPOT, E2E, MEDIA; NULL = off */
   const int32_t *lat_triples_dev; /* [n_lat] linear triple ids ((i*K)+k)*S+s to dump */
   int32_t n_lat;
+  /* Optional latency histograms (goodput against a range of latency
+   * targets, Sec. 6.3 Fig. 8): with n_bins > 0, a completed request of type
+   * t counts in bin b = the first bin whose four bounds
+   * hist_targets_host[t][b][0..3] (TTFT, TPOT, E2E, MEDIA, inclusive) it
+   * meets, or n_bins if none; the bounds must not decrease with b (1 <=
+   * n_bins <= 64).  hist_dev: [n_plans][K][S][T][n_bins + 1] (device). */
+  uint32_t *hist_dev;
+  const double *hist_targets_host;
+  int32_t n_bins;
 } cf_fine_out;
 
 /* Error text of the calling thread's last failed call (empty if none);
@@ -232,6 +241,21 @@ cf_status cf_eval_mc(const cf_model_desc *model, const cf_plan_table *plans, con
                      int32_t n_plans, const double *rd_dev, const uint64_t *moments_dev, double alpha,
                      const cf_trace *trace, int32_t seed_idx, int32_t n_sample, uint32_t *met_dev,
                      uint32_t *cnt_dev, double *goodput_t_dev, double *lat_dev, void *stream);
+
+/* Phase 2 with its latency CDFs (Alg. 2: F_{t,d} is the CDF of the
+ * accumulated latencies; G_{t,d} = alpha R_d pi_t F_{t,d}(L_t)) evaluated
+ * over a table of targets: everything cf_eval_mc computes, plus hist_dev
+ * [n_plans][T][n_bins + 1] (a sampled request of type t in the first bin b
+ * whose bounds hist_targets_host[t][b][0..3] it meets, n_bins if none; the
+ * bounds must not decrease with b; 1 <= n_bins <= 64) and curve_dev
+ * [n_plans][n_bins][T] = ((alpha R_d) pi_t) (H_t(b) / cnt_t), H_t(b) the
+ * requests in bins 0..b (0 if cnt_t = 0 or the plan is invalid).
+ * Errors: those of cf_eval_mc, CF_EINVAL for the target table. */
+cf_status cf_eval_mc_curve(const cf_model_desc *model, const cf_plan_table *plans, const int32_t *plan_ids_dev,
+                           int32_t n_plans, const double *rd_dev, const uint64_t *moments_dev, double alpha,
+                           const cf_trace *trace, int32_t seed_idx, int32_t n_sample, int32_t n_bins,
+                           const double *hist_targets_host, uint32_t *met_dev, uint32_t *cnt_dev,
+                           double *goodput_t_dev, uint32_t *hist_dev, double *curve_dev, void *stream);
 
 /* Pareto pruning (Alg. 2, after phases 2 and 3): keep_dev[i] = 0 iff some
  * other row of goodput_t_dev [n][T] (device) is >= in every component and >
@@ -327,6 +351,17 @@ cf_status cf_goodput_reduce(const uint32_t *met_dev, const uint32_t *cnt_dev, in
                             uint32_t theta_num, uint32_t theta_den, int32_t n_req,
                             int32_t *kstar_dev, double *goodput_t_dev, double *goodput_dev,
                             void *stream);
+
+/* Goodput against a range of latency targets (Sec. 6.3, per-type goodput
+ * vs. latency target): for every plan and bin b, cf_goodput_reduce's
+ * computation with M_t = the requests in bins 0..b of hist_dev (a
+ * cf_fine_out histogram [n_plans][K][S][T][n_bins + 1]).  Outputs:
+ * kstar_dev[n_plans][n_bins], goodput_t_dev[n_plans][n_bins][T],
+ * goodput_dev[n_plans][n_bins].  Limits: K <= 64, 1 <= n_bins <= 64. */
+cf_status cf_goodput_curve(const uint32_t *hist_dev, const uint32_t *cnt_dev, int32_t n_plans, int32_t K,
+                           int32_t S, int32_t T, int32_t n_bins, const double *rates_dev, uint32_t theta_num,
+                           uint32_t theta_den, int32_t n_req, int32_t *kstar_dev, double *goodput_t_dev,
+                           double *goodput_dev, void *stream);
 
 /* Selection (Alg. 2, last step): index of the largest goodput, ties to the
  * lowest index, written to best_dev[0]. */

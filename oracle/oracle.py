@@ -352,8 +352,10 @@ def goodput_reduce(met, cnt, rates, theta, n_req):
     kstar = np.zeros(n_plans, np.int32)
     gt = np.zeros((n_plans, T), np.float64)
     g = np.zeros(n_plans, np.float64)
-    lib().cfo_goodput_reduce(_ptr(np.ascontiguousarray(met)), _ptr(np.ascontiguousarray(cnt)),
-                             n_plans, K, S, T, _ptr(np.ascontiguousarray(rates)), int(theta[0]),
+    if np.asarray(met).max(initial=0) > 0xFFFFFFFF or np.asarray(cnt).max(initial=0) > 0xFFFFFFFF:
+        raise ValueError("counts above 32 bits")
+    lib().cfo_goodput_reduce(_ptr(np.ascontiguousarray(met, np.uint32)), _ptr(np.ascontiguousarray(cnt, np.uint32)),
+                             n_plans, K, S, T, _ptr(np.ascontiguousarray(rates, np.float64)), int(theta[0]),
                              int(theta[1]), int(n_req), _ptr(kstar), _ptr(gt), _ptr(g))
     return kstar, gt, g
 

@@ -75,7 +75,8 @@ LOGICAL_BYTES = 1 + 16 + 8 + 8 * 2 * 8  # sizeof(cf_logical)
 class cf_fine_out(C.Structure):
     _fields_ = [("met_dev", C.c_void_p), ("cnt_dev", C.c_void_p), ("events_dev", C.c_void_p),
                 ("status_dev", C.c_void_p), ("lat_dev", C.c_void_p), ("lat_triples_dev", C.c_void_p),
-                ("n_lat", C.c_int32)]
+                ("n_lat", C.c_int32), ("hist_dev", C.c_void_p), ("hist_targets_host", C.c_void_p),
+                ("n_bins", C.c_int32)]
 
 
 def _load():
@@ -95,6 +96,9 @@ def _load():
         "cf_goodput_reduce": ([vp, vp, i32, i32, i32, i32, vp, u32, u32, i32, vp, vp, vp, vp], i32),
         "cf_eval_mc": ([vp, vp, vp, i32, vp, vp, dbl, vp, i32, i32, vp, vp, vp, vp, vp], i32),
         "cf_pareto": ([vp, i32, i32, vp, vp, vp, i32, vp], i32),
+        "cf_eval_mc_curve": ([vp, vp, vp, i32, vp, vp, dbl, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp], i32),
+        "cf_goodput_curve": ([vp, vp, i32, i32, i32, i32, i32, vp, C.c_uint32, C.c_uint32, i32, vp, vp, vp, vp],
+                             i32),
         "cf_enum_logical": ([vp, vp, vp, i32, vp], i32),
         "cf_enum_count": ([vp, vp, vp, i32, vp, vp, vp], i32),
         "cf_enum_plans": ([vp, vp, vp, i32, vp, C.c_uint64, C.c_uint64, i32, vp, vp], i32),
@@ -112,7 +116,7 @@ def _load():
 
 _lib = _load()
 EXPORTED = ("cf_last_error", "cf_status_str", "cf_version", "cf_trace_gen", "cf_eval_coarse",
-            "cf_select_topk", "cf_rate_grid", "cf_eval_fine", "cf_eval_mc", "cf_pareto",
+            "cf_select_topk", "cf_rate_grid", "cf_eval_fine", "cf_eval_mc", "cf_eval_mc_curve", "cf_goodput_curve", "cf_pareto",
             "cf_enum_logical", "cf_enum_count", "cf_enum_plans",
             "cf_goodput_reduce", "cf_select_best", "cf_math_eval", "cf_philox_eval", "cf_release_scratch")
 
@@ -320,7 +324,16 @@ def cf_rate_grid(rd, ids, K, alpha_max=1.0):
     return rates
 
 
-def cf_eval_fine(desc, plans, plan_ids, rates, trace, lat_triples=None):
+def _targets(targets, T):
+    tg = np.ascontiguousarray(targets, np.float64)
+    if tg.ndim != 3 or tg.shape[0] != T or tg.shape[2] != 4:
+        raise CfError("targets must be [T][n_bins][4]")
+    return tg
+
+
+def cf_eval_fine(desc, plans, plan_ids, rates, trace, lat_triples=None, targets=None):
+    """Phase 3 of every (plan, rate, seed); with targets ([T][n_bins][4], bounds not
+    decreasing with the bin) also the latency histograms hist [n_plans][K][S][T][n_bins+1]."""
     n_plans, K = rates.shape
     S, T, dev = trace.n_seeds, desc.n_types, rates.device
     met = torch.empty((n_plans, K, S, T), dtype=torch.int32, device=dev)
@@ -335,10 +348,15 @@ def cf_eval_fine(desc, plans, plan_ids, rates, trace, lat_triples=None):
         lt = torch.as_tensor(np.asarray(lat_triples, np.int32), device=dev)
         lat = torch.zeros((len(lat_triples), trace.n_req, 4), dtype=torch.float64, device=dev)
         out.lat_dev, out.lat_triples_dev, out.n_lat = lat.data_ptr(), lt.data_ptr(), len(lat_triples)
+    hist = None
+    if targets is not None:
+        tg = _targets(targets, T)
+        hist = torch.empty((n_plans, K, S, T, tg.shape[1] + 1), dtype=torch.int32, device=dev)
+        out.hist_dev, out.hist_targets_host, out.n_bins = hist.data_ptr(), tg.ctypes.data, tg.shape[1]
     _check(_lib.cf_eval_fine(C.byref(desc), C.byref(plans.c), _p(plan_ids.contiguous()), int(n_plans),
                              _p(rates.contiguous()), int(K), C.byref(trace.c), 0, C.byref(out),
                              _stream()), "cf_eval_fine")
-    return dict(met=met, cnt=cnt, events=events, status=status, lat=lat)
+    return dict(met=met, cnt=cnt, events=events, status=status, lat=lat, hist=hist)
 
 
 def cf_eval_mc(desc, plans, plan_ids, rd, moments_seed, alpha, trace, seed_idx, n_sample,
@@ -353,6 +371,39 @@ def cf_eval_mc(desc, plans, plan_ids, rd, moments_seed, alpha, trace, seed_idx, 
                            _p(moments_seed.contiguous()), float(alpha), C.byref(trace.c), int(seed_idx),
                            int(n_sample), _p(met), _p(cnt), _p(gt), _p(lat), _stream()), "cf_eval_mc")
     return dict(met=met, cnt=cnt, goodput_t=gt, lat=lat)
+
+
+def cf_eval_mc_curve(desc, plans, plan_ids, rd, moments_seed, alpha, trace, seed_idx, n_sample, targets):
+    """Phase 2 with its latency CDF over a target table ([T][n_bins][4]): dict(met, cnt,
+    goodput_t, hist [n][T][n_bins+1], curve [n][n_bins][T])."""
+    n = int(plan_ids.numel())
+    T, dev = desc.n_types, rd.device
+    tg = _targets(targets, T)
+    nb = tg.shape[1]
+    met = torch.empty((n, T), dtype=torch.int32, device=dev)
+    cnt = torch.empty((n, T), dtype=torch.int32, device=dev)
+    gt = torch.empty((n, T), dtype=torch.float64, device=dev)
+    hist = torch.empty((n, T, nb + 1), dtype=torch.int32, device=dev)
+    curve = torch.empty((n, nb, T), dtype=torch.float64, device=dev)
+    _check(_lib.cf_eval_mc_curve(C.byref(desc), C.byref(plans.c), _p(plan_ids.contiguous()), n,
+                                 _p(rd.contiguous()), _p(moments_seed.contiguous()), float(alpha), C.byref(trace.c),
+                                 int(seed_idx), int(n_sample), int(nb), tg.ctypes.data_as(C.c_void_p), _p(met),
+                                 _p(cnt), _p(gt), _p(hist), _p(curve), _stream()), "cf_eval_mc_curve")
+    return dict(met=met, cnt=cnt, goodput_t=gt, hist=hist, curve=curve)
+
+
+def cf_goodput_curve(hist, cnt, rates, theta, n_req):
+    """Goodput against every target bin of a phase-3 histogram: kstar [n][nb],
+    goodput_t [n][nb][T], goodput [n][nb]."""
+    n_plans, K, S, T, hw = hist.shape
+    nb, dev = hw - 1, hist.device
+    kstar = torch.empty((n_plans, nb), dtype=torch.int32, device=dev)
+    gt = torch.empty((n_plans, nb, T), dtype=torch.float64, device=dev)
+    g = torch.empty((n_plans, nb), dtype=torch.float64, device=dev)
+    _check(_lib.cf_goodput_curve(_p(hist.contiguous()), _p(cnt.contiguous()), n_plans, K, S, T, nb,
+                                 _p(rates.contiguous()), int(theta[0]), int(theta[1]), int(n_req), _p(kstar),
+                                 _p(gt), _p(g), _stream()), "cf_goodput_curve")
+    return kstar, gt, g
 
 
 def cf_pareto(goodput_t, plan_ids=None, flags=None):

@@ -210,6 +210,28 @@ void *scratch_get(int slot, size_t bytes, cf_status *st) {
 }
 }  // namespace cf
 
+namespace cf {
+cf_status load_targets(int T, int n_bins, const double *host, const double **dev, hipStream_t s) {
+  if (n_bins < 1 || n_bins > 64) return set_error(CF_EINVAL, "n_bins must be in 1..64");
+  if (!host) return set_error(CF_EINVAL, "NULL target table");
+  for (int t = 0; t < T; t++)
+    for (int b = 0; b < n_bins; b++)
+      for (int j = 0; j < 4; j++) {
+        const double v = host[((size_t)t * n_bins + b) * 4 + j];
+        if (v != v) return set_error(CF_EINVAL, "NaN target [%d][%d][%d]", t, b, j);
+        if (b > 0 && v < host[((size_t)t * n_bins + b - 1) * 4 + j])
+          return set_error(CF_EINVAL, "targets decrease at [%d][%d][%d]", t, b, j);
+      }
+  cf_status st = CF_OK;
+  const size_t bytes = sizeof(double) * (size_t)T * n_bins * 4;
+  void *d = scratch_get(SCR_TARGETS, bytes, &st);
+  if (!d) return st;
+  st = hip_check(hipMemcpyAsync(d, host, bytes, hipMemcpyHostToDevice, s), "target table copy");
+  *dev = (const double *)d;
+  return st;
+}
+}  // namespace cf
+
 extern "C" cf_status cf_release_scratch(void) {
   int cur = 0;
   (void)hipGetDevice(&cur);

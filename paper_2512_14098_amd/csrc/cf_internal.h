@@ -113,6 +113,23 @@ __device__ __forceinline__ double dev_exp(double x) {
 namespace cf {
 // Per-device scratch owned by the library, grown on demand, one region per
 // purpose.  Calls that use the same region must not overlap on one device.
-enum ScratchSlot { SCR_TRACE = 0, SCR_SELECT = 1, SCR_FINE = 2, SCR_MC = 3, SCR_PARETO = 4, SCR_ENUM = 5, SCR_NSLOTS = 6 };
+// A latency-target table [T][n_bins][4] (TTFT, TPOT, E2E, MEDIA bounds, not
+// decreasing with the bin) checked on the host and copied to device scratch.
+cf_status load_targets(int T, int n_bins, const double *host, const double **dev, hipStream_t s);
+
+// The first bin b whose four bounds the latencies meet (n_bins if none), by
+// bisection: the bounds do not decrease with b, so meeting them is monotone.
+__device__ __forceinline__ int target_bin(const double *tg, int n_bins, int t, double l0, double l1, double l2,
+                                          double l3) {
+  int lo = 0, hi = n_bins;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    const double *b = tg + ((size_t)t * n_bins + mid) * 4;
+    if (l0 <= b[0] && l1 <= b[1] && l2 <= b[2] && l3 <= b[3]) hi = mid; else lo = mid + 1;
+  }
+  return lo;
+}
+
+enum ScratchSlot { SCR_TRACE = 0, SCR_SELECT = 1, SCR_FINE = 2, SCR_MC = 3, SCR_PARETO = 4, SCR_ENUM = 5, SCR_TARGETS = 6, SCR_NSLOTS = 7 };
 void *scratch_get(int slot, size_t bytes, cf_status *st);
 }  // namespace cf

@@ -125,6 +125,9 @@ struct FineArgs {
   double *lat;
   const int32_t *lat_triples;
   int n_lat;
+  uint32_t *hist;      // optional [n_plans][K][S][T][nb + 1] latency histograms
+  const double *tg;    // their target table [T][nb][4]
+  int nb;
   char *slab;
   Layout L;
   unsigned int *ticket;
@@ -280,6 +283,7 @@ struct Sim {
   uint64_t events, dirty, ta_exec_mask;
   uint32_t status, dl_head, dl_tail;
   int pool_top, pool_fresh, n_done, nx, lat_slot;
+  uint32_t *hrow;      // this triple's histogram rows, or null
   bool remote_gate;
   // k_fine<true>
   double *wake;        // per executor with a gated stage: next visibility time of a blocked request
@@ -830,6 +834,7 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
     const uint64_t dbal = __ballot(done);
     if (dbal) {
       bool ok = false;
+      int hbin = 0;
       if (done) {
         const double a = arrival_time(S, r);
         double ttft = 0.0, tpot = 0.0, media = 0.0;
@@ -843,6 +848,7 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
         const double e2e = now - a;
         if (ml.gen_out[t]) media = S.tim[r].tmedia - a;
         ok = ttft <= ml.slo[t][0] && tpot <= ml.slo[t][1] && e2e <= ml.slo[t][2] && media <= ml.slo[t][3];
+        if (S.hrow) hbin = target_bin(S.A->tg, S.A->nb, t, ttft, tpot, e2e, media);
         if (S.lat_slot >= 0) {
           double *Lp = S.A->lat + ((size_t)S.lat_slot * S.A->n + r) * 4;
           Lp[0] = ttft;
@@ -854,6 +860,7 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
       if (done) {
         atomicAdd(&S.sh->cnt[t], 1u);
         if (ok) atomicAdd(&S.sh->met[t], 1u);
+        if (S.hrow) atomicAdd(S.hrow + t * (S.A->nb + 1) + hbin, 1u);
       }
       S.events += (uint64_t)__popcll(dbal);
       S.n_done += __popcll(dbal);
@@ -1755,6 +1762,7 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
     S.n_done = 0;
     S.now = 0.0;
     S.lat_slot = -1;
+    S.hrow = A.hist ? A.hist + oidx * (size_t)m.nt * (size_t)(A.nb + 1) : nullptr;
     for (int j = 0; j < A.n_lat; j++)
       if (A.lat_triples[j] == (int32_t)oidx) S.lat_slot = j;
     if (lane < CF_MAX_TYPES) {
@@ -1865,6 +1873,10 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
 }
 
 __global__ void k_fine_reset(unsigned int *ticket) { *ticket = 0u; }
+__global__ void k_fine_zero(uint32_t *p, size_t n) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
 __global__ void k_fine_reset3(unsigned int *v) {
   v[0] = 0u;
   v[1] = 0u;
@@ -1985,6 +1997,9 @@ extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_tabl
   a.lat = out->lat_dev;
   a.lat_triples = out->lat_triples_dev;
   a.n_lat = out->lat_dev ? out->n_lat : 0;
+  a.hist = nullptr;
+  a.tg = nullptr;
+  a.nb = 0;
   a.L = make_layout(a.m, trace->n_req);
   a.total = (unsigned int)total;
   long long waves = 8192;
@@ -2028,6 +2043,18 @@ extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_tabl
                                     : kSiBytes * (size_t)a.nsi_cap;
   st = hip_check(hipMemcpyAsync(args_dev, &a, sizeof a, hipMemcpyHostToDevice, s), "copy fine args");
   if (st != CF_OK) return st;
+  if (out->n_bins > 0) {
+    // optional latency histograms: target table to the device, counters cleared by a kernel
+    if (!out->hist_dev) return set_error(CF_EINVAL, "n_bins > 0 without hist_dev");
+    st = load_targets(a.m.nt, out->n_bins, out->hist_targets_host, &a.tg, s);
+    if (st != CF_OK) return st;
+    a.hist = out->hist_dev;
+    a.nb = out->n_bins;
+    const size_t nh = total * (size_t)a.m.nt * (size_t)(a.nb + 1);
+    hipLaunchKernelGGL(k_fine_zero, dim3((unsigned)((nh + 255) / 256)), dim3(256), 0, s, a.hist, nh);
+    st = hip_check(hipMemcpyAsync(args_dev, &a, sizeof a, hipMemcpyHostToDevice, s), "copy fine args");
+    if (st != CF_OK) return st;
+  }
   hipLaunchKernelGGL(k_fine_reset, dim3(1), dim3(1), 0, s, a.ticket);
   if (a.m.gated_mask)
     hipLaunchKernelGGL(k_fine<true>, dim3((unsigned)waves), dim3(64), lds, s, (const FineArgs *)args_dev);

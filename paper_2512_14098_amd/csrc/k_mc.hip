@@ -45,6 +45,11 @@ struct McView {
   size_t toff;  // first sampled request: seed_idx * n_req
   int n_sample;
   const uint32_t *order;  // the sampled requests in walking order (a permutation of 0..n_sample-1)
+  // optional latency CDF over a target table [T][nb][4]: hist [n_plans][T][nb+1], curve [n_plans][nb][T]
+  const double *tg;
+  int nb;
+  uint32_t *hist;
+  double *curve;
   uint32_t *met, *cnt;
   double *gt, *lat;
 };
@@ -141,6 +146,7 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
   __shared__ uint32_t tinfo_s[CF_MAX_TYPES];  // path | outm << 8 | pfo << 16 | gen_out << 24
   __shared__ int8_t ta_s[CF_MAX_TYPES], th_s[CF_MAX_TYPES];
   __shared__ double slo_s[CF_MAX_TYPES][4];
+  __shared__ uint32_t hist_s[CF_MAX_TYPES * 65];
   const int i = blockIdx.x, lane = threadIdx.x;
   const int p = V.ids[i];
   const size_t P = (size_t)V.P;
@@ -160,6 +166,9 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
     th_s[lane] = m.th_c[lane];
   }
   if (lane < CF_MAX_TYPES * 4) (&slo_s[0][0])[lane] = (&m.slo[0][0])[lane];
+  const int hw = V.nb + 1;  // histogram row width
+  if (V.hist)
+    for (int q = lane; q < m.nt * hw; q += 64) hist_s[q] = 0;
   // per-type means of X and of the output length (phase 1's work per request)
   if (lane < m.nt * m.nc) {
     const int t = lane / m.nc, c = lane % m.nc;
@@ -369,6 +378,7 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
       const bool ok = ttft <= slo_s[t][0] && tpot <= slo_s[t][1] && completion <= slo_s[t][2] && md <= slo_s[t][3];
       atomicAdd(&cnt_s[t], 1u);
       if (ok) atomicAdd(&met_s[t], 1u);
+      if (V.hist) atomicAdd(&hist_s[t * hw + target_bin(V.tg, V.nb, t, ttft, tpot, completion, md)], 1u);
       if (V.lat) {
         double *L = V.lat + ((size_t)i * V.n_sample + r) * 4;
         L[0] = ttft;
@@ -390,6 +400,22 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
       g = ((V.alpha * V.rd[p]) * pi) * ((double)mt / (double)ct);
     }
     V.gt[oi] = g;
+  }
+  if (V.hist) {
+    for (int q = lane; q < m.nt * hw; q += 64) V.hist[(size_t)i * m.nt * hw + q] = hist_s[q];
+    // the CDF at each bin: requests in bins 0..b over the type's count
+    for (int q = lane; q < V.nb * m.nt; q += 64) {
+      const int b = q / m.nt, t = q - b * m.nt;
+      uint32_t h = 0;
+      for (int k = 0; k <= b; k++) h += hist_s[t * hw + k];
+      const uint32_t ct = cnt_s[t];
+      double g = 0.0;
+      if (valid_s && ct > 0) {
+        const double pi = (double)m.weight[t] / (double)m.wsum;
+        g = ((V.alpha * V.rd[p]) * pi) * ((double)h / (double)ct);
+      }
+      V.curve[((size_t)i * V.nb + b) * m.nt + t] = g;
+    }
   }
 }
 
@@ -495,11 +521,13 @@ __global__ void __launch_bounds__(kParBlock) k_pareto_global(const double *g, in
 }  // namespace
 }  // namespace cf
 
-extern "C" cf_status cf_eval_mc(const cf_model_desc *model, const cf_plan_table *plans, const int32_t *plan_ids_dev,
-                                int32_t n_plans, const double *rd_dev, const uint64_t *moments_dev, double alpha,
-                                const cf_trace *trace, int32_t seed_idx, int32_t n_sample, uint32_t *met_dev,
-                                uint32_t *cnt_dev, double *goodput_t_dev, double *lat_dev, void *stream) {
-  using namespace cf;
+namespace cf {
+namespace {
+cf_status eval_mc(const cf_model_desc *model, const cf_plan_table *plans, const int32_t *plan_ids_dev, int32_t n_plans,
+                  const double *rd_dev, const uint64_t *moments_dev, double alpha, const cf_trace *trace,
+                  int32_t seed_idx, int32_t n_sample, uint32_t *met_dev, uint32_t *cnt_dev, double *goodput_t_dev,
+                  double *lat_dev, int32_t n_bins, const double *targets_host, uint32_t *hist_dev, double *curve_dev,
+                  void *stream) {
   KModel m;
   cf_status st = lower_model(model, &m);
   if (st != CF_OK) return st;
@@ -542,6 +570,17 @@ extern "C" cf_status cf_eval_mc(const cf_model_desc *model, const cf_plan_table 
   V.gt = goodput_t_dev;
   V.lat = lat_dev;
   V.order = nullptr;
+  V.tg = nullptr;
+  V.nb = 0;
+  V.hist = nullptr;
+  V.curve = nullptr;
+  if (n_bins > 0) {
+    if (!hist_dev || !curve_dev) return set_error(CF_EINVAL, "NULL histogram or curve array");
+    if ((st = load_targets(m.nt, n_bins, targets_host, &V.tg, as_stream(stream))) != CF_OK) return st;
+    V.nb = n_bins;
+    V.hist = hist_dev;
+    V.curve = curve_dev;
+  }
   if (n_sample > 0) {
     uint32_t *order = (uint32_t *)scratch_get(SCR_MC, sizeof(uint32_t) * (size_t)n_sample, &st);
     if (!order) return st;
@@ -552,6 +591,28 @@ extern "C" cf_status cf_eval_mc(const cf_model_desc *model, const cf_plan_table 
   }
   hipLaunchKernelGGL(k_mc, dim3((unsigned)n_plans), dim3(64), 0, as_stream(stream), m, V);
   return hip_check(hipGetLastError(), "cf_eval_mc launch");
+}
+}  // namespace
+}  // namespace cf
+
+extern "C" cf_status cf_eval_mc(const cf_model_desc *model, const cf_plan_table *plans, const int32_t *plan_ids_dev,
+                                int32_t n_plans, const double *rd_dev, const uint64_t *moments_dev, double alpha,
+                                const cf_trace *trace, int32_t seed_idx, int32_t n_sample, uint32_t *met_dev,
+                                uint32_t *cnt_dev, double *goodput_t_dev, double *lat_dev, void *stream) {
+  return cf::eval_mc(model, plans, plan_ids_dev, n_plans, rd_dev, moments_dev, alpha, trace, seed_idx, n_sample,
+                     met_dev, cnt_dev, goodput_t_dev, lat_dev, 0, nullptr, nullptr, nullptr, stream);
+}
+
+extern "C" cf_status cf_eval_mc_curve(const cf_model_desc *model, const cf_plan_table *plans,
+                                      const int32_t *plan_ids_dev, int32_t n_plans, const double *rd_dev,
+                                      const uint64_t *moments_dev, double alpha, const cf_trace *trace,
+                                      int32_t seed_idx, int32_t n_sample, int32_t n_bins,
+                                      const double *hist_targets_host, uint32_t *met_dev, uint32_t *cnt_dev,
+                                      double *goodput_t_dev, uint32_t *hist_dev, double *curve_dev, void *stream) {
+  if (n_bins < 1) return cf::set_error(CF_EINVAL, "n_bins must be in 1..64");
+  return cf::eval_mc(model, plans, plan_ids_dev, n_plans, rd_dev, moments_dev, alpha, trace, seed_idx, n_sample,
+                     met_dev, cnt_dev, goodput_t_dev, nullptr, n_bins, hist_targets_host, hist_dev, curve_dev,
+                     stream);
 }
 
 extern "C" cf_status cf_pareto(const double *goodput_t_dev, int32_t n, int32_t T, uint8_t *keep_dev,

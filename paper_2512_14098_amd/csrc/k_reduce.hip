@@ -46,6 +46,45 @@ __global__ void __launch_bounds__(64) k_goodput(const uint32_t *met, const uint3
   }
 }
 
+// The same computation per latency-target bin b: block (i, b), lane k pools
+// rate k's requests in bins 0..b over seeds.
+__global__ void __launch_bounds__(64) k_goodput_curve(const uint32_t *hist, const uint32_t *cnt, int K, int S, int T,
+                                                     int nb, const double *rates, uint32_t tn, uint32_t td,
+                                                     double denom, int32_t *kstar, double *goodput_t,
+                                                     double *goodput) {
+  const int i = blockIdx.x, b = blockIdx.y, lane = threadIdx.x;
+  const int hw = nb + 1;
+  auto pooled = [&](int k, int t) {
+    uint64_t M = 0;
+    for (int s = 0; s < S; s++) {
+      const uint32_t *h = hist + ((((size_t)i * K + k) * S + s) * T + t) * hw;
+      for (int q = 0; q <= b; q++) M += h[q];
+    }
+    return M;
+  };
+  bool infeasible = false;
+  if (lane < K) {
+    for (int t = 0; t < T; t++) {
+      uint64_t N = 0;
+      for (int s = 0; s < S; s++) N += cnt[(((size_t)i * K + lane) * S + s) * T + t];
+      const uint64_t M = pooled(lane, t);
+      if (N > 0 && (uint64_t)td * M < (uint64_t)tn * N) infeasible = true;
+    }
+  }
+  const uint64_t bad = __ballot(infeasible);
+  const int ks = bad ? (__ffsll((long long)bad) - 2) : K - 1;
+  double gt = 0.0;
+  if (lane < T && ks >= 0) gt = (rates[(size_t)i * K + ks] * (double)pooled(ks, lane)) / denom;
+  const size_t ob = (size_t)i * nb + b;
+  if (lane < T) goodput_t[ob * T + lane] = gt;
+  double g = 0.0;
+  for (int t = 0; t < T; t++) g = g + __shfl(gt, t, 64);
+  if (lane == 0) {
+    kstar[ob] = ks;
+    goodput[ob] = g;
+  }
+}
+
 __global__ void __launch_bounds__(256) k_best(const double *g, int n, int32_t *best) {
   __shared__ double bv[256];
   __shared__ int bi[256];
@@ -116,6 +155,25 @@ extern "C" cf_status cf_goodput_reduce(const uint32_t *met_dev, const uint32_t *
   hipLaunchKernelGGL(k_goodput, dim3((unsigned)n_plans), dim3(64), 0, as_stream(stream), met_dev, cnt_dev, K, S, T,
                      rates_dev, theta_num, theta_den, denom, kstar_dev, goodput_t_dev, goodput_dev);
   return hip_check(hipGetLastError(), "cf_goodput_reduce launch");
+}
+
+extern "C" cf_status cf_goodput_curve(const uint32_t *hist_dev, const uint32_t *cnt_dev, int32_t n_plans, int32_t K,
+                                      int32_t S, int32_t T, int32_t n_bins, const double *rates_dev,
+                                      uint32_t theta_num, uint32_t theta_den, int32_t n_req, int32_t *kstar_dev,
+                                      double *goodput_t_dev, double *goodput_dev, void *stream) {
+  using namespace cf;
+  if (n_plans < 0 || K < 1 || S < 1 || T < 1 || T > CF_MAX_TYPES || n_req < 0 || theta_den == 0)
+    return set_error(CF_EINVAL, "sizes");
+  if (n_bins < 1 || n_bins > 64) return set_error(CF_EINVAL, "n_bins must be in 1..64");
+  if (K > 64) return set_error(CF_ECAPACITY, "K above 64 (one lane per rate)");
+  if (n_plans == 0) return CF_OK;
+  if (!hist_dev || !cnt_dev || !rates_dev || !kstar_dev || !goodput_t_dev || !goodput_dev)
+    return set_error(CF_EINVAL, "NULL device array");
+  const double denom = (double)((uint64_t)S * (uint64_t)n_req);
+  hipLaunchKernelGGL(k_goodput_curve, dim3((unsigned)n_plans, (unsigned)n_bins), dim3(64), 0, as_stream(stream),
+                     hist_dev, cnt_dev, K, S, T, n_bins, rates_dev, theta_num, theta_den, denom, kstar_dev,
+                     goodput_t_dev, goodput_dev);
+  return hip_check(hipGetLastError(), "cf_goodput_curve launch");
 }
 
 extern "C" cf_status cf_select_best(const double *goodput_dev, int32_t n, int32_t *best_dev, void *stream) {
