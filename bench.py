@@ -358,6 +358,9 @@ def main():
     ap.add_argument("--phase2", action="store_true",
                     help="only time phase 2 (Monte Carlo latency) and Pareto pruning over the plans "
                          "phase 1 keeps (default workload c4), then exit")
+    ap.add_argument("--curve", type=int, default=0, metavar="BINS",
+                    help="also emit phase-3 latency histograms over BINS latency-target scales (0.25x to 4x "
+                         "each type's bounds, log-spaced) and reduce them to goodput at every target")
     ap.add_argument("--enum", action="store_true",
                     help="only time plan enumeration on the device and phase-1 screening of the enumerated "
                          "table (default model: c2's omni graph on 16 GPUs), then exit")
@@ -412,6 +415,8 @@ def main():
     seeds = all_seeds[: args.seeds] if args.seeds > 0 else all_seeds
     w = pipeline.Workload(cfg, seeds=seeds)
     full_top = w.top_k
+    if args.curve > 0:
+        w.set_target_scales([0.25 * 16.0 ** (b / max(args.curve - 1, 1)) for b in range(args.curve)])
     if args.plans > 0:
         w.top_k = min(w.top_k, args.plans)
     for i in range(args.warmup):
@@ -451,6 +456,8 @@ def main():
         sample.append("first %d of its %d seeds" % (len(seeds), len(all_seeds)))
     if sample:
         workload += " (sample: %s)" % ", ".join(sample)
+    if args.curve > 0:
+        workload += "; goodput curves over %d latency-target scales" % args.curve
     res = {
         "metric": METRIC,
         "value": events / elapsed,

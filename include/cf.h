@@ -162,7 +162,7 @@ typedef struct cf_fine_out {
   const int32_t *lat_triples_dev; /* [n_lat] linear triple ids ((i*K)+k)*S+s to dump */
   int32_t n_lat;
   /* Optional latency histograms (goodput against a range of latency
-   * targets, Sec. 6.3 Fig. 8): with n_bins > 0, a completed request of type
+   * targets, Sec. 6.2 and Appendix B): with n_bins > 0, a completed request of type
    * t counts in bin b = the first bin whose four bounds
    * hist_targets_host[t][b][0..3] (TTFT, TPOT, E2E, MEDIA, inclusive) it
    * meets, or n_bins if none; the bounds must not decrease with b (1 <=
@@ -352,7 +352,7 @@ cf_status cf_goodput_reduce(const uint32_t *met_dev, const uint32_t *cnt_dev, in
                             int32_t *kstar_dev, double *goodput_t_dev, double *goodput_dev,
                             void *stream);
 
-/* Goodput against a range of latency targets (Sec. 6.3, per-type goodput
+/* Goodput against a range of latency targets (Sec. 6.2 and Appendix B, per-type goodput
  * vs. latency target): for every plan and bin b, cf_goodput_reduce's
  * computation with M_t = the requests in bins 0..b of hist_dev (a
  * cf_fine_out histogram [n_plans][K][S][T][n_bins + 1]).  Outputs:

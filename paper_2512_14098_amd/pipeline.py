@@ -39,6 +39,20 @@ class Workload:
         # phase 2 (optional): dict(K=sampled requests, alpha=headroom), or None to go
         # from phase 1 straight to phase 3 over the top_k plans
         self.phase2 = phase2 if phase2 is not None else cfg.get("phase2")
+        # optional latency-target table [T][n_bins][4]: phase 3 then also emits latency
+        # histograms, and the reduction goodput at every target
+        self.targets = None
+
+    def set_target_scales(self, scales):
+        """Targets = each type's own bounds times each scale (ascending)."""
+        T = len(self.cfg["model"]["types"])
+        tg = np.empty((T, len(scales), 4), np.float64)
+        for t, ty in enumerate(self.cfg["model"]["types"]):
+            slo = ty.get("slo", {})
+            for j, key in enumerate(("ttft", "tpot", "e2e", "media")):
+                bound = float(slo[key]) if key in slo else np.inf
+                tg[t, :, j] = [bound * float(sc) for sc in scales]
+        self.targets = tg
 
 
 def run_step(w, timers=None):
@@ -82,16 +96,45 @@ def run_step(w, timers=None):
         rates = cf.cf_rate_grid(rd, ids, w.K, w.alpha_max)
     mark("select")
     mark("fine")
-    fine = cf.cf_eval_fine(w.desc, w.plans, ids, rates, trace)
+    fine = cf.cf_eval_fine(w.desc, w.plans, ids, rates, trace, targets=w.targets)
     mark("fine")
     mark("reduce")
     kstar, gt, g = cf.cf_goodput_reduce(fine["met"], fine["cnt"], rates, w.theta, w.n_req)
     best = cf.cf_select_best(g) if ids.numel() > 0 else None
+    curve = None
+    if w.targets is not None and ids.numel() > 0:
+        curve = dict(zip(("kstar", "goodput_t", "goodput"),
+                         cf.cf_goodput_curve(fine["hist"], fine["cnt"], rates, w.theta, w.n_req)))
     mark("reduce")
     if timers is not None:
         timers.update(ev)
     return dict(trace=trace, moments=moments, rd=rd, bottleneck=bott, flags=flags, ids=ids,
-                rates=rates, fine=fine, kstar=kstar, goodput_t=gt, goodput=g, best=best, phase2=mc)
+                rates=rates, fine=fine, kstar=kstar, goodput_t=gt, goodput=g, best=best, phase2=mc,
+                curve=curve)
+
+
+def reweight(w, out, weights, K=1024, alpha=0.8):
+    """Phases 1 and 2 again under new request-type weights, on the samples already drawn
+    (Sec. 4.4: a change of the type fractions pi_t re-weights existing samples).  Only the
+    weights change: the trace, its per-type moments and the sampled requests of ``out``
+    (a run_step result) are kept; phase 1 recomputes R_d and the flags, phase 2 re-walks the
+    same sampled requests at the new effective batches, and Pareto pruning clears the keep
+    flag of dominated plans.  Phase 3 is not re-weighted: a different mix changes queueing,
+    so it needs a new simulation."""
+    mcfg = dict(w.cfg["model"])
+    if len(weights) != len(mcfg["types"]):
+        raise cf.CfError("one weight per request type")
+    mcfg["types"] = [dict(t, weight=int(wt)) for t, wt in zip(mcfg["types"], weights)]
+    desc = cf.model_desc(mcfg)
+    rd, bott, flags = cf.cf_eval_coarse(desc, w.plans, out["moments"][0], w.n_gpus)
+    cand = cf.cf_select_topk(rd, flags, MAX_PHASE2)
+    if cand.numel() >= MAX_PHASE2:
+        raise cf.CfError("phase 2 takes fewer than %d kept plans" % MAX_PHASE2)
+    K = min(int(K), w.n_req)
+    mc = cf.cf_eval_mc(desc, w.plans, cand, rd, out["moments"][0], float(alpha), out["trace"], 0, K)
+    mc["ids"] = cand
+    mc["keep"] = cf.cf_pareto(mc["goodput_t"], cand, flags)
+    return dict(desc=desc, rd=rd, bottleneck=bott, flags=flags, phase2=mc)
 
 
 def best_plan(out):

@@ -515,3 +515,35 @@ def test_pipeline_with_phase2(cf):
     assert np.array_equal(out["flags"].cpu().numpy(), fl2)
     assert np.array_equal(out["ids"].cpu().numpy(), O.select_topk(rd, fl2, 12))
     assert 0 < int(keep.sum()) < len(cand)
+
+
+def test_reweighting_without_resimulation(cf):
+    """Phases 1 and 2 under new type weights on the same samples, against the oracle with the
+    same weights and trace (a synthetic analogue of the workload-drift study: image share
+    25 % / 50 % / 75 %); R_d and the per-type goodput move with the mix."""
+    _say("reweight c1")
+    from paper_2512_14098_amd import pipeline
+    cfg = load_config("c1")
+    cfg["n_req"] = 2000
+    w = pipeline.Workload(cfg, seeds=[21, 22])
+    out = pipeline.run_step(w)
+    m0 = O.make_model(cfg["model"])
+    otr = O.trace_gen(m0, [21, 22], 2000)
+    rds, gts = [], []
+    for share in (25, 50, 75):
+        weights = [100 - share, share]
+        r = pipeline.reweight(w, out, weights, K=512, alpha=0.8)
+        mc = dict(cfg["model"])
+        mc["types"] = [dict(t, weight=wt) for t, wt in zip(mc["types"], weights)]
+        m = O.make_model(mc)
+        rd, bn, fl = O.eval_coarse(m, w.tab, otr["moments"][0], cfg["gpus"])
+        assert np.array_equal(r["rd"].cpu().numpy(), rd)
+        cand = O.select_topk(rd, fl, 65536)
+        met, cnt, gt = O.eval_mc(m, w.tab, cand, rd, otr["moments"][0], 0.8, otr, 0, 512)
+        keep = O.pareto(gt)
+        assert np.array_equal(r["phase2"]["ids"].cpu().numpy(), cand)
+        assert np.array_equal(r["phase2"]["goodput_t"].cpu().numpy(), gt)
+        assert np.array_equal(r["phase2"]["keep"].cpu().numpy(), keep)
+        rds.append(rd)
+        gts.append(gt)
+    assert not np.array_equal(rds[0], rds[2]) and not np.array_equal(gts[0], gts[2])

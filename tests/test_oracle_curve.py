@@ -1,6 +1,6 @@
 """Pins of the oracle's latency CDFs over target tables (Alg. 2: F_{t,d} is
 the CDF of accumulated latencies, evaluated at L_t; goodput against a range
-of latency targets, Sec. 6.3).
+of latency targets, Sec. 6.2 and Appendix B).
 
 Independent checks: with a one-bin table equal to each type's own bounds,
 bin 0 holds exactly the requests the SLO counters (a separate code path in
