@@ -203,6 +203,13 @@ int cfo_sim_triple(const cfo_model *m, const cfo_plans *pl, int32_t plan_id, dou
                    const cfo_trace *tr, int32_t seed_idx, uint32_t *met, uint32_t *cnt,
                    uint64_t *events, uint32_t *status, double *lat, double *diag);
 
+/* Rate bisection over each plan's grid (seeds pooled, the attainment test
+ * of cfo_goodput_reduce): kstar, goodput_t [n][T], goodput [n], n_eval
+ * (rates simulated per plan), events (request-events simulated per plan). */
+int cfo_bisect(const cfo_model *m, const cfo_plans *pl, const int32_t *plan_ids, int32_t n_plans,
+               const double *rates, int32_t K, const cfo_trace *tr, uint32_t theta_num, uint32_t theta_den,
+               int32_t *kstar, double *goodput_t, double *goodput, int32_t *n_eval, uint64_t *events);
+
 int cfo_goodput_reduce(const uint32_t *met, const uint32_t *cnt, int32_t n_plans, int32_t K,
                        int32_t S, int32_t T, const double *rates, uint32_t theta_num,
                        uint32_t theta_den, int32_t n_req, int32_t *kstar, double *goodput_t,

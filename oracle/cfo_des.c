@@ -525,3 +525,62 @@ int cfo_sim_triple(const cfo_model *m, const cfo_plans *pl, int32_t plan_id, dou
   free(S.h.a);
   return 0;
 }
+
+/* Rate bisection (the workload descriptions bisect rates over a grid):
+ * for plan plan_ids[i] and its grid rates[i][0..K), with feasible(k) the
+ * attainment test of cfo_goodput_reduce on the counts pooled over the S
+ * seeds at rate k, keep lo = -1 (feasible) and hi = K (infeasible), simulate
+ * every seed at mid = (lo + hi) / 2 and move lo or hi to mid, until
+ * hi = lo + 1.  kstar = lo, goodput_t = (rates[lo] M_t) / (S n) from the
+ * simulation at lo (0 if lo < 0).  On a monotone predicate this is the
+ * grid's first infeasible rate - 1, after at most ceil(log2(K + 1))
+ * rounds; n_eval[i] counts the rates simulated. */
+int cfo_bisect(const cfo_model *m, const cfo_plans *pl, const int32_t *plan_ids, int32_t n_plans,
+               const double *rates, int32_t K, const cfo_trace *tr, uint32_t theta_num, uint32_t theta_den,
+               int32_t *kstar, double *goodput_t, double *goodput, int32_t *n_eval, uint64_t *events) {
+  const int T = m->n_types, S = tr->n_seeds;
+  const double denom = (double)((uint64_t)S * (uint64_t)tr->n_req);
+  uint32_t met[CFO_MAXT], cnt[CFO_MAXT];
+  uint64_t Mlo[CFO_MAXT];
+  for (int i = 0; i < n_plans; i++) {
+    int lo = -1, hi = K, ne = 0;
+    uint64_t ev_total = 0;
+    for (int t = 0; t < T; t++) Mlo[t] = 0;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) / 2;
+      uint64_t M[CFO_MAXT], N[CFO_MAXT];
+      for (int t = 0; t < T; t++) M[t] = N[t] = 0;
+      for (int s = 0; s < S; s++) {
+        uint64_t ev = 0;
+        uint32_t st = 0;
+        cfo_sim_triple(m, pl, plan_ids[i], rates[(size_t)i * K + mid], tr, s, met, cnt, &ev, &st, NULL, NULL);
+        ev_total += ev;
+        for (int t = 0; t < T; t++) {
+          M[t] += met[t];
+          N[t] += cnt[t];
+        }
+      }
+      ne++;
+      int feasible = 1;
+      for (int t = 0; t < T; t++)
+        if (N[t] > 0 && (uint64_t)theta_den * M[t] < (uint64_t)theta_num * N[t]) feasible = 0;
+      if (feasible) {
+        lo = mid;
+        for (int t = 0; t < T; t++) Mlo[t] = M[t];
+      } else {
+        hi = mid;
+      }
+    }
+    kstar[i] = lo;
+    n_eval[i] = ne;
+    events[i] = ev_total;
+    double g = 0.0;
+    for (int t = 0; t < T; t++) {
+      const double gt = lo >= 0 ? (rates[(size_t)i * K + lo] * (double)Mlo[t]) / denom : 0.0;
+      goodput_t[(size_t)i * T + t] = gt;
+      g = g + gt;
+    }
+    goodput[i] = g;
+  }
+  return 0;
+}

@@ -100,6 +100,7 @@ def lib():
         L.cfo_sim_triple.argtypes = [vp, vp, i32, dbl, vp, i32, vp, vp, vp, vp, vp, vp]
         L.cfo_goodput_reduce.argtypes = [vp, vp, i32, i32, i32, i32, vp, C.c_uint32, C.c_uint32,
                                          i32, vp, vp, vp]
+        L.cfo_bisect.argtypes = [vp, vp, vp, i32, vp, i32, vp, C.c_uint32, C.c_uint32, vp, vp, vp, vp, vp]
         L.cfo_latency_hist.argtypes = [vp, vp, i32, i32, i32, vp, vp]
         L.cfo_mc_curve.argtypes = [vp, vp, vp, i32, vp, vp, dbl, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp]
         L.cfo_enum_logical.argtypes = [vp, vp, vp, i32, vp]
@@ -483,3 +484,19 @@ def scaled_targets(model, scales):
             for j in range(4):
                 out[t, b, j] = model.slo[t][j] * float(sc)
     return out
+
+
+def bisect(model, tab, plan_ids, rates, tr, theta):
+    """Rate bisection per plan over its grid: (kstar, goodput_t, goodput, n_eval, events)."""
+    ids = np.ascontiguousarray(plan_ids, np.int32)
+    rates = np.ascontiguousarray(rates, np.float64)
+    n, K, T = len(ids), rates.shape[1], model.n_types
+    ks = np.zeros(n, np.int32)
+    gt = np.zeros((n, T), np.float64)
+    g = np.zeros(n, np.float64)
+    ne = np.zeros(n, np.int32)
+    ev = np.zeros(n, np.uint64)
+    lib().cfo_bisect(C.byref(model), C.byref(plans_struct(tab)), _ptr(ids), n, _ptr(rates), int(K),
+                     C.byref(trace_struct(tr)), int(theta[0]), int(theta[1]), _ptr(ks), _ptr(gt), _ptr(g),
+                     _ptr(ne), _ptr(ev))
+    return ks, gt, g, ne, ev
