@@ -352,6 +352,27 @@ cf_status cf_goodput_reduce(const uint32_t *met_dev, const uint32_t *cnt_dev, in
                             int32_t *kstar_dev, double *goodput_t_dev, double *goodput_dev,
                             void *stream);
 
+/* Phase 3 with rate bisection (the workload descriptions bisect rates over
+ * a grid; Alg. 2 phase 3 simulates each plan at its rate): for plan
+ * plan_ids_dev[i] and its grid rates_dev[i][0..K), lo = -1 and hi = K;
+ * each round simulates every seed of the trace at mid = (lo + hi) / 2 for
+ * every plan with hi > lo + 1, and moves lo to mid if the pooled counts
+ * pass the attainment test of cf_goodput_reduce (theta), else hi.  At the
+ * end kstar = lo, goodput_t = (rates[lo] M_t) / (S n_req) with M_t the
+ * pooled met counts of the round at lo (0 if lo < 0), goodput = sum_t.  On
+ * a monotone feasibility this is cf_goodput_reduce's result with
+ * ceil(log2(K + 1)) rates simulated instead of K.
+ * Outputs (device): kstar_dev[n], goodput_t_dev[n][T], goodput_dev[n],
+ * n_eval_dev[n] (rates simulated), events_dev[n] (request-events simulated),
+ * status_dev[n] (CF_ST_* bits OR-ed over the plan's simulations).
+ * Synchronises the stream once per round.  Limits: K <= 64.
+ * Errors: those of cf_eval_fine; CF_EINVAL (sizes, theta). */
+cf_status cf_eval_bisect(const cf_model_desc *model, const cf_plan_table *plans, const int32_t *plan_ids_dev,
+                         int32_t n_plans, const double *rates_dev, int32_t K, const cf_trace *trace,
+                         uint32_t theta_num, uint32_t theta_den, int32_t *kstar_dev, double *goodput_t_dev,
+                         double *goodput_dev, int32_t *n_eval_dev, uint64_t *events_dev, uint32_t *status_dev,
+                         void *stream);
+
 /* Goodput against a range of latency targets (Sec. 6.2 and Appendix B, per-type goodput
  * vs. latency target): for every plan and bin b, cf_goodput_reduce's
  * computation with M_t = the requests in bins 0..b of hist_dev (a

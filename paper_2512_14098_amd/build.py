@@ -11,7 +11,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libcf.so")
-SOURCES = ["cf_abi.hip", "k_trace.hip", "k_coarse.hip", "k_select.hip", "k_reduce.hip", "k_fine.hip", "k_mc.hip", "k_enum.hip"]
+SOURCES = ["cf_abi.hip", "k_trace.hip", "k_coarse.hip", "k_select.hip", "k_reduce.hip", "k_fine.hip", "k_mc.hip", "k_enum.hip", "k_bisect.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=off",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

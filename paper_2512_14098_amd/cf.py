@@ -99,6 +99,7 @@ def _load():
         "cf_eval_mc_curve": ([vp, vp, vp, i32, vp, vp, dbl, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp], i32),
         "cf_goodput_curve": ([vp, vp, i32, i32, i32, i32, i32, vp, C.c_uint32, C.c_uint32, i32, vp, vp, vp, vp],
                              i32),
+        "cf_eval_bisect": ([vp, vp, vp, i32, vp, i32, vp, C.c_uint32, C.c_uint32, vp, vp, vp, vp, vp, vp, vp], i32),
         "cf_enum_logical": ([vp, vp, vp, i32, vp], i32),
         "cf_enum_count": ([vp, vp, vp, i32, vp, vp, vp], i32),
         "cf_enum_plans": ([vp, vp, vp, i32, vp, C.c_uint64, C.c_uint64, i32, vp, vp], i32),
@@ -116,7 +117,7 @@ def _load():
 
 _lib = _load()
 EXPORTED = ("cf_last_error", "cf_status_str", "cf_version", "cf_trace_gen", "cf_eval_coarse",
-            "cf_select_topk", "cf_rate_grid", "cf_eval_fine", "cf_eval_mc", "cf_eval_mc_curve", "cf_goodput_curve", "cf_pareto",
+            "cf_select_topk", "cf_rate_grid", "cf_eval_fine", "cf_eval_bisect", "cf_eval_mc", "cf_eval_mc_curve", "cf_goodput_curve", "cf_pareto",
             "cf_enum_logical", "cf_enum_count", "cf_enum_plans",
             "cf_goodput_reduce", "cf_select_best", "cf_math_eval", "cf_philox_eval", "cf_release_scratch")
 
@@ -357,6 +358,23 @@ def cf_eval_fine(desc, plans, plan_ids, rates, trace, lat_triples=None, targets=
                              _p(rates.contiguous()), int(K), C.byref(trace.c), 0, C.byref(out),
                              _stream()), "cf_eval_fine")
     return dict(met=met, cnt=cnt, events=events, status=status, lat=lat, hist=hist)
+
+
+def cf_eval_bisect(desc, plans, plan_ids, rates, trace, theta):
+    """Phase 3 with each plan's rate bisected over its grid: dict(kstar, goodput_t, goodput,
+    n_eval, events, status)."""
+    n, K = rates.shape
+    T, dev = desc.n_types, rates.device
+    ks = torch.empty(n, dtype=torch.int32, device=dev)
+    gt = torch.empty((n, T), dtype=torch.float64, device=dev)
+    g = torch.empty(n, dtype=torch.float64, device=dev)
+    ne = torch.empty(n, dtype=torch.int32, device=dev)
+    ev = torch.empty(n, dtype=torch.int64, device=dev)
+    st = torch.empty(n, dtype=torch.int32, device=dev)
+    _check(_lib.cf_eval_bisect(C.byref(desc), C.byref(plans.c), _p(plan_ids.contiguous()), int(n),
+                               _p(rates.contiguous()), int(K), C.byref(trace.c), int(theta[0]), int(theta[1]),
+                               _p(ks), _p(gt), _p(g), _p(ne), _p(ev), _p(st), _stream()), "cf_eval_bisect")
+    return dict(kstar=ks, goodput_t=gt, goodput=g, n_eval=ne, events=ev, status=st)
 
 
 def cf_eval_mc(desc, plans, plan_ids, rd, moments_seed, alpha, trace, seed_idx, n_sample,

@@ -130,6 +130,6 @@ __device__ __forceinline__ int target_bin(const double *tg, int n_bins, int t, d
   return lo;
 }
 
-enum ScratchSlot { SCR_TRACE = 0, SCR_SELECT = 1, SCR_FINE = 2, SCR_MC = 3, SCR_PARETO = 4, SCR_ENUM = 5, SCR_TARGETS = 6, SCR_NSLOTS = 7 };
+enum ScratchSlot { SCR_TRACE = 0, SCR_SELECT = 1, SCR_FINE = 2, SCR_MC = 3, SCR_PARETO = 4, SCR_ENUM = 5, SCR_TARGETS = 6, SCR_BISECT = 7, SCR_NSLOTS = 8 };
 void *scratch_get(int slot, size_t bytes, cf_status *st);
 }  // namespace cf

@@ -547,3 +547,44 @@ def test_reweighting_without_resimulation(cf):
         rds.append(rd)
         gts.append(gt)
     assert not np.array_equal(rds[0], rds[2]) and not np.array_equal(gts[0], gts[2])
+
+
+@pytest.mark.parametrize("name,n_plans,seeds,n", [("c0", 6, [0], 1000), ("c1", 24, [3, 4], 3000),
+                                                  ("c2", 4, [5], 4000), ("c3", 4, [6], 5000)])
+def test_bisect_parity(cf, name, n_plans, seeds, n):
+    """Rate bisection on the GPU against the oracle's: highest feasible rate, goodput, rates
+    simulated, request-events and status identical; equal to the full grid's reduction."""
+    _say(f"bisect {name}")
+    cfg = load_config(name)
+    tab = make_plans(cfg)
+    m = O.make_model(cfg["model"])
+    otr = O.trace_gen(m, seeds, n)
+    if "explicit" in cfg["rates"]:
+        ids = np.arange(min(n_plans, tab.P), dtype=np.int32)
+        rates = np.tile(np.asarray(cfg["rates"]["explicit"], np.float64), (len(ids), 1))
+    else:
+        rd, _, fl = O.eval_coarse(m, tab, otr["moments"][0], cfg["gpus"])
+        ids = O.select_topk(rd, fl, n_plans)
+        rates = O.rate_grid(rd, ids, cfg["rates"]["grid"])
+    theta = (9, 10)
+    want = O.bisect(m, tab, ids, rates, otr, theta)
+    desc = cf.model_desc(cfg["model"])
+    tr, _ = cf.cf_trace_gen(desc, seeds, n)
+    got = cf.cf_eval_bisect(desc, cf.DevicePlans(tab), torch.as_tensor(ids).cuda(), torch.from_numpy(rates).cuda(),
+                            tr, theta)
+    torch.cuda.synchronize()
+    assert np.array_equal(got["kstar"].cpu().numpy(), want[0])
+    assert np.array_equal(got["goodput_t"].cpu().numpy(), want[1])
+    assert np.array_equal(got["goodput"].cpu().numpy(), want[2])
+    assert np.array_equal(got["n_eval"].cpu().numpy(), want[3])
+    assert np.array_equal(got["events"].cpu().numpy().view(np.uint64), want[4])
+    assert np.all(got["status"].cpu().numpy() == 0)
+    # the grid's answer where its feasibility is monotone
+    g = cf.cf_eval_fine(desc, cf.DevicePlans(tab), torch.as_tensor(ids).cuda(), torch.from_numpy(rates).cuda(), tr)
+    ks, gt, gg = cf.cf_goodput_reduce(g["met"], g["cnt"], torch.from_numpy(rates).cuda(), theta, n)
+    met = g["met"].cpu().numpy().view(np.uint32).astype(np.uint64).sum(axis=2)
+    cnt = g["cnt"].cpu().numpy().view(np.uint32).astype(np.uint64).sum(axis=2)
+    feas = np.all((cnt == 0) | (theta[1] * met >= theta[0] * cnt), axis=2)
+    for i in range(len(ids)):
+        if np.all(np.diff(feas[i].astype(int)) <= 0):
+            assert ks[i].item() == want[0][i] and gg[i].item() == want[2][i]
