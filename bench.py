@@ -361,6 +361,9 @@ def main():
     ap.add_argument("--curve", type=int, default=0, metavar="BINS",
                     help="also emit phase-3 latency histograms over BINS latency-target scales (0.25x to 4x "
                          "each type's bounds, log-spaced) and reduce them to goodput at every target")
+    ap.add_argument("--bisect", action="store_true",
+                    help="phase 3 bisects each plan's rate over its grid (ceil(log2(K+1)) rates simulated per "
+                         "plan and seed) instead of simulating every grid rate")
     ap.add_argument("--enum", action="store_true",
                     help="only time plan enumeration on the device and phase-1 screening of the enumerated "
                          "table (default model: c2's omni graph on 16 GPUs), then exit")
@@ -415,6 +418,7 @@ def main():
     seeds = all_seeds[: args.seeds] if args.seeds > 0 else all_seeds
     w = pipeline.Workload(cfg, seeds=seeds)
     full_top = w.top_k
+    w.bisect = bool(args.bisect)
     if args.curve > 0:
         w.set_target_scales([0.25 * 16.0 ** (b / max(args.curve - 1, 1)) for b in range(args.curve)])
     if args.plans > 0:
@@ -458,6 +462,8 @@ def main():
         workload += " (sample: %s)" % ", ".join(sample)
     if args.curve > 0:
         workload += "; goodput curves over %d latency-target scales" % args.curve
+    if args.bisect:
+        workload += "; rates bisected over the grid"
     res = {
         "metric": METRIC,
         "value": events / elapsed,
@@ -474,7 +480,8 @@ def main():
         "plans_per_s": plans / elapsed,
         "config": {"workload": workload, "plans_screened": w.tab.P,
                    "plans_simulated": n_sel, "rates": w.K, "seeds": len(w.seeds), "requests": w.n_req,
-                   "triples": n_sel * w.K * len(w.seeds), "request_events_per_step": ev_step,
+                   "triples": (int(out["fine"]["n_eval"].sum().item()) * len(w.seeds) if w.bisect
+                               else n_sel * w.K * len(w.seeds)), "request_events_per_step": ev_step,
                    "status_counts": st, "fine_ms": fine_ms,
                    "stage_ms": {k: sum(v) / len(v) for k, v in stage_ms.items()}},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_LANE_OPS, "unit": "TOP/s",

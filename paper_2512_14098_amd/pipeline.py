@@ -42,6 +42,8 @@ class Workload:
         # optional latency-target table [T][n_bins][4]: phase 3 then also emits latency
         # histograms, and the reduction goodput at every target
         self.targets = None
+        # phase 3 by rate bisection over each plan's grid instead of every grid rate
+        self.bisect = False
 
     def set_target_scales(self, scales):
         """Targets = each type's own bounds times each scale (ascending)."""
@@ -96,13 +98,19 @@ def run_step(w, timers=None):
         rates = cf.cf_rate_grid(rd, ids, w.K, w.alpha_max)
     mark("select")
     mark("fine")
-    fine = cf.cf_eval_fine(w.desc, w.plans, ids, rates, trace, targets=w.targets)
+    if w.bisect:
+        fine = cf.cf_eval_bisect(w.desc, w.plans, ids, rates, trace, w.theta)
+    else:
+        fine = cf.cf_eval_fine(w.desc, w.plans, ids, rates, trace, targets=w.targets)
     mark("fine")
     mark("reduce")
-    kstar, gt, g = cf.cf_goodput_reduce(fine["met"], fine["cnt"], rates, w.theta, w.n_req)
+    if w.bisect:
+        kstar, gt, g = fine["kstar"], fine["goodput_t"], fine["goodput"]
+    else:
+        kstar, gt, g = cf.cf_goodput_reduce(fine["met"], fine["cnt"], rates, w.theta, w.n_req)
     best = cf.cf_select_best(g) if ids.numel() > 0 else None
     curve = None
-    if w.targets is not None and ids.numel() > 0:
+    if w.targets is not None and ids.numel() > 0 and not w.bisect:
         curve = dict(zip(("kstar", "goodput_t", "goodput"),
                          cf.cf_goodput_curve(fine["hist"], fine["cnt"], rates, w.theta, w.n_req)))
     mark("reduce")
