@@ -82,7 +82,17 @@ typedef struct {
   cfo_dist len[CFO_MAXT][4];    /* prompt, out, aud_in_ms, aud_out_ms */
   double slo[CFO_MAXT][4];      /* ttft, tpot, e2e, media (<=; +inf = none) */
   uint32_t theta_num, theta_den;
+  /* latency multiplier of component c on executors of g GPUs (tensor
+   * parallelism degree), tp_scale[c][min(g, 8) - 1]; 1 = the profiled
+   * single-GPU latency model */
+  double tp_scale[CFO_MAXC][8];
 } cfo_model;
+
+/* the multiplier of component c's iteration time on executors of g GPUs */
+static inline double cfo_tp(const cfo_model *m, int c, int g) {
+  const int k = g < 1 ? 1 : (g > 8 ? 8 : g);
+  return m->tp_scale[c][k - 1];
+}
 
 typedef struct {
   int32_t n_seeds, n_req;

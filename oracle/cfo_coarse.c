@@ -94,6 +94,8 @@ void cfo_node_demand(const cfo_model *m, const cfo_plans *pl, int p, const uint6
         /* seconds of executor time per request at batch B */
         double w = ((m->k0[c] / B) + m->k1[c] * ex) + m->k2[c];
         if (m->kind[c] == CFO_LLM) w = w + (en - 1.0) * ((m->d0[c] / B) + m->d1[c]);
+        /* on executors of g GPUs every iteration takes tp_scale times as long */
+        w = cfo_tp(m, c, P_AT(pl->node_gpus, v, P, p)) * w;
         u[v] = u[v] + (pi * q) * w;
       }
     }

@@ -111,6 +111,7 @@ enum { IT_BATCH = 0, IT_PREFILL = 1, IT_DECODE = 2 };
 
 typedef struct {
   int ns, comp[CFO_MAXC], beff[CFO_MAXC], stage_of[CFO_MAXC];
+  double tps[CFO_MAXC];  /* iteration-time multiplier of each stage (GPUs per executor) */
   int busy, ran, rr, cur_s, cur_kind;
   double t_end, last_end;
   ivec mem;                 /* members of the running iteration, in order */
@@ -307,7 +308,7 @@ static void start(sim_t *S, int xi, int s, double t) {
       iv_push(&X->mem, r);
       xs += x_of(S, r, c);
     }
-    dur = (m->k0[c] + m->k1[c] * (double)xs) + m->k2[c] * (double)n;
+    dur = X->tps[s] * ((m->k0[c] + m->k1[c] * (double)xs) + m->k2[c] * (double)n);
     if (m->kind[c] == CFO_ENC && (!X->ran || X->last_end < t)) dur = dur + m->cpu_pre_s;
     X->cur_kind = (m->kind[c] == CFO_LLM) ? IT_PREFILL : IT_BATCH;
   } else {
@@ -315,7 +316,7 @@ static void start(sim_t *S, int xi, int s, double t) {
       int r = iv_at(&X->run[s], i);
       if (eligible(S, r, c, xi, t)) iv_push(&X->mem, r);
     }
-    dur = m->d0[c] + m->d1[c] * (double)X->mem.n;
+    dur = X->tps[s] * (m->d0[c] + m->d1[c] * (double)X->mem.n);
     X->cur_kind = IT_DECODE;
   }
   X->busy = 1;
@@ -429,6 +430,7 @@ int cfo_sim_triple(const cfo_model *m, const cfo_plans *pl, int32_t plan_id, dou
   for (int v = 0; v < nv; v++) {
     int cm = P_AT(pl->node_comp, v, P, p);
     int bn = P_AT(pl->node_batch, v, P, p);
+    int gn = P_AT(pl->node_gpus, v, P, p);
     for (int j = base[v]; j < base[v + 1]; j++) {
       exec_t *X = &S.x[j];
       X->rr = -1;
@@ -437,6 +439,7 @@ int cfo_sim_triple(const cfo_model *m, const cfo_plans *pl, int32_t plan_id, dou
         if (!((cm >> c) & 1)) continue;
         X->comp[X->ns] = c;
         X->beff[X->ns] = bn < m->batch_cap[c] ? bn : m->batch_cap[c];
+        X->tps[X->ns] = cfo_tp(m, c, gn);
         X->stage_of[c] = X->ns;
         X->ns++;
       }

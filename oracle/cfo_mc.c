@@ -18,7 +18,8 @@
  *     b = clamp(ceil(B * (R_d / R_v)), 1, B), its share of the bottleneck's
  *     load;
  *   - an encoder or generator iteration is a static batch of b requests
- *     like this one: (k0 + k1 * (b * x)) + k2 * b; an LLM admits a request's
+ *     like this one: (k0 + k1 * (b * x)) + k2 * b (every iteration time
+ *     times the component's multiplier for the node's GPUs per executor); an LLM admits a request's
  *     prefill as soon as it arrives (with prefill priority the prefill batch
  *     holds the few requests that arrived during one iteration), so the
  *     prefill is this request alone, (k0 + k1 * x) + k2, and the decode
@@ -121,18 +122,19 @@ int cfo_eval_mc(const cfo_model *m, const cfo_plans *pl, const int32_t *ids, int
           if (ready > start) start = ready;
         }
         const int b = beff[v][c];
+        const double tps = cfo_tp(m, c, P_AT(pl->node_gpus, v, P, p));
         uint64_t x = 0;
         for (int at = 0; at < CFO_NATTR; at++)
           if ((m->x_sel[c] >> at) & 1u) x += attr(tr, o, at);
         if (m->kind[c] != CFO_LLM) {
-          const double dur = (m->k0[c] + m->k1[c] * (double)((uint64_t)b * x)) + m->k2[c] * (double)b;
+          const double dur = tps * ((m->k0[c] + m->k1[c] * (double)((uint64_t)b * x)) + m->k2[c] * (double)b);
           fin[c] = start + dur;
           first[c] = fin[c];
         } else {
-          const double dur = (m->k0[c] + m->k1[c] * (double)x) + m->k2[c] * 1.0;
+          const double dur = tps * ((m->k0[c] + m->k1[c] * (double)x) + m->k2[c] * 1.0);
           uint64_t no = ((m->prefill_only[ty] >> c) & 1u) ? 1u : attr(tr, o, m->nout_attr[c]);
           nout[c] = no < 1 ? 1 : (int)no;
-          const double D = m->d0[c] + m->d1[c] * (double)b;
+          const double D = tps * (m->d0[c] + m->d1[c] * (double)b);
           dstep[c] = D;
           first[c] = start + dur;
           double e = first[c];

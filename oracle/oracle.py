@@ -43,6 +43,7 @@ class Model(C.Structure):
         ("len", (Dist * 4) * MAXT),
         ("slo", (C.c_double * 4) * MAXT),
         ("theta_num", C.c_uint32), ("theta_den", C.c_uint32),
+        ("tp_scale", (C.c_double * 8) * 8),
     ]
 
 
@@ -152,6 +153,9 @@ def make_model(mcfg):
         m.nout_attr[i] = ATTR[c.get("n_out", "out")]
         m.gate_src[i] = names[c["gate"]] if c.get("gate") else -1
         m.batch_cap[i] = int(c.get("batch_cap", 256))
+        tps = {int(g): float(v) for g, v in c.get("tp_scale", {}).items()}
+        for g in range(1, 9):
+            m.tp_scale[i][g - 1] = tps.get(g, 1.0)
     m.comm_s = float(mcfg["comm_s"])
     m.cpu_pre_s = float(mcfg.get("cpu_pre_s", 0.0))
     for t, ty in enumerate(mcfg["types"]):
