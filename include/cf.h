@@ -120,6 +120,12 @@ typedef struct cf_model_desc {
   cf_dist len[CF_MAX_TYPES][4];      /* prompt, out, aud_in_ms, aud_out_ms */
   double slo[CF_MAX_TYPES][4];       /* bounds on TTFT, TPOT, E2E, MEDIA (<=; +inf = none) */
   uint32_t theta_num, theta_den;     /* attainment threshold (e.g. 9/10) */
+  /* Latency multiplier of component c on executors of g GPUs (the tensor
+   * parallelism degree of the configuration space): every iteration time
+   * of c (batch, prefill, decode step) on such an executor is
+   * tp_scale[c][min(g, 8) - 1] times its latency model, the product
+   * rounded once; CPU preprocessing is not scaled.  0 means 1. */
+  double tp_scale[CF_MAX_COMP][8];
 } cf_model_desc;
 
 /* Request trace: device arrays of n_seeds * n_req elements, seed-major. */

@@ -47,6 +47,7 @@ class cf_model_desc(C.Structure):
         ("img_hi", C.c_int32 * MAX_TYPES), ("patch_lo", C.c_int32), ("patch_hi", C.c_int32),
         ("len", (cf_dist * 4) * MAX_TYPES), ("slo", (C.c_double * 4) * MAX_TYPES),
         ("theta_num", C.c_uint32), ("theta_den", C.c_uint32),
+        ("tp_scale", (C.c_double * 8) * MAX_COMP),
     ]
 
 
@@ -179,6 +180,10 @@ def model_desc(mcfg):
         d.nout_attr[i] = ATTR[c.get("n_out", "out")]
         d.gate_src[i] = idx[c["gate"]] if c.get("gate") else -1
         d.batch_cap[i] = int(c.get("batch_cap", 256))
+        for g, v in c.get("tp_scale", {}).items():  # GPUs per executor -> latency multiplier
+            if not 1 <= int(g) <= 8:
+                raise CfError("tp_scale keys are GPUs per executor, 1..8")
+            d.tp_scale[i][int(g) - 1] = float(v)
     d.comm_s = float(mcfg["comm_s"])
     d.cpu_pre_s = float(mcfg.get("cpu_pre_s", 0.0))
     for t, ty in enumerate(mcfg["types"]):

@@ -65,6 +65,14 @@ cf_status lower_model(const cf_model_desc *d, KModel *k) {
     return set_error(CF_EINVAL, "comm_s and cpu_pre_s must be finite and >= 0");
   k->comm = d->comm_s;
   k->cpu_pre = d->cpu_pre_s;
+  k->tp_any = 0;
+  for (int c = 0; c < CF_MAX_COMP; c++)
+    for (int g = 0; g < 8; g++) {
+      const double v = c < nc ? d->tp_scale[c][g] : 0.0;
+      if (!(v >= 0.0) || v > 1e300) return set_error(CF_EINVAL, "tp_scale[%d][%d] must be finite and >= 0", c, g);
+      k->tps[c][g] = v == 0.0 ? 1.0 : v;
+      if (k->tps[c][g] != 1.0) k->tp_any = 1;
+    }
   if (d->patch_lo < 0 || d->patch_hi < d->patch_lo || d->patch_hi > 16383)
     return set_error(CF_EINVAL, "patch range");
   k->patch_lo = d->patch_lo;

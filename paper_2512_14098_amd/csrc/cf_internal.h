@@ -41,6 +41,8 @@ struct KModel {
   double slo[CF_MAX_TYPES][4];
   uint32_t theta_num, theta_den;
   int32_t max_path;                          // most components on one path
+  double tps[CF_MAX_COMP][8];                // iteration-time multiplier on executors of g GPUs, [c][min(g,8)-1]
+  int32_t tp_any;                            // some multiplier is not 1
 };
 
 // Host: validate a descriptor and lower it.  Returns CF_OK or sets the

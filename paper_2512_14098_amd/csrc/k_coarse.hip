@@ -28,7 +28,10 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
   __shared__ double u_s[CF_MAX_NODES][kBlock];
   __shared__ uint16_t b_s[CF_MAX_NODES][kBlock];  // node batch
   __shared__ uint8_t c_s[CF_MAX_NODES][kBlock];   // node component set
+  __shared__ uint8_t g_s[CF_MAX_NODES][kBlock];   // node GPUs per executor, as min(g, 8) - 1
+  __shared__ double tps_s[CF_MAX_COMP][8];        // iteration-time multipliers by GPUs per executor
   const int tid = threadIdx.x;
+  if (tid < CF_MAX_COMP * 8) (&tps_s[0][0])[tid] = (&m.tps[0][0])[tid];
   if (tid < m.nt * m.nc) {
     const int t = tid / m.nc, c = tid % m.nc;
     const uint64_t *mo = moments + (size_t)t * 8;
@@ -70,6 +73,7 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
     }
     c_s[v][tid] = (uint8_t)cm;
     b_s[v][tid] = (uint16_t)b;
+    if (m.tp_any) g_s[v][tid] = (uint8_t)(gp[v] < 1 ? 0 : (gp[v] > 8 ? 7 : gp[v] - 1));
   }
   bool valid = nv >= 1 && nv <= CF_MAX_NODES;
   int execs = 0;
@@ -127,6 +131,8 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
           const double B = (double)(bn < m.cap[c] ? bn : m.cap[c]);
           double w = ((m.k0[c] / B) + m.k1[c] * ex_s[t][c]) + m.k2[c];
           if (m.kind[c] == CF_LLM) w = w + (en_s[t][c] - 1.0) * ((m.d0[c] / B) + m.d1[c]);
+          // on executors of g GPUs every iteration takes tp_scale times as long
+          if (m.tp_any) w = tps_s[c][g_s[v][tid]] * w;
           u_s[v][tid] = u_s[v][tid] + pq * w;
         }
       }

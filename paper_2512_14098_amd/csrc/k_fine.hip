@@ -109,7 +109,7 @@ struct Layout {
 struct FineArgs {
   KModel m;
   int P;
-  const uint8_t *n_nodes, *node_comp, *node_rep, *n_alt, *alt_w, *alt_node;
+  const uint8_t *n_nodes, *node_comp, *node_rep, *node_gpus, *n_alt, *alt_w, *alt_node;
   const uint16_t *node_batch;
   const int32_t *plan_ids;
   int n_plans;
@@ -154,6 +154,7 @@ struct WaveShared {
   uint32_t ex_st[CF_MAX_EXEC];  // busy:1 ran:1 kind:2 rr:4 cur:4 nmem:9
   uint16_t ex_first[CF_MAX_EXEC];
   uint8_t ex_ns[CF_MAX_EXEC], ex_node[CF_MAX_EXEC];
+  uint8_t ex_tp[CF_MAX_EXEC];  // GPUs per executor as min(g, 8) - 1 (iteration-time multiplier index)
   uint8_t route[CF_MAX_TYPES][2][CF_MAX_COMP];
   uint8_t nalt[CF_MAX_TYPES], aw[CF_MAX_TYPES][2];
   uint8_t vbase[CF_MAX_NODES + 1], vrep[CF_MAX_NODES], vminc[CF_MAX_NODES], vcomp[CF_MAX_NODES];
@@ -893,6 +894,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     }
     xs = dpp_sum_u32(xs);
     dur = (m.k0[c] + m.k1[c] * (double)xs) + m.k2[c] * (double)n;
+    if (m.tp_any) dur = m.tps[c][sh.ex_tp[x]] * dur;
     if (S.si.flags[si] & SF_ENC) {
       const bool ran = (sh.ex_st[x] >> 1) & 1u;
       if (!ran || sh.ex_last[x] < S.now) dur = dur + m.cpu_pre;
@@ -901,6 +903,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
   } else if (!(S.si.flags[si] & SF_GATED)) {
     const int rn = S.si.rn[lx];
     dur = m.d0[c] + m.d1[c] * (double)rn;
+    if (m.tp_any) dur = m.tps[c][sh.ex_tp[x]] * dur;
     nmem = rn;
     // Decode run: while no input reaches this executor, its next steps are
     // decode steps of this stage with the same members, so the end of every
@@ -972,6 +975,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     }
     S.gmark_si = -1;
     dur = m.d0[c] + m.d1[c] * (double)cntm;
+    if (m.tp_any) dur = m.tps[c][sh.ex_tp[x]] * dur;
     nmem = (int)cntm;
     if constexpr (G) {
       if (S.si.flags[si] & SF_THINKER) {  // a gated stage that is also a gate source
@@ -1105,8 +1109,12 @@ __device__ __forceinline__ bool start_joint(Sim &S, int x, int lth, int sth, int
   WaveShared &sh = *S.sh;
   const int cth = S.si.comp[sth], cta = S.si.comp[sta];
   const int lx = S.si.lsi[sth], lg = S.si.lsi[sta];
-  const double d1 = m.d0[cth] + m.d1[cth] * (double)S.si.rn[lx];
-  const double d2 = m.d0[cta] + m.d1[cta] * (double)S.si.rn[lg];
+  double d1 = m.d0[cth] + m.d1[cth] * (double)S.si.rn[lx];
+  double d2 = m.d0[cta] + m.d1[cta] * (double)S.si.rn[lg];
+  if (m.tp_any) {
+    d1 = m.tps[cth][sh.ex_tp[x]] * d1;
+    d2 = m.tps[cta][sh.ex_tp[x]] * d2;
+  }
   if (!(d1 > 0.0) || !(d2 > 0.0)) return false;
   const uint32_t it0 = S.si.iter[lx];
   const uint32_t kth = S.si.minfin[lx] - it0;  // thinker steps up to its first finisher
@@ -1569,6 +1577,10 @@ __device__ bool setup_plan(Sim &S, int p) {
     for (int u = 0; u < v; u++) first += sh.vrep[u] * __popc(sh.vcomp[u]);
     first += (lane - sh.vbase[v]) * __popc(sh.vcomp[v]);
     sh.ex_node[lane] = (uint8_t)v;
+    if (m.tp_any) {
+      const uint32_t g = A.node_gpus[v * P + p];
+      sh.ex_tp[lane] = (uint8_t)(g < 1 ? 0 : (g > 8 ? 7 : g - 1));
+    }
     sh.ex_first[lane] = (uint16_t)first;
     sh.ex_ns[lane] = (uint8_t)__popc(sh.vcomp[v]);
     sh.ex_st[lane] = 15u << 4;  // idle, never ran, no stage run yet
@@ -1970,6 +1982,7 @@ extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_tabl
   a.n_nodes = plans->n_nodes_dev;
   a.node_comp = plans->node_comp_dev;
   a.node_rep = plans->node_rep_dev;
+  a.node_gpus = plans->node_gpus_dev;
   a.node_batch = plans->node_batch_dev;
   a.n_alt = plans->n_alt_dev;
   a.alt_w = plans->alt_w_dev;

@@ -132,6 +132,8 @@ __global__ void __launch_bounds__(kOrdThreads) k_mc_order(KModel m, McView V, ui
 
 __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
   __shared__ uint8_t vcomp[CF_MAX_NODES], vrep[CF_MAX_NODES], vminc[CF_MAX_NODES], vbase[CF_MAX_NODES];
+  __shared__ uint8_t vtp[CF_MAX_NODES];            // GPUs per executor, as min(g, 8) - 1
+  __shared__ double tps_s[CF_MAX_COMP][8];         // iteration-time multipliers by GPUs per executor
   __shared__ uint16_t vbatch[CF_MAX_NODES];
   __shared__ uint16_t beff[CF_MAX_NODES][CF_MAX_COMP];
   __shared__ uint8_t route[CF_MAX_TYPES][2][CF_MAX_COMP];
@@ -166,6 +168,7 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
     th_s[lane] = m.th_c[lane];
   }
   if (lane < CF_MAX_TYPES * 4) (&slo_s[0][0])[lane] = (&m.slo[0][0])[lane];
+  (&tps_s[0][0])[lane] = (&m.tps[0][0])[lane];
   const int hw = V.nb + 1;  // histogram row width
   if (V.hist)
     for (int q = lane; q < m.nt * hw; q += 64) hist_s[q] = 0;
@@ -193,6 +196,8 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
     vcomp[lane] = lane < nv ? V.node_comp[lane * P + p] : 0;
     vrep[lane] = lane < nv ? V.node_rep[lane * P + p] : 0;
     vbatch[lane] = lane < nv ? V.node_batch[lane * P + p] : 0;
+    const uint32_t g = lane < nv ? V.node_gpus[lane * P + p] : 1u;
+    vtp[lane] = (uint8_t)(g < 1 ? 0 : (g > 8 ? 7 : g - 1));
   }
   if (in_range) {
     for (int j = lane; j < CF_MAX_TYPES * 2 * CF_MAX_COMP; j += 64) (&route[0][0][0])[j] = V.alt_node[j * P + p];
@@ -243,6 +248,7 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
             const double B = (double)(bn < m.cap[c] ? bn : m.cap[c]);
             double w = ((m.k0[c] / B) + m.k1[c] * ex_s[t][c]) + m.k2[c];
             if (m.kind[c] == CF_LLM) w = w + (en_s[t][c] - 1.0) * ((m.d0[c] / B) + m.d1[c]);
+            if (m.tp_any) w = tps_s[c][vtp[v]] * w;
             u_s[v] = u_s[v] + pq * w;
           }
         }
@@ -315,18 +321,22 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
           start = ready > start ? ready : start;
         }
         const int b = beff[v][c];
+        const double tps = tps_s[c][vtp[v]];
         uint32_t x = 0;
         for (uint32_t sel = m.xsel[c]; sel; sel &= sel - 1) x += mc_attr(q, __ffs(sel) - 1);
         if (m.kind[c] != CF_LLM) {
-          const double dur = (m.k0[c] + m.k1[c] * (double)((uint64_t)b * x)) + m.k2[c] * (double)b;
+          double dur = (m.k0[c] + m.k1[c] * (double)((uint64_t)b * x)) + m.k2[c] * (double)b;
+          if (m.tp_any) dur = tps * dur;
           fin[c] = start + dur;
           first[c] = fin[c];
         } else {
-          const double dur = (m.k0[c] + m.k1[c] * (double)x) + m.k2[c] * 1.0;
+          double dur = (m.k0[c] + m.k1[c] * (double)x) + m.k2[c] * 1.0;
+          if (m.tp_any) dur = tps * dur;
           uint32_t no = ((pfo >> c) & 1u) ? 1u : mc_attr(q, m.nout_attr[c]);
           no = no < 1 ? 1u : no;
           nout[c] = (int)no;
-          const double D = m.d0[c] + m.d1[c] * (double)b;
+          double D = m.d0[c] + m.d1[c] * (double)b;
+          if (m.tp_any) D = tps * D;
           dstep[c] = D;
           first[c] = start + dur;
           double e = first[c];
