@@ -291,7 +291,7 @@ def enum_bench(args):
         cf.cf_eval_coarse(desc, out, mom[0], N)
     torch.cuda.synchronize()
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-    enum_ms, coarse_ms = [], []
+    enum_ms, coarse_ms, fused_ms = [], [], []
     t0 = time.perf_counter()
     for s0 in starts:
         ev[0].record()
@@ -303,6 +303,13 @@ def enum_bench(args):
         enum_ms.append(ev[0].elapsed_time(ev[1]))
         coarse_ms.append(ev[1].elapsed_time(ev[2]))
     elapsed = time.perf_counter() - t0
+    # the fused path: phase 1 of the same plans without writing their table
+    for s0 in starts:
+        ev[0].record()
+        cf.cf_enum_screen(desc, opts, ldev, offsets, total, s0, chunk, mom[0], N)
+        ev[1].record()
+        torch.cuda.synchronize()
+        fused_ms.append(ev[0].elapsed_time(ev[1]))
     e_s = sum(enum_ms) / len(enum_ms) / 1e3
     achieved = ENUM_PLAN_BYTES * chunk / e_s
     res = {"metric": "physical plans enumerated (Alg. 1, Eq. 1) and screened (phase 1)/sec, 1 GPU",
@@ -314,7 +321,8 @@ def enum_bench(args):
                                                                          chunk, len(starts)),
                       "logical_plans": int(len(logical)), "physical_plans": total, "logical_host_s": t_logical,
                       "enum_ms": enum_ms, "coarse_ms": coarse_ms, "enum_plans_per_s": chunk / e_s,
-                      "enum_coarse_plans_per_s": chunk / ((sum(enum_ms) + sum(coarse_ms)) / len(enum_ms) / 1e3)},
+                      "enum_coarse_plans_per_s": chunk / ((sum(enum_ms) + sum(coarse_ms)) / len(enum_ms) / 1e3),
+                      "fused_ms": fused_ms, "fused_plans_per_s": chunk / (sum(fused_ms) / len(fused_ms) / 1e3)},
            "roofline": {"bound": "hbm", "achieved": achieved / 1e9, "peak": 8000.0, "unit": "GB/s",
                         "frac": achieved / 8.0e12,
                         "traffic": ENUM_MEASURED_TRAFFIC.get((kernel_source_id(ENUM_KERNEL_SOURCES), chunk)),

@@ -358,6 +358,18 @@ cf_status cf_goodput_reduce(const uint32_t *met_dev, const uint32_t *cnt_dev, in
                             int32_t *kstar_dev, double *goodput_t_dev, double *goodput_dev,
                             void *stream);
 
+/* Enumeration fused with phase 1: for physical plans first .. first+count-1
+ * (numbered as cf_enum_plans numbers them), exactly what cf_eval_coarse
+ * writes for those plans' table columns -- rd_dev[count], bottleneck_dev
+ * [count], flags_dev[count] (device) -- without writing the plan table.
+ * moments_dev: the [T][8] per-type moments of one trace seed; n_gpus: the
+ * budget for the over-budget flag.  Asynchronous on stream.
+ * Errors: those of cf_enum_plans and cf_eval_coarse. */
+cf_status cf_enum_screen(const cf_model_desc *model, const cf_enum_opts *opts, const cf_logical *logical_dev,
+                         int32_t n_logical, const uint64_t *offsets_dev, uint64_t total, uint64_t first,
+                         int32_t count, const uint64_t *moments_dev, int32_t n_gpus, double *rd_dev,
+                         int32_t *bottleneck_dev, uint8_t *flags_dev, void *stream);
+
 /* Phase 3 with rate bisection (the workload descriptions bisect rates over
  * a grid; Alg. 2 phase 3 simulates each plan at its rate): for plan
  * plan_ids_dev[i] and its grid rates_dev[i][0..K), lo = -1 and hi = K;

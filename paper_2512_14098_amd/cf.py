@@ -101,6 +101,7 @@ def _load():
         "cf_goodput_curve": ([vp, vp, i32, i32, i32, i32, i32, vp, C.c_uint32, C.c_uint32, i32, vp, vp, vp, vp],
                              i32),
         "cf_eval_bisect": ([vp, vp, vp, i32, vp, i32, vp, C.c_uint32, C.c_uint32, vp, vp, vp, vp, vp, vp, vp], i32),
+        "cf_enum_screen": ([vp, vp, vp, i32, vp, C.c_uint64, C.c_uint64, i32, vp, i32, vp, vp, vp, vp], i32),
         "cf_enum_logical": ([vp, vp, vp, i32, vp], i32),
         "cf_enum_count": ([vp, vp, vp, i32, vp, vp, vp], i32),
         "cf_enum_plans": ([vp, vp, vp, i32, vp, C.c_uint64, C.c_uint64, i32, vp, vp], i32),
@@ -119,7 +120,7 @@ def _load():
 _lib = _load()
 EXPORTED = ("cf_last_error", "cf_status_str", "cf_version", "cf_trace_gen", "cf_eval_coarse",
             "cf_select_topk", "cf_rate_grid", "cf_eval_fine", "cf_eval_bisect", "cf_eval_mc", "cf_eval_mc_curve", "cf_goodput_curve", "cf_pareto",
-            "cf_enum_logical", "cf_enum_count", "cf_enum_plans",
+            "cf_enum_logical", "cf_enum_count", "cf_enum_plans", "cf_enum_screen",
             "cf_goodput_reduce", "cf_select_best", "cf_math_eval", "cf_philox_eval", "cf_release_scratch")
 
 
@@ -498,6 +499,19 @@ def cf_enum_plans(desc, opts, logical_dev, offsets, total, first, count, out=Non
                               int(logical_dev.shape[0]), _p(offsets), C.c_uint64(int(total)),
                               C.c_uint64(int(first)), int(count), C.byref(out.c), _stream()), "cf_enum_plans")
     return out
+
+
+def cf_enum_screen(desc, opts, logical_dev, offsets, total, first, count, moments_seed, n_gpus):
+    """Phase 1 of physical plans first..first+count-1 without their table: (rd, bottleneck, flags)."""
+    dev = logical_dev.device
+    rd = torch.empty(int(count), dtype=torch.float64, device=dev)
+    bott = torch.empty(int(count), dtype=torch.int32, device=dev)
+    flags = torch.empty(int(count), dtype=torch.uint8, device=dev)
+    _check(_lib.cf_enum_screen(C.byref(desc), C.byref(opts), _p(logical_dev.contiguous()), int(logical_dev.shape[0]),
+                               _p(offsets), C.c_uint64(int(total)), C.c_uint64(int(first)), int(count),
+                               _p(moments_seed.contiguous()), int(n_gpus), _p(rd), _p(bott), _p(flags), _stream()),
+           "cf_enum_screen")
+    return rd, bott, flags
 
 
 def cf_goodput_reduce(met, cnt, rates, theta, n_req):

@@ -9,6 +9,7 @@
 // bits.  Per-type means of X and of the output
 // length are computed once per block from the moments.
 #include "cf_internal.h"
+#include "cf_phase1.h"
 
 namespace cf {
 namespace {
@@ -32,23 +33,7 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
   __shared__ double tps_s[CF_MAX_COMP][8];        // iteration-time multipliers by GPUs per executor
   const int tid = threadIdx.x;
   if (tid < CF_MAX_COMP * 8) (&tps_s[0][0])[tid] = (&m.tps[0][0])[tid];
-  if (tid < m.nt * m.nc) {
-    const int t = tid / m.nc, c = tid % m.nc;
-    const uint64_t *mo = moments + (size_t)t * 8;
-    double ex = 0.0, en = 1.0;
-    if (mo[0] > 0) {
-      uint64_t xs = 0;
-      for (int a = 0; a < 7; a++)
-        if ((m.xsel[c] >> a) & 1u) xs += mo[1 + a];
-      ex = (double)xs / (double)mo[0];
-      if (m.kind[c] == CF_LLM && !((m.pfo[t] >> c) & 1u)) {
-        en = (double)mo[1 + m.nout_attr[c]] / (double)mo[0];
-        if (en < 1.0) en = 1.0;
-      }
-    }
-    ex_s[t][c] = ex;
-    en_s[t][c] = en;
-  }
+  phase1_means(m, moments, tid, ex_s, en_s);
   __syncthreads();
   const long long p = (long long)blockIdx.x * kBlock + tid;
   if (p >= pv.P) return;
@@ -127,12 +112,8 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
             valid = false;
             continue;
           }
-          const int bn = b_s[v][tid];
-          const double B = (double)(bn < m.cap[c] ? bn : m.cap[c]);
-          double w = ((m.k0[c] / B) + m.k1[c] * ex_s[t][c]) + m.k2[c];
-          if (m.kind[c] == CF_LLM) w = w + (en_s[t][c] - 1.0) * ((m.d0[c] / B) + m.d1[c]);
-          // on executors of g GPUs every iteration takes tp_scale times as long
-          if (m.tp_any) w = tps_s[c][g_s[v][tid]] * w;
+          const double w =
+              phase1_work(m, c, b_s[v][tid], ex_s[t][c], en_s[t][c], m.tp_any ? tps_s[c][g_s[v][tid]] : 1.0);
           u_s[v][tid] = u_s[v][tid] + pq * w;
         }
       }
@@ -144,34 +125,7 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
     flags[p] = CF_FLAG_INVALID;
     return;
   }
-  double best = __builtin_inf();
-  int bn = -1;
-  bool redundant = false;
-  uint64_t gpus = 0;
-#pragma unroll
-  for (int v = 0; v < CF_MAX_NODES; v++) {
-    if (v < nv) {
-      const double u = u_s[v][tid];
-      if (u > 0.0) {
-        const double r = (double)rep[v] / u;
-        if (r < best) { best = r; bn = v; }
-      }
-    }
-  }
-#pragma unroll
-  for (int v = 0; v < CF_MAX_NODES; v++) {
-    if (v < nv) {
-      const double u = u_s[v][tid];
-      gpus += (uint64_t)rep[v] * gp[v];
-      if (u == 0.0) redundant = true;
-      else if (rep[v] >= 2 && (double)(rep[v] - 1) / u >= best) redundant = true;
-    }
-  }
-  const bool over = gpus > (uint64_t)n_gpus;
-  rd[p] = best;
-  bott[p] = bn;
-  flags[p] = (uint8_t)(((!over && !redundant) ? CF_FLAG_KEEP : 0u) | (over ? CF_FLAG_OVER_BUDGET : 0u) |
-                       (redundant ? CF_FLAG_REDUNDANT : 0u));
+  phase1_result(nv, rep, gp, [&](int v) { return u_s[v][tid]; }, n_gpus, &rd[p], &bott[p], &flags[p]);
 #undef AT
 }
 

@@ -17,6 +17,7 @@
 //     are written slot-major, four plans per 32-bit store, so a wavefront
 //     fills 256 consecutive bytes of a slot row per store instruction.
 #include "cf_internal.h"
+#include "cf_phase1.h"
 
 #include <algorithm>
 #include <cstring>
@@ -336,6 +337,81 @@ __global__ void __launch_bounds__(256) k_enum_unrank(cf_enum_opts o, EnumView V,
   }
 }
 
+// Enumeration fused with phase 1: a thread numbers its plan, builds the
+// plan's nodes and routes in registers and LDS exactly as k_enum_unrank
+// would write them, and screens it as k_coarse would read them, writing only
+// R_d, the bottleneck and the flags (13 B per plan instead of the 233 B
+// table written and read back).
+constexpr int kScrBlock = 256;
+__global__ void __launch_bounds__(kScrBlock) k_enum_screen(cf_enum_opts o, EnumView V, const uint64_t *offsets,
+                                                          uint64_t first, int count, KModel m, const uint64_t *moments,
+                                                          int n_gpus, double *rd, int32_t *bott, uint8_t *flags) {
+  __shared__ OptsLds so;
+  __shared__ double ex_s[CF_MAX_TYPES][CF_MAX_COMP];
+  __shared__ double en_s[CF_MAX_TYPES][CF_MAX_COMP];
+  __shared__ double tps_s[CF_MAX_COMP][8];
+  __shared__ double u_s[CF_MAX_NODES][kScrBlock];
+  __shared__ uint16_t b_s[CF_MAX_NODES][kScrBlock];
+  __shared__ uint8_t g_s[CF_MAX_NODES][kScrBlock];
+  const int tid = threadIdx.x;
+  stage_opts(so, o, tid, blockDim.x);
+  if (tid < CF_MAX_COMP * 8) (&tps_s[0][0])[tid] = (&m.tps[0][0])[tid];
+  phase1_means(m, moments, tid, ex_s, en_s);
+  __syncthreads();
+  const int p = blockIdx.x * kScrBlock + tid;
+  if (p >= count) return;
+  Cursor cur = locate(V, offsets, first + (uint64_t)p, true);
+  const int nv = cur.nv;
+  uint32_t rep[CF_MAX_NODES], gp[CF_MAX_NODES];
+#pragma unroll
+  for (int v = 0; v < CF_MAX_NODES; v++) {
+    const NodeCfg nc = place(V, so, cur, v);
+    rep[v] = nc.rep;
+    gp[v] = nc.gpus;
+    b_s[v][tid] = nc.batch;
+    if (m.tp_any) g_s[v][tid] = (uint8_t)(nc.gpus < 1 ? 0 : (nc.gpus > 8 ? 7 : nc.gpus - 1));
+    u_s[v][tid] = 0.0;
+  }
+  if (!cur.ok || nv < 1) {
+    rd[p] = 0.0;
+    bott[p] = -1;
+    flags[p] = CF_FLAG_INVALID;
+    return;
+  }
+  const cf_logical &L = V.logical[cur.l];
+  const double wsum = (double)m.wsum;
+  int i2 = 0;
+  for (int t = 0; t < m.nt; t++) {
+    const uint32_t path = m.path[t];
+    const uint32_t na = L.n_alt[t];
+    uint32_t wl[2] = {10u, 0u};
+    if (na == 2) {
+      wl[0] = (cur.w >> (4 * i2)) & 15u;
+      wl[1] = 10u - wl[0];
+      i2++;
+    }
+    const double pi = (double)m.weight[t] / wsum;
+    const uint32_t wtot = na > 1 ? wl[0] + wl[1] : 1u;
+#pragma unroll
+    for (int a = 0; a < 2; a++) {
+      if (a < (int)na) {
+        const uint32_t wa = na > 1 ? wl[a] : 1u;
+        const double q = (double)wa / (double)wtot;
+        const double pq = pi * q;
+#pragma unroll
+        for (int c = 0; c < CF_MAX_COMP; c++) {
+          if (!((path >> c) & 1u)) continue;
+          const int v = L.alt_node[t][a][c];
+          const double w =
+              phase1_work(m, c, b_s[v][tid], ex_s[t][c], en_s[t][c], m.tp_any ? tps_s[c][g_s[v][tid]] : 1.0);
+          u_s[v][tid] = u_s[v][tid] + pq * w;
+        }
+      }
+    }
+  }
+  phase1_result(nv, rep, gp, [&](int v) { return u_s[v][tid]; }, n_gpus, &rd[p], &bott[p], &flags[p]);
+}
+
 cf_status run_tables(const cf_enum_opts *opts, const cf_logical *logical_dev, int n_logical, uint64_t **tab_out,
                      uint64_t **totals_out, hipStream_t s) {
   cf_status st = CF_OK;
@@ -548,4 +624,32 @@ extern "C" cf_status cf_enum_plans(const cf_model_desc *model, const cf_enum_opt
   hipLaunchKernelGGL(k_enum_unrank, dim3((threads + 255) / 256), dim3(256), 0, s, *opts, V, offsets_dev, first,
                      count, o);
   return hip_check(hipGetLastError(), "cf_enum_plans launch");
+}
+
+extern "C" cf_status cf_enum_screen(const cf_model_desc *model, const cf_enum_opts *opts, const cf_logical *logical_dev,
+                                    int32_t n_logical, const uint64_t *offsets_dev, uint64_t total, uint64_t first,
+                                    int32_t count, const uint64_t *moments_dev, int32_t n_gpus, double *rd_dev,
+                                    int32_t *bottleneck_dev, uint8_t *flags_dev, void *stream) {
+  using namespace cf;
+  cf_status st = check_opts(model, opts);
+  if (st != CF_OK) return st;
+  KModel m;
+  if ((st = lower_model(model, &m)) != CF_OK) return st;
+  if (count < 0) return set_error(CF_EINVAL, "count < 0");
+  if (count == 0) return CF_OK;
+  if (n_logical < 1 || !logical_dev || !offsets_dev || !moments_dev || !rd_dev || !bottleneck_dev || !flags_dev)
+    return set_error(CF_EINVAL, "NULL argument");
+  if (first > total || (uint64_t)count > total - first) return set_error(CF_EINVAL, "first + count > total");
+  hipStream_t s = as_stream(stream);
+  uint64_t *tab = nullptr, *totals = nullptr;
+  if ((st = run_tables(opts, logical_dev, n_logical, &tab, &totals, s)) != CF_OK) return st;
+  EnumView V;
+  V.N = opts->n_gpus;
+  V.logical = logical_dev;
+  V.n_logical = n_logical;
+  V.tab = tab;
+  V.totals = totals;
+  hipLaunchKernelGGL(k_enum_screen, dim3((unsigned)((count + kScrBlock - 1) / kScrBlock)), dim3(kScrBlock), 0, s,
+                     *opts, V, offsets_dev, first, count, m, moments_dev, n_gpus, rd_dev, bottleneck_dev, flags_dev);
+  return hip_check(hipGetLastError(), "cf_enum_screen launch");
 }

@@ -115,3 +115,35 @@ def test_enumerated_plans_screen_like_the_oracle(cf):
     assert np.array_equal(rd.cpu().numpy(), want[0])
     assert np.array_equal(fl.cpu().numpy(), want[2])
     assert not np.any(fl.cpu().numpy() & 6)  # none invalid or over budget
+
+
+@pytest.mark.parametrize("name,N,extra", [("c1", 8, {}), ("c2", 16, {}),
+                                          ("c2", 16, {"gpus": {"E_img": [1, 2], "E_aud": [1], "L_th": [1, 2, 4],
+                                                               "L_ta": [1, 2], "G": [1]}})])
+def test_enum_screen_fused_equals_table_path(cf, name, N, extra):
+    """Phase 1 of enumerated plans without their table: identical to cf_eval_coarse on the
+    enumerated table and to the oracle on its own enumeration, over windows of the space."""
+    _say(f"enum screen {name} {bool(extra)}")
+    cfg = load_config(name)
+    mc = dict(cfg["model"])
+    if extra:
+        mc["components"] = [dict(c, tp_scale={"2": 0.55, "4": 0.3}) for c in mc["components"]]
+    spec = {"k_s": 2, "share": True, "batch": {c["name"]: KNOBS for c in mc["components"]}}
+    spec.update(extra)
+    desc, opts = cf.model_desc(mc), cf.enum_opts(mc, spec, N)
+    ldev = torch.from_numpy(cf.cf_enum_logical(desc, opts)).cuda()
+    offsets, total = cf.cf_enum_count(desc, opts, ldev)
+    m, oo = O.make_model(mc), O.enum_opts(mc, spec, N)
+    Ls = O.enum_logical(m, oo)
+    tr, mom = cf.cf_trace_gen(desc, [0], 3000)
+    mom_h = mom[0].cpu().numpy().view(np.uint64)
+    for first in (0, total // 5, total - 7000):
+        cnt = min(7000, total - first)
+        rd, bn, fl = cf.cf_enum_screen(desc, opts, ldev, offsets, total, first, cnt, mom[0], N)
+        plans = cf.cf_enum_plans(desc, opts, ldev, offsets, total, first, cnt)
+        rd2, bn2, fl2 = cf.cf_eval_coarse(desc, plans, mom[0], N)
+        assert np.array_equal(rd.cpu().numpy(), rd2.cpu().numpy())
+        assert np.array_equal(bn.cpu().numpy(), bn2.cpu().numpy())
+        assert np.array_equal(fl.cpu().numpy(), fl2.cpu().numpy())
+        want = O.eval_coarse(m, O.enum_plans(m, oo, Ls, first, cnt), mom_h, N)
+        assert np.array_equal(rd.cpu().numpy(), want[0]) and np.array_equal(fl.cpu().numpy(), want[2])
