@@ -40,7 +40,11 @@ MEASURED_TRAFFIC = {
      "screening of 10^6 sampled plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 "
      "requests (sample: first 250 of its 1000 selected plans, first 1 of its 64 seeds)"): 4.2482e12,
 }
-ENUM_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_enum.hip", "paper_2512_14098_amd/csrc/cf_internal.h")
+# VALU lane rate of the k_fine launch by rocprofv3 counters (SQ_INSTS_VALU x SQ_THREAD_CYCLES_VALU /
+# SQ_ACTIVE_INST_VALU / kernel time / PEAK_LANE_OPS), keyed like MEASURED_TRAFFIC
+MEASURED_LANE_FRAC = {}
+ENUM_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_enum.hip", "paper_2512_14098_amd/csrc/cf_internal.h",
+                       "paper_2512_14098_amd/csrc/cf_phase1.h")
 # bytes per k_enum_unrank launch of 2^25 plans (the write counter reads exactly the table bytes)
 ENUM_MEASURED_TRAFFIC = {("005cc5e0965d8685", 1 << 25): 7.8190e9}
 MC_MEASURED_TRAFFIC = {
@@ -495,6 +499,9 @@ def main():
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_LANE_OPS, "unit": "TOP/s",
                      "frac": achieved / PEAK_LANE_OPS,
                      "traffic": MEASURED_TRAFFIC.get((kernel_source_id(), workload)),
+                     # the same kernel's VALU lane rate by the counters (instructions x active
+                     # lanes / time) as a fraction of the same peak, for this source and workload
+                     "counter_valu_lane_frac": MEASURED_LANE_FRAC.get((kernel_source_id(), workload)),
                      "kernel": "k_fine", "ops_per_event": OPS_PER_EVENT,
                      "kernel_ms": sum(fine_ms) / len(fine_ms)},
     }
