@@ -34,22 +34,28 @@ MC_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_mc.hip", "paper_2512_14098_amd
 # source the counters were taken on and the workload (with its sample); any other source or
 # workload reports null
 MEASURED_TRAFFIC = {
-    ("f354693d35f4b610", "c1: MLLM graph E->L on 8 simulated GPUs (7B LLM, 600M ViT); ~1000 plans; "
-     "16-point rate grid; 32 seeds x 10000 requests"): 2.1135e12,
-    ("f354693d35f4b610", "c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse "
+    ("23c58bc812fa441f", "c1: MLLM graph E->L on 8 simulated GPUs (7B LLM, 600M ViT); ~1000 plans; "
+     "16-point rate grid; 32 seeds x 10000 requests"): 2.0510e12,
+    ("23c58bc812fa441f", "c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse "
      "screening of 10^6 sampled plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 "
-     "requests (sample: first 250 of its 1000 selected plans, first 1 of its 64 seeds)"): 4.2482e12,
+     "requests (sample: first 250 of its 1000 selected plans, first 1 of its 64 seeds)"): 4.0341e12,
 }
 # VALU lane rate of the k_fine launch by rocprofv3 counters (SQ_INSTS_VALU x SQ_THREAD_CYCLES_VALU /
 # SQ_ACTIVE_INST_VALU / kernel time / PEAK_LANE_OPS), keyed like MEASURED_TRAFFIC
-MEASURED_LANE_FRAC = {}
+MEASURED_LANE_FRAC = {
+    ("23c58bc812fa441f", "c1: MLLM graph E->L on 8 simulated GPUs (7B LLM, 600M ViT); ~1000 plans; "
+     "16-point rate grid; 32 seeds x 10000 requests"): 0.422,
+    ("23c58bc812fa441f", "c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse "
+     "screening of 10^6 sampled plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 "
+     "requests (sample: first 250 of its 1000 selected plans, first 1 of its 64 seeds)"): 0.181,
+}
 ENUM_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_enum.hip", "paper_2512_14098_amd/csrc/cf_internal.h",
                        "paper_2512_14098_amd/csrc/cf_phase1.h")
 # bytes per k_enum_unrank launch of 2^25 plans (the write counter reads exactly the table bytes)
-ENUM_MEASURED_TRAFFIC = {("005cc5e0965d8685", 1 << 25): 7.8190e9}
+ENUM_MEASURED_TRAFFIC = {("960f3fbf7af75a5d", 1 << 25): 7.8190e9}
 MC_MEASURED_TRAFFIC = {
-    ("6c5ec9b2b6f241d8", "c4 phase 2: the 17444 plans phase 1 keeps of 1000000, 1024 sampled requests (seed 0), "
-     "alpha 0.8, then Pareto pruning"): 3.7078e8,
+    ("dfdb2b4408dfe475", "c4 phase 2: the 17444 plans phase 1 keeps of 1000000, 1024 sampled requests (seed 0), "
+     "alpha 0.8, then Pareto pruning"): 3.7237e8,
 }
 
 
