@@ -17,7 +17,9 @@
 // whose state changed since it went idle may start one iteration.
 //
 // Memory: the plan, executor state and every stage's queue / running-set
-// descriptor live in LDS (sized per launch from the largest plan); queue
+// descriptor live in LDS (sized per launch from the largest plan), except
+// that k_fine<true> keeps its executors' times in registers (lane x for
+// executor x) to leave more LDS per CU to its larger stage tables; queue
 // entries (chunked lists in a per-wavefront pool), running slots and the
 // 16-byte per-request records live in HBM.  The members of a completed
 // iteration are processed lane-parallel, 64 at a time: delay-line appends,
@@ -146,11 +148,7 @@ struct ModelLds {
 };
 
 struct WaveShared {
-  double ex_tend[CF_MAX_EXEC];
-  double ex_last[CF_MAX_EXEC];
-  double ex_t0[CF_MAX_EXEC];    // decode run: start of its first step
-  double ex_dur[CF_MAX_EXEC];   // decode run: duration of every step
-  uint32_t ex_itgt[CF_MAX_EXEC];  // decode run: step counter of its stage at ex_tend
+  uint32_t ex_itgt[CF_MAX_EXEC];  // decode run: step counter of its stage at the end of the running step
   uint32_t ex_st[CF_MAX_EXEC];  // busy:1 ran:1 kind:2 rr:4 cur:4 nmem:9
   uint16_t ex_first[CF_MAX_EXEC];
   uint8_t ex_ns[CF_MAX_EXEC], ex_node[CF_MAX_EXEC];
@@ -182,6 +180,16 @@ constexpr size_t kSiBytes = 1 + 1 + 1 + 1 + 2 + 2 + 4 * 7;
 // k_fine<true>: bytes per stage instance, per LLM stage instance, per thinker slot
 constexpr size_t kSiBytesG = 4 * 3 + 2 * 2 + 4, kLlmBytesG = 4 * 4 + 2, kThBytesG = 8 + 4;
 static_assert(sizeof(WaveShared) % 8 == 0, "the dynamic LDS table after WaveShared holds 8-byte words");
+// a wavefront's static LDS: k_fine<false> also holds the executors' times
+template <bool G>
+struct WaveLds {
+  double xt[4 * CF_MAX_EXEC];
+  WaveShared w;
+};
+template <>
+struct WaveLds<true> {
+  WaveShared w;
+};
 
 template <bool G>
 __device__ __forceinline__ int lx_of(const SiLds &si, int s) {
@@ -197,6 +205,13 @@ __device__ __forceinline__ uint64_t ru64(uint64_t v) {
 }
 __device__ __forceinline__ double rdb(double v) {
   return __longlong_as_double((long long)ru64((uint64_t)__double_as_longlong(v)));
+}
+// the value lane x holds (x wave-uniform)
+__device__ __forceinline__ double lane_val(double v, int x) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, x);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), x);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 __device__ __forceinline__ uint32_t lanes_below(uint64_t bal) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
@@ -286,13 +301,58 @@ struct Sim {
   int pool_top, pool_fresh, n_done, nx, lat_slot;
   uint32_t *hrow;      // this triple's histogram rows, or null
   bool remote_gate;
-  // k_fine<true>
-  double *wake;        // per executor with a gated stage: next visibility time of a blocked request
-  double *dur2;        // per executor in a joint run: duration of its talker steps
+  // Per-executor times: end of the running iteration, end of the last one,
+  // and for a decode run the start of its first step and the duration of
+  // every step.  k_fine<false> keeps them in LDS (xt, [4][CF_MAX_EXEC]);
+  // k_fine<true> keeps them in registers, lane x holding executor x, which
+  // leaves its LDS to the stage table that bounds its occupancy.
+  double *xt;
+  double r_tend, r_last, r_t0, r_dur;
+  // k_fine<true>, lane x for executor x
+  double r_wake;       // next visibility time of a blocked request of a gated stage
+  double r_dur2;       // in a joint run: duration of its talker steps
   uint64_t rewake;     // executors whose wake time is to be recomputed in this instant
   int gmark_si;        // gated stage whose running slots runnable_kind has just marked (-1: none)
   uint32_t gmark_n;    // the number of slots it marked eligible
 };
+
+enum { XT_END = 0, XT_LAST = 1, XT_T0 = 2, XT_DUR = 3 };
+template <int F>
+__device__ __forceinline__ double &xt_reg(Sim &S) {
+  if constexpr (F == XT_END) return S.r_tend;
+  else if constexpr (F == XT_LAST) return S.r_last;
+  else if constexpr (F == XT_T0) return S.r_t0;
+  else return S.r_dur;
+}
+template <int F>
+__device__ __forceinline__ double xt_regv(const Sim &S) {
+  if constexpr (F == XT_END) return S.r_tend;
+  else if constexpr (F == XT_LAST) return S.r_last;
+  else if constexpr (F == XT_T0) return S.r_t0;
+  else return S.r_dur;
+}
+// time F of executor x (x wave-uniform)
+template <bool G, int F>
+__device__ __forceinline__ double xt_get(const Sim &S, int x) {
+  if constexpr (G) return lane_val(xt_regv<F>(S), x);
+  else return S.xt[F * CF_MAX_EXEC + x];
+}
+// set time F of executor x to the wave-uniform v (every lane active)
+template <bool G, int F>
+__device__ __forceinline__ void xt_set(Sim &S, int x, double v) {
+  if constexpr (G) {
+    double &r = xt_reg<F>(S);
+    r = lane_id() == x ? v : r;
+  } else {
+    S.xt[F * CF_MAX_EXEC + x] = v;
+  }
+}
+// time F of the executor this lane holds
+template <bool G, int F>
+__device__ __forceinline__ double xt_own(const Sim &S) {
+  if constexpr (G) return xt_regv<F>(S);
+  else return S.xt[F * CF_MAX_EXEC + lane_id()];
+}
 
 __device__ __forceinline__ Rec rec_get(const Sim &S, uint32_t r) {
   CF_GLOBAL Rec &q = S.rec[r];
@@ -897,7 +957,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     if (m.tp_any) dur = m.tps[c][sh.ex_tp[x]] * dur;
     if (S.si.flags[si] & SF_ENC) {
       const bool ran = (sh.ex_st[x] >> 1) & 1u;
-      if (!ran || sh.ex_last[x] < S.now) dur = dur + m.cpu_pre;
+      if (!ran || xt_get<G, XT_LAST>(S, x) < S.now) dur = dur + m.cpu_pre;
     }
     nmem = n;
   } else if (!(S.si.flags[si] & SF_GATED)) {
@@ -935,10 +995,10 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
         S.si.sched[slot] = itgt;
       }
     }
-    sh.ex_t0[x] = S.now;
-    sh.ex_dur[x] = dur;
+    xt_set<G, XT_T0>(S, x, S.now);
+    xt_set<G, XT_DUR>(S, x, dur);
     sh.ex_itgt[x] = itgt;
-    sh.ex_tend[x] = tend;
+    xt_set<G, XT_END>(S, x, tend);
     sh.ex_st[x] = (sh.ex_st[x] & 2u) | 1u | ((uint32_t)kind << 2) | ((uint32_t)l << 4) | ((uint32_t)l << 8) |
                   ((uint32_t)nmem << 12) | (itgt > it0 + 1u ? EX_RUN : 0u);
     return;
@@ -986,7 +1046,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
       }
     }
   }
-  sh.ex_tend[x] = S.now + dur;
+  xt_set<G, XT_END>(S, x, S.now + dur);
   sh.ex_itgt[x] = S.si.iter[lx] + 1u;
   sh.ex_st[x] = (sh.ex_st[x] & 2u) | 1u | ((uint32_t)kind << 2) | ((uint32_t)l << 4) | ((uint32_t)l << 8) |
                 ((uint32_t)nmem << 12);
@@ -1128,11 +1188,11 @@ __device__ __forceinline__ bool start_joint(Sim &S, int x, int lth, int sth, int
     if ((i & 1u) && lane_id() == 0) h[(it0 + ((i + 1u) >> 1)) & (kRing - 1)] = t;
   }
   S.si.sched[slot] = it0 + ((n + 1u) >> 1);
-  sh.ex_t0[x] = S.now;
-  sh.ex_dur[x] = d1;
-  S.dur2[x] = d2;
+  xt_set<true, XT_T0>(S, x, S.now);
+  xt_set<true, XT_DUR>(S, x, d1);
+  S.r_dur2 = lane_id() == x ? d2 : S.r_dur2;
   sh.ex_itgt[x] = n;  // steps of the run, thinker first
-  sh.ex_tend[x] = t;
+  xt_set<true, XT_END>(S, x, t);
   const uint32_t lta = (uint32_t)(sta - sh.ex_first[x]);
   sh.ex_st[x] = (sh.ex_st[x] & 2u) | 1u | (IT_JOINT << 2) | ((uint32_t)lth << 4) | ((uint32_t)lth << 8) | EX_RUN |
                 (lta << 22);
@@ -1192,19 +1252,19 @@ template <bool G>
 __device__ void cut_run(Sim &S, int x) {
   WaveShared &sh = *S.sh;
   const uint32_t st = sh.ex_st[x];
-  if (!(st & EX_RUN) || !(sh.ex_tend[x] > S.now)) return;
+  if (!(st & EX_RUN) || !(xt_get<G, XT_END>(S, x) > S.now)) return;
   const int si = sh.ex_first[x] + ((st >> 8) & 15u);
   if constexpr (G) {
     if (((st >> 2) & 3u) == IT_JOINT) {
       const uint32_t n = sh.ex_itgt[x];
-      const double d1 = sh.ex_dur[x], d2 = S.dur2[x];
-      double t = sh.ex_t0[x] + d1;
+      const double d1 = xt_get<true, XT_DUR>(S, x), d2 = lane_val(S.r_dur2, x);
+      double t = xt_get<true, XT_T0>(S, x) + d1;
       uint32_t j = 1;
       while (t < S.now && j < n) {
         j++;
         t = t + ((j & 1u) ? d1 : d2);
       }
-      sh.ex_tend[x] = t;
+      xt_set<true, XT_END>(S, x, t);
       sh.ex_itgt[x] = j;
       if (j < n) {
         const int lx = S.si.lsi[si];
@@ -1218,11 +1278,11 @@ __device__ void cut_run(Sim &S, int x) {
   const int lx = lx_of<G>(S.si, si);
   const uint32_t it0 = S.si.iter[lx];
   const uint32_t itgt = sh.ex_itgt[x];
-  const double dur = sh.ex_dur[x];
+  const double dur = xt_get<G, XT_DUR>(S, x);
   uint32_t taken = 0;
-  const double t = run_walk(sh.ex_t0[x] + dur, dur, itgt - (it0 + 1u), S.now, &taken);
+  const double t = run_walk(xt_get<G, XT_T0>(S, x) + dur, dur, itgt - (it0 + 1u), S.now, &taken);
   const uint32_t j = it0 + 1u + taken;
-  sh.ex_tend[x] = t;
+  xt_set<G, XT_END>(S, x, t);
   sh.ex_itgt[x] = j;
   if (j <= it0 + 1u) sh.ex_st[x] = st & ~EX_RUN;
   if constexpr (G) {
@@ -1325,7 +1385,7 @@ __device__ __forceinline__ void complete_joint(Sim &S, int x, uint32_t st) {
   const uint32_t nth_s = (n + 1u) >> 1, nta_s = n >> 1;
   const uint32_t llast = (n & 1u) ? (uint32_t)lth : (uint32_t)lta;
   sh.ex_st[x] = (st & ~(1u | EX_RUN | (15u << 4) | (15u << 22))) | 2u | (llast << 4);
-  sh.ex_last[x] = S.now;
+  xt_set<true, XT_LAST>(S, x, S.now);
   S.dirty |= 1ull << x;
   // thinker
   const int lx = S.si.lsi[sth];
@@ -1387,7 +1447,7 @@ __device__ __forceinline__ void complete_iter(Sim &S, int x) {
   const int c = S.si.comp[si];
   const uint8_t fl = S.si.flags[si];
   sh.ex_st[x] = (st & ~(1u | EX_RUN)) | 2u;  // idle, has run
-  sh.ex_last[x] = S.now;
+  xt_set<G, XT_LAST>(S, x, S.now);
   S.dirty |= 1ull << x;
   if (kind == IT_BATCH || kind == IT_PREFILL) {
     S.events += (uint64_t)nmem;
@@ -1487,7 +1547,7 @@ __device__ __forceinline__ bool gate_wake(Sim &S, int y) {
     w = wave_min_time(w);
     now_el = __ballot(now_el) != 0;
   }
-  if (lane_id() == 0) S.wake[y] = w;
+  S.r_wake = lane_id() == y ? w : S.r_wake;  // w is wave-uniform here
   return now_el;
 }
 
@@ -1570,6 +1630,14 @@ __device__ bool setup_plan(Sim &S, int p) {
     }
   }
   // executors, one lane each
+  if constexpr (G) {
+    S.r_tend = __builtin_inf();
+    S.r_last = 0.0;
+    S.r_t0 = 0.0;
+    S.r_dur = 0.0;
+    S.r_wake = __builtin_inf();
+    S.r_dur2 = 0.0;
+  }
   if (lane < S.nx) {
     int v = 0;
     while (v + 1 < nv && sh.vbase[v + 1] <= lane) v++;
@@ -1584,12 +1652,13 @@ __device__ bool setup_plan(Sim &S, int p) {
     sh.ex_first[lane] = (uint16_t)first;
     sh.ex_ns[lane] = (uint8_t)__popc(sh.vcomp[v]);
     sh.ex_st[lane] = 15u << 4;  // idle, never ran, no stage run yet
-    sh.ex_tend[lane] = __builtin_inf();
-    sh.ex_last[lane] = 0.0;
-    sh.ex_t0[lane] = 0.0;
-    sh.ex_dur[lane] = 0.0;
+    if constexpr (!G) {
+      S.xt[XT_END * CF_MAX_EXEC + lane] = __builtin_inf();
+      S.xt[XT_LAST * CF_MAX_EXEC + lane] = 0.0;
+      S.xt[XT_T0 * CF_MAX_EXEC + lane] = 0.0;
+      S.xt[XT_DUR * CF_MAX_EXEC + lane] = 0.0;
+    }
     sh.ex_itgt[lane] = 0;
-    if constexpr (G) S.wake[lane] = __builtin_inf();
   }
   if constexpr (G) S.rewake = 0;
   // stage instances, one lane each (prefix sums give run-slot and ring offsets)
@@ -1664,7 +1733,8 @@ template <bool G>
 // k_fine<false> is held to 72 VGPRs (7 wavefronts per SIMD); k_fine<true>,
 // whose LDS table allows fewer wavefronts per CU, to 128.
 __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restrict__ Ap) {
-  __shared__ WaveShared sh;
+  __shared__ WaveLds<G> wl;
+  WaveShared &sh = wl.w;
   const FineArgs &A = *Ap;
   const KModel &m = A.m;
   const int lane = lane_id();
@@ -1710,11 +1780,7 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
       S.si.qtp = (uint8_t *)p; p += cap;
     }
   }
-  if constexpr (G) {
-    __shared__ double wake_lds[CF_MAX_EXEC], dur2_lds[CF_MAX_EXEC];
-    S.wake = wake_lds;
-    S.dur2 = dur2_lds;
-  }
+  if constexpr (!G) S.xt = wl.xt;
   // model tables for per-lane indexing
   for (int j = lane; j < CF_MAX_TYPES * CF_MAX_COMP; j += 64) {
     (&sh.ml.child[0][0])[j] = (&m.child[0][0])[j];
@@ -1791,10 +1857,10 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
       for (;;) {
         // --- next pending time
         double te = __builtin_inf();
-        if (lane < S.nx && (sh.ex_st[lane] & 1u)) te = sh.ex_tend[lane];
+        if (lane < S.nx && (sh.ex_st[lane] & 1u)) te = xt_own<G, XT_END>(S);
         if constexpr (G) {
           if (lane < S.nx) {
-            const double wk = S.wake[lane];
+            const double wk = S.r_wake;
             te = wk < te ? wk : te;
           }
         }
@@ -1809,11 +1875,11 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
         }
         // --- step 1: iterations ending at t, ascending executor
         if (te == t) {
-          uint64_t done = __ballot(lane < S.nx && (sh.ex_st[lane] & 1u) && sh.ex_tend[lane] == t);
+          uint64_t done = __ballot(lane < S.nx && (sh.ex_st[lane] & 1u) && xt_own<G, XT_END>(S) == t);
           if constexpr (G) {
             // wake times due: the executor examines its stages in step 3
-            const bool wk = lane < S.nx && S.wake[lane] == t;
-            if (wk) S.wake[lane] = __builtin_inf();
+            const bool wk = lane < S.nx && S.r_wake == t;
+            if (wk) S.r_wake = __builtin_inf();
             S.dirty |= __ballot(wk);
           }
           while (done) {
