@@ -33,21 +33,20 @@ MC_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_mc.hip", "paper_2512_14098_amd
 # WRITE_SIZE x 1.0, the scale factors a plain 1 GiB device copy gives), keyed by the kernel
 # source the counters were taken on and the workload (with its sample); any other source or
 # workload reports null
+_W_C1 = ("c1: MLLM graph E->L on 8 simulated GPUs (7B LLM, 600M ViT); ~1000 plans; 16-point rate grid; "
+         "32 seeds x 10000 requests")
+_W_C4_SEED0 = ("c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse screening of 10^6 "
+               "sampled plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 requests "
+               "(sample: first 1 of its 64 seeds)")
 MEASURED_TRAFFIC = {
-    ("23c58bc812fa441f", "c1: MLLM graph E->L on 8 simulated GPUs (7B LLM, 600M ViT); ~1000 plans; "
-     "16-point rate grid; 32 seeds x 10000 requests"): 2.0510e12,
-    ("23c58bc812fa441f", "c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse "
-     "screening of 10^6 sampled plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 "
-     "requests (sample: first 250 of its 1000 selected plans, first 1 of its 64 seeds)"): 4.0341e12,
+    ("790107b81d035f18", _W_C1): 2.1129e12,
+    ("790107b81d035f18", _W_C4_SEED0): 1.6472e13,
 }
 # VALU lane rate of the k_fine launch by rocprofv3 counters (SQ_INSTS_VALU x SQ_THREAD_CYCLES_VALU /
 # SQ_ACTIVE_INST_VALU / kernel time / PEAK_LANE_OPS), keyed like MEASURED_TRAFFIC
 MEASURED_LANE_FRAC = {
-    ("23c58bc812fa441f", "c1: MLLM graph E->L on 8 simulated GPUs (7B LLM, 600M ViT); ~1000 plans; "
-     "16-point rate grid; 32 seeds x 10000 requests"): 0.422,
-    ("23c58bc812fa441f", "c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse "
-     "screening of 10^6 sampled plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 "
-     "requests (sample: first 250 of its 1000 selected plans, first 1 of its 64 seeds)"): 0.181,
+    ("790107b81d035f18", _W_C1): 0.4215,
+    ("790107b81d035f18", _W_C4_SEED0): 0.2710,
 }
 ENUM_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_enum.hip", "paper_2512_14098_amd/csrc/cf_internal.h",
                        "paper_2512_14098_amd/csrc/cf_phase1.h")
