@@ -80,13 +80,15 @@ def test_fine_histograms_and_curves(cf, name, n_plans, seeds, n):
                 want[i, k, s] = O.latency_hist(des["lat"], otr["type"][s * n:(s + 1) * n], T, tg)
     assert np.array_equal(hist, want)
     # the histogram at the SLO bin equals the met counter; all bins sum to the count
-    cum = np.cumsum(hist, axis=-1).astype(np.uint32)
-    assert np.array_equal(cum[..., SCALES.index(1.0)], out["met"].cpu().numpy().view(np.uint32))
-    assert np.array_equal(cum[..., -1], out["cnt"].cpu().numpy().view(np.uint32))
-    # goodput against every target: the plain reduction of the cumulative counts, bin by bin
+    cum = np.cumsum(want, axis=-1).astype(np.uint32)  # the oracle's cumulative counts
+    assert np.array_equal(np.cumsum(hist, axis=-1).astype(np.uint32)[..., SCALES.index(1.0)],
+                          out["met"].cpu().numpy().view(np.uint32))
+    assert np.array_equal(np.cumsum(hist, axis=-1).astype(np.uint32)[..., -1],
+                          out["cnt"].cpu().numpy().view(np.uint32))
+    # goodput against every target: the plain reduction of the oracle's cumulative counts, bin by bin
     ks, gt, g = cf.cf_goodput_curve(out["hist"], out["cnt"], torch.from_numpy(rates).cuda(), (9, 10), n)
     ks, gt, g = ks.cpu().numpy(), gt.cpu().numpy(), g.cpu().numpy()
-    cnt = out["cnt"].cpu().numpy().view(np.uint32)
+    cnt = np.ascontiguousarray(cum[..., -1])
     for b in range(nb):
         wk, wgt, wg = O.goodput_reduce(np.ascontiguousarray(cum[..., b]), cnt, rates, (9, 10), n)
         assert np.array_equal(ks[:, b], wk) and np.array_equal(gt[:, b], wgt) and np.array_equal(g[:, b], wg), b

@@ -89,7 +89,7 @@ def test_coarse_select_grid_parity(cf, name):
     m = O.make_model(cfg["model"])
     desc = cf.model_desc(cfg["model"])
     tr, mom = cf.cf_trace_gen(desc, [0], 4000)
-    mom0 = mom[0].cpu().numpy().view(np.uint64)
+    mom0 = O.trace_gen(m, [0], 4000)["moments"][0]
     plans = cf.DevicePlans(tab)
     rd, bn, fl = cf.cf_eval_coarse(desc, plans, mom[0], cfg["gpus"])
     want = O.eval_coarse(m, tab, mom0, cfg["gpus"])
@@ -100,9 +100,10 @@ def test_coarse_select_grid_parity(cf, name):
         ids = cf.cf_select_topk(rd, fl, k).cpu().numpy()
         assert np.array_equal(ids, O.select_topk(want[0], want[2], k)), k
     ids = cf.cf_select_topk(rd, fl, min(tab.P, 65536))
+    ids_o = O.select_topk(want[0], want[2], min(tab.P, 65536))
     for K, alpha in ((16, 1.0), (32, 0.75)):
         got = cf.cf_rate_grid(rd, ids, K, alpha).cpu().numpy()
-        assert np.array_equal(got, O.rate_grid(want[0], ids.cpu().numpy(), K, alpha))
+        assert np.array_equal(got, O.rate_grid(want[0], ids_o, K, alpha))
 
 
 def test_coarse_invalid_and_over_budget(cf):
@@ -115,7 +116,8 @@ def test_coarse_invalid_and_over_budget(cf):
     desc = cf.model_desc(cfg["model"])
     _, mom = cf.cf_trace_gen(desc, [0], 500)
     rd, bn, fl = cf.cf_eval_coarse(desc, cf.DevicePlans(bad), mom[0], 2)
-    want = O.eval_coarse(O.make_model(cfg["model"]), bad, mom[0].cpu().numpy().view(np.uint64), 2)
+    m = O.make_model(cfg["model"])
+    want = O.eval_coarse(m, bad, O.trace_gen(m, [0], 500)["moments"][0], 2)
     assert np.array_equal(fl.cpu().numpy(), want[2])
     assert list(fl.cpu().numpy()) == [4, 2, 4]
 
@@ -200,6 +202,33 @@ def test_fine_parity_subsets(cf, name, n_plans, seeds, n, rate_step):
     ids = _subset(tab, n_plans, seed=len(name), kept=kept[: max(50, n_plans)])
     rates = O.rate_grid(rd, np.asarray(ids, np.int32), cfg["rates"]["grid"])[:, rate_step - 1::rate_step]
     g, want, _, _ = _fine_pair(cf, cfg, tab, ids, np.ascontiguousarray(rates), seeds, n)
+    _assert_fine_equal(g, want)
+    assert np.all(g["status"] == 0)
+
+
+def test_fine_c4_widest_selected_plans(cf):
+    """c4's top 1000 of 10^6 plans hold plans with 64 executors and 320 stage
+    instances, which size the stage table of the launch and use every lane of
+    the executor registers: the widest of them by stage instances, the next
+    with 64 executors and a median one, at every 8th rate of their grids."""
+    _say("fine c4 widest selected plans")
+    cfg = load_config("c4")
+    tab = make_plans(cfg)
+    m = O.make_model(cfg["model"])
+    n = 20000
+    mtr = O.trace_gen(m, [0], n)
+    rd, bn, fl = O.eval_coarse(m, tab, mtr["moments"][0], cfg["gpus"])
+    kept = O.select_topk(rd, fl, tab.P)[: cfg["top_k"]]
+    nx = np.array([int(tab.node_rep[: tab.n_nodes[p], p].astype(int).sum()) for p in kept])
+    nsi = np.array([sum(int(tab.node_rep[v, p]) * bin(int(tab.node_comp[v, p])).count("1")
+                        for v in range(tab.n_nodes[p])) for p in kept])
+    i1 = int(np.argmax(nsi))
+    i2 = next(int(i) for i in np.argsort(-nx, kind="stable") if i != i1)
+    i3 = int(np.argsort(nsi, kind="stable")[len(nsi) // 2])
+    ids = [int(kept[i]) for i in (i1, i2, i3)]
+    assert nsi[i1] == 320 and nx[i1] == 64 and nx[i2] == 64
+    rates = O.rate_grid(rd, np.asarray(ids, np.int32), cfg["rates"]["grid"])[:, 3::8]
+    g, want, _, _ = _fine_pair(cf, cfg, tab, ids, np.ascontiguousarray(rates), [0], n)
     _assert_fine_equal(g, want)
     assert np.all(g["status"] == 0)
 
@@ -380,15 +409,19 @@ def test_full_size_c1_sampled(cf):
     w = pipeline.Workload("c1")
     out = pipeline.run_step(w)
     torch.cuda.synchronize()
-    ids = out["ids"].cpu().numpy()
-    rates = out["rates"].cpu().numpy()
+    # the oracle's own phase 1, selection and rate grid choose the triples it simulates
+    m = O.make_model(w.cfg["model"])
+    ord_, _, ofl = O.eval_coarse(m, w.tab, O.trace_gen(m, [w.seeds[0]], w.n_req)["moments"][0], w.n_gpus)
+    ids = O.select_topk(ord_, ofl, w.top_k)
+    rates = O.rate_grid(ord_, ids, w.K, w.alpha_max)
+    assert np.array_equal(out["ids"].cpu().numpy(), ids)
+    assert np.array_equal(out["rates"].cpu().numpy(), rates)
     met = out["fine"]["met"].cpu().numpy().view(np.uint32)
     cnt = out["fine"]["cnt"].cpu().numpy().view(np.uint32)
     ev = out["fine"]["events"].cpu().numpy().view(np.uint64)
     st = out["fine"]["status"].cpu().numpy()
     assert np.all(st == 0)
     assert np.all(cnt.sum(axis=3) == w.n_req)
-    m = O.make_model(w.cfg["model"])
     rng = np.random.default_rng(42)
     samp = [(int(rng.integers(len(ids))), int(rng.integers(w.K)), int(rng.integers(len(w.seeds))))
             for _ in range(24)]
@@ -579,11 +612,12 @@ def test_bisect_parity(cf, name, n_plans, seeds, n):
     assert np.array_equal(got["n_eval"].cpu().numpy(), want[3])
     assert np.array_equal(got["events"].cpu().numpy().view(np.uint64), want[4])
     assert np.all(got["status"].cpu().numpy() == 0)
-    # the grid's answer where its feasibility is monotone
+    # the grid's answer where its feasibility (by the oracle's own simulation) is monotone
     g = cf.cf_eval_fine(desc, cf.DevicePlans(tab), torch.as_tensor(ids).cuda(), torch.from_numpy(rates).cuda(), tr)
     ks, gt, gg = cf.cf_goodput_reduce(g["met"], g["cnt"], torch.from_numpy(rates).cuda(), theta, n)
-    met = g["met"].cpu().numpy().view(np.uint32).astype(np.uint64).sum(axis=2)
-    cnt = g["cnt"].cpu().numpy().view(np.uint32).astype(np.uint64).sum(axis=2)
+    om, oc, _, _ = O.eval_fine(m, tab, ids, rates, otr)
+    met = om.astype(np.uint64).sum(axis=2)
+    cnt = oc.astype(np.uint64).sum(axis=2)
     feas = np.all((cnt == 0) | (theta[1] * met >= theta[0] * cnt), axis=2)
     for i in range(len(ids)):
         if np.all(np.diff(feas[i].astype(int)) <= 0):
