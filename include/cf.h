@@ -210,6 +210,22 @@ cf_status cf_eval_coarse(const cf_model_desc *model, const cf_plan_table *plans,
 cf_status cf_select_topk(const double *rd_dev, const uint8_t *flags_dev, int32_t P, int32_t k,
                          int32_t *ids_dev, int32_t *n_selected_host, void *stream);
 
+/* Running top-k over a plan space screened window by window (Alg. 2 phase 1
+ * keeps the plans with the largest R_d; cf_enum_screen screens one window of
+ * an enumerated space at a time).  Running list: rd_run_dev[n_run] and plan
+ * numbers gid_run_dev[n_run], in the order of cf_select_topk (R_d descending,
+ * ties by plan number ascending; R_d compared by its bits, as there).
+ * Window: ids_win_dev[n_win], the ids cf_select_topk returned for the
+ * window's rd_win_dev, plan number win_first + id.  Writes the first
+ * min(k, n_run + n_win) plans of the merged order to rd_out_dev[k] and
+ * gid_out_dev[k], which must not alias the running list.  The two lists
+ * must hold distinct plan numbers (windows that do not overlap).
+ * Asynchronous on stream.  Limits: 1 <= k <= 65536, 0 <= n_run, n_win <= 65536.
+ * Errors: CF_ECAPACITY (k), CF_EINVAL (sizes, NULL pointers, aliasing). */
+cf_status cf_topk_merge(const double *rd_run_dev, const uint64_t *gid_run_dev, int32_t n_run,
+                        const double *rd_win_dev, const int32_t *ids_win_dev, int32_t n_win, uint64_t win_first,
+                        int32_t k, double *rd_out_dev, uint64_t *gid_out_dev, void *stream);
+
 /* rates_dev[i][k] = (R_d[ids_dev[i]] * alpha_max * (k+1)) / K, i < n, k < K. */
 cf_status cf_rate_grid(const double *rd_dev, const int32_t *ids_dev, int32_t n, int32_t K,
                        double alpha_max, double *rates_dev, void *stream);

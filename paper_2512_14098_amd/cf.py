@@ -93,6 +93,7 @@ def _load():
         "cf_eval_coarse": ([vp, vp, vp, i32, vp, vp, vp, vp], i32),
         "cf_select_topk": ([vp, vp, i32, i32, vp, vp, vp], i32),
         "cf_rate_grid": ([vp, vp, i32, i32, dbl, vp, vp], i32),
+        "cf_topk_merge": ([vp, vp, i32, vp, vp, i32, C.c_uint64, i32, vp, vp, vp], i32),
         "cf_eval_fine": ([vp, vp, vp, i32, vp, i32, vp, u32, vp, vp], i32),
         "cf_goodput_reduce": ([vp, vp, i32, i32, i32, i32, vp, u32, u32, i32, vp, vp, vp, vp], i32),
         "cf_eval_mc": ([vp, vp, vp, i32, vp, vp, dbl, vp, i32, i32, vp, vp, vp, vp, vp], i32),
@@ -119,7 +120,8 @@ def _load():
 
 _lib = _load()
 EXPORTED = ("cf_last_error", "cf_status_str", "cf_version", "cf_trace_gen", "cf_eval_coarse",
-            "cf_select_topk", "cf_rate_grid", "cf_eval_fine", "cf_eval_bisect", "cf_eval_mc", "cf_eval_mc_curve", "cf_goodput_curve", "cf_pareto",
+            "cf_select_topk", "cf_topk_merge", "cf_rate_grid", "cf_eval_fine", "cf_eval_bisect", "cf_eval_mc",
+            "cf_eval_mc_curve", "cf_goodput_curve", "cf_pareto",
             "cf_enum_logical", "cf_enum_count", "cf_enum_plans", "cf_enum_screen",
             "cf_goodput_reduce", "cf_select_best", "cf_math_eval", "cf_philox_eval", "cf_release_scratch")
 
@@ -322,6 +324,19 @@ def cf_select_topk(rd, flags, k):
     _check(_lib.cf_select_topk(_p(rd), _p(flags), int(rd.numel()), int(k), _p(ids), C.byref(n),
                                _stream()), "cf_select_topk")
     return ids[:n.value]
+
+
+def cf_topk_merge(rd_run, gid_run, rd_win, ids_win, win_first, k):
+    """Running top-k of a space screened window by window: the first min(k, n_run + n_win)
+    plans of the merged order, as (rd float64, plan number int64) device tensors."""
+    dev = rd_win.device
+    n = min(int(k), int(rd_run.numel()) + int(ids_win.numel()))
+    rd = torch.empty(max(int(k), 1), dtype=torch.float64, device=dev)
+    gid = torch.empty(max(int(k), 1), dtype=torch.int64, device=dev)
+    _check(_lib.cf_topk_merge(_p(rd_run.contiguous()), _p(gid_run.contiguous()), int(rd_run.numel()), _p(rd_win),
+                              _p(ids_win.contiguous()), int(ids_win.numel()), C.c_uint64(int(win_first)), int(k),
+                              _p(rd), _p(gid), _stream()), "cf_topk_merge")
+    return rd[:n], gid[:n]
 
 
 def cf_rate_grid(rd, ids, K, alpha_max=1.0):

@@ -6,6 +6,11 @@
 // 96-bit value (bits of R_d, ~id): unique per plan, so the K largest keys
 // are found by an MSD radix select of 12 eight-bit digits, compacted, and
 // placed by rank (number of larger keys).
+//
+// cf_topk_merge keeps the top-K of a plan space screened window by window:
+// the window's selection and the running list are both in key order, so
+// each element's place in the merged list is its index in its own list plus
+// the number of elements of the other list ahead of it (a binary search).
 #include <cmath>
 
 #include "cf_internal.h"
@@ -126,6 +131,54 @@ __global__ void __launch_bounds__(256) k_sel_rank(const unsigned long long *khi,
   if (i < n) ids[rank] = (int32_t)(0xFFFFFFFFu - lo);
 }
 
+// (R_d bits, plan number) of a precedes b: larger R_d, or equal R_d and a
+// smaller plan number (the order of cf_select_topk, with 64-bit numbers)
+__device__ __forceinline__ bool key_ahead(unsigned long long ra, uint64_t ga, unsigned long long rb, uint64_t gb) {
+  return ra > rb || (ra == rb && ga < gb);
+}
+
+__global__ void k_topk_merge(const double *rd_run, const uint64_t *gid_run, int n_run, const double *rd_win,
+                             const int32_t *ids_win, int n_win, uint64_t first, int k, double *rd_out,
+                             uint64_t *gid_out) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_run + n_win) return;
+  const bool in_run = i < n_run;
+  const int own = in_run ? i : i - n_run;
+  double r;
+  uint64_t g;
+  if (in_run) {
+    r = rd_run[own];
+    g = gid_run[own];
+  } else {
+    const int32_t id = ids_win[own];
+    r = rd_win[id];
+    g = first + (uint64_t)id;
+  }
+  const unsigned long long rb = (unsigned long long)__double_as_longlong(r);
+  // elements of the other list ahead of this one: a prefix of that list
+  int lo = 0, hi = in_run ? n_win : n_run;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    unsigned long long ro;
+    uint64_t go;
+    if (in_run) {
+      const int32_t id = ids_win[mid];
+      ro = (unsigned long long)__double_as_longlong(rd_win[id]);
+      go = first + (uint64_t)id;
+    } else {
+      ro = (unsigned long long)__double_as_longlong(rd_run[mid]);
+      go = gid_run[mid];
+    }
+    if (key_ahead(ro, go, rb, g)) lo = mid + 1;
+    else hi = mid;
+  }
+  const int pos = own + lo;
+  if (pos < k) {
+    rd_out[pos] = r;
+    gid_out[pos] = g;
+  }
+}
+
 __global__ void k_rate_grid(const double *rd, const int32_t *ids, int n, int K, double alpha, double *rates) {
   const long long j = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= (long long)n * K) return;
@@ -183,4 +236,24 @@ extern "C" cf_status cf_rate_grid(const double *rd_dev, const int32_t *ids_dev, 
   hipLaunchKernelGGL(k_rate_grid, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, as_stream(stream), rd_dev,
                      ids_dev, n, K, alpha_max, rates_dev);
   return hip_check(hipGetLastError(), "cf_rate_grid launch");
+}
+
+extern "C" cf_status cf_topk_merge(const double *rd_run_dev, const uint64_t *gid_run_dev, int32_t n_run,
+                                   const double *rd_win_dev, const int32_t *ids_win_dev, int32_t n_win,
+                                   uint64_t win_first, int32_t k, double *rd_out_dev, uint64_t *gid_out_dev,
+                                   void *stream) {
+  using namespace cf;
+  if (k < 1 || k > 65536) return set_error(CF_ECAPACITY, "k out of 1..65536");
+  if (n_run < 0 || n_run > 65536 || n_win < 0 || n_win > 65536)
+    return set_error(CF_EINVAL, "n_run and n_win must be in 0..65536");
+  if (!rd_out_dev || !gid_out_dev) return set_error(CF_EINVAL, "NULL output");
+  if (n_run > 0 && (!rd_run_dev || !gid_run_dev)) return set_error(CF_EINVAL, "NULL running list");
+  if (n_win > 0 && (!rd_win_dev || !ids_win_dev)) return set_error(CF_EINVAL, "NULL window");
+  if ((const void *)rd_out_dev == (const void *)rd_run_dev || (const void *)gid_out_dev == (const void *)gid_run_dev)
+    return set_error(CF_EINVAL, "outputs alias the running list");
+  const int n = n_run + n_win;
+  if (n == 0) return CF_OK;
+  hipLaunchKernelGGL(k_topk_merge, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, as_stream(stream), rd_run_dev,
+                     gid_run_dev, n_run, rd_win_dev, ids_win_dev, n_win, win_first, k, rd_out_dev, gid_out_dev);
+  return hip_check(hipGetLastError(), "cf_topk_merge launch");
 }

@@ -145,6 +145,30 @@ def reweight(w, out, weights, K=1024, alpha=0.8):
     return dict(desc=desc, rd=rd, bottleneck=bott, flags=flags, phase2=mc)
 
 
+def screen_space(desc, opts, logical_dev, offsets, total, moments_seed, n_gpus, k, first=0, count=None,
+                 window=1 << 24):
+    """Phase 1 (Alg. 2) over plans first .. first+count-1 of an enumerated space (Alg. 1),
+    one window of at most ``window`` plans at a time without writing their table
+    (cf_enum_screen), keeping the k plans with the largest R_d among those phase 1 keeps
+    (cf_select_topk per window, cf_topk_merge across windows).  Returns (rd, plan numbers)
+    as device tensors in the order of cf_select_topk: R_d descending, ties by plan number."""
+    count = int(total) - int(first) if count is None else int(count)
+    if not 1 <= window <= 1 << 24:
+        raise cf.CfError("window must be in 1..2^24 plans")
+    dev = logical_dev.device
+    rd_run = torch.empty(0, dtype=torch.float64, device=dev)
+    gid_run = torch.empty(0, dtype=torch.int64, device=dev)
+    w0, end = int(first), int(first) + count
+    while w0 < end:
+        c = min(int(window), end - w0)
+        rd, _, flags = cf.cf_enum_screen(desc, opts, logical_dev, offsets, total, w0, c, moments_seed, n_gpus)
+        ids = cf.cf_select_topk(rd, flags, k)
+        if ids.numel():
+            rd_run, gid_run = cf.cf_topk_merge(rd_run, gid_run, rd, ids, w0, k)
+        w0 += c
+    return rd_run, gid_run
+
+
 def best_plan(out):
     """Host-side summary of a step's selection."""
     if out["best"] is None:

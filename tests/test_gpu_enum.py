@@ -64,7 +64,7 @@ def test_enum_omni_graph_windows(cf):
     desc, opts, ldev, offsets, total, m, oo, Ls = _setup(cf, "c2", 16)
     counts = [O.enum_count(m, oo, L) for L in Ls]
     assert total == sum(counts) == 50378648407914
-    offs = offsets.cpu().numpy().view(np.uint64)
+    offs = np.concatenate([[0], np.cumsum(counts)])  # the oracle's own offsets place the windows
     rng = np.random.default_rng(7)
     starts = [0, int(offs[1]) - 1000, int(offs[37]) - 17, total // 3, total - 5000]
     starts += [int(x) for x in rng.integers(0, total - 5000, size=4)]
@@ -111,7 +111,7 @@ def test_enumerated_plans_screen_like_the_oracle(cf):
     plans = cf.cf_enum_plans(desc, opts, ldev, offsets, total, first, 20000)
     tr, mom = cf.cf_trace_gen(desc, [0], 2000)
     rd, bn, fl = cf.cf_eval_coarse(desc, plans, mom[0], 16)
-    want = O.eval_coarse(m, O.enum_plans(m, oo, Ls, first, 20000), mom[0].cpu().numpy().view(np.uint64), 16)
+    want = O.eval_coarse(m, O.enum_plans(m, oo, Ls, first, 20000), O.trace_gen(m, [0], 2000)["moments"][0], 16)
     assert np.array_equal(rd.cpu().numpy(), want[0])
     assert np.array_equal(fl.cpu().numpy(), want[2])
     assert not np.any(fl.cpu().numpy() & 6)  # none invalid or over budget
@@ -136,7 +136,7 @@ def test_enum_screen_fused_equals_table_path(cf, name, N, extra):
     m, oo = O.make_model(mc), O.enum_opts(mc, spec, N)
     Ls = O.enum_logical(m, oo)
     tr, mom = cf.cf_trace_gen(desc, [0], 3000)
-    mom_h = mom[0].cpu().numpy().view(np.uint64)
+    mom_h = O.trace_gen(m, [0], 3000)["moments"][0]
     for first in (0, total // 5, total - 7000):
         cnt = min(7000, total - first)
         rd, bn, fl = cf.cf_enum_screen(desc, opts, ldev, offsets, total, first, cnt, mom[0], N)
@@ -147,3 +147,57 @@ def test_enum_screen_fused_equals_table_path(cf, name, N, extra):
         assert np.array_equal(fl.cpu().numpy(), fl2.cpu().numpy())
         want = O.eval_coarse(m, O.enum_plans(m, oo, Ls, first, cnt), mom_h, N)
         assert np.array_equal(rd.cpu().numpy(), want[0]) and np.array_equal(fl.cpu().numpy(), want[2])
+
+
+@pytest.mark.parametrize("name,N,logical,count,window,k", [
+    ("c1", 8, 0, 60000, 997, 50),
+    ("c2", 16, 400, 50000, 4096, 300),
+    ("c2", 16, 100, 9000, 1 << 24, 20000),
+])
+def test_space_screened_in_windows_keeps_the_top_k(cf, name, N, logical, count, window, k):
+    """A range of an enumerated space screened window by window (cf_enum_screen, then
+    cf_select_topk per window and cf_topk_merge across windows) keeps the same k plans, in
+    the same order, as the oracle's selection over the whole range at once; R_d ties (plans
+    that differ off their bottleneck) are broken by plan number across windows too."""
+    _say(f"screen space {name} window={window} k={k}")
+    from paper_2512_14098_amd import pipeline
+    desc, opts, ldev, offsets, total, m, oo, Ls = _setup(cf, name, N)
+    first = sum(O.enum_count(m, oo, L) for L in Ls[:logical])  # from the start of a logical plan
+    tr, mom = cf.cf_trace_gen(desc, [0], 3000)
+    rd, gid = pipeline.screen_space(desc, opts, ldev, offsets, total, mom[0], N, k, first, count, window)
+    torch.cuda.synchronize()
+    ord_rd, _, fl = O.eval_coarse(m, O.enum_plans(m, oo, Ls, first, count), O.trace_gen(m, [0], 3000)["moments"][0], N)
+    want = O.select_topk(ord_rd, fl, count)[:k]
+    assert np.array_equal(gid.cpu().numpy(), first + np.asarray(want, np.int64))
+    assert np.array_equal(rd.cpu().numpy().view(np.uint64), ord_rd[want].view(np.uint64))
+    kept = ord_rd[fl & 1 != 0]
+    assert len(kept) > 0 and len(np.unique(kept)) < len(kept)  # the range holds R_d ties
+
+
+def test_topk_merge_edges(cf):
+    dev = "cuda"
+    rd = torch.tensor([3.0, 2.0, 2.0, 1.0], dtype=torch.float64, device=dev)
+    e = torch.empty(0, dtype=torch.float64, device=dev)
+    eg = torch.empty(0, dtype=torch.int64, device=dev)
+    ids = torch.tensor([0, 1, 2, 3], dtype=torch.int32, device=dev)
+    # an empty running list takes the window's first k
+    r, g = cf.cf_topk_merge(e, eg, rd, ids, 100, 3)
+    assert g.cpu().tolist() == [100, 101, 102] and r.cpu().tolist() == [3.0, 2.0, 2.0]
+    # ties with the running list: the smaller plan number first
+    r2, g2 = cf.cf_topk_merge(r, g, torch.tensor([2.0, 0.5], dtype=torch.float64, device=dev),
+                              torch.tensor([0, 1], dtype=torch.int32, device=dev), 50, 4)
+    assert g2.cpu().tolist() == [100, 50, 101, 102] and r2.cpu().tolist() == [3.0, 2.0, 2.0, 2.0]
+    # an empty window keeps the running list
+    r3, g3 = cf.cf_topk_merge(r2, g2, rd, ids[:0], 7, 4)
+    assert g3.cpu().tolist() == g2.cpu().tolist()
+    # a window longer than k keeps its first k
+    r4, g4 = cf.cf_topk_merge(e, eg, rd, ids, 0, 2)
+    assert g4.cpu().tolist() == [0, 1]
+    with pytest.raises(cf.CfError):
+        cf.cf_topk_merge(e, eg, rd, ids, 0, 0)       # k below 1
+    buf = torch.empty(4, dtype=torch.float64, device=dev)
+    bg = torch.empty(4, dtype=torch.int64, device=dev)
+    rc = cf._lib.cf_topk_merge(cf._p(buf), cf._p(bg), 2, cf._p(rd), cf._p(ids), 2, 0, 4, cf._p(buf), cf._p(bg), None)
+    assert rc == -1                                  # outputs alias the running list
+    rc = cf._lib.cf_topk_merge(cf._p(r2), cf._p(g2), -1, cf._p(rd), cf._p(ids), 2, 0, 4, cf._p(buf), cf._p(bg), None)
+    assert rc == -1                                  # a negative count
