@@ -319,6 +319,16 @@ def enum_bench(args):
         ev[1].record()
         torch.cuda.synchronize()
         fused_ms.append(ev[0].elapsed_time(ev[1]))
+    # a range screened window by window keeping the best 1000 (cf_enum_screen, cf_select_topk,
+    # cf_topk_merge), host synchronisation of the selection included
+    from paper_2512_14098_amd import pipeline
+    win = min(chunk, 1 << 24)
+    span = min(4 * win, total)  # the first plans of the space: small replica counts, many of them kept
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    top_rd, top_gid = pipeline.screen_space(desc, opts, ldev, offsets, total, mom[0], N, 1000, 0, span, win)
+    torch.cuda.synchronize()
+    topk_s = time.perf_counter() - t1
     e_s = sum(enum_ms) / len(enum_ms) / 1e3
     achieved = ENUM_PLAN_BYTES * chunk / e_s
     res = {"metric": "physical plans enumerated (Alg. 1, Eq. 1) and screened (phase 1)/sec, 1 GPU",
@@ -331,7 +341,10 @@ def enum_bench(args):
                       "logical_plans": int(len(logical)), "physical_plans": total, "logical_host_s": t_logical,
                       "enum_ms": enum_ms, "coarse_ms": coarse_ms, "enum_plans_per_s": chunk / e_s,
                       "enum_coarse_plans_per_s": chunk / ((sum(enum_ms) + sum(coarse_ms)) / len(enum_ms) / 1e3),
-                      "fused_ms": fused_ms, "fused_plans_per_s": chunk / (sum(fused_ms) / len(fused_ms) / 1e3)},
+                      "fused_ms": fused_ms, "fused_plans_per_s": chunk / (sum(fused_ms) / len(fused_ms) / 1e3),
+                      "screen_topk": {"first": 0, "plans": span, "window": win, "k": 1000,
+                                      "kept_in_top": int(top_gid.numel()),
+                                      "ms": topk_s * 1e3, "plans_per_s": span / topk_s}},
            "roofline": {"bound": "hbm", "achieved": achieved / 1e9, "peak": 8000.0, "unit": "GB/s",
                         "frac": achieved / 8.0e12,
                         "traffic": ENUM_MEASURED_TRAFFIC.get((kernel_source_id(ENUM_KERNEL_SOURCES), chunk)),
