@@ -21,6 +21,10 @@
  *    row-major with the last index fastest.
  *  - The library allocates internal scratch (per-wave simulation state) on
  *    first use and keeps it for later calls; cf_release_scratch() frees it.
+ *    Scratch is per device and shared by every call on that device: calls
+ *    that overlap in time on one device (from other streams or host threads)
+ *    race on it and must be serialised by the caller.  Growing a scratch
+ *    region synchronises the device.
  */
 #ifndef CF_H
 #define CF_H
