@@ -148,7 +148,6 @@ struct ModelLds {
 };
 
 struct WaveShared {
-  uint32_t ex_itgt[CF_MAX_EXEC];  // decode run: step counter of its stage at the end of the running step
   uint32_t ex_st[CF_MAX_EXEC];  // busy:1 ran:1 kind:2 rr:4 cur:4 nmem:9
   uint16_t ex_first[CF_MAX_EXEC];
   uint8_t ex_ns[CF_MAX_EXEC], ex_node[CF_MAX_EXEC];
@@ -167,23 +166,33 @@ struct WaveShared {
 // instances only, at index lsi[si], and the thinker-only fields (sched,
 // watch) per thinker ring slot hist[lsi[si]].
 struct SiLds {
-  uint8_t *comp, *flags, *qhp, *qtp;
+  uint8_t *comp, *flags;
+  uint8_t *qhp, *qtp;  // k_fine<false>: queue head and tail positions in their chunks
+  int *qhc, *qtc;      // k_fine<false>: queue head and tail chunks
+  uint32_t *qh, *qt;   // k_fine<true>: queue head and tail, chunk and position packed by qend
   uint16_t *beff;
   uint16_t *lsi;    // k_fine<true>: index of an LLM stage instance in the LLM-only fields
   int16_t *hist;
-  int *qhc, *qtc, *qn, *roff, *rn;
+  int *qn, *roff, *rn;
   uint32_t *iter, *minfin;
   uint64_t *watch;  // k_fine<true>, thinker stages: executors to notify when its decode steps are (re)scheduled
   uint32_t *sched;  // k_fine<true>, thinker stages: last step whose end is known (completed or in the running run)
 };
 constexpr size_t kSiBytes = 1 + 1 + 1 + 1 + 2 + 2 + 4 * 7;
 // k_fine<true>: bytes per stage instance, per LLM stage instance, per thinker slot
-constexpr size_t kSiBytesG = 4 * 3 + 2 * 2 + 4, kLlmBytesG = 4 * 4 + 2, kThBytesG = 8 + 4;
+constexpr size_t kSiBytesG = 4 * 3 + 2 * 2 + 2, kLlmBytesG = 4 * 4 + 2, kThBytesG = 8 + 4;
+// a queue end, chunk c (-1: none) and position p <= kChunk in it, as one word
+// (chunk indices stay below 2^25: at most 2^26 requests on 8 components)
+__device__ __forceinline__ uint32_t qend(int c, int p) { return ((uint32_t)(c + 1) << 7) | (uint32_t)p; }
+__device__ __forceinline__ int qend_chunk(uint32_t w) { return (int)(w >> 7) - 1; }
+__device__ __forceinline__ int qend_pos(uint32_t w) { return (int)(w & 127u); }
 static_assert(sizeof(WaveShared) % 8 == 0, "the dynamic LDS table after WaveShared holds 8-byte words");
-// a wavefront's static LDS: k_fine<false> also holds the executors' times
+// a wavefront's static LDS: k_fine<false> also holds the executors' times and
+// decode-run step counters
 template <bool G>
 struct WaveLds {
   double xt[4 * CF_MAX_EXEC];
+  uint32_t ex_itgt[CF_MAX_EXEC];  // decode run: step counter of its stage at the end of the running step
   WaveShared w;
 };
 template <>
@@ -308,6 +317,10 @@ struct Sim {
   // leaves its LDS to the stage table that bounds its occupancy.
   double *xt;
   double r_tend, r_last, r_t0, r_dur;
+  // decode run: step counter of the executor's stage at the end of its running
+  // step (k_fine<false>: LDS; k_fine<true>: lane x's register)
+  uint32_t *itgt;
+  uint32_t r_itgt;
   // k_fine<true>, lane x for executor x
   double r_wake;       // next visibility time of a blocked request of a gated stage
   double r_dur2;       // in a joint run: duration of its talker steps
@@ -346,6 +359,16 @@ __device__ __forceinline__ void xt_set(Sim &S, int x, double v) {
   } else {
     S.xt[F * CF_MAX_EXEC + x] = v;
   }
+}
+template <bool G>
+__device__ __forceinline__ uint32_t itgt_get(const Sim &S, int x) {
+  if constexpr (G) return (uint32_t)__builtin_amdgcn_readlane((int)S.r_itgt, x);
+  else return S.itgt[x];
+}
+template <bool G>
+__device__ __forceinline__ void itgt_set(Sim &S, int x, uint32_t v) {
+  if constexpr (G) S.r_itgt = lane_id() == x ? v : S.r_itgt;
+  else S.itgt[x] = v;
 }
 // time F of the executor this lane holds
 template <bool G, int F>
@@ -425,10 +448,19 @@ __device__ __forceinline__ void chunk_free(Sim &S, int c) {
 }
 
 // appends, in lane order, the requests r of the lanes set in bal to stage si's queue
+template <bool G>
 __device__ void q_push_lanes(Sim &S, int si, uint64_t bal, uint32_t r) {
   const int cnt = __popcll(bal);
   if (cnt == 0) return;
-  int qn = S.si.qn[si], tc = S.si.qtc[si], tp = S.si.qtp[si];
+  int qn = S.si.qn[si], tc, tp;
+  if constexpr (G) {
+    const uint32_t qt = S.si.qt[si];
+    tc = qend_chunk(qt);
+    tp = qend_pos(qt);
+  } else {
+    tc = S.si.qtc[si];
+    tp = S.si.qtp[si];
+  }
   if (qn > 0 && (tc < 0 || tc >= S.A->L.n_chunks || tp < 0 || tp > kChunk)) {
     S.status |= CF_ST_OVERFLOW;
     return;
@@ -436,8 +468,12 @@ __device__ void q_push_lanes(Sim &S, int si, uint64_t bal, uint32_t r) {
   if (qn == 0) {
     const int c = chunk_alloc(S);
     if (c < 0) return;
-    S.si.qhc[si] = c;
-    S.si.qhp[si] = 0;
+    if constexpr (G) {
+      S.si.qh[si] = qend(c, 0);
+    } else {
+      S.si.qhc[si] = c;
+      S.si.qhp[si] = 0;
+    }
     tc = c;
     tp = 0;
   }
@@ -455,7 +491,9 @@ __device__ void q_push_lanes(Sim &S, int si, uint64_t bal, uint32_t r) {
     const int pos = k < room ? tp + k : k - room;
     S.pool[(uint32_t)(ch * kChunk + pos)] = r;
   }
-  if (cnt <= room) {
+  if constexpr (G) {
+    S.si.qt[si] = cnt <= room ? qend(tc, tp + cnt) : qend(c1, cnt - room);
+  } else if (cnt <= room) {
     S.si.qtc[si] = tc;
     S.si.qtp[si] = (uint8_t)(tp + cnt);
   } else {
@@ -466,9 +504,21 @@ __device__ void q_push_lanes(Sim &S, int si, uint64_t bal, uint32_t r) {
 }
 
 // pops the first k entries of stage si's queue into dst[0..k)
+template <bool G>
 __device__ void q_pop(Sim &S, int si, int k, GPtr<uint32_t> dst) {
-  int hc = S.si.qhc[si], hp = S.si.qhp[si];
-  const int tc = S.si.qtc[si], tp = S.si.qtp[si];
+  int hc, hp, tc, tp;
+  if constexpr (G) {
+    const uint32_t qh = S.si.qh[si], qt = S.si.qt[si];
+    hc = qend_chunk(qh);
+    hp = qend_pos(qh);
+    tc = qend_chunk(qt);
+    tp = qend_pos(qt);
+  } else {
+    hc = S.si.qhc[si];
+    hp = S.si.qhp[si];
+    tc = S.si.qtc[si];
+    tp = S.si.qtp[si];
+  }
   if (k <= 0) return;
   if (k > S.si.qn[si] || hc < 0 || hc >= S.A->L.n_chunks) {
     S.status |= CF_ST_OVERFLOW;
@@ -508,13 +558,18 @@ __device__ void q_pop(Sim &S, int si, int k, GPtr<uint32_t> dst) {
     hc = nx;
     hp = 0;
   }
-  S.si.qhc[si] = hc;
-  S.si.qhp[si] = (uint8_t)hp;
+  if constexpr (G) {
+    S.si.qh[si] = qend(hc, hp);
+  } else {
+    S.si.qhc[si] = hc;
+    S.si.qhp[si] = (uint8_t)hp;
+  }
 }
 
+template <bool G>
 __device__ __forceinline__ void enqueue1(Sim &S, uint32_t r, int c, int x) {
   S.events++;
-  q_push_lanes(S, stage_of(S, x, c), 1ull, r);
+  q_push_lanes<G>(S, stage_of(S, x, c), 1ull, r);
   S.dirty |= 1ull << x;
 }
 
@@ -694,6 +749,7 @@ __device__ __forceinline__ void notify(Sim &S, int slot) {
 }
 
 // ------------------------------------------------------------------ requests
+template <bool G>
 __device__ void arrive(Sim &S, uint32_t r) {
   const KModel &m = S.A->m;
   const FineArgs &A = *S.A;
@@ -732,11 +788,12 @@ __device__ void arrive(Sim &S, uint32_t r) {
   while (src) {
     const int c = __ffs(src) - 1;
     src &= src - 1;
-    enqueue1(S, r, c, ex_byte(ex, c));
+    enqueue1<G>(S, r, c, ex_byte(ex, c));
   }
 }
 
 // step 2: a delayed delivery of request r to component c2
+template <bool G>
 __device__ void dl_deliver(Sim &S, uint32_t r, int c2) {
   const Rec R = rec_get(S, r);
   const uint64_t ex = ru64(R.ex);
@@ -744,7 +801,7 @@ __device__ void dl_deliver(Sim &S, uint32_t r, int c2) {
   const uint32_t misc = ru(R.misc);
   if (lane_id() == 0) S.rec[r].join = join;
   const int t = rtype(misc);
-  if (((join >> (4 * c2)) & 15u) == S.A->m.npar[t][c2]) enqueue1(S, r, c2, ex_byte(ex, c2));
+  if (((join >> (4 * c2)) & 15u) == S.A->m.npar[t][c2]) enqueue1<G>(S, r, c2, ex_byte(ex, c2));
 }
 
 // Lane-parallel processing of the n members mem[0..n) of a completed
@@ -887,7 +944,7 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
         const uint64_t bal = __ballot((ready >> c2) & 1u);
         if (!bal) continue;
         S.events += (uint64_t)__popcll(bal);
-        q_push_lanes(S, stage_of(S, x, c2), bal, r);
+        q_push_lanes<G>(S, stage_of(S, x, c2), bal, r);
         S.dirty |= 1ull << x;
       }
     }
@@ -944,7 +1001,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     const int room = kind == IT_PREFILL ? beff - S.si.rn[lx] : beff;
     const int n = qn < room ? qn : room;
     const GPtr<uint32_t> dst = S.mem + (uint32_t)(x * CF_MAX_BATCH);
-    q_pop(S, si, n, dst);
+    q_pop<G>(S, si, n, dst);
     if (S.status & CF_ST_OVERFLOW) return;  // the triple is abandoned at the end of this instant
     uint32_t xs = 0;
     const uint32_t sel = m.xsel[c];
@@ -997,7 +1054,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     }
     xt_set<G, XT_T0>(S, x, S.now);
     xt_set<G, XT_DUR>(S, x, dur);
-    sh.ex_itgt[x] = itgt;
+    itgt_set<G>(S, x, itgt);
     xt_set<G, XT_END>(S, x, tend);
     sh.ex_st[x] = (sh.ex_st[x] & 2u) | 1u | ((uint32_t)kind << 2) | ((uint32_t)l << 4) | ((uint32_t)l << 8) |
                   ((uint32_t)nmem << 12) | (itgt > it0 + 1u ? EX_RUN : 0u);
@@ -1047,7 +1104,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     }
   }
   xt_set<G, XT_END>(S, x, S.now + dur);
-  sh.ex_itgt[x] = S.si.iter[lx] + 1u;
+  itgt_set<G>(S, x, S.si.iter[lx] + 1u);
   sh.ex_st[x] = (sh.ex_st[x] & 2u) | 1u | ((uint32_t)kind << 2) | ((uint32_t)l << 4) | ((uint32_t)l << 8) |
                 ((uint32_t)nmem << 12);
 }
@@ -1191,7 +1248,7 @@ __device__ __forceinline__ bool start_joint(Sim &S, int x, int lth, int sth, int
   xt_set<true, XT_T0>(S, x, S.now);
   xt_set<true, XT_DUR>(S, x, d1);
   S.r_dur2 = lane_id() == x ? d2 : S.r_dur2;
-  sh.ex_itgt[x] = n;  // steps of the run, thinker first
+  itgt_set<true>(S, x, n);  // steps of the run, thinker first
   xt_set<true, XT_END>(S, x, t);
   const uint32_t lta = (uint32_t)(sta - sh.ex_first[x]);
   sh.ex_st[x] = (sh.ex_st[x] & 2u) | 1u | (IT_JOINT << 2) | ((uint32_t)lth << 4) | ((uint32_t)lth << 8) | EX_RUN |
@@ -1256,7 +1313,7 @@ __device__ void cut_run(Sim &S, int x) {
   const int si = sh.ex_first[x] + ((st >> 8) & 15u);
   if constexpr (G) {
     if (((st >> 2) & 3u) == IT_JOINT) {
-      const uint32_t n = sh.ex_itgt[x];
+      const uint32_t n = itgt_get<true>(S, x);
       const double d1 = xt_get<true, XT_DUR>(S, x), d2 = lane_val(S.r_dur2, x);
       double t = xt_get<true, XT_T0>(S, x) + d1;
       uint32_t j = 1;
@@ -1265,7 +1322,7 @@ __device__ void cut_run(Sim &S, int x) {
         t = t + ((j & 1u) ? d1 : d2);
       }
       xt_set<true, XT_END>(S, x, t);
-      sh.ex_itgt[x] = j;
+      itgt_set<true>(S, x, j);
       if (j < n) {
         const int lx = S.si.lsi[si];
         const int slot = S.si.hist[lx];
@@ -1277,13 +1334,13 @@ __device__ void cut_run(Sim &S, int x) {
   }
   const int lx = lx_of<G>(S.si, si);
   const uint32_t it0 = S.si.iter[lx];
-  const uint32_t itgt = sh.ex_itgt[x];
+  const uint32_t itgt = itgt_get<G>(S, x);
   const double dur = xt_get<G, XT_DUR>(S, x);
   uint32_t taken = 0;
   const double t = run_walk(xt_get<G, XT_T0>(S, x) + dur, dur, itgt - (it0 + 1u), S.now, &taken);
   const uint32_t j = it0 + 1u + taken;
   xt_set<G, XT_END>(S, x, t);
-  sh.ex_itgt[x] = j;
+  itgt_set<G>(S, x, j);
   if (j <= it0 + 1u) sh.ex_st[x] = st & ~EX_RUN;
   if constexpr (G) {
     if ((S.si.flags[si] & SF_THINKER) && j < itgt) {
@@ -1381,7 +1438,7 @@ __device__ __forceinline__ void complete_joint(Sim &S, int x, uint32_t st) {
   const int first = sh.ex_first[x];
   const int lth = (st >> 8) & 15u, lta = (st >> 22) & 15u;
   const int sth = first + lth, sta = first + lta;
-  const uint32_t n = sh.ex_itgt[x];
+  const uint32_t n = itgt_get<true>(S, x);
   const uint32_t nth_s = (n + 1u) >> 1, nta_s = n >> 1;
   const uint32_t llast = (n & 1u) ? (uint32_t)lth : (uint32_t)lta;
   sh.ex_st[x] = (st & ~(1u | EX_RUN | (15u << 4) | (15u << 22))) | 2u | (llast << 4);
@@ -1460,7 +1517,7 @@ __device__ __forceinline__ void complete_iter(Sim &S, int x) {
   const int lx = lx_of<G>(S.si, si);
   const int rn = S.si.rn[lx];
   const uint32_t it0 = S.si.iter[lx];
-  const uint32_t it = (fl & SF_GATED) ? it0 + 1u : sh.ex_itgt[x];
+  const uint32_t it = (fl & SF_GATED) ? it0 + 1u : itgt_get<G>(S, x);
   S.si.iter[lx] = it;  // k_fine<true>: a thinker's ring already holds the end of these steps
   if constexpr (!G) {
     if ((fl & SF_THINKER) && lane_id() == 0) S.hist[(uint32_t)(S.si.hist[si] * kHist) + (it & (kHist - 1))] = S.now;
@@ -1637,6 +1694,7 @@ __device__ bool setup_plan(Sim &S, int p) {
     S.r_dur = 0.0;
     S.r_wake = __builtin_inf();
     S.r_dur2 = 0.0;
+    S.r_itgt = 0;
   }
   if (lane < S.nx) {
     int v = 0;
@@ -1658,7 +1716,7 @@ __device__ bool setup_plan(Sim &S, int p) {
       S.xt[XT_T0 * CF_MAX_EXEC + lane] = 0.0;
       S.xt[XT_DUR * CF_MAX_EXEC + lane] = 0.0;
     }
-    sh.ex_itgt[lane] = 0;
+    if constexpr (!G) S.itgt[lane] = 0;
   }
   if constexpr (G) S.rewake = 0;
   // stage instances, one lane each (prefix sums give run-slot and ring offsets)
@@ -1693,10 +1751,15 @@ __device__ bool setup_plan(Sim &S, int p) {
                                 (m.kind[c] == CF_GEN ? SF_GEN : 0));
       S.si.beff[s] = (uint16_t)beff;
       S.si.qn[s] = 0;
-      S.si.qhc[s] = -1;
-      S.si.qtc[s] = -1;
-      S.si.qhp[s] = 0;
-      S.si.qtp[s] = 0;
+      if constexpr (G) {
+        S.si.qh[s] = qend(-1, 0);
+        S.si.qt[s] = qend(-1, 0);
+      } else {
+        S.si.qhc[s] = -1;
+        S.si.qtc[s] = -1;
+        S.si.qhp[s] = 0;
+        S.si.qtp[s] = 0;
+      }
       if constexpr (G) {
         const int ls = l_carry + (int)lo, slot = hs_carry + (int)ho;
         S.si.lsi[s] = llm ? (uint16_t)ls : (uint16_t)0xFFFFu;
@@ -1749,8 +1812,8 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
       // static LDS a multiple of 8 bytes, so every array is aligned
       const int lcap = A.nl_cap, tcap = A.nt_cap;
       S.si.watch = (uint64_t *)p; p += 8 * tcap;
-      S.si.qhc = (int *)p; p += 4 * cap;
-      S.si.qtc = (int *)p; p += 4 * cap;
+      S.si.qh = (uint32_t *)p; p += 4 * cap;
+      S.si.qt = (uint32_t *)p; p += 4 * cap;
       S.si.qn = (int *)p; p += 4 * cap;
       S.si.roff = (int *)p; p += 4 * lcap;
       S.si.rn = (int *)p; p += 4 * lcap;
@@ -1762,8 +1825,6 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
       S.si.hist = (int16_t *)p; p += 2 * lcap;
       S.si.comp = (uint8_t *)p; p += cap;
       S.si.flags = (uint8_t *)p; p += cap;
-      S.si.qhp = (uint8_t *)p; p += cap;
-      S.si.qtp = (uint8_t *)p; p += cap;
     } else {
       S.si.qhc = (int *)p; p += 4 * cap;
       S.si.qtc = (int *)p; p += 4 * cap;
@@ -1780,7 +1841,10 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
       S.si.qtp = (uint8_t *)p; p += cap;
     }
   }
-  if constexpr (!G) S.xt = wl.xt;
+  if constexpr (!G) {
+    S.xt = wl.xt;
+    S.itgt = wl.ex_itgt;
+  }
   // model tables for per-lane indexing
   for (int j = lane; j < CF_MAX_TYPES * CF_MAX_COMP; j += 64) {
     (&sh.ml.child[0][0])[j] = (&m.child[0][0])[j];
@@ -1894,10 +1958,10 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
           S.dl_head++;
           S.dl_head_t = S.dl_head != S.dl_tail ? rdb(S.dl_t[S.dl_head & L.dl_mask]) : __builtin_inf();
           if (((v >> 3) & 1u) == DL_TICK) S.dirty |= S.ta_exec_mask;
-          else dl_deliver(S, v >> 4, (int)(v & 7u));
+          else dl_deliver<G>(S, v >> 4, (int)(v & 7u));
         }
         while (next_arr < (uint32_t)A.n && S.t_arr == t) {
-          arrive(S, next_arr);
+          arrive<G>(S, next_arr);
           next_arr++;
           S.t_arr = next_arr < (uint32_t)A.n ? rdb(arrival_time(S, next_arr)) : __builtin_inf();
         }
