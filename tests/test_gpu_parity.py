@@ -233,6 +233,46 @@ def test_fine_c4_widest_selected_plans(cf):
     assert np.all(g["status"] == 0)
 
 
+def test_full_size_c4_sampled(cf):
+    """c4 at full trace length (10^5 requests) in the launch shape of its bench: plans from
+    the top 1000 of its 10^6 by phase 1 (every 32nd, and the widest), seed 0; triples sampled
+    across plans and rates checked against the oracle one by one."""
+    if os.environ.get("CF_SKIP_FULL"):
+        pytest.skip("CF_SKIP_FULL set")
+    _say("full c4 sampled")
+    cfg = load_config("c4")
+    tab = make_plans(cfg)
+    m = O.make_model(cfg["model"])
+    n = int(cfg["n_req"])
+    otr = O.trace_gen(m, [0], n)
+    rd, _, fl = O.eval_coarse(m, tab, otr["moments"][0], cfg["gpus"])
+    kept = O.select_topk(rd, fl, cfg["top_k"])
+    nsi = [sum(int(tab.node_rep[v, p]) * bin(int(tab.node_comp[v, p])).count("1") for v in range(tab.n_nodes[p]))
+           for p in kept]
+    ids = sorted(set(int(p) for p in kept[::32]) | {int(kept[int(np.argmax(nsi))])})
+    # every other rate of the upper three quarters of the grid (the lowest rates make the
+    # longest simulations, on both sides)
+    rates = np.ascontiguousarray(O.rate_grid(rd, np.asarray(ids, np.int32), cfg["rates"]["grid"])[:, 8::2])
+    desc = cf.model_desc(cfg["model"])
+    tr, _ = cf.cf_trace_gen(desc, [0], n)
+    _say(f"  {len(ids)} plans x {rates.shape[1]} rates on the GPU")
+    out = cf.cf_eval_fine(desc, cf.DevicePlans(tab), torch.as_tensor(np.asarray(ids, np.int32)).cuda(),
+                          torch.from_numpy(rates).cuda(), tr)
+    torch.cuda.synchronize()
+    _say("  oracle on sampled triples")
+    met = out["met"].cpu().numpy().view(np.uint32)
+    cnt = out["cnt"].cpu().numpy().view(np.uint32)
+    ev = out["events"].cpu().numpy().view(np.uint64)
+    assert np.all(out["status"].cpu().numpy() == 0)
+    assert np.all(cnt.sum(axis=3) == n)
+    rng = np.random.default_rng(4)
+    for _ in range(6):
+        i, k = int(rng.integers(len(ids))), int(rng.integers(rates.shape[1]))
+        o = O.sim_triple(m, tab, ids[i], float(rates[i, k]), otr, 0)
+        assert np.array_equal(met[i, k, 0], o["met"]) and np.array_equal(cnt[i, k, 0], o["cnt"]), (i, k)
+        assert int(ev[i, k, 0]) == o["events"], (i, k)
+
+
 def test_fine_c2_gating_latencies(cf):
     """Omni plans with disaggregated and colocated thinker/talker: latencies of every request."""
     _say("fine c2 latencies")
