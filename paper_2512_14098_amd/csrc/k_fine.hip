@@ -59,6 +59,7 @@ namespace cf {
 namespace {
 
 constexpr int kMaxSI = CF_MAX_EXEC * CF_MAX_COMP;  // stage instances
+static_assert(kMaxSI <= 512, "an LLM stage instance index fits the 9 bits of a gate word");
 constexpr int kChunk = 64;                          // queue chunk entries
 constexpr int kHist = 64;                           // k_fine<false>: ring of the last thinker step ends
 constexpr int kRing = 256;                          // k_fine<true>: thinker step-time ring
@@ -76,10 +77,10 @@ constexpr uint32_t MARK = 0x80000000u;  // gated running slot: in the current de
 constexpr uint32_t RK_TOK = 0xFFFFu;
 __device__ __forceinline__ uint32_t rk_own(uint32_t v) { return (v >> 16) & 0x7FFFu; }
 // k_fine<true>: gate word of a gated stage's running slot, fixed when the
-// request joined: the request's type is gated at the stage (bit 31), its
-// thinker component (bits 24..26), the thinker's executor (bits 16..21) and
-// the thinker's token count (bits 0..15); run_q holds the request's join
-// step in the thinker's stage.
+// request joined: the request's type is gated at the stage (bit 31), the
+// LLM index of its thinker's stage instance (bits 22..30), the thinker's
+// executor (bits 16..21) and the thinker's token count (bits 0..15); run_q
+// holds the request's join step in the thinker's stage.
 constexpr uint32_t RG_GATED = 0x80000000u;
 constexpr uint32_t EX_RUN = 1u << 21;   // executor state: busy with a multi-step decode run
 // k_fine<true>: executor state kind of a joint thinker/talker run (IT_FINISH
@@ -692,7 +693,6 @@ __device__ __forceinline__ double slot_vis_g(const Sim &S, uint32_t r, uint32_t 
   xth = x;
   wsi = -1;
   if (!(g & RG_GATED)) return -__builtin_inf();
-  const int th = (int)((g >> 24) & 7u);
   xth = (int)((g >> 16) & 63u);
   const uint32_t nth = g & 0xFFFFu;
   const uint32_t k = tok + 1u < nth ? tok + 1u : nth;
@@ -701,7 +701,7 @@ __device__ __forceinline__ double slot_vis_g(const Sim &S, uint32_t r, uint32_t 
   if (k <= 1) {
     e = S.tim[r].tfirst;
   } else {
-    const int lx = S.si.lsi[stage_of(S, xth, th)];
+    const int lx = (int)((g >> 22) & 511u);
     const int slot = S.si.hist[lx];
     const uint32_t q = q0 + k - 1u;
     if (q > S.si.sched[slot]) {
@@ -846,8 +846,9 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
       fin = no == 1;
       key = gated ? (1u | (no << 16)) : iter_s + no - 1u;
       if (gated && ml.ta_c[t] == c) {
-        const int th = ml.th_c[t];
-        gw = RG_GATED | ((uint32_t)th << 24) | ((uint32_t)ex_byte(R.ex, th) << 16) | nout_of(S, r, t, th);
+        const int th = ml.th_c[t], xth = ex_byte(R.ex, th);
+        gw = RG_GATED | ((uint32_t)S.si.lsi[stage_of(S, xth, th)] << 22) | ((uint32_t)xth << 16) |
+             nout_of(S, r, t, th);
         gq = S.tim[r].thjoin;
       }
     } else if (valid && kind == IT_FINISH) {
@@ -1168,15 +1169,15 @@ struct GateView {
 };
 __device__ __forceinline__ GateView local_gate_view(const Sim &S, int x, int si) {
   const int ns = S.sh->ex_ns[x], first = S.sh->ex_first[x];
-  const int cth = S.si.comp[si];
-  const uint32_t next = S.si.iter[S.si.lsi[si]] + 1u;
+  const int lth = S.si.lsi[si];
+  const uint32_t next = S.si.iter[lth] + 1u;
   uint32_t qmin = kNone, kta = kNone;
   int gsi = -1, nbusy = 0;
   bool other = false;  // a running request that does not wait for the next step of si
   for (int g = first; g < first + ns; g++) {
     if (!(S.si.flags[g] & SF_GATED)) continue;
     const int lg = S.si.lsi[g];
-    const int c = S.si.comp[g], rn = S.si.rn[lg];
+    const int rn = S.si.rn[lg];
     if (rn == 0) continue;
     nbusy++;
     gsi = g;
@@ -1189,7 +1190,7 @@ __device__ __forceinline__ GateView local_gate_view(const Sim &S, int x, int si)
         const uint32_t v = rk[j], g = rg[j];
         const uint32_t tok = v & RK_TOK;
         bool waits_next = false;
-        if ((g & RG_GATED) && (int)((g >> 24) & 7u) == cth && (int)((g >> 16) & 63u) == x) {
+        if ((g & RG_GATED) && (int)((g >> 22) & 511u) == lth && (int)((g >> 16) & 63u) == x) {
           const uint32_t nth = g & 0xFFFFu;
           const uint32_t k = tok + 1u < nth ? tok + 1u : nth;
           const uint32_t q = rq[j] + k - 1u;
@@ -1455,7 +1456,6 @@ __device__ __forceinline__ void complete_joint(Sim &S, int x, uint32_t st) {
   const int lg = S.si.lsi[sta];
   const int cta = S.si.comp[sta];
   const int rng = S.si.rn[lg];
-  const GPtr<uint32_t> rrg = S.run_r + (uint32_t)S.si.roff[lg];
   const GPtr<uint32_t> rkg = S.run_k + (uint32_t)S.si.roff[lg];
   bool fin[CF_MAX_BATCH / 64];
 #pragma unroll
@@ -1522,7 +1522,6 @@ __device__ __forceinline__ void complete_iter(Sim &S, int x) {
   if constexpr (!G) {
     if ((fl & SF_THINKER) && lane_id() == 0) S.hist[(uint32_t)(S.si.hist[si] * kHist) + (it & (kHist - 1))] = S.now;
   }
-  const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lx];
   const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
   if (!(fl & SF_GATED)) {
     S.events += (uint64_t)rn * (uint64_t)(it - it0);
@@ -1582,7 +1581,7 @@ __device__ __forceinline__ bool gate_wake(Sim &S, int y) {
     for (int g = first; g < first + ns; g++) {
       if (!(S.si.flags[g] & SF_GATED)) continue;
       const int lg = S.si.lsi[g];
-      const int c = S.si.comp[g], rn = S.si.rn[lg];
+      const int rn = S.si.rn[lg];
       const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lg];
       const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lg];
       const GPtr<uint32_t> rg = S.run_g + (uint32_t)S.si.roff[lg];
