@@ -149,6 +149,17 @@ def _p(t):
     return C.c_void_p(t.data_ptr())
 
 
+def _in(t, dtype, what, numel=None, ndim=None):
+    """A caller's device tensor checked for the element type (and size) the C ABI reads."""
+    if t.dtype != dtype:
+        raise CfError("%s: expected %s, got %s" % (what, dtype, t.dtype))
+    if numel is not None and t.numel() != numel:
+        raise CfError("%s: expected %d elements, got %d" % (what, numel, t.numel()))
+    if ndim is not None and t.dim() != ndim:
+        raise CfError("%s: expected %d dimensions, got %d" % (what, ndim, t.dim()))
+    return _p(t.contiguous())
+
+
 # ------------------------------------------------------------------ model
 def _dist(spec, audio):
     d = cf_dist()
@@ -313,7 +324,8 @@ def cf_eval_coarse(desc, plans, moments_seed, n_gpus):
     rd = torch.empty(P, dtype=torch.float64, device=dev)
     bott = torch.empty(P, dtype=torch.int32, device=dev)
     flags = torch.empty(P, dtype=torch.uint8, device=dev)
-    _check(_lib.cf_eval_coarse(C.byref(desc), C.byref(plans.c), _p(moments_seed.contiguous()),
+    mom = _in(moments_seed, torch.int64, "moments", desc.n_types * 8)
+    _check(_lib.cf_eval_coarse(C.byref(desc), C.byref(plans.c), mom,
                                int(n_gpus), _p(rd), _p(bott), _p(flags), _stream()), "cf_eval_coarse")
     return rd, bott, flags
 
@@ -321,7 +333,8 @@ def cf_eval_coarse(desc, plans, moments_seed, n_gpus):
 def cf_select_topk(rd, flags, k):
     ids = torch.empty(max(int(k), 1), dtype=torch.int32, device=rd.device)
     n = C.c_int32(0)
-    _check(_lib.cf_select_topk(_p(rd), _p(flags), int(rd.numel()), int(k), _p(ids), C.byref(n),
+    _check(_lib.cf_select_topk(_in(rd, torch.float64, "rd"), _in(flags, torch.uint8, "flags", rd.numel()),
+                               int(rd.numel()), int(k), _p(ids), C.byref(n),
                                _stream()), "cf_select_topk")
     return ids[:n.value]
 
@@ -333,15 +346,18 @@ def cf_topk_merge(rd_run, gid_run, rd_win, ids_win, win_first, k):
     n = min(int(k), int(rd_run.numel()) + int(ids_win.numel()))
     rd = torch.empty(max(int(k), 1), dtype=torch.float64, device=dev)
     gid = torch.empty(max(int(k), 1), dtype=torch.int64, device=dev)
-    _check(_lib.cf_topk_merge(_p(rd_run.contiguous()), _p(gid_run.contiguous()), int(rd_run.numel()), _p(rd_win),
-                              _p(ids_win.contiguous()), int(ids_win.numel()), C.c_uint64(int(win_first)), int(k),
+    run_rd = _in(rd_run, torch.float64, "rd_run")
+    run_gid = _in(gid_run, torch.int64, "gid_run", rd_run.numel())
+    win_ids = _in(ids_win, torch.int32, "ids_win")
+    _check(_lib.cf_topk_merge(run_rd, run_gid, int(rd_run.numel()), _in(rd_win, torch.float64, "rd_win"),
+                              win_ids, int(ids_win.numel()), C.c_uint64(int(win_first)), int(k),
                               _p(rd), _p(gid), _stream()), "cf_topk_merge")
     return rd[:n], gid[:n]
 
 
 def cf_rate_grid(rd, ids, K, alpha_max=1.0):
     rates = torch.empty((ids.numel(), int(K)), dtype=torch.float64, device=rd.device)
-    _check(_lib.cf_rate_grid(_p(rd), _p(ids.contiguous()), int(ids.numel()), int(K),
+    _check(_lib.cf_rate_grid(_in(rd, torch.float64, "rd"), _in(ids, torch.int32, "ids"), int(ids.numel()), int(K),
                              float(alpha_max), _p(rates), _stream()), "cf_rate_grid")
     return rates
 
@@ -375,8 +391,9 @@ def cf_eval_fine(desc, plans, plan_ids, rates, trace, lat_triples=None, targets=
         tg = _targets(targets, T)
         hist = torch.empty((n_plans, K, S, T, tg.shape[1] + 1), dtype=torch.int32, device=dev)
         out.hist_dev, out.hist_targets_host, out.n_bins = hist.data_ptr(), tg.ctypes.data, tg.shape[1]
-    _check(_lib.cf_eval_fine(C.byref(desc), C.byref(plans.c), _p(plan_ids.contiguous()), int(n_plans),
-                             _p(rates.contiguous()), int(K), C.byref(trace.c), 0, C.byref(out),
+    _check(_lib.cf_eval_fine(C.byref(desc), C.byref(plans.c), _in(plan_ids, torch.int32, "plan_ids", n_plans),
+                             int(n_plans), _in(rates, torch.float64, "rates", ndim=2), int(K), C.byref(trace.c), 0,
+                             C.byref(out),
                              _stream()), "cf_eval_fine")
     return dict(met=met, cnt=cnt, events=events, status=status, lat=lat, hist=hist)
 
@@ -392,8 +409,9 @@ def cf_eval_bisect(desc, plans, plan_ids, rates, trace, theta):
     ne = torch.empty(n, dtype=torch.int32, device=dev)
     ev = torch.empty(n, dtype=torch.int64, device=dev)
     st = torch.empty(n, dtype=torch.int32, device=dev)
-    _check(_lib.cf_eval_bisect(C.byref(desc), C.byref(plans.c), _p(plan_ids.contiguous()), int(n),
-                               _p(rates.contiguous()), int(K), C.byref(trace.c), int(theta[0]), int(theta[1]),
+    _check(_lib.cf_eval_bisect(C.byref(desc), C.byref(plans.c), _in(plan_ids, torch.int32, "plan_ids", n), int(n),
+                               _in(rates, torch.float64, "rates", ndim=2), int(K), C.byref(trace.c),
+                               int(theta[0]), int(theta[1]),
                                _p(ks), _p(gt), _p(g), _p(ne), _p(ev), _p(st), _stream()), "cf_eval_bisect")
     return dict(kstar=ks, goodput_t=gt, goodput=g, n_eval=ne, events=ev, status=st)
 
@@ -406,8 +424,9 @@ def cf_eval_mc(desc, plans, plan_ids, rd, moments_seed, alpha, trace, seed_idx, 
     cnt = torch.empty((n, T), dtype=torch.int32, device=dev)
     gt = torch.empty((n, T), dtype=torch.float64, device=dev)
     lat = torch.empty((n, int(n_sample), 4), dtype=torch.float64, device=dev) if want_lat else None
-    _check(_lib.cf_eval_mc(C.byref(desc), C.byref(plans.c), _p(plan_ids.contiguous()), n, _p(rd.contiguous()),
-                           _p(moments_seed.contiguous()), float(alpha), C.byref(trace.c), int(seed_idx),
+    mom = _in(moments_seed, torch.int64, "moments", T * 8)
+    _check(_lib.cf_eval_mc(C.byref(desc), C.byref(plans.c), _in(plan_ids, torch.int32, "plan_ids"), n,
+                           _in(rd, torch.float64, "rd"), mom, float(alpha), C.byref(trace.c), int(seed_idx),
                            int(n_sample), _p(met), _p(cnt), _p(gt), _p(lat), _stream()), "cf_eval_mc")
     return dict(met=met, cnt=cnt, goodput_t=gt, lat=lat)
 
@@ -424,8 +443,9 @@ def cf_eval_mc_curve(desc, plans, plan_ids, rd, moments_seed, alpha, trace, seed
     gt = torch.empty((n, T), dtype=torch.float64, device=dev)
     hist = torch.empty((n, T, nb + 1), dtype=torch.int32, device=dev)
     curve = torch.empty((n, nb, T), dtype=torch.float64, device=dev)
-    _check(_lib.cf_eval_mc_curve(C.byref(desc), C.byref(plans.c), _p(plan_ids.contiguous()), n,
-                                 _p(rd.contiguous()), _p(moments_seed.contiguous()), float(alpha), C.byref(trace.c),
+    _check(_lib.cf_eval_mc_curve(C.byref(desc), C.byref(plans.c), _in(plan_ids, torch.int32, "plan_ids"), n,
+                                 _in(rd, torch.float64, "rd"), _in(moments_seed, torch.int64, "moments", T * 8),
+                                 float(alpha), C.byref(trace.c),
                                  int(seed_idx), int(n_sample), int(nb), tg.ctypes.data_as(C.c_void_p), _p(met),
                                  _p(cnt), _p(gt), _p(hist), _p(curve), _stream()), "cf_eval_mc_curve")
     return dict(met=met, cnt=cnt, goodput_t=gt, hist=hist, curve=curve)
@@ -439,9 +459,10 @@ def cf_goodput_curve(hist, cnt, rates, theta, n_req):
     kstar = torch.empty((n_plans, nb), dtype=torch.int32, device=dev)
     gt = torch.empty((n_plans, nb, T), dtype=torch.float64, device=dev)
     g = torch.empty((n_plans, nb), dtype=torch.float64, device=dev)
-    _check(_lib.cf_goodput_curve(_p(hist.contiguous()), _p(cnt.contiguous()), n_plans, K, S, T, nb,
-                                 _p(rates.contiguous()), int(theta[0]), int(theta[1]), int(n_req), _p(kstar),
-                                 _p(gt), _p(g), _stream()), "cf_goodput_curve")
+    _check(_lib.cf_goodput_curve(_in(hist, torch.int32, "hist"), _in(cnt, torch.int32, "cnt", n_plans * K * S * T),
+                                 n_plans, K, S, T, nb, _in(rates, torch.float64, "rates", n_plans * K),
+                                 int(theta[0]), int(theta[1]), int(n_req), _p(kstar), _p(gt), _p(g), _stream()),
+           "cf_goodput_curve")
     return kstar, gt, g
 
 
@@ -455,9 +476,10 @@ def cf_pareto(goodput_t, plan_ids=None, flags=None):
     if flags is not None and (flags.dtype != torch.uint8 or not flags.is_contiguous()):
         raise CfError("cf_pareto: flags must be a contiguous uint8 tensor (updated in place)")
     nf = int(flags.numel()) if flags is not None else 0
-    _check(_lib.cf_pareto(_p(goodput_t.contiguous()), int(n), int(T), _p(keep),
-                          _p(plan_ids.contiguous()) if plan_ids is not None else None,
-                          _p(flags) if flags is not None else None, nf, _stream()), "cf_pareto")
+    _check(_lib.cf_pareto(_in(goodput_t, torch.float64, "goodput_t", ndim=2), int(n), int(T), _p(keep),
+                          _in(plan_ids, torch.int32, "plan_ids", n) if plan_ids is not None else None,
+                          _in(flags, torch.uint8, "flags") if flags is not None else None, nf, _stream()),
+           "cf_pareto")
     return keep
 
 
@@ -524,7 +546,8 @@ def cf_enum_screen(desc, opts, logical_dev, offsets, total, first, count, moment
     flags = torch.empty(int(count), dtype=torch.uint8, device=dev)
     _check(_lib.cf_enum_screen(C.byref(desc), C.byref(opts), _p(logical_dev.contiguous()), int(logical_dev.shape[0]),
                                _p(offsets), C.c_uint64(int(total)), C.c_uint64(int(first)), int(count),
-                               _p(moments_seed.contiguous()), int(n_gpus), _p(rd), _p(bott), _p(flags), _stream()),
+                               _in(moments_seed, torch.int64, "moments", desc.n_types * 8), int(n_gpus), _p(rd),
+                               _p(bott), _p(flags), _stream()),
            "cf_enum_screen")
     return rd, bott, flags
 
@@ -535,7 +558,8 @@ def cf_goodput_reduce(met, cnt, rates, theta, n_req):
     kstar = torch.empty(n_plans, dtype=torch.int32, device=dev)
     gt = torch.empty((n_plans, T), dtype=torch.float64, device=dev)
     g = torch.empty(n_plans, dtype=torch.float64, device=dev)
-    _check(_lib.cf_goodput_reduce(_p(met), _p(cnt), n_plans, K, S, T, _p(rates.contiguous()),
+    _check(_lib.cf_goodput_reduce(_in(met, torch.int32, "met"), _in(cnt, torch.int32, "cnt", met.numel()), n_plans, K,
+                                  S, T, _in(rates, torch.float64, "rates", n_plans * K),
                                   int(theta[0]), int(theta[1]), int(n_req), _p(kstar), _p(gt), _p(g),
                                   _stream()), "cf_goodput_reduce")
     return kstar, gt, g
@@ -543,7 +567,8 @@ def cf_goodput_reduce(met, cnt, rates, theta, n_req):
 
 def cf_select_best(goodput):
     best = torch.empty(1, dtype=torch.int32, device=goodput.device)
-    _check(_lib.cf_select_best(_p(goodput), int(goodput.numel()), _p(best), _stream()), "cf_select_best")
+    _check(_lib.cf_select_best(_in(goodput, torch.float64, "goodput"), int(goodput.numel()), _p(best), _stream()),
+           "cf_select_best")
     return best
 
 

@@ -420,6 +420,26 @@ def test_edge_cases(cf):
     _assert_fine_equal(g, want)
 
 
+def test_binding_rejects_wrong_element_types(cf):
+    """The binding checks the element type and size of every caller tensor the C ABI reads."""
+    cfg = load_config("c0")
+    desc = cf.model_desc(cfg["model"])
+    tr, mom = cf.cf_trace_gen(desc, [0], 100)
+    plans = cf.DevicePlans(make_plans(cfg))
+    rates = torch.ones((2, 2), dtype=torch.float64, device="cuda")
+    with pytest.raises(cf.CfError):
+        cf.cf_eval_fine(desc, plans, torch.zeros(2, dtype=torch.int64, device="cuda"), rates, tr)
+    with pytest.raises(cf.CfError):
+        cf.cf_eval_fine(desc, plans, torch.zeros(3, dtype=torch.int32, device="cuda"), rates, tr)
+    with pytest.raises(cf.CfError):
+        cf.cf_eval_coarse(desc, plans, mom[0].double(), 2)
+    rd, _, fl = cf.cf_eval_coarse(desc, plans, mom[0], 2)
+    with pytest.raises(cf.CfError):
+        cf.cf_select_topk(rd.float(), fl, 4)
+    with pytest.raises(cf.CfError):
+        cf.cf_select_topk(rd, fl[:3], 4)
+
+
 def test_fine_is_deterministic_and_order_free(cf):
     """Running twice gives identical bits; permuting the plan list permutes the results."""
     _say("determinism")
