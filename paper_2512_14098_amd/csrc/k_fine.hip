@@ -756,13 +756,17 @@ __device__ void arrive(Sim &S, uint32_t r) {
   const WaveShared &sh = *S.sh;
   S.events++;
   const size_t o = S.soff + r;
-  const int t = ri(gload(A.type, o));
+  // every field of the request is loaded before any is used (one memory latency)
+  const uint8_t tv = gload(A.type, o);
+  const uint64_t k0v = gload(A.rkey0, o), k1v = gload(A.rkey1, o);
+  const uint32_t akv = gload(A.akey, o);
+  const int t = ri(tv);
   if (t >= m.nt) {
     S.status |= CF_ST_INVALID;
     return;
   }
-  const uint64_t k0 = ru64(gload(A.rkey0, o)), k1 = ru64(gload(A.rkey1, o));
-  const uint32_t ak = ru(gload(A.akey, o));
+  const uint64_t k0 = ru64(k0v), k1 = ru64(k1v);
+  const uint32_t ak = ru(akv);
   int alt = 0;
   if (sh.nalt[t] == 2) {
     const uint64_t w0 = sh.aw[t][0], w1 = sh.aw[t][1];
@@ -1960,9 +1964,11 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
           else dl_deliver<G>(S, v >> 4, (int)(v & 7u));
         }
         while (next_arr < (uint32_t)A.n && S.t_arr == t) {
+          // the next arrival's time is loaded while this one is handled
+          const uint64_t tk = next_arr + 1u < (uint32_t)A.n ? gload(A.ticks, S.soff + next_arr + 1u) : 0ull;
           arrive<G>(S, next_arr);
           next_arr++;
-          S.t_arr = next_arr < (uint32_t)A.n ? rdb(arrival_time(S, next_arr)) : __builtin_inf();
+          S.t_arr = next_arr < (uint32_t)A.n ? rdb(((double)tk * 0x1p-32) / S.lam) : __builtin_inf();
         }
         // --- step 3: idle executors whose state changed may start an iteration
         uint64_t cand = S.dirty;
