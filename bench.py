@@ -39,14 +39,14 @@ _W_C4_SEED0 = ("c4: Full coarse-to-fine sweep of the omni graph on 64 simulated 
                "sampled plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 requests "
                "(sample: first 1 of its 64 seeds)")
 MEASURED_TRAFFIC = {
-    ("bce288febc1ae82f", _W_C1): 2.1131e12,
-    ("bce288febc1ae82f", _W_C4_SEED0): 1.7598e13,
+    ("c54c478f1dc57905", _W_C1): 2.0539e12,
+    ("c54c478f1dc57905", _W_C4_SEED0): 1.7606e13,
 }
 # VALU lane rate of the k_fine launch by rocprofv3 counters (SQ_INSTS_VALU x SQ_THREAD_CYCLES_VALU /
 # SQ_ACTIVE_INST_VALU / kernel time / PEAK_LANE_OPS), keyed like MEASURED_TRAFFIC
 MEASURED_LANE_FRAC = {
-    ("bce288febc1ae82f", _W_C1): 0.4211,
-    ("bce288febc1ae82f", _W_C4_SEED0): 0.2832,
+    ("c54c478f1dc57905", _W_C1): 0.4244,
+    ("c54c478f1dc57905", _W_C4_SEED0): 0.2844,
 }
 ENUM_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_enum.hip", "paper_2512_14098_amd/csrc/cf_internal.h",
                        "paper_2512_14098_amd/csrc/cf_phase1.h")
