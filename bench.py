@@ -105,10 +105,27 @@ def cpu_baseline_all_cores(w, ids, rates, order, seeds_needed, budget_s, workers
                       "processes (%d request-events, longest worker %.1f s)" % (n, workers, ev, dt)}
 
 
-def cpu_baseline(w, budget_s, all_cores=0):
-    """The oracle, single-threaded on this host, on a bounded sample of the
-    same workload's triples (spread over plans, rates and seeds); the oracle's
-    own phase 1, selection and rate grid choose the plans and rates."""
+def host_info():
+    """CPU model and core count of this host, for the CPU-baseline record."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "nproc": os.cpu_count(),
+            "affinity": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None}
+
+
+def cpu_baseline(w, budget_s, all_cores=0, events_per_step=None):
+    """The oracle, single-threaded on this host (pinned to one core), on a
+    bounded sample of the same workload's triples (spread over plans, rates and
+    seeds); the oracle's own phase 1, selection and rate grid choose the plans
+    and rates.  With events_per_step, also the time one full step would take at
+    the measured rate (extrapolated linearly in request-events)."""
     import numpy as np
 
     from oracle import oracle as O
@@ -127,6 +144,12 @@ def cpu_baseline(w, budget_s, all_cores=0):
     seeds_needed = sorted({s for _, _, s in order[:256]})
     otr = O.trace_gen(m, [w.seeds[s] for s in seeds_needed], w.n_req)
     pst, tst = O.plans_struct(w.tab), O.trace_struct(otr)
+    host = host_info()
+    pinned = None
+    if hasattr(os, "sched_setaffinity"):
+        saved = os.sched_getaffinity(0)
+        pinned = min(saved)
+        os.sched_setaffinity(0, {pinned})
     ev, n, t0 = 0, 0, time.perf_counter()
     for (i, k, s) in order:
         if s not in seeds_needed:
@@ -138,11 +161,19 @@ def cpu_baseline(w, budget_s, all_cores=0):
         if time.perf_counter() - t0 > budget_s:
             break
     dt = time.perf_counter() - t0
+    if pinned is not None:
+        os.sched_setaffinity(0, saved)
     res = {"value": ev / dt, "unit": "request-events/s", "cores": 1, "kind": "oracle",
            "sample": "%d triples of this workload drawn uniformly over plans, rates and seeds "
-                     "(%d request-events in %.1f s, single thread)" % (n, ev, dt)}
+                     "(%d request-events in %.1f s, single thread%s)"
+                     % (n, ev, dt, "" if pinned is None else ", pinned to core %d" % pinned),
+           "host": host}
+    if events_per_step:
+        res["full_step_s_extrapolated"] = events_per_step / res["value"]
     if all_cores > 1:
         res["all_cores"] = cpu_baseline_all_cores(w, ids, rates, order, seeds_needed, budget_s, all_cores)
+        if events_per_step:
+            res["all_cores"]["full_step_s_extrapolated"] = events_per_step / res["all_cores"]["value"]
     return res
 
 
@@ -576,7 +607,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("bench: cpu baseline (oracle, %.0f s budget)" % args.cpu_budget, file=sys.stderr, flush=True)
-        res["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, args.cpu_workers)
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, args.cpu_workers,
+                                           res["config"]["request_events_per_step"])
     print(json.dumps(res), flush=True)
 
 
