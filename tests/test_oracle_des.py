@@ -411,3 +411,23 @@ def test_invalid_route_is_reported():
     mc = _enc_llm_model()
     o = run(mc, plan, [dict(t=0.0, patches=300, prompt=10, out=2)])
     assert o["status"] & O.ST_INVALID
+
+
+def test_golden_fixtures():
+    """Fixtures under tests/golden: scenarios worked by hand, stored as decimals."""
+    import glob
+    import json
+    import os
+    files = sorted(glob.glob(os.path.join(os.path.dirname(__file__), "golden", "*.json")))
+    assert files
+    for fn in files:
+        g = json.load(open(fn))
+        md = g["model"]
+        mcfg = model([comp("L", "LLM", [md["p0"], md["p1"], 0.0], x=["prompt"], decode=(md["d0"], md["d1"]),
+                           batch_cap=256)], [rtype("t", ["L"], slo={"ttft": 10.0})])
+        plan = one_plan([(1, 1, md["batch"])], [[(10, {0: 0})]])
+        o = run(mcfg, plan, g["requests"])
+        lat = o["lat"]
+        for j, key in enumerate(("ttft", "tpot", "e2e")):
+            np.testing.assert_allclose(lat[:, j], g["expect"][key], rtol=g["rel_tol"], atol=0, err_msg=fn)
+        assert o["events"] == g["expect"]["request_events"], fn
