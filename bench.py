@@ -38,14 +38,19 @@ _W_C1 = ("c1: MLLM graph E->L on 8 simulated GPUs (7B LLM, 600M ViT); ~1000 plan
 _W_C4_SEED0 = ("c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse screening of 10^6 "
                "sampled plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 requests "
                "(sample: first 1 of its 64 seeds)")
+_W_C3_SEED0 = ("c3: Text-to-image graph L -> 50-step diffusion G (1024^2) mixed 50/50 with text-only LLM requests "
+               "on 32 simulated GPUs; ~50000 sampled plans; 16 rates; 64 seeds x 50000 requests "
+               "(sample: first 1 of its 64 seeds)")
 MEASURED_TRAFFIC = {
     ("c54c478f1dc57905", _W_C1): 2.0539e12,
+    ("c54c478f1dc57905", _W_C3_SEED0): 1.9634e12,
     ("c54c478f1dc57905", _W_C4_SEED0): 1.7606e13,
 }
 # VALU lane rate of the k_fine launch by rocprofv3 counters (SQ_INSTS_VALU x SQ_THREAD_CYCLES_VALU /
 # SQ_ACTIVE_INST_VALU / kernel time / PEAK_LANE_OPS), keyed like MEASURED_TRAFFIC
 MEASURED_LANE_FRAC = {
     ("c54c478f1dc57905", _W_C1): 0.4244,
+    ("c54c478f1dc57905", _W_C3_SEED0): 0.3977,
     ("c54c478f1dc57905", _W_C4_SEED0): 0.2844,
 }
 ENUM_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_enum.hip", "paper_2512_14098_amd/csrc/cf_internal.h",
