@@ -41,8 +41,11 @@ _W_C4_SEED0 = ("c4: Full coarse-to-fine sweep of the omni graph on 64 simulated 
 _W_C3_SEED0 = ("c3: Text-to-image graph L -> 50-step diffusion G (1024^2) mixed 50/50 with text-only LLM requests "
                "on 32 simulated GPUs; ~50000 sampled plans; 16 rates; 64 seeds x 50000 requests "
                "(sample: first 1 of its 64 seeds)")
+_W_C2_SEEDS2 = ("c2: Omni graph (E_img, E_aud) -> thinker -> gated talker -> audio generator on 16 simulated GPUs; "
+                "~10000 sampled plans; 16 rates; 32 seeds x 20000 requests (sample: first 2 of its 32 seeds)")
 MEASURED_TRAFFIC = {
     ("c54c478f1dc57905", _W_C1): 2.0539e12,
+    ("c54c478f1dc57905", _W_C2_SEEDS2): 9.1424e11,
     ("c54c478f1dc57905", _W_C3_SEED0): 1.9634e12,
     ("c54c478f1dc57905", _W_C4_SEED0): 1.7606e13,
 }
@@ -50,6 +53,7 @@ MEASURED_TRAFFIC = {
 # SQ_ACTIVE_INST_VALU / kernel time / PEAK_LANE_OPS), keyed like MEASURED_TRAFFIC
 MEASURED_LANE_FRAC = {
     ("c54c478f1dc57905", _W_C1): 0.4244,
+    ("c54c478f1dc57905", _W_C2_SEEDS2): 0.3076,
     ("c54c478f1dc57905", _W_C3_SEED0): 0.3977,
     ("c54c478f1dc57905", _W_C4_SEED0): 0.2844,
 }
