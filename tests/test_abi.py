@@ -12,7 +12,8 @@ LIB = os.path.join(ROOT, "paper_2512_14098_amd", "libcf.so")
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    with open(HEADER) as fh:
+        text = fh.read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][\w\s\*]*?\b(cf_\w+)\s*\(", text, flags=re.M)
     return sorted(set(names))
@@ -46,5 +47,6 @@ def test_product_path_does_not_import_the_oracle():
     for dirpath, _, files in os.walk(pkg):
         for f in files:
             if f.endswith((".py", ".hip", ".h", ".cpp")):
-                text = open(os.path.join(dirpath, f)).read()
+                with open(os.path.join(dirpath, f)) as fh:
+                    text = fh.read()
                 assert "oracle" not in re.sub(r"#.*|//.*", "", text).lower() or f == "__init__.py", f

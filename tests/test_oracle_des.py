@@ -421,7 +421,8 @@ def test_golden_fixtures():
     files = sorted(glob.glob(os.path.join(os.path.dirname(__file__), "golden", "*.json")))
     assert files
     for fn in files:
-        g = json.load(open(fn))
+        with open(fn) as f:
+            g = json.load(f)
         md = g["model"]
         mcfg = model([comp("L", "LLM", [md["p0"], md["p1"], 0.0], x=["prompt"], decode=(md["d0"], md["d1"]),
                            batch_cap=256)], [rtype("t", ["L"], slo={"ttft": 10.0})])
