@@ -8,10 +8,15 @@ reduction and selection.  Default workload: c1 (E->L on 8 simulated GPUs,
 requests).  Prints one JSON line.
 
 Other modes (each prints its own JSON line and exits): --enum times plan
-enumeration on the device and phase-1 screening of its output; --phase2 times phase 2
-(Monte Carlo latency of every plan phase 1 keeps, default workload c4) and
-Pareto pruning; --stress times the HBM-bound steps at full c4 size;
---copy-probe runs the plain copy the HBM byte counters are calibrated on.
+enumeration on the device, phase-1 screening of its output, the fused
+enumeration-and-screening kernel and a windowed screening with a running top-k;
+--phase2 times phase 2 (Monte Carlo latency of every plan phase 1 keeps, default
+workload c4) and Pareto pruning; --stress times the HBM-bound steps at full c4
+size; --copy-probe runs the plain copy the HBM byte counters are calibrated on.
+Variants of the default step: --curve N adds goodput curves over N latency-target
+scales, --bisect bisects each plan's rate instead of simulating every grid rate,
+--config/--seeds/--plans pick another workload or a sample of one.  The default
+run also times the oracle on the host (single core, then one process per core).
 """
 import argparse
 import json
