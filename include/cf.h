@@ -81,6 +81,11 @@ typedef int32_t cf_status;
 #define CF_FLAG_INVALID 4u
 #define CF_FLAG_REDUNDANT 8u
 
+/* cf_eval_fine flags (request-level simulation, Alg. 2 phase 3) */
+#define CF_FULL 0u        /* every triple is simulated until its last request completes */
+#define CF_DUMP_LAT 1u    /* also write per-request latencies of the listed triples (cf_fine_out.lat_dev) */
+#define CF_EARLY_EXIT 2u  /* stop a (plan, rate) once its attainment is certainly below theta: not built */
+
 /* cf_eval_fine per-triple status bits */
 #define CF_ST_INVALID 1u   /* a request's route does not fit the plan */
 #define CF_ST_DEADLOCK 2u  /* nothing pending but requests unfinished */
@@ -180,6 +185,16 @@ typedef struct cf_fine_out {
   uint32_t *hist_dev;
   const double *hist_targets_host;
   int32_t n_bins;
+  /* Capacity limits for tests (0 = the capacity the library sizes): every
+   * simulation of the call may hold at most lim_chunks queue chunks of 64
+   * entries, lim_delay entries in its delay line (a power of two, >= 2) and
+   * take at most lim_instants instants.  A simulation that needs more stops
+   * and reports CF_ST_OVERFLOW (chunks, delay line) or CF_ST_DEADLOCK
+   * (instants) in its status word; the kernel exits normally.  Limits above
+   * the library's own capacity are clamped to it.  Lets tests force the
+   * failure statuses from the host. */
+  int32_t lim_chunks, lim_delay;
+  uint64_t lim_instants;
 } cf_fine_out;
 
 /* Error text of the calling thread's last failed call (empty if none);
@@ -207,10 +222,15 @@ cf_status cf_eval_coarse(const cf_model_desc *model, const cf_plan_table *plans,
                          const uint64_t *moments_dev, int32_t n_gpus, double *rd_dev,
                          int32_t *bottleneck_dev, uint8_t *flags_dev, void *stream);
 
-/* Plans with CF_FLAG_KEEP ordered by R_d descending, ties by plan id
- * ascending; the first min(k, kept) ids go to ids_dev[k].  Synchronises the
- * stream and writes the number selected to *n_selected_host.
- * Limits: 1 <= k <= 65536, P <= 2^24. */
+/* The candidates phase 1 passes on (Alg. 2: plans not pruned as redundant
+ * or over budget, i.e. with CF_FLAG_KEEP, ranked by their flow-based
+ * throughput R_d; the top K go to the finer phases): plans with CF_FLAG_KEEP
+ * ordered by R_d descending, ties by plan id ascending; the first min(k,
+ * kept) ids go to ids_dev[k] (device).  rd_dev, flags_dev: cf_eval_coarse's
+ * outputs, P elements each (device).  Synchronises the stream and writes the
+ * number selected to *n_selected_host.
+ * Limits: 1 <= k <= 65536, P <= 2^24.  Errors: CF_EINVAL (NULL arrays,
+ * sizes), CF_ECAPACITY (k or P above the limits). */
 cf_status cf_select_topk(const double *rd_dev, const uint8_t *flags_dev, int32_t P, int32_t k,
                          int32_t *ids_dev, int32_t *n_selected_host, void *stream);
 
@@ -230,14 +250,25 @@ cf_status cf_topk_merge(const double *rd_run_dev, const uint64_t *gid_run_dev, i
                         const double *rd_win_dev, const int32_t *ids_win_dev, int32_t n_win, uint64_t win_first,
                         int32_t k, double *rd_out_dev, uint64_t *gid_out_dev, void *stream);
 
-/* rates_dev[i][k] = (R_d[ids_dev[i]] * alpha_max * (k+1)) / K, i < n, k < K. */
+/* Arrival-rate grid of phase 3: R_d is an ideal upper bound, so the planner
+ * simulates a plan at alpha R_d with headroom alpha <= 1 (Sec. 4.3, Alg. 2
+ * phase 3; alpha in 0.5..0.8 in Table 5); here K rates up to alpha_max R_d:
+ * rates_dev[i][k] = ((R_d[ids_dev[i]] * alpha_max) * (k+1)) / K, i < n, k < K
+ * (device arrays; rd_dev indexed by plan id).  alpha_max > 0, 1 <= K.
+ * Asynchronous on stream.  Errors: CF_EINVAL (NULL arrays, sizes, alpha). */
 cf_status cf_rate_grid(const double *rd_dev, const int32_t *ids_dev, int32_t n, int32_t K,
                        double alpha_max, double *rates_dev, void *stream);
 
 /* Phase 3 (Sec. 4.3, Alg. 2): request-level simulation of every triple
  * (plan plan_ids_dev[i], rate rates_dev[i][k], trace seed s) for i <
- * n_plans, k < K, s < trace->n_seeds, one wavefront per triple.  flags: 0.
- * Errors: CF_EINVAL (descriptor, sizes), CF_ECAPACITY, CF_ENOMEM. */
+ * n_plans, k < K, s < trace->n_seeds, one wavefront per triple.  Outputs in
+ * *out (device arrays, caller-owned).  flags: CF_FULL, or CF_DUMP_LAT to
+ * also write out->lat_dev for the out->n_lat triples listed in
+ * out->lat_triples_dev (both required with the flag, ignored without it);
+ * CF_EARLY_EXIT is not built and returns CF_EUNSUPPORTED.  Synchronises
+ * the stream (the argument block is copied from host memory).
+ * Errors: CF_EINVAL (descriptor, sizes, flags), CF_ECAPACITY, CF_ENOMEM,
+ * CF_EUNSUPPORTED. */
 cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_table *plans,
                        const int32_t *plan_ids_dev, int32_t n_plans, const double *rates_dev,
                        int32_t K, const cf_trace *trace, uint32_t flags, const cf_fine_out *out,
@@ -367,16 +398,19 @@ cf_status cf_enum_plans(const cf_model_desc *model, const cf_enum_opts *opts, co
                         int32_t n_logical, const uint64_t *offsets_dev, uint64_t total, uint64_t first,
                         int32_t count, const cf_plan_table *out, void *stream);
 
-/* Goodput (Sec. 3.2) at the highest feasible rate (Sec. 6.1): M_t, N_t
- * pooled over seeds; rate k feasible iff theta_den*M_t >= theta_num*N_t for
+/* Goodput (Sec. 3.2) at the highest feasible rate (Sec. 6.1) from the
+ * outputs of cf_eval_fine: fine->met_dev, cnt_dev [n_plans][K][S][T] and
+ * status_dev [n_plans][K][S] (device; the other fields are not read).
+ * M_t, N_t pooled over seeds; rate k is feasible iff every seed's
+ * simulation ended with status 0 and theta_den*M_t >= theta_num*N_t for
  * every type with N_t > 0; kstar = first infeasible - 1; goodput_t =
  * (rates[i][kstar] * M_t) / (S * n_req) (0 if kstar < 0); goodput = sum_t.
- * Outputs: kstar_dev[n_plans], goodput_t_dev[n_plans][T], goodput_dev[n_plans]. */
-cf_status cf_goodput_reduce(const uint32_t *met_dev, const uint32_t *cnt_dev, int32_t n_plans,
-                            int32_t K, int32_t S, int32_t T, const double *rates_dev,
-                            uint32_t theta_num, uint32_t theta_den, int32_t n_req,
-                            int32_t *kstar_dev, double *goodput_t_dev, double *goodput_dev,
-                            void *stream);
+ * Outputs: kstar_dev[n_plans], goodput_t_dev[n_plans][T], goodput_dev[n_plans].
+ * Asynchronous on stream.  Limits: K <= 64.  Errors: CF_EINVAL (NULL
+ * arrays, sizes, theta_den = 0), CF_ECAPACITY (K). */
+cf_status cf_goodput_reduce(const cf_fine_out *fine, int32_t n_plans, int32_t K, int32_t S, int32_t T,
+                            const double *rates_dev, uint32_t theta_num, uint32_t theta_den, int32_t n_req,
+                            int32_t *kstar_dev, double *goodput_t_dev, double *goodput_dev, void *stream);
 
 /* Enumeration fused with phase 1: for physical plans first .. first+count-1
  * (numbered as cf_enum_plans numbers them), exactly what cf_eval_coarse
@@ -413,14 +447,14 @@ cf_status cf_eval_bisect(const cf_model_desc *model, const cf_plan_table *plans,
 
 /* Goodput against a range of latency targets (Sec. 6.2 and Appendix B, per-type goodput
  * vs. latency target): for every plan and bin b, cf_goodput_reduce's
- * computation with M_t = the requests in bins 0..b of hist_dev (a
- * cf_fine_out histogram [n_plans][K][S][T][n_bins + 1]).  Outputs:
+ * computation with M_t = the requests in bins 0..b of fine->hist_dev (the
+ * cf_eval_fine histogram [n_plans][K][S][T][fine->n_bins + 1]), N_t from
+ * fine->cnt_dev and the status words fine->status_dev.  Outputs:
  * kstar_dev[n_plans][n_bins], goodput_t_dev[n_plans][n_bins][T],
  * goodput_dev[n_plans][n_bins].  Limits: K <= 64, 1 <= n_bins <= 64. */
-cf_status cf_goodput_curve(const uint32_t *hist_dev, const uint32_t *cnt_dev, int32_t n_plans, int32_t K,
-                           int32_t S, int32_t T, int32_t n_bins, const double *rates_dev, uint32_t theta_num,
-                           uint32_t theta_den, int32_t n_req, int32_t *kstar_dev, double *goodput_t_dev,
-                           double *goodput_dev, void *stream);
+cf_status cf_goodput_curve(const cf_fine_out *fine, int32_t n_plans, int32_t K, int32_t S, int32_t T,
+                           const double *rates_dev, uint32_t theta_num, uint32_t theta_den, int32_t n_req,
+                           int32_t *kstar_dev, double *goodput_t_dev, double *goodput_dev, void *stream);
 
 /* Selection (Alg. 2, last step): index of the largest goodput, ties to the
  * lowest index, written to best_dev[0]. */

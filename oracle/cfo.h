@@ -214,13 +214,18 @@ int cfo_sim_triple(const cfo_model *m, const cfo_plans *pl, int32_t plan_id, dou
                    uint64_t *events, uint32_t *status, double *lat, double *diag);
 
 /* Rate bisection over each plan's grid (seeds pooled, the attainment test
- * of cfo_goodput_reduce): kstar, goodput_t [n][T], goodput [n], n_eval
+ * of cfo_goodput_reduce; a rate where some seed's simulation fails is
+ * infeasible): kstar, goodput_t [n][T], goodput [n], n_eval
  * (rates simulated per plan), events (request-events simulated per plan). */
 int cfo_bisect(const cfo_model *m, const cfo_plans *pl, const int32_t *plan_ids, int32_t n_plans,
                const double *rates, int32_t K, const cfo_trace *tr, uint32_t theta_num, uint32_t theta_den,
                int32_t *kstar, double *goodput_t, double *goodput, int32_t *n_eval, uint64_t *events);
 
-int cfo_goodput_reduce(const uint32_t *met, const uint32_t *cnt, int32_t n_plans, int32_t K,
+/* Goodput at the highest feasible grid rate (Sec. 3.2, Sec. 6.1): met, cnt
+ * [n][K][S][T], status [n][K][S]; rate k is feasible iff every seed's
+ * simulation ended with status 0 and theta_den M_t >= theta_num N_t for
+ * every type with N_t > 0 (counts pooled over seeds). */
+int cfo_goodput_reduce(const uint32_t *met, const uint32_t *cnt, const uint32_t *status, int32_t n_plans, int32_t K,
                        int32_t S, int32_t T, const double *rates, uint32_t theta_num,
                        uint32_t theta_den, int32_t n_req, int32_t *kstar, double *goodput_t,
                        double *goodput);

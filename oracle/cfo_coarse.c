@@ -172,8 +172,8 @@ int cfo_rate_grid(const double *rd, const int32_t *ids, int32_t n, int32_t K, do
 }
 
 /* ---------------- goodput ---------------- */
-int cfo_goodput_reduce(const uint32_t *met, const uint32_t *cnt, int32_t n_plans, int32_t K,
-                       int32_t S, int32_t T, const double *rates, uint32_t theta_num,
+int cfo_goodput_reduce(const uint32_t *met, const uint32_t *cnt, const uint32_t *status, int32_t n_plans,
+                       int32_t K, int32_t S, int32_t T, const double *rates, uint32_t theta_num,
                        uint32_t theta_den, int32_t n_req, int32_t *kstar, double *goodput_t,
                        double *goodput) {
   double denom = (double)((uint64_t)S * (uint64_t)n_req);
@@ -181,6 +181,9 @@ int cfo_goodput_reduce(const uint32_t *met, const uint32_t *cnt, int32_t n_plans
     int ks = K - 1;
     for (int k = 0; k < K; k++) {
       int feasible = 1;
+      /* a simulation that failed (nonzero status) leaves counts that prove nothing */
+      for (int s = 0; s < S; s++)
+        if (status[((size_t)i * K + k) * S + s] != 0) feasible = 0;
       for (int t = 0; t < T; t++) {
         uint64_t M = 0, N = 0;
         for (int s = 0; s < S; s++) {

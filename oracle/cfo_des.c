@@ -418,6 +418,8 @@ int cfo_sim_triple(const cfo_model *m, const cfo_plans *pl, int32_t plan_id, dou
   *events = 0;
   *status = 0;
   if (diag) for (int i = 0; i < 4; i++) diag[i] = 0.0;
+  /* a Poisson arrival rate is positive and finite; a plan id names a column of the table */
+  if (p < 0 || p >= P || !(rate > 0.0) || !(rate < __builtin_inf())) { *status = CFO_ST_INVALID; return 0; }
 
   /* executors: replicas of each node, numbered node by node */
   int nv = pl->n_nodes[p];
@@ -553,18 +555,20 @@ int cfo_bisect(const cfo_model *m, const cfo_plans *pl, const int32_t *plan_ids,
       const int mid = (lo + hi) / 2;
       uint64_t M[CFO_MAXT], N[CFO_MAXT];
       for (int t = 0; t < T; t++) M[t] = N[t] = 0;
+      int failed = 0;
       for (int s = 0; s < S; s++) {
         uint64_t ev = 0;
         uint32_t st = 0;
         cfo_sim_triple(m, pl, plan_ids[i], rates[(size_t)i * K + mid], tr, s, met, cnt, &ev, &st, NULL, NULL);
         ev_total += ev;
+        if (st != 0) failed = 1;
         for (int t = 0; t < T; t++) {
           M[t] += met[t];
           N[t] += cnt[t];
         }
       }
       ne++;
-      int feasible = 1;
+      int feasible = !failed;
       for (int t = 0; t < T; t++)
         if (N[t] > 0 && (uint64_t)theta_den * M[t] < (uint64_t)theta_num * N[t]) feasible = 0;
       if (feasible) {

@@ -99,7 +99,7 @@ def lib():
         L.cfo_select_topk.argtypes = [vp, vp, i32, i32, vp, vp]
         L.cfo_rate_grid.argtypes = [vp, vp, i32, i32, dbl, vp]
         L.cfo_sim_triple.argtypes = [vp, vp, i32, dbl, vp, i32, vp, vp, vp, vp, vp, vp]
-        L.cfo_goodput_reduce.argtypes = [vp, vp, i32, i32, i32, i32, vp, C.c_uint32, C.c_uint32,
+        L.cfo_goodput_reduce.argtypes = [vp, vp, vp, i32, i32, i32, i32, vp, C.c_uint32, C.c_uint32,
                                          i32, vp, vp, vp]
         L.cfo_bisect.argtypes = [vp, vp, vp, i32, vp, i32, vp, C.c_uint32, C.c_uint32, vp, vp, vp, vp, vp]
         L.cfo_latency_hist.argtypes = [vp, vp, i32, i32, i32, vp, vp]
@@ -352,15 +352,21 @@ def pareto(g):
     return keep
 
 
-def goodput_reduce(met, cnt, rates, theta, n_req):
+def goodput_reduce(met, cnt, rates, theta, n_req, status=None):
+    """Highest feasible rate and goodput per plan; status [n_plans, K, S] (None: every
+    simulation ended normally) makes a rate with a failed simulation infeasible."""
     n_plans, K, S, T = met.shape
+    if status is None:
+        status = np.zeros((n_plans, K, S), np.uint32)
+    status = np.ascontiguousarray(status, np.uint32)
+    assert status.shape == (n_plans, K, S)
     kstar = np.zeros(n_plans, np.int32)
     gt = np.zeros((n_plans, T), np.float64)
     g = np.zeros(n_plans, np.float64)
     if np.asarray(met).max(initial=0) > 0xFFFFFFFF or np.asarray(cnt).max(initial=0) > 0xFFFFFFFF:
         raise ValueError("counts above 32 bits")
     lib().cfo_goodput_reduce(_ptr(np.ascontiguousarray(met, np.uint32)), _ptr(np.ascontiguousarray(cnt, np.uint32)),
-                             n_plans, K, S, T, _ptr(np.ascontiguousarray(rates, np.float64)), int(theta[0]),
+                             _ptr(status), n_plans, K, S, T, _ptr(np.ascontiguousarray(rates, np.float64)), int(theta[0]),
                              int(theta[1]), int(n_req), _ptr(kstar), _ptr(gt), _ptr(g))
     return kstar, gt, g
 

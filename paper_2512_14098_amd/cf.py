@@ -21,6 +21,7 @@ ATTR = {"prompt": 0, "out": 1, "patches": 2, "aud_in_ms": 3, "aud_out_ms": 4, "a
         "aud_out_tok": 6}
 FLAG_KEEP, FLAG_OVER_BUDGET, FLAG_INVALID, FLAG_REDUNDANT = 1, 2, 4, 8
 ST_INVALID, ST_DEADLOCK, ST_OVERFLOW = 1, 2, 4
+CF_FULL, CF_DUMP_LAT, CF_EARLY_EXIT = 0, 1, 2  # cf_eval_fine flags
 
 
 class CfError(RuntimeError):
@@ -77,7 +78,8 @@ class cf_fine_out(C.Structure):
     _fields_ = [("met_dev", C.c_void_p), ("cnt_dev", C.c_void_p), ("events_dev", C.c_void_p),
                 ("status_dev", C.c_void_p), ("lat_dev", C.c_void_p), ("lat_triples_dev", C.c_void_p),
                 ("n_lat", C.c_int32), ("hist_dev", C.c_void_p), ("hist_targets_host", C.c_void_p),
-                ("n_bins", C.c_int32)]
+                ("n_bins", C.c_int32), ("lim_chunks", C.c_int32), ("lim_delay", C.c_int32),
+                ("lim_instants", C.c_uint64)]
 
 
 def _load():
@@ -95,12 +97,11 @@ def _load():
         "cf_rate_grid": ([vp, vp, i32, i32, dbl, vp, vp], i32),
         "cf_topk_merge": ([vp, vp, i32, vp, vp, i32, C.c_uint64, i32, vp, vp, vp], i32),
         "cf_eval_fine": ([vp, vp, vp, i32, vp, i32, vp, u32, vp, vp], i32),
-        "cf_goodput_reduce": ([vp, vp, i32, i32, i32, i32, vp, u32, u32, i32, vp, vp, vp, vp], i32),
+        "cf_goodput_reduce": ([vp, i32, i32, i32, i32, vp, u32, u32, i32, vp, vp, vp, vp], i32),
         "cf_eval_mc": ([vp, vp, vp, i32, vp, vp, dbl, vp, i32, i32, vp, vp, vp, vp, vp], i32),
         "cf_pareto": ([vp, i32, i32, vp, vp, vp, i32, vp], i32),
         "cf_eval_mc_curve": ([vp, vp, vp, i32, vp, vp, dbl, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp], i32),
-        "cf_goodput_curve": ([vp, vp, i32, i32, i32, i32, i32, vp, C.c_uint32, C.c_uint32, i32, vp, vp, vp, vp],
-                             i32),
+        "cf_goodput_curve": ([vp, i32, i32, i32, i32, vp, C.c_uint32, C.c_uint32, i32, vp, vp, vp, vp], i32),
         "cf_eval_bisect": ([vp, vp, vp, i32, vp, i32, vp, C.c_uint32, C.c_uint32, vp, vp, vp, vp, vp, vp, vp], i32),
         "cf_enum_screen": ([vp, vp, vp, i32, vp, C.c_uint64, C.c_uint64, i32, vp, i32, vp, vp, vp, vp], i32),
         "cf_enum_logical": ([vp, vp, vp, i32, vp], i32),
@@ -369,9 +370,11 @@ def _targets(targets, T):
     return tg
 
 
-def cf_eval_fine(desc, plans, plan_ids, rates, trace, lat_triples=None, targets=None):
+def cf_eval_fine(desc, plans, plan_ids, rates, trace, lat_triples=None, targets=None, limits=None):
     """Phase 3 of every (plan, rate, seed); with targets ([T][n_bins][4], bounds not
-    decreasing with the bin) also the latency histograms hist [n_plans][K][S][T][n_bins+1]."""
+    decreasing with the bin) also the latency histograms hist [n_plans][K][S][T][n_bins+1];
+    with lat_triples the per-request latencies of those triples (CF_DUMP_LAT); limits: a
+    dict of the test capacity limits (chunks, delay, instants) of cf_fine_out."""
     n_plans, K = rates.shape
     S, T, dev = trace.n_seeds, desc.n_types, rates.device
     met = torch.empty((n_plans, K, S, T), dtype=torch.int32, device=dev)
@@ -381,19 +384,24 @@ def cf_eval_fine(desc, plans, plan_ids, rates, trace, lat_triples=None, targets=
     out = cf_fine_out()
     out.met_dev, out.cnt_dev = met.data_ptr(), cnt.data_ptr()
     out.events_dev, out.status_dev = events.data_ptr(), status.data_ptr()
-    lat = None
+    lat, flags = None, CF_FULL
     if lat_triples is not None and len(lat_triples) > 0:
         lt = torch.as_tensor(np.asarray(lat_triples, np.int32), device=dev)
         lat = torch.zeros((len(lat_triples), trace.n_req, 4), dtype=torch.float64, device=dev)
         out.lat_dev, out.lat_triples_dev, out.n_lat = lat.data_ptr(), lt.data_ptr(), len(lat_triples)
+        flags |= CF_DUMP_LAT
+    if limits:
+        out.lim_chunks = int(limits.get("chunks", 0))
+        out.lim_delay = int(limits.get("delay", 0))
+        out.lim_instants = int(limits.get("instants", 0))
     hist = None
     if targets is not None:
         tg = _targets(targets, T)
         hist = torch.empty((n_plans, K, S, T, tg.shape[1] + 1), dtype=torch.int32, device=dev)
         out.hist_dev, out.hist_targets_host, out.n_bins = hist.data_ptr(), tg.ctypes.data, tg.shape[1]
     _check(_lib.cf_eval_fine(C.byref(desc), C.byref(plans.c), _in(plan_ids, torch.int32, "plan_ids", n_plans),
-                             int(n_plans), _in(rates, torch.float64, "rates", ndim=2), int(K), C.byref(trace.c), 0,
-                             C.byref(out),
+                             int(n_plans), _in(rates, torch.float64, "rates", ndim=2), int(K), C.byref(trace.c),
+                             flags, C.byref(out),
                              _stream()), "cf_eval_fine")
     return dict(met=met, cnt=cnt, events=events, status=status, lat=lat, hist=hist)
 
@@ -451,16 +459,31 @@ def cf_eval_mc_curve(desc, plans, plan_ids, rd, moments_seed, alpha, trace, seed
     return dict(met=met, cnt=cnt, goodput_t=gt, hist=hist, curve=curve)
 
 
-def cf_goodput_curve(hist, cnt, rates, theta, n_req):
-    """Goodput against every target bin of a phase-3 histogram: kstar [n][nb],
-    goodput_t [n][nb][T], goodput [n][nb]."""
-    n_plans, K, S, T, hw = hist.shape
-    nb, dev = hw - 1, hist.device
+def _fine_view(fine, with_hist):
+    """cf_fine_out over the arrays of a cf_eval_fine result (met, cnt, status[, hist])."""
+    n_plans, K, S, T = fine["met"].shape
+    o = cf_fine_out()
+    o.met_dev = _in(fine["met"], torch.int32, "met")
+    o.cnt_dev = _in(fine["cnt"], torch.int32, "cnt", n_plans * K * S * T)
+    o.status_dev = _in(fine["status"], torch.int32, "status", n_plans * K * S)
+    if with_hist:
+        hist = fine["hist"]
+        if hist is None or hist.dim() != 5 or tuple(hist.shape[:4]) != (n_plans, K, S, T):
+            raise CfError("hist must be [n_plans][K][S][T][n_bins + 1]")
+        o.hist_dev = _in(hist, torch.int32, "hist")
+        o.n_bins = int(hist.shape[4]) - 1
+    return o, (n_plans, K, S, T)
+
+
+def cf_goodput_curve(fine, rates, theta, n_req):
+    """Goodput against every target bin of a phase-3 histogram (fine: a cf_eval_fine
+    result with hist): kstar [n][nb], goodput_t [n][nb][T], goodput [n][nb]."""
+    o, (n_plans, K, S, T) = _fine_view(fine, True)
+    nb, dev = o.n_bins, fine["met"].device
     kstar = torch.empty((n_plans, nb), dtype=torch.int32, device=dev)
     gt = torch.empty((n_plans, nb, T), dtype=torch.float64, device=dev)
     g = torch.empty((n_plans, nb), dtype=torch.float64, device=dev)
-    _check(_lib.cf_goodput_curve(_in(hist, torch.int32, "hist"), _in(cnt, torch.int32, "cnt", n_plans * K * S * T),
-                                 n_plans, K, S, T, nb, _in(rates, torch.float64, "rates", n_plans * K),
+    _check(_lib.cf_goodput_curve(C.byref(o), n_plans, K, S, T, _in(rates, torch.float64, "rates", n_plans * K),
                                  int(theta[0]), int(theta[1]), int(n_req), _p(kstar), _p(gt), _p(g), _stream()),
            "cf_goodput_curve")
     return kstar, gt, g
@@ -552,14 +575,15 @@ def cf_enum_screen(desc, opts, logical_dev, offsets, total, first, count, moment
     return rd, bott, flags
 
 
-def cf_goodput_reduce(met, cnt, rates, theta, n_req):
-    n_plans, K, S, T = met.shape
-    dev = met.device
+def cf_goodput_reduce(fine, rates, theta, n_req):
+    """Highest feasible rate and goodput per plan from a cf_eval_fine result (met, cnt,
+    status): kstar [n], goodput_t [n][T], goodput [n]."""
+    o, (n_plans, K, S, T) = _fine_view(fine, False)
+    dev = fine["met"].device
     kstar = torch.empty(n_plans, dtype=torch.int32, device=dev)
     gt = torch.empty((n_plans, T), dtype=torch.float64, device=dev)
     g = torch.empty(n_plans, dtype=torch.float64, device=dev)
-    _check(_lib.cf_goodput_reduce(_in(met, torch.int32, "met"), _in(cnt, torch.int32, "cnt", met.numel()), n_plans, K,
-                                  S, T, _in(rates, torch.float64, "rates", n_plans * K),
+    _check(_lib.cf_goodput_reduce(C.byref(o), n_plans, K, S, T, _in(rates, torch.float64, "rates", n_plans * K),
                                   int(theta[0]), int(theta[1]), int(n_req), _p(kstar), _p(gt), _p(g),
                                   _stream()), "cf_goodput_reduce")
     return kstar, gt, g

@@ -28,6 +28,30 @@ hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
 
 static bool finite_nonneg(double v) { return isfinite(v) && v >= 0.0; }
 
+// largest value attribute a (CF_ATTR_*) of a type-t request can take
+static uint64_t attr_hi(const cf_model_desc *d, int t, int a) {
+  auto len_hi = [&](int j) -> uint64_t {
+    const cf_dist &L = d->len[t][j];
+    if (L.kind == CF_DIST_NONE) return 0;
+    if (L.kind == CF_DIST_CONST) return (uint64_t)ceil(L.p0);
+    return (uint64_t)L.hi;
+  };
+  switch (a) {
+    case CF_ATTR_PROMPT: return len_hi(0);
+    case CF_ATTR_OUT: return len_hi(1);
+    case CF_ATTR_PATCHES: {
+      if (d->img_kind[t] == CF_IMG_NONE) return 0;
+      const uint64_t n = (uint64_t)(d->img_lo[t] > d->img_hi[t] ? d->img_lo[t] : d->img_hi[t]);
+      return n * (uint64_t)d->patch_hi;
+    }
+    case CF_ATTR_AUDIN_MS: return len_hi(2);
+    case CF_ATTR_AUDOUT_MS: return len_hi(3);
+    case CF_ATTR_AUDIN_TOK: return (len_hi(2) + 79u) / 80u;
+    case CF_ATTR_AUDOUT_TOK: return (len_hi(3) + 79u) / 80u;
+    default: return 0;
+  }
+}
+
 cf_status lower_model(const cf_model_desc *d, KModel *k) {
   if (!d) return set_error(CF_EINVAL, "model descriptor is NULL");
   memset(k, 0, sizeof *k);
@@ -145,6 +169,16 @@ cf_status lower_model(const cf_model_desc *d, KModel *k) {
     for (int j = 0; j < 4; j++) {
       if (isnan(d->slo[t][j])) return set_error(CF_EINVAL, "slo[%d][%d] is NaN", t, j);
       k->slo[t][j] = d->slo[t][j];
+    }
+  }
+  // the simulator of models with a gated stage keeps that stage's own output
+  // length of a running request in 15 bits
+  for (int c = 0; c < nc; c++) {
+    if (!((k->gated_mask >> c) & 1u)) continue;
+    for (int t = 0; t < nt; t++) {
+      if (!((d->path_mask[t] >> c) & 1u) || ((d->prefill_only[t] >> c) & 1u)) continue;
+      if (attr_hi(d, t, d->nout_attr[c]) > 32767u)
+        return set_error(CF_EUNSUPPORTED, "gated component %d: output length of type %d can exceed 32767 tokens", c, t);
     }
   }
   if (wsum == 0 || wsum > 0xFFFFFFFFull) return set_error(CF_EINVAL, "type weights must sum to 1..2^32-1");

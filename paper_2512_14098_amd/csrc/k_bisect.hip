@@ -96,6 +96,7 @@ __global__ void k_bisect_update(BisectState B, int n_act, int S, int T, uint32_t
   B.events[i] += ev;
   B.status[i] |= st;
   B.n_eval[i] += 1;
+  if (st != 0) feasible = false;  // counts of a failed simulation are not evidence of attainment
   if (feasible) {
     B.lo[i] = mid;
     for (int t = 0; t < T; t++) B.mlo[(size_t)i * T + t] = M[t];

@@ -137,6 +137,7 @@ struct FineArgs {
   unsigned int total;
   int nsi_cap;  // stage instances provided in LDS
   int nl_cap, nt_cap;  // k_fine<true>: LLM stage instances and thinker ring slots provided in LDS
+  uint64_t lim_instants;  // instants a simulation may take (a test limit; ~0 = none)
 };
 
 // model tables read with per-lane (divergent) indices
@@ -1936,7 +1937,7 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
         t = S.t_arr < t ? S.t_arr : t;
         if (t == __builtin_inf()) break;
         S.now = t;
-        if (++instants > 2 * S.events + 16ull * (uint64_t)A.n + 4096ull) {
+        if (++instants > 2 * S.events + 16ull * (uint64_t)A.n + 4096ull || instants > A.lim_instants) {
           S.status |= CF_ST_DEADLOCK;
           break;
         }
@@ -2101,15 +2102,20 @@ extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_tabl
   cf_status st = lower_model(model, &a.m);
   if (st != CF_OK) return st;
   if (!plans || !trace || !out) return set_error(CF_EINVAL, "NULL argument");
-  if (flags != 0) return set_error(CF_EUNSUPPORTED, "flags must be 0");
+  if (flags & ~(CF_DUMP_LAT | CF_EARLY_EXIT)) return set_error(CF_EINVAL, "unknown flags");
+  if (flags & CF_EARLY_EXIT) return set_error(CF_EUNSUPPORTED, "CF_EARLY_EXIT is not built");
+  const bool dump = (flags & CF_DUMP_LAT) != 0;
   if (n_plans < 0 || K < 1 || trace->n_seeds < 1 || trace->n_req < 0 || plans->P < 0)
     return set_error(CF_EINVAL, "sizes");
   if (n_plans == 0) return CF_OK;
   if (!plan_ids_dev || !rates_dev) return set_error(CF_EINVAL, "NULL argument");
   if (!out->met_dev || !out->cnt_dev || !out->events_dev || !out->status_dev)
     return set_error(CF_EINVAL, "NULL output array");
-  if (out->lat_dev && (out->n_lat < 0 || (out->n_lat > 0 && !out->lat_triples_dev)))
+  if (dump && (!out->lat_dev || out->n_lat < 0 || (out->n_lat > 0 && !out->lat_triples_dev)))
     return set_error(CF_EINVAL, "latency dump arguments");
+  if (out->lim_chunks < 0 || out->lim_delay < 0 ||
+      (out->lim_delay != 0 && (out->lim_delay < 2 || (out->lim_delay & (out->lim_delay - 1)) != 0)))
+    return set_error(CF_EINVAL, "test limits: lim_chunks >= 0, lim_delay 0 or a power of two >= 2");
   if (trace->n_req > (1 << 26)) return set_error(CF_ECAPACITY, "n_req above 2^26");
   const unsigned long long total = (unsigned long long)n_plans * K * trace->n_seeds;
   if (total >= 0xFFFFFFFFull - 65536ull) return set_error(CF_ECAPACITY, "too many triples in one call");
@@ -2142,14 +2148,18 @@ extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_tabl
   a.cnt = out->cnt_dev;
   a.events = out->events_dev;
   a.status = out->status_dev;
-  a.lat = out->lat_dev;
-  a.lat_triples = out->lat_triples_dev;
-  a.n_lat = out->lat_dev ? out->n_lat : 0;
+  a.lat = dump ? out->lat_dev : nullptr;
+  a.lat_triples = dump ? out->lat_triples_dev : nullptr;
+  a.n_lat = dump ? out->n_lat : 0;
   a.hist = nullptr;
   a.tg = nullptr;
   a.nb = 0;
   a.L = make_layout(a.m, trace->n_req);
   a.total = (unsigned int)total;
+  // test limits: smaller capacities inside the same slab (every index stays below the capped value)
+  if (out->lim_chunks > 0 && out->lim_chunks < a.L.n_chunks) a.L.n_chunks = out->lim_chunks;
+  if (out->lim_delay > 0 && (uint32_t)(out->lim_delay - 1) < a.L.dl_mask) a.L.dl_mask = (uint32_t)(out->lim_delay - 1);
+  a.lim_instants = out->lim_instants ? out->lim_instants : ~0ull;
   long long waves = 8192;
   if (const char *e = getenv("CF_FINE_WAVES")) waves = atoll(e);
   if (waves < 1) waves = 1;

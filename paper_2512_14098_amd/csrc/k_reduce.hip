@@ -7,18 +7,22 @@
 // maximises the sum over types (Alg. 2).  One wavefront per plan: lane k
 // pools rate k's counts over seeds (u64, exact), a ballot of the infeasible
 // rates gives the first failure (what bisection over a monotone predicate
-// returns), and lanes t compute the per-type goodput at that rate.
+// returns), and lanes t compute the per-type goodput at that rate.  A rate
+// at which some seed's simulation ended with a nonzero status word (invalid
+// plan or rate, exceeded capacity, deadlock) is infeasible: its counts are
+// truncated and say nothing about attainment.
 #include "cf_internal.h"
 
 namespace cf {
 namespace {
 
-__global__ void __launch_bounds__(64) k_goodput(const uint32_t *met, const uint32_t *cnt, int K, int S, int T,
-                                               const double *rates, uint32_t tn, uint32_t td, double denom,
-                                               int32_t *kstar, double *goodput_t, double *goodput) {
+__global__ void __launch_bounds__(64) k_goodput(const uint32_t *met, const uint32_t *cnt, const uint32_t *status,
+                                               int K, int S, int T, const double *rates, uint32_t tn, uint32_t td,
+                                               double denom, int32_t *kstar, double *goodput_t, double *goodput) {
   const int i = blockIdx.x, lane = threadIdx.x;
   bool infeasible = false;
   if (lane < K) {
+    for (int s = 0; s < S; s++) infeasible |= status[((size_t)i * K + lane) * S + s] != 0u;
     for (int t = 0; t < T; t++) {
       uint64_t M = 0, N = 0;
       for (int s = 0; s < S; s++) {
@@ -48,10 +52,10 @@ __global__ void __launch_bounds__(64) k_goodput(const uint32_t *met, const uint3
 
 // The same computation per latency-target bin b: block (i, b), lane k pools
 // rate k's requests in bins 0..b over seeds.
-__global__ void __launch_bounds__(64) k_goodput_curve(const uint32_t *hist, const uint32_t *cnt, int K, int S, int T,
-                                                     int nb, const double *rates, uint32_t tn, uint32_t td,
-                                                     double denom, int32_t *kstar, double *goodput_t,
-                                                     double *goodput) {
+__global__ void __launch_bounds__(64) k_goodput_curve(const uint32_t *hist, const uint32_t *cnt,
+                                                     const uint32_t *status, int K, int S, int T, int nb,
+                                                     const double *rates, uint32_t tn, uint32_t td, double denom,
+                                                     int32_t *kstar, double *goodput_t, double *goodput) {
   const int i = blockIdx.x, b = blockIdx.y, lane = threadIdx.x;
   const int hw = nb + 1;
   auto pooled = [&](int k, int t) {
@@ -64,6 +68,7 @@ __global__ void __launch_bounds__(64) k_goodput_curve(const uint32_t *hist, cons
   };
   bool infeasible = false;
   if (lane < K) {
+    for (int s = 0; s < S; s++) infeasible |= status[((size_t)i * K + lane) * S + s] != 0u;
     for (int t = 0; t < T; t++) {
       uint64_t N = 0;
       for (int s = 0; s < S; s++) N += cnt[(((size_t)i * K + lane) * S + s) * T + t];
@@ -139,40 +144,44 @@ __global__ void k_philox(const uint64_t *ctr, const uint64_t *key, uint64_t *out
 }  // namespace
 }  // namespace cf
 
-extern "C" cf_status cf_goodput_reduce(const uint32_t *met_dev, const uint32_t *cnt_dev, int32_t n_plans,
-                                       int32_t K, int32_t S, int32_t T, const double *rates_dev,
-                                       uint32_t theta_num, uint32_t theta_den, int32_t n_req,
-                                       int32_t *kstar_dev, double *goodput_t_dev, double *goodput_dev,
-                                       void *stream) {
+extern "C" cf_status cf_goodput_reduce(const cf_fine_out *fine, int32_t n_plans, int32_t K, int32_t S, int32_t T,
+                                       const double *rates_dev, uint32_t theta_num, uint32_t theta_den,
+                                       int32_t n_req, int32_t *kstar_dev, double *goodput_t_dev,
+                                       double *goodput_dev, void *stream) {
   using namespace cf;
-  if (!met_dev || !cnt_dev || !rates_dev || !kstar_dev || !goodput_t_dev || !goodput_dev)
+  if (!fine || !fine->met_dev || !fine->cnt_dev || !fine->status_dev || !rates_dev || !kstar_dev ||
+      !goodput_t_dev || !goodput_dev)
     return set_error(CF_EINVAL, "NULL argument");
   if (n_plans < 0 || K < 1 || S < 1 || T < 1 || T > CF_MAX_TYPES || n_req < 0 || theta_den == 0)
     return set_error(CF_EINVAL, "sizes");
   if (K > 64) return set_error(CF_ECAPACITY, "K above 64 (one lane per rate)");
   if (n_plans == 0) return CF_OK;
   const double denom = (double)((uint64_t)S * (uint64_t)n_req);
-  hipLaunchKernelGGL(k_goodput, dim3((unsigned)n_plans), dim3(64), 0, as_stream(stream), met_dev, cnt_dev, K, S, T,
-                     rates_dev, theta_num, theta_den, denom, kstar_dev, goodput_t_dev, goodput_dev);
+  hipLaunchKernelGGL(k_goodput, dim3((unsigned)n_plans), dim3(64), 0, as_stream(stream), fine->met_dev,
+                     fine->cnt_dev, fine->status_dev, K, S, T, rates_dev, theta_num, theta_den, denom, kstar_dev,
+                     goodput_t_dev, goodput_dev);
   return hip_check(hipGetLastError(), "cf_goodput_reduce launch");
 }
 
-extern "C" cf_status cf_goodput_curve(const uint32_t *hist_dev, const uint32_t *cnt_dev, int32_t n_plans, int32_t K,
-                                      int32_t S, int32_t T, int32_t n_bins, const double *rates_dev,
-                                      uint32_t theta_num, uint32_t theta_den, int32_t n_req, int32_t *kstar_dev,
-                                      double *goodput_t_dev, double *goodput_dev, void *stream) {
+extern "C" cf_status cf_goodput_curve(const cf_fine_out *fine, int32_t n_plans, int32_t K, int32_t S, int32_t T,
+                                      const double *rates_dev, uint32_t theta_num, uint32_t theta_den,
+                                      int32_t n_req, int32_t *kstar_dev, double *goodput_t_dev, double *goodput_dev,
+                                      void *stream) {
   using namespace cf;
+  if (!fine) return set_error(CF_EINVAL, "NULL argument");
+  const int32_t n_bins = fine->n_bins;
   if (n_plans < 0 || K < 1 || S < 1 || T < 1 || T > CF_MAX_TYPES || n_req < 0 || theta_den == 0)
     return set_error(CF_EINVAL, "sizes");
   if (n_bins < 1 || n_bins > 64) return set_error(CF_EINVAL, "n_bins must be in 1..64");
   if (K > 64) return set_error(CF_ECAPACITY, "K above 64 (one lane per rate)");
   if (n_plans == 0) return CF_OK;
-  if (!hist_dev || !cnt_dev || !rates_dev || !kstar_dev || !goodput_t_dev || !goodput_dev)
+  if (!fine->hist_dev || !fine->cnt_dev || !fine->status_dev || !rates_dev || !kstar_dev || !goodput_t_dev ||
+      !goodput_dev)
     return set_error(CF_EINVAL, "NULL device array");
   const double denom = (double)((uint64_t)S * (uint64_t)n_req);
   hipLaunchKernelGGL(k_goodput_curve, dim3((unsigned)n_plans, (unsigned)n_bins), dim3(64), 0, as_stream(stream),
-                     hist_dev, cnt_dev, K, S, T, n_bins, rates_dev, theta_num, theta_den, denom, kstar_dev,
-                     goodput_t_dev, goodput_dev);
+                     fine->hist_dev, fine->cnt_dev, fine->status_dev, K, S, T, n_bins, rates_dev, theta_num,
+                     theta_den, denom, kstar_dev, goodput_t_dev, goodput_dev);
   return hip_check(hipGetLastError(), "cf_goodput_curve launch");
 }
 

@@ -107,12 +107,12 @@ def run_step(w, timers=None):
     if w.bisect:
         kstar, gt, g = fine["kstar"], fine["goodput_t"], fine["goodput"]
     else:
-        kstar, gt, g = cf.cf_goodput_reduce(fine["met"], fine["cnt"], rates, w.theta, w.n_req)
+        kstar, gt, g = cf.cf_goodput_reduce(fine, rates, w.theta, w.n_req)
     best = cf.cf_select_best(g) if ids.numel() > 0 else None
     curve = None
     if w.targets is not None and ids.numel() > 0 and not w.bisect:
         curve = dict(zip(("kstar", "goodput_t", "goodput"),
-                         cf.cf_goodput_curve(fine["hist"], fine["cnt"], rates, w.theta, w.n_req)))
+                         cf.cf_goodput_curve(fine, rates, w.theta, w.n_req)))
     mark("reduce")
     if timers is not None:
         timers.update(ev)

@@ -26,6 +26,28 @@ def test_header_declares_the_path():
         assert f in names
 
 
+def _comment_before(text, name):
+    """The block comment that ends right before the declaration of name."""
+    m = re.search(r"/\*((?:(?!\*/).)*?)\*/\s*(?:const\s+)?[A-Za-z_][\w\s\*]*?\b" + name + r"\s*\(", text, flags=re.S)
+    assert m, name
+    return m.group(1)
+
+
+def test_path_calls_cite_the_passage_they_follow():
+    """Each call of the hot path names the section, algorithm or equation it follows, and the
+    capacity / flag contract of cf_eval_fine and cf_goodput_reduce is stated."""
+    with open(HEADER) as fh:
+        text = fh.read()
+    cite = re.compile(r"Sec\. \d|Alg\. \d|Eq\. \(\d|Table \d")
+    for f in ("cf_trace_gen", "cf_eval_coarse", "cf_select_topk", "cf_rate_grid", "cf_eval_fine",
+              "cf_goodput_reduce", "cf_select_best"):
+        assert cite.search(_comment_before(text, f)), f
+    for flag in ("CF_FULL", "CF_DUMP_LAT", "CF_EARLY_EXIT"):
+        assert re.search(r"#define " + flag + r"\b", text), flag
+        assert flag in _comment_before(text, "cf_eval_fine"), flag
+    assert "status" in _comment_before(text, "cf_goodput_reduce")
+
+
 @pytest.mark.skipif(not os.path.exists(LIB), reason="libcf.so not built")
 def test_library_exports_every_declared_function():
     lib = ctypes.CDLL(LIB)

@@ -86,7 +86,7 @@ def test_fine_histograms_and_curves(cf, name, n_plans, seeds, n):
     assert np.array_equal(np.cumsum(hist, axis=-1).astype(np.uint32)[..., -1],
                           out["cnt"].cpu().numpy().view(np.uint32))
     # goodput against every target: the plain reduction of the oracle's cumulative counts, bin by bin
-    ks, gt, g = cf.cf_goodput_curve(out["hist"], out["cnt"], torch.from_numpy(rates).cuda(), (9, 10), n)
+    ks, gt, g = cf.cf_goodput_curve(out, torch.from_numpy(rates).cuda(), (9, 10), n)
     ks, gt, g = ks.cpu().numpy(), gt.cpu().numpy(), g.cpu().numpy()
     cnt = np.ascontiguousarray(cum[..., -1])
     for b in range(nb):

@@ -164,11 +164,10 @@ def test_fine_c0_all_triples_and_latencies(cf):
         np.testing.assert_allclose(g["lat"][j], o["lat"], rtol=1e-9, atol=0)
         assert np.array_equal(g["lat"][j], o["lat"])  # same operations, same order
     # goodput reduction and selection on the GPU results
-    gpu_met = torch.from_numpy(g["met"]).cuda()
-    gpu_cnt = torch.from_numpy(g["cnt"]).cuda()
+    gpu_fine = {k: torch.from_numpy(g[k]).cuda() for k in ("met", "cnt", "status")}
     rt = torch.from_numpy(rates).cuda()
-    ks, gt, gg = cf.cf_goodput_reduce(gpu_met, gpu_cnt, rt, (9, 10), 1000)
-    wk, wgt, wg = O.goodput_reduce(want[0], want[1], rates, (9, 10), 1000)
+    ks, gt, gg = cf.cf_goodput_reduce(gpu_fine, rt, (9, 10), 1000)
+    wk, wgt, wg = O.goodput_reduce(want[0], want[1], rates, (9, 10), 1000, status=want[3])
     assert np.array_equal(ks.cpu().numpy(), wk)
     np.testing.assert_allclose(gg.cpu().numpy(), wg, rtol=1e-6)
     assert np.array_equal(gt.cpu().numpy(), wgt)
@@ -674,7 +673,7 @@ def test_bisect_parity(cf, name, n_plans, seeds, n):
     assert np.all(got["status"].cpu().numpy() == 0)
     # the grid's answer where its feasibility (by the oracle's own simulation) is monotone
     g = cf.cf_eval_fine(desc, cf.DevicePlans(tab), torch.as_tensor(ids).cuda(), torch.from_numpy(rates).cuda(), tr)
-    ks, gt, gg = cf.cf_goodput_reduce(g["met"], g["cnt"], torch.from_numpy(rates).cuda(), theta, n)
+    ks, gt, gg = cf.cf_goodput_reduce(g, torch.from_numpy(rates).cuda(), theta, n)
     om, oc, _, _ = O.eval_fine(m, tab, ids, rates, otr)
     met = om.astype(np.uint64).sum(axis=2)
     cnt = oc.astype(np.uint64).sum(axis=2)

@@ -58,3 +58,21 @@ def test_bisection_single_rate():
     met, cnt, _, _ = O.eval_fine(m, tab, [0, 0], rates, tr)
     wk, wgt, wg = O.goodput_reduce(met, cnt, rates, (9, 10), 300)
     assert np.array_equal(ks, wk) and np.array_equal(gt, wgt)
+
+
+def test_bisection_treats_a_failed_simulation_as_infeasible():
+    """Rates below zero make every simulation of a plan invalid (status != 0): its
+    truncated counts (no request simulated) would pass the attainment test, but bisection
+    must not take them as feasible, and neither does the grid reduction."""
+    cfg = load_config("c0")
+    m = O.make_model(cfg["model"])
+    tab = make_plans(cfg)
+    tr = O.trace_gen(m, [1], 200)
+    rates = np.array([[-1.0, -0.5, 1.0, 2.0], [1.0, 2.0, 4.0, 8.0]])
+    ks, gt, g, ne, ev = O.bisect(m, tab, [0, 0], rates, tr, (9, 10))
+    met, cnt, _, st = O.eval_fine(m, tab, [0, 0], rates, tr)
+    assert np.all(st[0, :2] != 0) and np.all(st[0, 2:] == 0) and np.all(st[1] == 0)
+    wk, wgt, wg = O.goodput_reduce(met, cnt, rates, (9, 10), 200, status=st)
+    assert wk[0] == -1 and wg[0] == 0.0
+    assert ks[0] == -1 and g[0] == 0.0
+    assert ks[1] == wk[1] and g[1] == wg[1]

@@ -183,3 +183,29 @@ def test_goodput_reduce_against_bisection():
     tot = cnt[:, -1].sum(axis=(1, 2)).astype(np.float64)
     assert np.allclose(g2, rates[:, -1] * tot / (S * n), rtol=1e-14)
     assert O.argmax(np.array([1.0, 3.0, 3.0, 2.0])) == 1
+
+
+def test_failed_simulation_makes_its_rate_infeasible():
+    """A rate whose simulation of some seed failed (nonzero status: invalid, deadlock,
+    overflow) is infeasible, however good its truncated counts look; the bisection of the
+    same counts with that rate failing gives the same answer."""
+    rng = np.random.default_rng(7)
+    n_plans, K, S, T, n = 12, 16, 4, 3, 500
+    cnt = rng.integers(50, 200, (n_plans, 1, S, T)).astype(np.uint32).repeat(K, axis=1)
+    met = cnt.copy()  # every rate meets every target on its counts
+    rates = np.sort(rng.uniform(0.1, 10, (n_plans, K)), axis=1)
+    status = np.zeros((n_plans, K, S), np.uint32)
+    fail_at = rng.integers(0, K, n_plans)
+    for i in range(n_plans):
+        status[i, fail_at[i], rng.integers(0, S)] = [1, 2, 4][i % 3]
+    ks, gt, g = O.goodput_reduce(met, cnt, rates, (9, 10), n, status=status)
+    assert np.array_equal(ks, fail_at - 1)
+    for i in range(n_plans):
+        if fail_at[i] == 0:
+            assert g[i] == 0.0 and np.all(gt[i] == 0.0)
+        else:
+            M = met[i, fail_at[i] - 1].sum(axis=0).astype(np.float64)
+            assert np.array_equal(gt[i], (rates[i, fail_at[i] - 1] * M) / (S * n))
+    # without the status words the same counts are feasible everywhere
+    ks0, _, _ = O.goodput_reduce(met, cnt, rates, (9, 10), n)
+    assert np.all(ks0 == K - 1)
