@@ -72,3 +72,25 @@ def test_product_path_does_not_import_the_oracle():
                 with open(os.path.join(dirpath, f)) as fh:
                     text = fh.read()
                 assert "oracle" not in re.sub(r"#.*|//.*", "", text).lower() or f == "__init__.py", f
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="libcf.so not built")
+def test_gated_output_length_beyond_15_bits_is_rejected_on_the_host():
+    """The gated stage's own output length of a running request is kept in 15 bits: a model
+    whose talker length can exceed 32767 tokens is refused before any device work."""
+    from paper_2512_14098_amd import cf
+    from paper_2512_14098_amd.inputs import load_config
+    desc = cf.model_desc(load_config("c2")["model"])
+    lib = ctypes.CDLL(LIB)
+    lib.cf_eval_fine.restype = ctypes.c_int32
+    args = [ctypes.byref(desc), None, None, 0, None, 1, None, 0, None, None]
+    assert lib.cf_eval_fine(*args) != -6  # accepted model: fails later on the NULL plans instead
+    gated = [c for c in range(desc.n_comp) if desc.gate_src[c] >= 0]
+    assert gated
+    for t in range(desc.n_types):
+        if (desc.path_mask[t] >> gated[0]) & 1:
+            desc.len[t][3].hi = 80 * 32768  # aud_out_ms: ceil(hi / 80) = 32768 talker tokens
+    assert lib.cf_eval_fine(*args) == -6  # CF_EUNSUPPORTED
+    buf = ctypes.create_string_buffer(256)
+    lib.cf_last_error(buf, 256)
+    assert b"32767" in buf.value
