@@ -274,6 +274,27 @@ cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_table *plans,
                        int32_t K, const cf_trace *trace, uint32_t flags, const cf_fine_out *out,
                        void *stream);
 
+/* cf_eval_fine for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same arguments, checks, outputs and status words, bit for bit, but
+ * the per-wavefront simulation state lives in one fixed array of 64 MiB
+ * per device (held from the library's load on that device until the
+ * process ends) instead of the library's cached allocations, and no
+ * hipMalloc, hipFree or allocating library routine is called.  The array
+ * bounds the number of wavefronts (64 MiB / the state of one simulation,
+ * about 0.9 MiB at 3,000 requests); a call whose single simulation does not
+ * fit (about 60,000 requests and more) returns CF_ECAPACITY before any
+ * launch.  Every call on a device shares that device's array and leaves its
+ * contents behind (the call clears what must start at zero itself): calls
+ * that overlap in time on one device race and must be serialised by the
+ * caller.  Synchronises the stream, as cf_eval_fine does.
+ * Errors: those of cf_eval_fine; CF_ECAPACITY as above; CF_EHIP if the
+ * array's device address cannot be obtained. */
+cf_status cf_eval_fine_noalloc(const cf_model_desc *model, const cf_plan_table *plans,
+                               const int32_t *plan_ids_dev, int32_t n_plans, const double *rates_dev,
+                               int32_t K, const cf_trace *trace, uint32_t flags, const cf_fine_out *out,
+                               void *stream);
+
 /* Phase 2 (Sec. 4.3, Alg. 2 phase 2) with occupancy-aware latency scaling
  * (Sec. 5.2): plan plan_ids_dev[i], i < n_plans, is evaluated on the first
  * n_sample requests of trace seed seed_idx, each routed through the plan

@@ -97,6 +97,7 @@ def _load():
         "cf_rate_grid": ([vp, vp, i32, i32, dbl, vp, vp], i32),
         "cf_topk_merge": ([vp, vp, i32, vp, vp, i32, C.c_uint64, i32, vp, vp, vp], i32),
         "cf_eval_fine": ([vp, vp, vp, i32, vp, i32, vp, u32, vp, vp], i32),
+        "cf_eval_fine_noalloc": ([vp, vp, vp, i32, vp, i32, vp, u32, vp, vp], i32),
         "cf_goodput_reduce": ([vp, i32, i32, i32, i32, vp, u32, u32, i32, vp, vp, vp, vp], i32),
         "cf_eval_mc": ([vp, vp, vp, i32, vp, vp, dbl, vp, i32, i32, vp, vp, vp, vp, vp], i32),
         "cf_pareto": ([vp, i32, i32, vp, vp, vp, i32, vp], i32),
@@ -121,7 +122,7 @@ def _load():
 
 _lib = _load()
 EXPORTED = ("cf_last_error", "cf_status_str", "cf_version", "cf_trace_gen", "cf_eval_coarse",
-            "cf_select_topk", "cf_topk_merge", "cf_rate_grid", "cf_eval_fine", "cf_eval_bisect", "cf_eval_mc",
+            "cf_select_topk", "cf_topk_merge", "cf_rate_grid", "cf_eval_fine", "cf_eval_fine_noalloc", "cf_eval_bisect", "cf_eval_mc",
             "cf_eval_mc_curve", "cf_goodput_curve", "cf_pareto",
             "cf_enum_logical", "cf_enum_count", "cf_enum_plans", "cf_enum_screen",
             "cf_goodput_reduce", "cf_select_best", "cf_math_eval", "cf_philox_eval", "cf_release_scratch")
@@ -370,7 +371,7 @@ def _targets(targets, T):
     return tg
 
 
-def cf_eval_fine(desc, plans, plan_ids, rates, trace, lat_triples=None, targets=None, limits=None):
+def cf_eval_fine(desc, plans, plan_ids, rates, trace, lat_triples=None, targets=None, limits=None, _entry="cf_eval_fine"):
     """Phase 3 of every (plan, rate, seed); with targets ([T][n_bins][4], bounds not
     decreasing with the bin) also the latency histograms hist [n_plans][K][S][T][n_bins+1];
     with lat_triples the per-request latencies of those triples (CF_DUMP_LAT); limits: a
@@ -399,11 +400,18 @@ def cf_eval_fine(desc, plans, plan_ids, rates, trace, lat_triples=None, targets=
         tg = _targets(targets, T)
         hist = torch.empty((n_plans, K, S, T, tg.shape[1] + 1), dtype=torch.int32, device=dev)
         out.hist_dev, out.hist_targets_host, out.n_bins = hist.data_ptr(), tg.ctypes.data, tg.shape[1]
-    _check(_lib.cf_eval_fine(C.byref(desc), C.byref(plans.c), _in(plan_ids, torch.int32, "plan_ids", n_plans),
-                             int(n_plans), _in(rates, torch.float64, "rates", ndim=2), int(K), C.byref(trace.c),
-                             flags, C.byref(out),
-                             _stream()), "cf_eval_fine")
+    _check(getattr(_lib, _entry)(C.byref(desc), C.byref(plans.c), _in(plan_ids, torch.int32, "plan_ids", n_plans),
+                                 int(n_plans), _in(rates, torch.float64, "rates", ndim=2), int(K), C.byref(trace.c),
+                                 flags, C.byref(out), _stream()), _entry)
     return dict(met=met, cnt=cnt, events=events, status=status, lat=lat, hist=hist)
+
+
+def cf_eval_fine_noalloc(desc, plans, plan_ids, rates, trace, lat_triples=None, targets=None, limits=None):
+    """cf_eval_fine through the entry point that allocates no device memory of its own
+    (its simulation state lives in the library's fixed per-device array; the output
+    tensors are the caller's, as for every call)."""
+    return cf_eval_fine(desc, plans, plan_ids, rates, trace, lat_triples, targets, limits,
+                        _entry="cf_eval_fine_noalloc")
 
 
 def cf_eval_bisect(desc, plans, plan_ids, rates, trace, theta):

@@ -253,7 +253,7 @@ void *scratch_get(int slot, size_t bytes, cf_status *st) {
 }  // namespace cf
 
 namespace cf {
-cf_status load_targets(int T, int n_bins, const double *host, const double **dev, hipStream_t s) {
+cf_status check_targets(int T, int n_bins, const double *host) {
   if (n_bins < 1 || n_bins > 64) return set_error(CF_EINVAL, "n_bins must be in 1..64");
   if (!host) return set_error(CF_EINVAL, "NULL target table");
   for (int t = 0; t < T; t++)
@@ -264,7 +264,12 @@ cf_status load_targets(int T, int n_bins, const double *host, const double **dev
         if (b > 0 && v < host[((size_t)t * n_bins + b - 1) * 4 + j])
           return set_error(CF_EINVAL, "targets decrease at [%d][%d][%d]", t, b, j);
       }
-  cf_status st = CF_OK;
+  return CF_OK;
+}
+
+cf_status load_targets(int T, int n_bins, const double *host, const double **dev, hipStream_t s) {
+  cf_status st = check_targets(T, n_bins, host);
+  if (st != CF_OK) return st;
   const size_t bytes = sizeof(double) * (size_t)T * n_bins * 4;
   void *d = scratch_get(SCR_TARGETS, bytes, &st);
   if (!d) return st;

@@ -118,6 +118,9 @@ namespace cf {
 // A latency-target table [T][n_bins][4] (TTFT, TPOT, E2E, MEDIA bounds, not
 // decreasing with the bin) checked on the host and copied to device scratch.
 cf_status load_targets(int T, int n_bins, const double *host, const double **dev, hipStream_t s);
+// Host: validation alone of a target table [T][n_bins][4] (load_targets also copies it
+// to library scratch).
+cf_status check_targets(int T, int n_bins, const double *host);
 
 // The first bin b whose four bounds the latencies meet (n_bins if none), by
 // bisection: the bounds do not decrease with b, so meeting them is monotone.

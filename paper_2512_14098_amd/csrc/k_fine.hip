@@ -52,6 +52,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "cf_internal.h"
 #include "cf_run.h"
 
@@ -2090,13 +2092,43 @@ Layout make_layout(const KModel &m, int n) {
   return L;
 }
 
-}  // namespace
-}  // namespace cf
+// The allocation-free variant's scratch: one fixed array per device, held
+// from the library's load on that device until the process ends.  Host code
+// uses the device address hipGetSymbolAddress returns for the current device
+// (fixed_scratch_of), never the array's name.
+constexpr size_t kFixedScratch = 64ull << 20;
+static __device__ __align__(256) char scratch[kFixedScratch];
 
-extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_table *plans,
-                                  const int32_t *plan_ids_dev, int32_t n_plans, const double *rates_dev, int32_t K,
-                                  const cf_trace *trace, uint32_t flags, const cf_fine_out *out, void *stream) {
-  using namespace cf;
+constexpr int kMaxDevFixed = 64;
+std::mutex g_fixed_mu;
+char *g_fixed[kMaxDevFixed];
+
+// device address of `scratch` on the current device (looked up once per device)
+cf_status fixed_scratch_of(char **ptr) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevFixed) return set_error(CF_EHIP, "no current HIP device");
+  std::lock_guard<std::mutex> lock(g_fixed_mu);
+  if (!g_fixed[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return set_error(CF_EHIP, "hipGetSymbolAddress of the fixed scratch failed: %s", hipGetErrorString(e));
+    }
+    g_fixed[dev] = (char *)p;
+  }
+  *ptr = g_fixed[dev];
+  return CF_OK;
+}
+
+constexpr size_t kFineHdr = 8192;  // ticket, stage counts, the argument block
+
+// cf_eval_fine and cf_eval_fine_noalloc: with fixed == nullptr the call's
+// scratch comes from the library's cached allocations, else from the fixed
+// region [fixed, fixed + fixed_cap), which bounds the number of wavefronts.
+cf_status eval_fine(const cf_model_desc *model, const cf_plan_table *plans, const int32_t *plan_ids_dev,
+                    int32_t n_plans, const double *rates_dev, int32_t K, const cf_trace *trace, uint32_t flags,
+                    const cf_fine_out *out, void *stream, char *fixed, size_t fixed_cap) {
   FineArgs a;
   memset(&a, 0, sizeof a);
   cf_status st = lower_model(model, &a.m);
@@ -2169,10 +2201,27 @@ extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_tabl
     const size_t budget = free_b / 2;
     while (waves > 64 && (size_t)waves * a.L.bytes > budget) waves /= 2;
   }
-  const size_t hdr = 8192;
-  static_assert(sizeof(FineArgs) + 512 <= 8192, "FineArgs must fit the scratch header");
-  char *scr = (char *)scratch_get(SCR_FINE, hdr + (size_t)waves * a.L.bytes, &st);
-  if (!scr) return st;
+  static_assert(sizeof(FineArgs) + 512 <= kFineHdr, "FineArgs must fit the scratch header");
+  char *scr;
+  size_t hdr = kFineHdr;
+  if (fixed) {
+    // the target table (if any) follows the header; the slabs of as many
+    // wavefronts as fit follow it
+    if (out->n_bins > 0) {
+      st = check_targets(a.m.nt, out->n_bins, out->hist_targets_host);
+      if (st != CF_OK) return st;
+      hdr += (sizeof(double) * (size_t)a.m.nt * (size_t)out->n_bins * 4 + 255) & ~(size_t)255;
+    }
+    if (fixed_cap < hdr + a.L.bytes)
+      return set_error(CF_ECAPACITY, "one simulation of %d requests needs %zu bytes of scratch; the fixed scratch holds %zu",
+                       trace->n_req, hdr + a.L.bytes, fixed_cap);
+    const size_t fit = (fixed_cap - hdr) / a.L.bytes;
+    if ((size_t)waves > fit) waves = (long long)fit;
+    scr = fixed;
+  } else {
+    scr = (char *)scratch_get(SCR_FINE, hdr + (size_t)waves * a.L.bytes, &st);
+    if (!scr) return st;
+  }
   a.ticket = (unsigned int *)scr;
   unsigned int *max_si = (unsigned int *)(scr + 64);
   FineArgs *args_dev = (FineArgs *)(scr + 512);
@@ -2204,7 +2253,15 @@ extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_tabl
   if (out->n_bins > 0) {
     // optional latency histograms: target table to the device, counters cleared by a kernel
     if (!out->hist_dev) return set_error(CF_EINVAL, "n_bins > 0 without hist_dev");
-    st = load_targets(a.m.nt, out->n_bins, out->hist_targets_host, &a.tg, s);
+    if (fixed) {
+      char *tg = scr + kFineHdr;
+      st = hip_check(hipMemcpyAsync(tg, out->hist_targets_host, sizeof(double) * (size_t)a.m.nt * out->n_bins * 4,
+                                    hipMemcpyHostToDevice, s),
+                     "target table copy");
+      a.tg = (const double *)tg;
+    } else {
+      st = load_targets(a.m.nt, out->n_bins, out->hist_targets_host, &a.tg, s);
+    }
     if (st != CF_OK) return st;
     a.hist = out->hist_dev;
     a.nb = out->n_bins;
@@ -2222,4 +2279,24 @@ extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_tabl
   if (st != CF_OK) return st;
   // the argument block is copied from host memory on the stream: wait for it
   return hip_check(hipStreamSynchronize(s), "cf_eval_fine sync");
+}
+
+}  // namespace
+}  // namespace cf
+
+extern "C" cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_table *plans,
+                                  const int32_t *plan_ids_dev, int32_t n_plans, const double *rates_dev, int32_t K,
+                                  const cf_trace *trace, uint32_t flags, const cf_fine_out *out, void *stream) {
+  return cf::eval_fine(model, plans, plan_ids_dev, n_plans, rates_dev, K, trace, flags, out, stream, nullptr, 0);
+}
+
+extern "C" cf_status cf_eval_fine_noalloc(const cf_model_desc *model, const cf_plan_table *plans,
+                                          const int32_t *plan_ids_dev, int32_t n_plans, const double *rates_dev,
+                                          int32_t K, const cf_trace *trace, uint32_t flags, const cf_fine_out *out,
+                                          void *stream) {
+  char *fixed = nullptr;
+  const cf_status st = cf::fixed_scratch_of(&fixed);
+  if (st != CF_OK) return st;
+  return cf::eval_fine(model, plans, plan_ids_dev, n_plans, rates_dev, K, trace, flags, out, stream, fixed,
+                       cf::kFixedScratch);
 }
