@@ -143,109 +143,193 @@ def _disaggregated(model, fam, gpus):
     return out
 
 
-def _canon(pl):
-    parts = [tuple(n) for n in pl["nodes"]]
-    routes = tuple(tuple((w, tuple(sorted(m.items()))) for w, m in alts) for alts in pl["routes"])
-    return (tuple(parts), routes)
+def _candidate(ctx, j):
+    """Candidate plan j of the sampler (its own Philox stream, keyed by the config's seed
+    with counter j), as its canonical encoding, or None if it does not fit the budget."""
+    T, C, paths, edges, colocatable, knobs, gpus, seed = ctx
+    rng = np.random.Generator(np.random.Philox(key=seed, counter=j))
+    ns = 1 if rng.random() < 0.5 or T == 1 else 2
+    if ns == 1:
+        cover = [list(range(T))]
+    else:
+        while True:
+            assign = rng.integers(0, 3, size=T)
+            s0 = [t for t in range(T) if assign[t] in (0, 2)]
+            s1 = [t for t in range(T) if assign[t] in (1, 2)]
+            if s0 and s1:
+                break
+        cover = [s0, s1]
+    nodes, node_of, sub_nodes = [], [], []
+    for si, types_s in enumerate(cover):
+        comps = sorted(set(c for t in types_s for c in paths[t]))
+        es = sorted(set(e for t in types_s for e in edges[t]))
+        par = {c: c for c in comps}
+
+        def find(c):
+            while par[c] != c:
+                c = par[c]
+            return c
+        for (a, b) in es:
+            if colocatable is not None and (a, b) not in colocatable:
+                continue
+            if rng.random() < 0.5:
+                ra, rb = find(a), find(b)
+                if ra != rb:
+                    par[max(ra, rb)] = min(ra, rb)
+        groups = {}
+        for c in comps:
+            groups.setdefault(find(c), 0)
+            groups[find(c)] |= 1 << c
+        nmap, mine = {}, []
+        for root in sorted(groups):
+            mask = groups[root]
+            shared = None
+            if si == 1 and rng.random() < 0.5:
+                for v in sub_nodes[0]:
+                    if nodes[v] == mask:
+                        shared = v
+                        break
+            if shared is None:
+                shared = len(nodes)
+                nodes.append(mask)
+            mine.append(shared)
+            for c in range(C):
+                if (mask >> c) & 1:
+                    nmap[c] = shared
+        node_of.append(nmap)
+        sub_nodes.append(mine)
+    V = len(nodes)
+    if V > gpus or V > MAXV:
+        return None
+    reps = [1] * V
+    extra = gpus - V
+    k = int(rng.integers(0, extra + 1))
+    if k:  # k draws of the node that gets one more replica
+        for v, more in enumerate(np.bincount(rng.integers(0, V, size=k), minlength=V).tolist()):
+            reps[v] += more
+    batch = []
+    for mask in nodes:
+        first = (mask & -mask).bit_length() - 1
+        batch.append(int(knobs[first][int(rng.integers(0, len(knobs[first])))]))
+    routes = []
+    for t in range(T):
+        alts = [si for si in range(ns) if t in cover[si]]
+        if len(alts) == 1:
+            routes.append([(10, {c: node_of[alts[0]][c] for c in paths[t]})])
+        else:
+            w0 = int(rng.integers(1, 10))
+            routes.append([(w0, {c: node_of[alts[0]][c] for c in paths[t]}),
+                           (10 - w0, {c: node_of[alts[1]][c] for c in paths[t]})])
+    return _row(dict(nodes=[(nodes[v], reps[v], batch[v], 1) for v in range(V)], routes=routes))
+
+
+def _candidates(ctx, lo, hi):
+    return [_candidate(ctx, j) for j in range(lo, hi)]
+
+
+# One plan as the bytes of its table column (a canonical encoding: two plans are equal
+# iff their columns are): n_nodes, node_comp[16], node_rep[16], node_batch[16] (u16,
+# little endian), node_gpus[16], n_alt[8], alt_w[16], alt_node[128].
+_ROW_OFF = dict(n_nodes=0, node_comp=1, node_rep=1 + MAXV, node_batch=1 + 2 * MAXV, node_gpus=1 + 4 * MAXV,
+                n_alt=1 + 5 * MAXV, alt_w=1 + 5 * MAXV + MAXT, alt_node=1 + 5 * MAXV + 3 * MAXT)
+ROW_BYTES = _ROW_OFF["alt_node"] + 2 * MAXT * MAXC
+_ROW_TEMPLATE = bytes(_ROW_OFF["alt_node"]) + bytes([255]) * (2 * MAXT * MAXC)
+
+
+def _row(pl):
+    b = bytearray(_ROW_TEMPLATE)
+    b[0] = len(pl["nodes"])
+    o = _ROW_OFF
+    for v, (cm, rep, bt, g) in enumerate(pl["nodes"]):
+        b[o["node_comp"] + v] = cm
+        b[o["node_rep"] + v] = rep
+        b[o["node_batch"] + 2 * v] = bt & 255
+        b[o["node_batch"] + 2 * v + 1] = bt >> 8
+        b[o["node_gpus"] + v] = g
+    for t, alts in enumerate(pl["routes"]):
+        b[o["n_alt"] + t] = len(alts)
+        for a, (w, cmap) in enumerate(alts):
+            b[o["alt_w"] + 2 * t + a] = w
+            for c, v in cmap.items():
+                b[o["alt_node"] + (2 * t + a) * MAXC + c] = v
+    return bytes(b)
+
+
+def table_from_rows(rows):
+    """Plan table from column bytes (``_row``), in order."""
+    P = len(rows)
+    tab = PlanTable(P)
+    if P == 0:
+        return tab
+    R = np.frombuffer(b"".join(rows), np.uint8).reshape(P, ROW_BYTES)
+    o = _ROW_OFF
+    tab.n_nodes = np.ascontiguousarray(R[:, 0])
+    tab.node_comp = np.ascontiguousarray(R[:, o["node_comp"]:o["node_comp"] + MAXV].T)
+    tab.node_rep = np.ascontiguousarray(R[:, o["node_rep"]:o["node_rep"] + MAXV].T)
+    nb = np.ascontiguousarray(R[:, o["node_batch"]:o["node_batch"] + 2 * MAXV]).view("<u2")
+    tab.node_batch = np.ascontiguousarray(nb.T.astype(np.uint16))
+    tab.node_gpus = np.ascontiguousarray(R[:, o["node_gpus"]:o["node_gpus"] + MAXV].T)
+    tab.n_alt = np.ascontiguousarray(R[:, o["n_alt"]:o["n_alt"] + MAXT].T)
+    tab.alt_w = np.ascontiguousarray(R[:, o["alt_w"]:o["alt_w"] + 2 * MAXT].T)
+    tab.alt_node = np.ascontiguousarray(R[:, o["alt_node"]:o["alt_node"] + 2 * MAXT * MAXC].T)
+    return tab
 
 
 def _sample(model, spec, gpus, have, total, progress=True):
-    """Seeded mixed / compound plans until ``total`` distinct plans exist."""
+    """Seeded mixed / compound plans until ``total`` distinct plans exist, as column bytes:
+    candidates j = 0, 1, 2, ... in order, each drawn from its own Philox stream (key = the
+    config's seed, counter = j), the ones over the budget or already present (``have``:
+    column bytes) skipped.  Large counts draw the candidates in worker processes; the
+    result does not depend on how."""
     names, idx, paths, edges = _model_index(model)
     T, C = len(paths), len(names)
     colocatable = model.get("colocatable")
     if colocatable is not None:
         colocatable = {(idx[a], idx[b]) for a, b in colocatable}
     knobs = [spec["batch"][n] for n in names]
-    rng = np.random.Generator(np.random.Philox(key=int(spec["seed"])))
+    ctx = (T, C, paths, edges, colocatable, knobs, int(gpus), int(spec["seed"]))
+    need = total - len(have)
+    seen = set(have)
     out = []
-    seen = set(_canon(p) for p in have)
-    tries = 0
-    step = max(total // 10, 1)
-    while len(have) + len(out) < total:
-        if total >= 200000 and (len(have) + len(out)) % step == 0 and len(out) and tries and progress:
-            print("plans: %d of %d sampled" % (len(have) + len(out), total), file=sys.stderr, flush=True)
-        tries += 1
-        if tries > 50 * total + 1000:
-            raise RuntimeError("plan sampler could not reach the requested count")
-        ns = 1 if rng.random() < 0.5 or T == 1 else 2
-        if ns == 1:
-            cover = [list(range(T))]
-        else:
-            while True:
-                assign = rng.integers(0, 3, size=T)
-                s0 = [t for t in range(T) if assign[t] in (0, 2)]
-                s1 = [t for t in range(T) if assign[t] in (1, 2)]
-                if s0 and s1:
-                    break
-            cover = [s0, s1]
-        nodes, node_of, sub_nodes = [], [], []
-        for si, types_s in enumerate(cover):
-            comps = sorted(set(c for t in types_s for c in paths[t]))
-            es = sorted(set(e for t in types_s for e in edges[t]))
-            par = {c: c for c in comps}
+    workers = min(16, os.cpu_count() or 1) if need >= 50000 else 1
+    block = 1 << 16 if workers > 1 else 4096
+    pool = None
+    if workers > 1:
+        import concurrent.futures as cfut
+        import multiprocessing as mp
+        pool = cfut.ProcessPoolExecutor(max_workers=workers, mp_context=mp.get_context("spawn"))
 
-            def find(c):
-                while par[c] != c:
-                    c = par[c]
-                return c
-            for (a, b) in es:
-                if colocatable is not None and (a, b) not in colocatable:
+    def submit(j):
+        if pool is None:
+            return j
+        step = block // workers
+        return [pool.submit(_candidates, ctx, a, a + step) for a in range(j, j + block, step)]
+
+    def collect(h):
+        if pool is None:
+            return _candidates(ctx, h, h + block)
+        return [k for f in h for k in f.result()]
+    try:
+        j = 0
+        pending = submit(j)
+        while len(out) < need:
+            if j > 50 * total + 1000:
+                raise RuntimeError("plan sampler could not reach the requested count")
+            keys = collect(pending)
+            j += block
+            pending = submit(j)  # the next block is drawn while this one is merged
+            for key in keys:
+                if key is None or key in seen:
                     continue
-                if rng.random() < 0.5:
-                    ra, rb = find(a), find(b)
-                    if ra != rb:
-                        par[max(ra, rb)] = min(ra, rb)
-            groups = {}
-            for c in comps:
-                groups.setdefault(find(c), 0)
-                groups[find(c)] |= 1 << c
-            nmap, mine = {}, []
-            for root in sorted(groups):
-                mask = groups[root]
-                shared = None
-                if si == 1 and rng.random() < 0.5:
-                    for v in sub_nodes[0]:
-                        if nodes[v] == mask:
-                            shared = v
-                            break
-                if shared is None:
-                    shared = len(nodes)
-                    nodes.append(mask)
-                mine.append(shared)
-                for c in range(C):
-                    if (mask >> c) & 1:
-                        nmap[c] = shared
-            node_of.append(nmap)
-            sub_nodes.append(mine)
-        V = len(nodes)
-        if V > gpus or V > MAXV:
-            continue
-        reps = [1] * V
-        extra = gpus - V
-        k = int(rng.integers(0, extra + 1))
-        if k:  # k draws of the node that gets one more replica (one vector draw: same stream)
-            for v, more in enumerate(np.bincount(rng.integers(0, V, size=k), minlength=V).tolist()):
-                reps[v] += more
-        batch = []
-        for mask in nodes:
-            first = (mask & -mask).bit_length() - 1
-            batch.append(int(knobs[first][int(rng.integers(0, len(knobs[first])))]))
-        routes = []
-        for t in range(T):
-            alts = [si for si in range(ns) if t in cover[si]]
-            if len(alts) == 1:
-                routes.append([(10, {c: node_of[alts[0]][c] for c in paths[t]})])
-            else:
-                w0 = int(rng.integers(1, 10))
-                routes.append([(w0, {c: node_of[alts[0]][c] for c in paths[t]}),
-                               (10 - w0, {c: node_of[alts[1]][c] for c in paths[t]})])
-        pl = dict(nodes=[(nodes[v], reps[v], batch[v], 1) for v in range(V)], routes=routes)
-        key = _canon(pl)
-        if key in seen:
-            continue
-        seen.add(key)
-        out.append(pl)
+                seen.add(key)
+                out.append(key)
+                if len(out) == need:
+                    break
+            if total >= 200000 and progress:
+                print("plans: %d of %d sampled" % (len(have) + len(out), total), file=sys.stderr, flush=True)
+    finally:
+        if pool is not None:
+            pool.shutdown(cancel_futures=True)
     return out
 
 
@@ -273,16 +357,15 @@ def make_plans(cfg, cache=True):
             plans += _disaggregated(model, fam, gpus)
         else:
             raise ValueError(fam["family"])
-    seen, uniq = set(), []
+    seen, rows = set(), []
     for p in plans:
-        k = _canon(p)
+        k = _row(p)
         if k not in seen:
             seen.add(k)
-            uniq.append(p)
-    plans = uniq
+            rows.append(k)
     if "sampled" in spec:
-        plans += _sample(model, spec["sampled"], gpus, plans, int(spec["sampled"]["total"]))
-    tab = plan_table_from_list(plans)
+        rows += _sample(model, spec["sampled"], gpus, rows, int(spec["sampled"]["total"]))
+    tab = table_from_rows(rows)
     if cache and tab.P >= 5000:
         os.makedirs(os.path.dirname(cpath), exist_ok=True)
         tmp = cpath + ".tmp%d.npz" % os.getpid()
