@@ -115,8 +115,9 @@ def cpu_baseline_all_cores(w, ids, rates, order, seeds_needed, budget_s, workers
         res = pool.starmap(_oracle_triples, [(w.cfg, seeds, w.n_req, jb, budget_s) for jb in jobs])
     ev, n, dt = sum(r[0] for r in res), sum(r[1] for r in res), max(r[2] for r in res)
     return {"value": ev / dt, "unit": "request-events/s", "cores": workers, "kind": "oracle",
-            "sample": "%d triples of this workload drawn uniformly over plans, rates and seeds, in %d "
-                      "processes (%d request-events, longest worker %.1f s)" % (n, workers, ev, dt)}
+            "sample": "%d triples of this workload drawn uniformly over its selected plans, its rates and "
+                      "its first %d seeds, in %d processes (%d request-events, longest worker %.1f s)"
+                      % (n, len(seeds_needed), workers, ev, dt)}
 
 
 def host_info():
@@ -150,7 +151,9 @@ def cpu_baseline(w, budget_s, all_cores=0, events_per_step=None):
         rates = np.tile(np.asarray(w.explicit_rates, np.float64), (len(ids), 1))
     else:
         rates = O.rate_grid(rd, ids, w.K, w.alpha_max)
-    S = len(w.seeds)
+    # seeds drawn from the first few only: the oracle generates the trace of every seed it
+    # samples, which for 64 seeds of 10^5 requests would cost more than the timed budget
+    S = min(len(w.seeds), 4)
     order = []
     rng = np.random.default_rng(0)
     for _ in range(32768):  # enough for every core's budget
@@ -183,9 +186,9 @@ def cpu_baseline(w, budget_s, all_cores=0, events_per_step=None):
         except OSError:
             pass
     res = {"value": ev / dt, "unit": "request-events/s", "cores": 1, "kind": "oracle",
-           "sample": "%d triples of this workload drawn uniformly over plans, rates and seeds "
-                     "(%d request-events in %.1f s, single thread%s)"
-                     % (n, ev, dt, "" if pinned is None else ", pinned to core %d" % pinned),
+           "sample": "%d triples of this workload drawn uniformly over its selected plans, its rates and "
+                     "its first %d seeds (%d request-events in %.1f s, single thread%s)"
+                     % (n, S, ev, dt, "" if pinned is None else ", pinned to core %d" % pinned),
            "host": host}
     if events_per_step:
         res["full_step_s_extrapolated"] = events_per_step / res["value"]
@@ -469,7 +472,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=2)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--config", default="c1")
+    ap.add_argument("--config", default="c4")
+    ap.add_argument("--slices", type=int, default=-1, metavar="F",
+                    help="each step simulates one slice of the fine stage: every F-th selected plan (all "
+                         "grid rates) on one seed, step g taking plan slice g %% F of seed g // F (default: 4 "
+                         "for the whole c4 workload, else none: every plan on every seed per step)")
     ap.add_argument("--seeds", type=int, default=0, metavar="N",
                     help="simulate only the first N seeds of the workload (a sample of a workload "
                          "too large to run whole; stated in the output)")
@@ -554,18 +561,34 @@ def main():
         w.set_target_scales([0.25 * 16.0 ** (b / max(args.curve - 1, 1)) for b in range(args.curve)])
     if args.plans > 0:
         w.top_k = min(w.top_k, args.plans)
+    F = args.slices
+    if F < 0:
+        F = 4 if (args.config == "c4" and args.seeds == 0 and args.plans == 0 and not args.bisect) else 0
+    S = len(w.seeds)
+
+    def set_slice(g):
+        if F > 0:
+            w.slice = (g % F, F, (g // F) % S)
     for i in range(args.warmup):
+        set_slice(i)
         out = pipeline.run_step(w)
         torch.cuda.synchronize()
         print("bench: warmup %d done, %d request-events" % (i, pipeline.events_total(out)),
               file=sys.stderr, flush=True)
     torch.cuda.synchronize()
-    events, plans, fine_ms, timers_all = 0, 0, [], []
+    events, plans, fine_ms, timers_all, ev_tensors, st_tensors = 0, 0, [], [], [], []
+    fine_plans = []
     t0 = time.perf_counter()
     for i in range(args.steps):
+        set_slice(args.warmup + i)
         timers = {}
         out = pipeline.run_step(w, timers=timers)
         timers_all.append(timers)
+        ev_tensors.append(out["fine"]["events"])
+        st_tensors.append(out["fine"]["status"])
+        fine_plans.append(int(out["fine_ids"].numel()))
+        if i == 0 or (i + 1) % 5 == 0:
+            print("bench: step %d launched" % i, file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     stage_ms = {}
@@ -574,9 +597,13 @@ def main():
         fine_ms.append(s.elapsed_time(e))
         for k, (s, e) in timers.items():
             stage_ms.setdefault(k, []).append(s.elapsed_time(e))
-    events = pipeline.events_total(out) * args.steps
-    plans = int(out["ids"].numel()) * args.steps
-    st = pipeline.status_summary(out)
+    events = sum(int(e.sum().item()) for e in ev_tensors)
+    st = {}
+    for t in st_tensors:
+        for k, v in pipeline.status_summary({"fine": {"status": t}}).items():
+            st[k] = st.get(k, 0) + v
+    # plans fully evaluated (every rate on every seed): a sliced step does 1/S of that for its plans
+    plans = sum(fine_plans) / (S if F > 0 else 1)
     elapsed = t1 - t0
     ms_per_step = elapsed * 1e3 / args.steps
     ev_step = events / args.steps
@@ -584,6 +611,11 @@ def main():
     achieved = OPS_PER_EVENT * ev_step / fine_avg_s / 1e12
     n_sel = int(out["ids"].numel())
     workload = "%s: %s" % (args.config, w.cfg["summary"])
+    if F > 0:
+        workload += ("; each step: the trace of all %d seeds, phase 1 over all %d plans, the top %d and their "
+                     "%d-rate grid, phase 3 of every %d-th selected plan at every rate on one seed (plan slice "
+                     "g mod %d of seed g div %d at step g), their goodput reduction"
+                     % (S, w.tab.P, n_sel, w.K, F, F, F))
     sample = []
     if args.plans > 0 and w.top_k < full_top:
         sample.append("first %d of its %d selected plans" % (w.top_k, full_top))
@@ -612,9 +644,13 @@ def main():
         "config": {"workload": workload, "plans_screened": w.tab.P,
                    "plans_simulated": n_sel, "rates": w.K, "seeds": len(w.seeds), "requests": w.n_req,
                    "triples": (int(out["fine"]["n_eval"].sum().item()) * len(w.seeds) if w.bisect
-                               else n_sel * w.K * len(w.seeds)), "request_events_per_step": ev_step,
+                               else n_sel * w.K * len(w.seeds)) if F <= 0 else None,
+                   "triples_per_step": (sum(fine_plans) * w.K // args.steps) if F > 0 else None,
+                   "request_events_per_step": ev_step,
                    "status_counts": st, "fine_ms": fine_ms,
-                   "stage_ms": {k: sum(v) / len(v) for k, v in stage_ms.items()}},
+                   "stage_ms": {k: sum(v) / len(v) for k, v in stage_ms.items()},
+                   # the whole fine stage (every selected plan, rate and seed) at this step's rate
+                   "fine_stage_s_extrapolated": (fine_avg_s * F * S) if F > 0 else fine_avg_s},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_LANE_OPS, "unit": "TOP/s",
                      "frac": achieved / PEAK_LANE_OPS,
                      "traffic": MEASURED_TRAFFIC.get((kernel_source_id(), workload)),

@@ -245,6 +245,19 @@ class DeviceTrace:
         for f, _ in TRACE_FIELDS:
             setattr(self.c, f + "_dev", self.t[f].data_ptr())
 
+    def seed_view(self, s):
+        """The trace of seed index s alone (a one-seed view of the same device arrays)."""
+        if not 0 <= s < self.n_seeds:
+            raise CfError("seed index %d outside 0..%d" % (s, self.n_seeds - 1))
+        v = DeviceTrace.__new__(DeviceTrace)
+        v.n_seeds, v.n_req = 1, self.n_req
+        v.t = {f: self.t[f][s * self.n_req:(s + 1) * self.n_req] for f, _ in TRACE_FIELDS}
+        v.c = cf_trace()
+        v.c.n_seeds, v.c.n_req = 1, self.n_req
+        for f, _ in TRACE_FIELDS:
+            setattr(v.c, f + "_dev", v.t[f].data_ptr())
+        return v
+
     def to_numpy(self):
         """Host copy with the unsigned dtypes of the C layout."""
         unsigned = {"arr_ticks": np.uint64, "type": np.uint8, "n_img": np.uint8, "patches": np.uint16,

@@ -311,11 +311,20 @@ def _sample(model, spec, gpus, have, total, progress=True):
         return [k for f in h for k in f.result()]
     try:
         j = 0
-        pending = submit(j)
+        try:
+            pending = submit(j)
+            keys0 = collect(pending)
+        except Exception:  # no worker processes here (e.g. a caller without a main guard)
+            if pool is None:
+                raise
+            pool.shutdown(cancel_futures=True)
+            pool, block = None, 4096
+            keys0 = None
+        pending = j if keys0 is None else None
         while len(out) < need:
             if j > 50 * total + 1000:
                 raise RuntimeError("plan sampler could not reach the requested count")
-            keys = collect(pending)
+            keys = keys0 if pending is None else collect(pending)
             j += block
             pending = submit(j)  # the next block is drawn while this one is merged
             for key in keys:
@@ -340,7 +349,10 @@ def _cache_path(cfg):
 
 
 def make_plans(cfg, cache=True):
-    """Plan table for a configuration (deterministic; cached on disk when large)."""
+    """Plan table for a configuration (deterministic; cached on disk when large).  A large
+    sampled table is drawn in spawned worker processes, which import the caller's main
+    script: a script that builds one needs the usual ``if __name__ == "__main__"`` guard
+    (without it the table is drawn in this process, with the same result)."""
     cpath = _cache_path(cfg)
     if cache and os.path.exists(cpath):
         z = np.load(cpath)

@@ -44,6 +44,10 @@ class Workload:
         self.targets = None
         # phase 3 by rate bisection over each plan's grid instead of every grid rate
         self.bisect = False
+        # phase 3 of one slice of the stage: (part, parts, seed index) simulates the selected
+        # plans part, part + parts, part + 2 parts, ... at every grid rate on that one seed, and
+        # reduces them over it; None simulates every plan on every seed
+        self.slice = None
 
     def set_target_scales(self, scales):
         """Targets = each type's own bounds times each scale (ascending)."""
@@ -97,28 +101,32 @@ def run_step(w, timers=None):
     else:
         rates = cf.cf_rate_grid(rd, ids, w.K, w.alpha_max)
     mark("select")
+    f_ids, f_rates, f_trace = ids, rates, trace
+    if w.slice is not None:
+        part, parts, s = w.slice
+        f_ids, f_rates, f_trace = ids[part::parts].contiguous(), rates[part::parts].contiguous(), trace.seed_view(s)
     mark("fine")
     if w.bisect:
-        fine = cf.cf_eval_bisect(w.desc, w.plans, ids, rates, trace, w.theta)
+        fine = cf.cf_eval_bisect(w.desc, w.plans, f_ids, f_rates, f_trace, w.theta)
     else:
-        fine = cf.cf_eval_fine(w.desc, w.plans, ids, rates, trace, targets=w.targets)
+        fine = cf.cf_eval_fine(w.desc, w.plans, f_ids, f_rates, f_trace, targets=w.targets)
     mark("fine")
     mark("reduce")
     if w.bisect:
         kstar, gt, g = fine["kstar"], fine["goodput_t"], fine["goodput"]
     else:
-        kstar, gt, g = cf.cf_goodput_reduce(fine, rates, w.theta, w.n_req)
-    best = cf.cf_select_best(g) if ids.numel() > 0 else None
+        kstar, gt, g = cf.cf_goodput_reduce(fine, f_rates, w.theta, w.n_req)
+    best = cf.cf_select_best(g) if f_ids.numel() > 0 else None
     curve = None
-    if w.targets is not None and ids.numel() > 0 and not w.bisect:
+    if w.targets is not None and f_ids.numel() > 0 and not w.bisect:
         curve = dict(zip(("kstar", "goodput_t", "goodput"),
-                         cf.cf_goodput_curve(fine, rates, w.theta, w.n_req)))
+                         cf.cf_goodput_curve(fine, f_rates, w.theta, w.n_req)))
     mark("reduce")
     if timers is not None:
         timers.update(ev)
     return dict(trace=trace, moments=moments, rd=rd, bottleneck=bott, flags=flags, ids=ids,
-                rates=rates, fine=fine, kstar=kstar, goodput_t=gt, goodput=g, best=best, phase2=mc,
-                curve=curve)
+                rates=rates, fine_ids=f_ids, fine_rates=f_rates, fine=fine, kstar=kstar, goodput_t=gt, goodput=g,
+                best=best, phase2=mc, curve=curve)
 
 
 def reweight(w, out, weights, K=1024, alpha=0.8):
@@ -174,7 +182,7 @@ def best_plan(out):
     if out["best"] is None:
         return None
     b = int(out["best"].item())
-    return dict(index=b, plan_id=int(out["ids"][b].item()), goodput=float(out["goodput"][b].item()),
+    return dict(index=b, plan_id=int(out["fine_ids"][b].item()), goodput=float(out["goodput"][b].item()),
                 kstar=int(out["kstar"][b].item()))
 
 
