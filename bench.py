@@ -48,7 +48,10 @@ _W_C3_SEED0 = ("c3: Text-to-image graph L -> 50-step diffusion G (1024^2) mixed 
                "(sample: first 1 of its 64 seeds)")
 _W_C2_SEEDS2 = ("c2: Omni graph (E_img, E_aud) -> thinker -> gated talker -> audio generator on 16 simulated GPUs; "
                 "~10000 sampled plans; 16 rates; 32 seeds x 20000 requests (sample: first 2 of its 32 seeds)")
+_W_C4_STEP = ('c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse screening of 10^6 sampl'
+              'ed plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 requests; each step: the trace of all 64 seeds, phase 1 over all 1000000 plans, the top 1000 and their 32-rate grid, phase 3 of every 4-th selected plan at every rate on one seed (plan slice g mod 4 of seed g div 4 at step g), their goodput reduction')
 MEASURED_TRAFFIC = {
+    ('c8fea1958289865f', _W_C4_STEP): 4.1436e+12,
     ("c54c478f1dc57905", _W_C1): 2.0539e12,
     ("c54c478f1dc57905", _W_C2_SEEDS2): 9.1424e11,
     ("c54c478f1dc57905", _W_C3_SEED0): 1.9634e12,
@@ -57,6 +60,7 @@ MEASURED_TRAFFIC = {
 # VALU lane rate of the k_fine launch by rocprofv3 counters (SQ_INSTS_VALU x SQ_THREAD_CYCLES_VALU /
 # SQ_ACTIVE_INST_VALU / kernel time / PEAK_LANE_OPS), keyed like MEASURED_TRAFFIC
 MEASURED_LANE_FRAC = {
+    ('c8fea1958289865f', _W_C4_STEP): 0.1955,
     ("c54c478f1dc57905", _W_C1): 0.4244,
     ("c54c478f1dc57905", _W_C2_SEEDS2): 0.3076,
     ("c54c478f1dc57905", _W_C3_SEED0): 0.3977,
