@@ -115,7 +115,52 @@ typedef struct {
   const uint8_t *n_alt;       /* [8][P] */
   const uint8_t *alt_w;       /* [8][2][P] weight in tenths */
   const uint8_t *alt_node;    /* [8][2][8][P] node per component, 255 = none */
+  /* A node may hold executors of two configurations (Eq. (1): n_{v,k} executors of
+   * configuration k): node_rep2 > 0 executors of batch node_batch2 and node_gpus2 GPUs next
+   * to the node_rep of the first, and a request reaching the node goes to the first group
+   * with probability node_w / 10, to the second with (10 - node_w) / 10 (routing between the
+   * executors of a node in steps of 0.1, Sec. 4.2).  NULL arrays: every node has one
+   * configuration. */
+  const uint8_t *node_rep2;    /* [16][P] */
+  const uint16_t *node_batch2; /* [16][P] */
+  const uint8_t *node_gpus2;   /* [16][P] */
+  const uint8_t *node_w;       /* [16][P] tenths for the first group (1..9 when node_rep2 > 0) */
 } cfo_plans;
+
+/* the executor groups of node v of plan p (one or two) */
+typedef struct {
+  int rep, batch, gpus;
+  double share;  /* probability that a request reaching the node goes to this group */
+} cfo_group;
+
+static inline int cfo_node_groups(const cfo_plans *pl, int v, int p, cfo_group g[2]) {
+  const size_t o = (size_t)v * (size_t)pl->P + (size_t)p;
+  const int rep2 = pl->node_rep2 ? pl->node_rep2[o] : 0;
+  g[0].rep = pl->node_rep[o];
+  g[0].batch = pl->node_batch[o];
+  g[0].gpus = pl->node_gpus[o];
+  g[0].share = 1.0;
+  if (rep2 == 0) return 1;
+  const int w = pl->node_w[o];
+  g[0].share = (double)w / 10.0;
+  g[1].rep = rep2;
+  g[1].batch = pl->node_batch2[o];
+  g[1].gpus = pl->node_gpus2[o];
+  g[1].share = (double)(10 - w) / 10.0;
+  return 2;
+}
+
+/* The executor of node v (index among its executors, the first group's first) that serves
+ * a request with 16-bit replica key `key` for that node: the key space [0, 2^16) is cut at
+ * w/10 between the two groups, and a group's part into equal parts for its executors. */
+static inline int cfo_node_pick(uint64_t key, const cfo_group *g, int ng, const cfo_plans *pl, int v, int p) {
+  if (ng == 1) return (int)((key * (uint64_t)g[0].rep) >> 16);
+  const uint64_t w = pl->node_w[(size_t)v * (size_t)pl->P + (size_t)p];
+  const uint64_t pos = key * 10u;  /* the key's place in [0, 10 * 2^16) */
+  const uint64_t cut = w << 16;
+  if (pos < cut) return (int)((pos * (uint64_t)g[0].rep) / cut);
+  return g[0].rep + (int)(((pos - cut) * (uint64_t)g[1].rep) / ((10u - w) << 16));
+}
 
 /* --- primitives (exposed for the tests that pin them) --- */
 void cfo_philox(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]);
@@ -131,10 +176,11 @@ int cfo_eval_coarse(const cfo_model *m, const cfo_plans *pl, const uint64_t *mom
                     int32_t n_gpus, double *rd, int32_t *bottleneck, uint8_t *flags);
 
 /* phase-1 helpers shared inside the oracle: structural validity of plan p,
- * and the per-node demand u_v (seconds of executor time per request). */
+ * and the demand u[v][g] of every executor group (seconds of executor time
+ * per request). */
 int cfo_plan_valid(const cfo_model *m, const cfo_plans *pl, int p);
 void cfo_node_demand(const cfo_model *m, const cfo_plans *pl, int p, const uint64_t *moments,
-                     double u[CFO_MAXV]);
+                     double u[CFO_MAXV][2]);
 
 /* Phase 2 (Monte Carlo latency with occupancy-aware scaling) for plans
  * ids[0..n): the first n_sample requests of trace seed seed_idx, routed

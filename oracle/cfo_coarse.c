@@ -32,10 +32,16 @@ int cfo_plan_valid(const cfo_model *m, const cfo_plans *pl, int p) {
   for (int v = 0; v < nv; v++) {
     int cm = P_AT(pl->node_comp, v, P, p);
     if (cm == 0 || (cm >> m->n_comp) != 0) return 0;
-    int rep = P_AT(pl->node_rep, v, P, p);
-    int b = P_AT(pl->node_batch, v, P, p);
-    if (rep < 1 || b < 1 || b > CFO_MAXB || P_AT(pl->node_gpus, v, P, p) < 1) return 0;
-    execs += rep;
+    cfo_group g[2];
+    int ng = cfo_node_groups(pl, v, p, g);
+    if (ng == 2) {
+      int w = P_AT(pl->node_w, v, P, p);
+      if (w < 1 || w > 9) return 0;
+    }
+    for (int k = 0; k < ng; k++) {
+      if (g[k].rep < 1 || g[k].batch < 1 || g[k].batch > CFO_MAXB || g[k].gpus < 1) return 0;
+      execs += g[k].rep;
+    }
   }
   if (execs > CFO_MAXX) return 0;
   for (int t = 0; t < m->n_types; t++) {
@@ -54,16 +60,18 @@ int cfo_plan_valid(const cfo_model *m, const cfo_plans *pl, int p) {
   return 1;
 }
 
-/* u_v: seconds of executor time that one request of the workload mix puts
- * on node v (summed over its replicas) at the node's configured batch:
- * u_v += (pi_t * q_a) * w(c, t, B) in the order t, a, c ascending. */
+/* u[v][g]: seconds of executor time that one request of the workload mix puts
+ * on executor group g of node v (summed over its executors) at the group's
+ * configured batch: u[v][g] += ((pi_t * q_a) * s_g) * w(c, t, B_g) in the
+ * order t, a, c, g ascending, s_g the group's share of the node's requests
+ * (1 for a node of one configuration). */
 void cfo_node_demand(const cfo_model *m, const cfo_plans *pl, int p, const uint64_t *moments,
-                     double u[CFO_MAXV]) {
+                     double u[CFO_MAXV][2]) {
   int P = pl->P;
   uint64_t wsum_i = 0;
   for (int t = 0; t < m->n_types; t++) wsum_i += m->weight[t];
   double wsum = (double)wsum_i;
-  for (int v = 0; v < CFO_MAXV; v++) u[v] = 0.0;
+  for (int v = 0; v < CFO_MAXV; v++) u[v][0] = u[v][1] = 0.0;
   for (int t = 0; t < m->n_types; t++) {
     const uint64_t *mo = moments + (size_t)t * 8;
     double pi = (double)m->weight[t] / wsum;
@@ -76,9 +84,6 @@ void cfo_node_demand(const cfo_model *m, const cfo_plans *pl, int p, const uint6
       for (int c = 0; c < m->n_comp; c++) {
         if (!((m->path_mask[t] >> c) & 1u)) continue;
         int v = P_AT(pl->alt_node, (t * 2 + a) * 8 + c, P, p);
-        int bnode = P_AT(pl->node_batch, v, P, p);
-        int beff = bnode < m->batch_cap[c] ? bnode : m->batch_cap[c];
-        double B = (double)beff;
         /* per-type mean of X and of the output length */
         double ex = 0.0, en = 1.0;
         if (mo[0] > 0) {
@@ -91,12 +96,18 @@ void cfo_node_demand(const cfo_model *m, const cfo_plans *pl, int p, const uint6
             if (en < 1.0) en = 1.0;
           }
         }
-        /* seconds of executor time per request at batch B */
-        double w = ((m->k0[c] / B) + m->k1[c] * ex) + m->k2[c];
-        if (m->kind[c] == CFO_LLM) w = w + (en - 1.0) * ((m->d0[c] / B) + m->d1[c]);
-        /* on executors of g GPUs every iteration takes tp_scale times as long */
-        w = cfo_tp(m, c, P_AT(pl->node_gpus, v, P, p)) * w;
-        u[v] = u[v] + (pi * q) * w;
+        cfo_group grp[2];
+        int ng = cfo_node_groups(pl, v, p, grp);
+        for (int k = 0; k < ng; k++) {
+          int beff = grp[k].batch < m->batch_cap[c] ? grp[k].batch : m->batch_cap[c];
+          double B = (double)beff;
+          /* seconds of executor time per request at batch B */
+          double w = ((m->k0[c] / B) + m->k1[c] * ex) + m->k2[c];
+          if (m->kind[c] == CFO_LLM) w = w + (en - 1.0) * ((m->d0[c] / B) + m->d1[c]);
+          /* on executors of g GPUs every iteration takes tp_scale times as long */
+          w = cfo_tp(m, c, grp[k].gpus) * w;
+          u[v][k] = u[v][k] + ((pi * q) * grp[k].share) * w;
+        }
       }
     }
   }
@@ -111,23 +122,33 @@ int cfo_eval_coarse(const cfo_model *m, const cfo_plans *pl, const uint64_t *mom
       continue;
     }
     int nv = pl->n_nodes[p];
-    double u[CFO_MAXV];
+    double u[CFO_MAXV][2];
     cfo_node_demand(m, pl, p, moments, u);
+    /* capacity m/u of every executor group; R_d is the smallest, its node the bottleneck */
     double best = INFINITY;
     int bn = -1;
     for (int v = 0; v < nv; v++) {
-      if (u[v] > 0.0) {
-        double r = (double)P_AT(pl->node_rep, v, P, p) / u[v];
-        if (r < best) { best = r; bn = v; }
+      cfo_group g[2];
+      int ng = cfo_node_groups(pl, v, p, g);
+      for (int k = 0; k < ng; k++) {
+        if (u[v][k] > 0.0) {
+          double r = (double)g[k].rep / u[v][k];
+          if (r < best) { best = r; bn = v; }
+        }
       }
     }
+    /* Eq. (1) budget over every configuration; redundant: a group that receives no work, or
+     * one whose capacity without one executor still reaches R_d */
     int redundant = 0;
     uint64_t gpus = 0;
     for (int v = 0; v < nv; v++) {
-      int rep = P_AT(pl->node_rep, v, P, p);
-      gpus += (uint64_t)rep * P_AT(pl->node_gpus, v, P, p);
-      if (u[v] == 0.0) redundant = 1;
-      else if (rep >= 2 && (double)(rep - 1) / u[v] >= best) redundant = 1;
+      cfo_group g[2];
+      int ng = cfo_node_groups(pl, v, p, g);
+      for (int k = 0; k < ng; k++) {
+        gpus += (uint64_t)g[k].rep * (uint64_t)g[k].gpus;
+        if (u[v][k] == 0.0) redundant = 1;
+        else if (g[k].rep >= 2 && (double)(g[k].rep - 1) / u[v][k] >= best) redundant = 1;
+      }
     }
     int over = gpus > (uint64_t)n_gpus;
     rd[p] = best;

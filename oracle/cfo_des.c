@@ -421,19 +421,32 @@ int cfo_sim_triple(const cfo_model *m, const cfo_plans *pl, int32_t plan_id, dou
   /* a Poisson arrival rate is positive and finite; a plan id names a column of the table */
   if (p < 0 || p >= P || !(rate > 0.0) || !(rate < __builtin_inf())) { *status = CFO_ST_INVALID; return 0; }
 
-  /* executors: replicas of each node, numbered node by node */
+  /* executors: those of each node numbered node by node, a node's first
+   * executor group before its second */
   int nv = pl->n_nodes[p];
+  if (nv < 1 || nv > CFO_MAXV) { *status = CFO_ST_INVALID; return 0; }
   int base[CFO_MAXV + 1];
+  cfo_group grp[CFO_MAXV][2];
+  int ngrp[CFO_MAXV];
   base[0] = 0;
-  for (int v = 0; v < nv; v++) base[v + 1] = base[v] + P_AT(pl->node_rep, v, P, p);
+  for (int v = 0; v < nv; v++) {
+    ngrp[v] = cfo_node_groups(pl, v, p, grp[v]);
+    if (ngrp[v] == 2 && (P_AT(pl->node_w, v, P, p) < 1 || P_AT(pl->node_w, v, P, p) > 9)) {
+      *status = CFO_ST_INVALID;
+      return 0;
+    }
+    base[v + 1] = base[v];
+    for (int k = 0; k < ngrp[v]; k++) base[v + 1] += grp[v][k].rep;
+  }
   S.nx = base[nv];
-  if (nv < 1 || nv > CFO_MAXV || S.nx < 1 || S.nx > CFO_MAXX) { *status = CFO_ST_INVALID; return 0; }
+  if (S.nx < 1 || S.nx > CFO_MAXX) { *status = CFO_ST_INVALID; return 0; }
   S.x = (exec_t *)calloc((size_t)S.nx, sizeof(exec_t));
   for (int v = 0; v < nv; v++) {
     int cm = P_AT(pl->node_comp, v, P, p);
-    int bn = P_AT(pl->node_batch, v, P, p);
-    int gn = P_AT(pl->node_gpus, v, P, p);
     for (int j = base[v]; j < base[v + 1]; j++) {
+      const int k = j - base[v] < grp[v][0].rep ? 0 : 1;
+      int bn = grp[v][k].batch;
+      int gn = grp[v][k].gpus;
       exec_t *X = &S.x[j];
       X->rr = -1;
       for (int c = 0; c < CFO_MAXC; c++) X->stage_of[c] = -1;
@@ -474,7 +487,7 @@ int cfo_sim_triple(const cfo_model *m, const cfo_plans *pl, int32_t plan_id, dou
       int minc = __builtin_ctz(P_AT(pl->node_comp, v, P, p));
       uint64_t word = minc < 4 ? tr->rkey0[o] : tr->rkey1[o];
       uint64_t key = (word >> (16 * (minc & 3))) & 0xFFFFu;
-      int j = (int)((key * (uint64_t)P_AT(pl->node_rep, v, P, p)) >> 16);
+      int j = cfo_node_pick(key, grp[v], ngrp[v], pl, v, p);
       q->ex[c] = base[v] + j;
       if (m->kind[c] == CFO_LLM) {
         if (q->ttft_c < 0) q->ttft_c = c;

@@ -68,22 +68,30 @@ int cfo_eval_mc(const cfo_model *m, const cfo_plans *pl, const int32_t *ids, int
     const int nv = pl->n_nodes[p];
     const double R_d = rd[p];
     /* capacities and effective batches */
-    double u[CFO_MAXV];
+    double u[CFO_MAXV][2];
     cfo_node_demand(m, pl, p, moments, u);
-    int beff[CFO_MAXV][CFO_MAXC];
+    /* effective batch of component c on executor group g of node v: the group's share of
+     * the bottleneck's load */
+    int beff[CFO_MAXV][2][CFO_MAXC];
+    cfo_group grp[CFO_MAXV][2];
+    int ngrp[CFO_MAXV];
     int base[CFO_MAXV + 1];
     base[0] = 0;
     for (int v = 0; v < nv; v++) {
-      const int rep = P_AT(pl->node_rep, v, P, p);
-      base[v + 1] = base[v] + rep;
-      const double Rv = u[v] > 0.0 ? (double)rep / u[v] : INFINITY;
-      const double q = R_d / Rv;
-      for (int c = 0; c < NC; c++) {
-        const int bnode = P_AT(pl->node_batch, v, P, p);
-        const int B = bnode < m->batch_cap[c] ? bnode : m->batch_cap[c];
-        double bb = ceil((double)B * q);
-        int b = bb < 1.0 ? 1 : (bb > (double)B ? B : (int)bb);
-        beff[v][c] = b;
+      ngrp[v] = cfo_node_groups(pl, v, p, grp[v]);
+      base[v + 1] = base[v];
+      for (int k = 0; k < ngrp[v]; k++) {
+        const int rep = grp[v][k].rep;
+        base[v + 1] += rep;
+        const double Rv = u[v][k] > 0.0 ? (double)rep / u[v][k] : INFINITY;
+        const double q = R_d / Rv;
+        for (int c = 0; c < NC; c++) {
+          const int bnode = grp[v][k].batch;
+          const int B = bnode < m->batch_cap[c] ? bnode : m->batch_cap[c];
+          double bb = ceil((double)B * q);
+          int b = bb < 1.0 ? 1 : (bb > (double)B ? B : (int)bb);
+          beff[v][k][c] = b;
+        }
       }
     }
     /* the sampled requests */
@@ -109,7 +117,9 @@ int cfo_eval_mc(const cfo_model *m, const cfo_plans *pl, const int32_t *ids, int
         const int minc = __builtin_ctz(cm);
         const uint64_t word = minc < 4 ? tr->rkey0[o] : tr->rkey1[o];
         const uint64_t key = (word >> (16 * (minc & 3))) & 0xFFFFu;
-        ex[c] = base[v] + (int)((key * (uint64_t)P_AT(pl->node_rep, v, P, p)) >> 16);
+        const int j = cfo_node_pick(key, grp[v], ngrp[v], pl, v, p);
+        const int gk = j < grp[v][0].rep ? 0 : 1;  /* the executor's group */
+        ex[c] = base[v] + j;
         node[c] = v;
         /* start: the last input to arrive */
         const int src = m->gate_src[c];
@@ -121,8 +131,8 @@ int cfo_eval_mc(const cfo_model *m, const cfo_plans *pl, const int32_t *ids, int
           const double ready = (gated_here && pc == src) ? first[pc] + hop : fin[pc] + hop;
           if (ready > start) start = ready;
         }
-        const int b = beff[v][c];
-        const double tps = cfo_tp(m, c, P_AT(pl->node_gpus, v, P, p));
+        const int b = beff[v][gk][c];
+        const double tps = cfo_tp(m, c, grp[v][gk].gpus);
         uint64_t x = 0;
         for (int at = 0; at < CFO_NATTR; at++)
           if ((m->x_sel[c] >> at) & 1u) x += attr(tr, o, at);

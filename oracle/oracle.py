@@ -58,7 +58,9 @@ class Trace(C.Structure):
 class Plans(C.Structure):
     _fields_ = [("P", C.c_int32), ("n_nodes", C.c_void_p), ("node_comp", C.c_void_p),
                 ("node_rep", C.c_void_p), ("node_batch", C.c_void_p), ("node_gpus", C.c_void_p),
-                ("n_alt", C.c_void_p), ("alt_w", C.c_void_p), ("alt_node", C.c_void_p)]
+                ("n_alt", C.c_void_p), ("alt_w", C.c_void_p), ("alt_node", C.c_void_p),
+                ("node_rep2", C.c_void_p), ("node_batch2", C.c_void_p), ("node_gpus2", C.c_void_p),
+                ("node_w", C.c_void_p)]
 
 
 class EnumOpts(C.Structure):
@@ -239,7 +241,9 @@ def plans_struct(tab):
     st.P = tab.P
     keep = []
     for f in ("n_nodes", "node_comp", "node_rep", "node_batch", "node_gpus", "n_alt", "alt_w",
-              "alt_node"):
+              "alt_node", "node_rep2", "node_batch2", "node_gpus2", "node_w"):
+        if getattr(tab, f, None) is None:  # a table without second executor groups
+            continue
         a = np.ascontiguousarray(getattr(tab, f))
         keep.append(a)
         setattr(st, f, a.ctypes.data)

@@ -18,6 +18,10 @@ node_comp      uint8    [16, P]      component bitmask hosted by node v
 node_rep       uint8    [16, P]      executors (replicas) of node v
 node_batch     uint16   [16, P]      max batch of node v (<= 256)
 node_gpus      uint8    [16, P]      GPUs per executor of node v
+node_rep2      uint8    [16, P]      executors of node v's second configuration (0: none)
+node_batch2    uint16   [16, P]      max batch of that second configuration
+node_gpus2     uint8    [16, P]      GPUs per executor of that second configuration
+node_w         uint8    [16, P]      tenths of node v's requests to its first configuration
 n_alt          uint8    [8, P]       alternatives of type t (1 or 2)
 alt_w          uint8    [16, P]      slot 2t+a: weight of alternative a, tenths
 alt_node       uint8    [128, P]     slot (2t+a)*8+c: node serving component c
@@ -28,7 +32,11 @@ fully disaggregated (one node per component; replicas by coin change,
 Eq. 1), and seeded samples of mixed / compound plans: one or two subplans,
 each covering a subset of the types, each edge of a subplan kept or merged,
 optional node sharing between the two subplans, replicas drawn within the
-GPU budget, batches from the knob set, routing weights in tenths.
+GPU budget, batches from the knob set, routing weights in tenths, and (with the
+sampler option ``het`` > 0, the probability per node of two or more executors)
+a node's executors split between two batch configurations with the share of the
+node's requests for the first drawn in tenths (Eq. 1's executors of several
+configurations per node).
 """
 import hashlib
 import itertools
@@ -42,7 +50,7 @@ MAXV, MAXT, MAXC = 16, 8, 8
 
 class PlanTable:
     FIELDS = ("n_nodes", "node_comp", "node_rep", "node_batch", "node_gpus", "n_alt", "alt_w",
-              "alt_node")
+              "alt_node", "node_rep2", "node_batch2", "node_gpus2", "node_w")
 
     def __init__(self, P):
         self.P = int(P)
@@ -54,6 +62,12 @@ class PlanTable:
         self.n_alt = np.zeros((MAXT, P), np.uint8)
         self.alt_w = np.zeros((2 * MAXT, P), np.uint8)
         self.alt_node = np.full((2 * MAXT * MAXC, P), 255, np.uint8)
+        # a node's second executor configuration (Eq. 1: executors of several configurations
+        # per node): none by default, all of a node's requests to its first (10 tenths)
+        self.node_rep2 = np.zeros((MAXV, P), np.uint8)
+        self.node_batch2 = np.zeros((MAXV, P), np.uint16)
+        self.node_gpus2 = np.zeros((MAXV, P), np.uint8)
+        self.node_w = np.full((MAXV, P), 10, np.uint8)
 
     def subset(self, ids):
         ids = np.asarray(ids, dtype=np.int64)
@@ -67,7 +81,9 @@ class PlanTable:
         """Readable dict of plan p (for reports and tests)."""
         nv = int(self.n_nodes[p])
         nodes = [dict(comp=int(self.node_comp[v, p]), rep=int(self.node_rep[v, p]),
-                      batch=int(self.node_batch[v, p]), gpus=int(self.node_gpus[v, p]))
+                      batch=int(self.node_batch[v, p]), gpus=int(self.node_gpus[v, p]),
+                      rep2=int(self.node_rep2[v, p]), batch2=int(self.node_batch2[v, p]),
+                      gpus2=int(self.node_gpus2[v, p]), w=int(self.node_w[v, p]))
                  for v in range(nv)]
         routes = []
         for t in range(MAXT):
@@ -89,16 +105,21 @@ def _model_index(model):
 
 
 def plan_table_from_list(plans, P=None):
-    """plans: list of dict(nodes=[(comp_mask, rep, batch, gpus)], routes=[[(w, {c: node})]])."""
+    """plans: list of dict(nodes=[(comp_mask, rep, batch, gpus[, rep2, batch2, gpus2, w])],
+    routes=[[(w, {c: node})]]); the optional second executor configuration of a node: rep2
+    executors of batch2 and gpus2, w tenths of the node's requests to the first."""
     P = len(plans) if P is None else P
     tab = PlanTable(P)
     for p, pl in enumerate(plans):
         tab.n_nodes[p] = len(pl["nodes"])
-        for v, (cm, rep, b, g) in enumerate(pl["nodes"]):
+        for v, nd in enumerate(pl["nodes"]):
+            cm, rep, b, g = nd[:4]
             tab.node_comp[v, p] = cm
             tab.node_rep[v, p] = rep
             tab.node_batch[v, p] = b
             tab.node_gpus[v, p] = g
+            if len(nd) > 4:
+                tab.node_rep2[v, p], tab.node_batch2[v, p], tab.node_gpus2[v, p], tab.node_w[v, p] = nd[4:8]
         for t, alts in enumerate(pl["routes"]):
             tab.n_alt[t, p] = len(alts)
             for a, (w, cmap) in enumerate(alts):
@@ -146,7 +167,7 @@ def _disaggregated(model, fam, gpus):
 def _candidate(ctx, j):
     """Candidate plan j of the sampler (its own Philox stream, keyed by the config's seed
     with counter j), as its canonical encoding, or None if it does not fit the budget."""
-    T, C, paths, edges, colocatable, knobs, gpus, seed = ctx
+    T, C, paths, edges, colocatable, knobs, gpus, seed, het = ctx
     rng = np.random.Generator(np.random.Philox(key=seed, counter=j))
     ns = 1 if rng.random() < 0.5 or T == 1 else 2
     if ns == 1:
@@ -211,6 +232,18 @@ def _candidate(ctx, j):
     for mask in nodes:
         first = (mask & -mask).bit_length() - 1
         batch.append(int(knobs[first][int(rng.integers(0, len(knobs[first])))]))
+    second = [()] * V
+    if het > 0:  # a node of 2+ executors may split them between two batch configurations
+        for v, mask in enumerate(nodes):
+            if reps[v] >= 2 and rng.random() < het:
+                first = (mask & -mask).bit_length() - 1
+                others = [int(b) for b in knobs[first] if int(b) != batch[v]]
+                if others:
+                    r2 = int(rng.integers(1, reps[v]))
+                    b2 = others[int(rng.integers(0, len(others)))]
+                    w = int(rng.integers(1, 10))
+                    second[v] = (r2, b2, 1, w)
+                    reps[v] -= r2
     routes = []
     for t in range(T):
         alts = [si for si in range(ns) if t in cover[si]]
@@ -220,7 +253,7 @@ def _candidate(ctx, j):
             w0 = int(rng.integers(1, 10))
             routes.append([(w0, {c: node_of[alts[0]][c] for c in paths[t]}),
                            (10 - w0, {c: node_of[alts[1]][c] for c in paths[t]})])
-    return _row(dict(nodes=[(nodes[v], reps[v], batch[v], 1) for v in range(V)], routes=routes))
+    return _row(dict(nodes=[(nodes[v], reps[v], batch[v], 1) + second[v] for v in range(V)], routes=routes))
 
 
 def _candidates(ctx, lo, hi):
@@ -229,23 +262,37 @@ def _candidates(ctx, lo, hi):
 
 # One plan as the bytes of its table column (a canonical encoding: two plans are equal
 # iff their columns are): n_nodes, node_comp[16], node_rep[16], node_batch[16] (u16,
-# little endian), node_gpus[16], n_alt[8], alt_w[16], alt_node[128].
+# little endian), node_gpus[16], n_alt[8], alt_w[16], alt_node[128], node_rep2[16],
+# node_batch2[16] (u16), node_gpus2[16], node_w[16].
 _ROW_OFF = dict(n_nodes=0, node_comp=1, node_rep=1 + MAXV, node_batch=1 + 2 * MAXV, node_gpus=1 + 4 * MAXV,
                 n_alt=1 + 5 * MAXV, alt_w=1 + 5 * MAXV + MAXT, alt_node=1 + 5 * MAXV + 3 * MAXT)
-ROW_BYTES = _ROW_OFF["alt_node"] + 2 * MAXT * MAXC
-_ROW_TEMPLATE = bytes(_ROW_OFF["alt_node"]) + bytes([255]) * (2 * MAXT * MAXC)
+_ROW_OFF["node_rep2"] = _ROW_OFF["alt_node"] + 2 * MAXT * MAXC
+_ROW_OFF["node_batch2"] = _ROW_OFF["node_rep2"] + MAXV
+_ROW_OFF["node_gpus2"] = _ROW_OFF["node_batch2"] + 2 * MAXV
+_ROW_OFF["node_w"] = _ROW_OFF["node_gpus2"] + MAXV
+ROW_BYTES = _ROW_OFF["node_w"] + MAXV
+_ROW_TEMPLATE = (bytes(_ROW_OFF["alt_node"]) + bytes([255]) * (2 * MAXT * MAXC) + bytes(4 * MAXV)
+                 + bytes([10]) * MAXV)
 
 
 def _row(pl):
     b = bytearray(_ROW_TEMPLATE)
     b[0] = len(pl["nodes"])
     o = _ROW_OFF
-    for v, (cm, rep, bt, g) in enumerate(pl["nodes"]):
+    for v, nd in enumerate(pl["nodes"]):
+        cm, rep, bt, g = nd[:4]
         b[o["node_comp"] + v] = cm
         b[o["node_rep"] + v] = rep
         b[o["node_batch"] + 2 * v] = bt & 255
         b[o["node_batch"] + 2 * v + 1] = bt >> 8
         b[o["node_gpus"] + v] = g
+        if len(nd) > 4:
+            r2, b2, g2, w = nd[4:8]
+            b[o["node_rep2"] + v] = r2
+            b[o["node_batch2"] + 2 * v] = b2 & 255
+            b[o["node_batch2"] + 2 * v + 1] = b2 >> 8
+            b[o["node_gpus2"] + v] = g2
+            b[o["node_w"] + v] = w
     for t, alts in enumerate(pl["routes"]):
         b[o["n_alt"] + t] = len(alts)
         for a, (w, cmap) in enumerate(alts):
@@ -272,6 +319,11 @@ def table_from_rows(rows):
     tab.n_alt = np.ascontiguousarray(R[:, o["n_alt"]:o["n_alt"] + MAXT].T)
     tab.alt_w = np.ascontiguousarray(R[:, o["alt_w"]:o["alt_w"] + 2 * MAXT].T)
     tab.alt_node = np.ascontiguousarray(R[:, o["alt_node"]:o["alt_node"] + 2 * MAXT * MAXC].T)
+    tab.node_rep2 = np.ascontiguousarray(R[:, o["node_rep2"]:o["node_rep2"] + MAXV].T)
+    nb2 = np.ascontiguousarray(R[:, o["node_batch2"]:o["node_batch2"] + 2 * MAXV]).view("<u2")
+    tab.node_batch2 = np.ascontiguousarray(nb2.T.astype(np.uint16))
+    tab.node_gpus2 = np.ascontiguousarray(R[:, o["node_gpus2"]:o["node_gpus2"] + MAXV].T)
+    tab.node_w = np.ascontiguousarray(R[:, o["node_w"]:o["node_w"] + MAXV].T)
     return tab
 
 
@@ -287,7 +339,7 @@ def _sample(model, spec, gpus, have, total, progress=True):
     if colocatable is not None:
         colocatable = {(idx[a], idx[b]) for a, b in colocatable}
     knobs = [spec["batch"][n] for n in names]
-    ctx = (T, C, paths, edges, colocatable, knobs, int(gpus), int(spec["seed"]))
+    ctx = (T, C, paths, edges, colocatable, knobs, int(gpus), int(spec["seed"]), float(spec.get("het", 0.0)))
     need = total - len(have)
     seen = set(have)
     out = []
@@ -343,7 +395,7 @@ def _sample(model, spec, gpus, have, total, progress=True):
 
 
 def _cache_path(cfg):
-    h = hashlib.sha1(repr((cfg["model"], cfg["plans"], cfg["gpus"])).encode()).hexdigest()[:16]
+    h = hashlib.sha1(repr((cfg["model"], cfg["plans"], cfg["gpus"], PlanTable.FIELDS)).encode()).hexdigest()[:16]
     d = os.environ.get("CF_PLAN_CACHE", os.path.join(os.path.expanduser("~"), ".cache", "cf_plans"))
     return os.path.join(d, "%s_%s.npz" % (cfg.get("name", "cfg"), h))
 
