@@ -164,6 +164,18 @@ typedef struct cf_plan_table {
   const uint8_t *n_alt_dev;      /* [8][P] alternatives per type (1 or 2) */
   const uint8_t *alt_w_dev;      /* [16][P] slot 2t+a: routing weight in tenths */
   const uint8_t *alt_node_dev;   /* [128][P] slot (2t+a)*8+c: node serving c */
+  /* Optional second executor configuration of each node (Eq. (1): n_{v,k} executors of
+   * each configuration k of a node): node_rep2 more executors (0: none) of max batch
+   * node_batch2 and node_gpus2 GPUs, and node_w, the tenths of the node's requests that go
+   * to the first configuration (1..9 where node_rep2 > 0; routing between the executors
+   * of a node in steps of 0.1, Sec. 4.2).  A request's replica key for the node (16 bits)
+   * picks the executor: keys below node_w * 2^16 / 10 go to the first configuration, the
+   * others to the second, each part cut into equal parts for that configuration's
+   * executors, numbered after the first's.  All four NULL: one configuration per node. */
+  const uint8_t *node_rep2_dev;   /* [16][P] */
+  const uint16_t *node_batch2_dev;/* [16][P] */
+  const uint8_t *node_gpus2_dev;  /* [16][P] */
+  const uint8_t *node_w_dev;      /* [16][P] */
 } cf_plan_table;
 
 /* Outputs of cf_eval_fine, device arrays, triple (i, k, s) = plan i, rate k,

@@ -430,8 +430,16 @@ int cfo_sim_triple(const cfo_model *m, const cfo_plans *pl, int32_t plan_id, dou
   int ngrp[CFO_MAXV];
   base[0] = 0;
   for (int v = 0; v < nv; v++) {
+    /* a node hosts components of the model and has executors of valid batches; a second
+     * configuration has a share in 1..9 tenths and GPUs */
+    int cm = P_AT(pl->node_comp, v, P, p);
     ngrp[v] = cfo_node_groups(pl, v, p, grp[v]);
-    if (ngrp[v] == 2 && (P_AT(pl->node_w, v, P, p) < 1 || P_AT(pl->node_w, v, P, p) > 9)) {
+    int bad_node = cm == 0 || (cm >> m->n_comp) != 0;
+    for (int k = 0; k < ngrp[v]; k++)
+      if (grp[v][k].rep < 1 || grp[v][k].batch < 1 || grp[v][k].batch > CFO_MAXB) bad_node = 1;
+    if (ngrp[v] == 2 && (P_AT(pl->node_w, v, P, p) < 1 || P_AT(pl->node_w, v, P, p) > 9 || grp[v][1].gpus < 1))
+      bad_node = 1;
+    if (bad_node) {
       *status = CFO_ST_INVALID;
       return 0;
     }

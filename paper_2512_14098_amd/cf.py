@@ -61,7 +61,8 @@ class cf_trace(C.Structure):
 class cf_plan_table(C.Structure):
     _fields_ = [("P", C.c_int32)] + [
         (f + "_dev", C.c_void_p) for f in ("n_nodes", "node_comp", "node_rep", "node_batch",
-                                           "node_gpus", "n_alt", "alt_w", "alt_node")]
+                                           "node_gpus", "n_alt", "alt_w", "alt_node",
+                                           "node_rep2", "node_batch2", "node_gpus2", "node_w")]
 
 
 class cf_enum_opts(C.Structure):
@@ -283,13 +284,16 @@ class DevicePlans:
 
     FIELDS = ("n_nodes", "node_comp", "node_rep", "node_batch", "node_gpus", "n_alt", "alt_w",
               "alt_node")
+    # a node's second executor configuration: copied only when some node of the table has one
+    GROUP_FIELDS = ("node_rep2", "node_batch2", "node_gpus2", "node_w")
 
     def __init__(self, tab, device="cuda"):
         self.P = tab.P
         self.t = {}
         self.c = cf_plan_table()
         self.c.P = tab.P
-        for f in self.FIELDS:
+        split = getattr(tab, "node_rep2", None) is not None and bool(np.any(tab.node_rep2))
+        for f in self.FIELDS + (self.GROUP_FIELDS if split else ()):
             a = np.ascontiguousarray(getattr(tab, f))
             if a.dtype == np.uint16:
                 a = a.view(np.int16)

@@ -138,3 +138,19 @@ __device__ __forceinline__ int target_bin(const double *tg, int n_bins, int t, d
 enum ScratchSlot { SCR_TRACE = 0, SCR_SELECT = 1, SCR_FINE = 2, SCR_MC = 3, SCR_PARETO = 4, SCR_ENUM = 5, SCR_TARGETS = 6, SCR_BISECT = 7, SCR_NSLOTS = 8 };
 void *scratch_get(int slot, size_t bytes, cf_status *st);
 }  // namespace cf
+
+namespace cf {
+// The executor, among a node's executors (those of its first configuration
+// first), that serves a request whose 16-bit replica key for the node is key.
+// A node of one configuration (w == 0) cuts the key range into rep1 equal
+// parts.  A node with rep2 executors of a second configuration gives the keys
+// below w * 2^16 / 10 to the first configuration and the rest to the second,
+// each part cut into equal parts for its executors (every product stays below
+// 10 * 2^16 * 64 < 2^32).
+__device__ __forceinline__ int node_exec(uint32_t key, uint32_t rep1, uint32_t rep2, uint32_t w) {
+  if (w == 0) return (int)((key * rep1) >> 16);
+  const uint32_t pos = key * 10u, cut = w << 16;
+  if (pos < cut) return (int)((pos * rep1) / cut);
+  return (int)rep1 + (int)(((pos - cut) * rep2) / ((10u - w) << 16));
+}
+}  // namespace cf

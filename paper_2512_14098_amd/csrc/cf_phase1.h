@@ -77,4 +77,51 @@ __device__ __forceinline__ void phase1_result(int nv, const uint32_t *rep, const
                      (redundant ? CF_FLAG_REDUNDANT : 0u));
 }
 
+// phase1_result for plans whose nodes may hold a second executor
+// configuration: the capacity m/u of every executor group, in node order and a
+// node's first configuration before its second (rep2[v] = 0: none), gives R_d
+// and the bottleneck node; the budget counts both configurations; a group
+// receiving no work, or keeping R_d without one of its executors, makes the
+// plan redundant.
+template <class U, class U2>
+__device__ __forceinline__ void phase1_result_groups(int nv, const uint32_t *rep, const uint32_t *gp,
+                                                     const uint32_t *rep2, const uint32_t *gp2, U u_at, U2 u2_at,
+                                                     int n_gpus, double *rd, int32_t *bott, uint8_t *flags) {
+  double best = __builtin_inf();
+  int bn = -1;
+  bool redundant = false;
+  uint64_t gpus = 0;
+  for (int v = 0; v < nv; v++) {
+    const double u = u_at(v);
+    if (u > 0.0) {
+      const double r = (double)rep[v] / u;
+      if (r < best) { best = r; bn = v; }
+    }
+    if (rep2[v] > 0) {
+      const double u2 = u2_at(v);
+      if (u2 > 0.0) {
+        const double r = (double)rep2[v] / u2;
+        if (r < best) { best = r; bn = v; }
+      }
+    }
+  }
+  for (int v = 0; v < nv; v++) {
+    const double u = u_at(v);
+    gpus += (uint64_t)rep[v] * gp[v];
+    if (u == 0.0) redundant = true;
+    else if (rep[v] >= 2 && (double)(rep[v] - 1) / u >= best) redundant = true;
+    if (rep2[v] > 0) {
+      const double u2 = u2_at(v);
+      gpus += (uint64_t)rep2[v] * gp2[v];
+      if (u2 == 0.0) redundant = true;
+      else if (rep2[v] >= 2 && (double)(rep2[v] - 1) / u2 >= best) redundant = true;
+    }
+  }
+  const bool over = gpus > (uint64_t)n_gpus;
+  *rd = best;
+  *bott = bn;
+  *flags = (uint8_t)(((!over && !redundant) ? CF_FLAG_KEEP : 0u) | (over ? CF_FLAG_OVER_BUDGET : 0u) |
+                     (redundant ? CF_FLAG_REDUNDANT : 0u));
+}
+
 }  // namespace cf

@@ -15,27 +15,39 @@ namespace cf {
 namespace {
 
 constexpr int kBlock = 256;
+// plans whose nodes may hold a second executor configuration: a smaller block
+// for the second set of per-node LDS arrays
+constexpr int kBlockGroups = 128;
 
 struct PlanView {
   int P;
   const uint8_t *n_nodes, *node_comp, *node_rep, *node_gpus, *n_alt, *alt_w, *alt_node;
   const uint16_t *node_batch;
+  const uint8_t *node_rep2, *node_gpus2, *node_w;  // second configurations (HET kernel only)
+  const uint16_t *node_batch2;
 };
 
-__global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const uint64_t *moments,
-                                                   int n_gpus, double *rd, int32_t *bott, uint8_t *flags) {
+template <bool HET>
+__global__ void __launch_bounds__(HET ? kBlockGroups : kBlock)
+    k_coarse(KModel m, PlanView pv, const uint64_t *moments, int n_gpus, double *rd, int32_t *bott, uint8_t *flags) {
+  constexpr int NB = HET ? kBlockGroups : kBlock;
   __shared__ double ex_s[CF_MAX_TYPES][CF_MAX_COMP];
   __shared__ double en_s[CF_MAX_TYPES][CF_MAX_COMP];
-  __shared__ double u_s[CF_MAX_NODES][kBlock];
-  __shared__ uint16_t b_s[CF_MAX_NODES][kBlock];  // node batch
-  __shared__ uint8_t c_s[CF_MAX_NODES][kBlock];   // node component set
-  __shared__ uint8_t g_s[CF_MAX_NODES][kBlock];   // node GPUs per executor, as min(g, 8) - 1
-  __shared__ double tps_s[CF_MAX_COMP][8];        // iteration-time multipliers by GPUs per executor
+  __shared__ double u_s[CF_MAX_NODES][NB];
+  __shared__ uint16_t b_s[CF_MAX_NODES][NB];  // node batch
+  __shared__ uint8_t c_s[CF_MAX_NODES][NB];   // node component set
+  __shared__ uint8_t g_s[CF_MAX_NODES][NB];   // node GPUs per executor, as min(g, 8) - 1
+  __shared__ double tps_s[CF_MAX_COMP][8];    // iteration-time multipliers by GPUs per executor
+  // second configuration of a node (HET): demand, batch, GPUs index, tenths to the first
+  __shared__ double u2_s[HET ? CF_MAX_NODES : 1][HET ? NB : 1];
+  __shared__ uint16_t b2_s[HET ? CF_MAX_NODES : 1][HET ? NB : 1];
+  __shared__ uint8_t g2_s[HET ? CF_MAX_NODES : 1][HET ? NB : 1];
+  __shared__ uint8_t w_s[HET ? CF_MAX_NODES : 1][HET ? NB : 1];
   const int tid = threadIdx.x;
   if (tid < CF_MAX_COMP * 8) (&tps_s[0][0])[tid] = (&m.tps[0][0])[tid];
   phase1_means(m, moments, tid, ex_s, en_s);
   __syncthreads();
-  const long long p = (long long)blockIdx.x * kBlock + tid;
+  const long long p = (long long)blockIdx.x * NB + tid;
   if (p >= pv.P) return;
   const size_t P = (size_t)pv.P;
 #define AT(arr, slot) (arr)[(size_t)(slot) * P + (size_t)p]
@@ -45,6 +57,7 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
   // count are not fetched.
   const int nv = pv.n_nodes[p];
   uint32_t rep[CF_MAX_NODES], gp[CF_MAX_NODES];
+  uint32_t rep2[HET ? CF_MAX_NODES : 1], gp2[HET ? CF_MAX_NODES : 1];
 #pragma unroll
   for (int v = 0; v < CF_MAX_NODES; v++) {
     uint32_t cm = 0, b = 0;
@@ -59,6 +72,20 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
     c_s[v][tid] = (uint8_t)cm;
     b_s[v][tid] = (uint16_t)b;
     if (m.tp_any) g_s[v][tid] = (uint8_t)(gp[v] < 1 ? 0 : (gp[v] > 8 ? 7 : gp[v] - 1));
+    if constexpr (HET) {
+      uint32_t b2 = 0, w = 0;
+      rep2[v] = 0;
+      gp2[v] = 0;
+      if (v < nv) {
+        rep2[v] = AT(pv.node_rep2, v);
+        b2 = AT(pv.node_batch2, v);
+        gp2[v] = AT(pv.node_gpus2, v);
+        w = AT(pv.node_w, v);
+      }
+      b2_s[v][tid] = (uint16_t)b2;
+      w_s[v][tid] = (uint8_t)(rep2[v] > 0 ? w : 0u);
+      if (m.tp_any) g2_s[v][tid] = (uint8_t)(gp2[v] < 1 ? 0 : (gp2[v] > 8 ? 7 : gp2[v] - 1));
+    }
   }
   bool valid = nv >= 1 && nv <= CF_MAX_NODES;
   int execs = 0;
@@ -68,6 +95,13 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
       const uint32_t cm = c_s[v][tid], b = b_s[v][tid];
       if (cm == 0 || (cm >> m.nc) || rep[v] < 1 || b < 1 || b > CF_MAX_BATCH || gp[v] < 1) valid = false;
       execs += (int)rep[v];
+      if constexpr (HET) {
+        if (rep2[v] > 0) {
+          const uint32_t b2 = b2_s[v][tid], w = w_s[v][tid];
+          if (b2 < 1 || b2 > CF_MAX_BATCH || gp2[v] < 1 || w < 1 || w > 9) valid = false;
+          execs += (int)rep2[v];
+        }
+      }
     }
   }
   if (execs > CF_MAX_EXEC) valid = false;
@@ -78,8 +112,13 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
     return;
   }
   // per type: the routes of both alternatives are loaded together, then
-  // checked and accumulated: u_v += (pi_t q_a) w in the order t, a, c
-  for (int v = 0; v < nv; v++) u_s[v][tid] = 0.0;
+  // checked and accumulated: u_v += (pi_t q_a) w in the order t, a, c (and,
+  // for a node of two configurations, u_v += ((pi_t q_a) s) w for each
+  // configuration, s its share of the node's requests)
+  for (int v = 0; v < nv; v++) {
+    u_s[v][tid] = 0.0;
+    if constexpr (HET) u2_s[v][tid] = 0.0;
+  }
   const double wsum = (double)m.wsum;
   for (int t = 0; t < m.nt; t++) {
     const uint32_t path = m.path[t];
@@ -114,6 +153,16 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
           }
           const double w =
               phase1_work(m, c, b_s[v][tid], ex_s[t][c], en_s[t][c], m.tp_any ? tps_s[c][g_s[v][tid]] : 1.0);
+          if constexpr (HET) {
+            const uint32_t ws = w_s[v][tid];
+            if (ws) {
+              const double w2 = phase1_work(m, c, b2_s[v][tid], ex_s[t][c], en_s[t][c],
+                                            m.tp_any ? tps_s[c][g2_s[v][tid]] : 1.0);
+              u_s[v][tid] = u_s[v][tid] + (pq * ((double)ws / 10.0)) * w;
+              u2_s[v][tid] = u2_s[v][tid] + (pq * ((double)(10u - ws) / 10.0)) * w2;
+              continue;
+            }
+          }
           u_s[v][tid] = u_s[v][tid] + pq * w;
         }
       }
@@ -125,7 +174,11 @@ __global__ void __launch_bounds__(kBlock) k_coarse(KModel m, PlanView pv, const 
     flags[p] = CF_FLAG_INVALID;
     return;
   }
-  phase1_result(nv, rep, gp, [&](int v) { return u_s[v][tid]; }, n_gpus, &rd[p], &bott[p], &flags[p]);
+  if constexpr (HET)
+    phase1_result_groups(nv, rep, gp, rep2, gp2, [&](int v) { return u_s[v][tid]; },
+                         [&](int v) { return u2_s[v][tid]; }, n_gpus, &rd[p], &bott[p], &flags[p]);
+  else
+    phase1_result(nv, rep, gp, [&](int v) { return u_s[v][tid]; }, n_gpus, &rd[p], &bott[p], &flags[p]);
 #undef AT
 }
 
@@ -146,9 +199,19 @@ extern "C" cf_status cf_eval_coarse(const cf_model_desc *model, const cf_plan_ta
   if (!plans->n_nodes_dev || !plans->node_comp_dev || !plans->node_rep_dev || !plans->node_batch_dev ||
       !plans->node_gpus_dev || !plans->n_alt_dev || !plans->alt_w_dev || !plans->alt_node_dev)
     return set_error(CF_EINVAL, "NULL plan array");
-  PlanView pv{plans->P, plans->n_nodes_dev, plans->node_comp_dev, plans->node_rep_dev, plans->node_gpus_dev,
-              plans->n_alt_dev, plans->alt_w_dev, plans->alt_node_dev, plans->node_batch_dev};
-  hipLaunchKernelGGL(k_coarse, dim3((unsigned)((plans->P + kBlock - 1) / kBlock)), dim3(kBlock), 0,
-                     as_stream(stream), m, pv, moments_dev, n_gpus, rd_dev, bottleneck_dev, flags_dev);
+  const int ngroups = (plans->node_rep2_dev != nullptr) + (plans->node_batch2_dev != nullptr) +
+                      (plans->node_gpus2_dev != nullptr) + (plans->node_w_dev != nullptr);
+  if (ngroups != 0 && ngroups != 4) return set_error(CF_EINVAL, "second-configuration arrays: all four or none");
+  PlanView pv{plans->P,          plans->n_nodes_dev,  plans->node_comp_dev,  plans->node_rep_dev,
+              plans->node_gpus_dev, plans->n_alt_dev,   plans->alt_w_dev,      plans->alt_node_dev,
+              plans->node_batch_dev, plans->node_rep2_dev, plans->node_gpus2_dev, plans->node_w_dev,
+              plans->node_batch2_dev};
+  if (ngroups)
+    hipLaunchKernelGGL(k_coarse<true>, dim3((unsigned)((plans->P + kBlockGroups - 1) / kBlockGroups)),
+                       dim3(kBlockGroups), 0, as_stream(stream), m, pv, moments_dev, n_gpus, rd_dev, bottleneck_dev,
+                       flags_dev);
+  else
+    hipLaunchKernelGGL(k_coarse<false>, dim3((unsigned)((plans->P + kBlock - 1) / kBlock)), dim3(kBlock), 0,
+                       as_stream(stream), m, pv, moments_dev, n_gpus, rd_dev, bottleneck_dev, flags_dev);
   return hip_check(hipGetLastError(), "cf_eval_coarse launch");
 }

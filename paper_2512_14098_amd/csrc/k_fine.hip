@@ -116,6 +116,8 @@ struct FineArgs {
   int P;
   const uint8_t *n_nodes, *node_comp, *node_rep, *node_gpus, *n_alt, *alt_w, *alt_node;
   const uint16_t *node_batch;
+  const uint8_t *node_rep2, *node_gpus2, *node_w;  // a node's second configuration (NULL: none)
+  const uint16_t *node_batch2;
   const int32_t *plan_ids;
   int n_plans;
   const double *rates;
@@ -160,6 +162,11 @@ struct WaveShared {
   uint8_t nalt[CF_MAX_TYPES], aw[CF_MAX_TYPES][2];
   uint8_t vbase[CF_MAX_NODES + 1], vrep[CF_MAX_NODES], vminc[CF_MAX_NODES], vcomp[CF_MAX_NODES];
   uint16_t vbatch[CF_MAX_NODES];
+  // a node's executors: vrep in all, the first vrep1 of batch vbatch, the
+  // others of batch vbatch2; vw tenths of its requests to the first (0: one
+  // configuration)
+  uint8_t vrep1[CF_MAX_NODES], vw[CF_MAX_NODES];
+  uint16_t vbatch2[CF_MAX_NODES];
   uint32_t met[CF_MAX_TYPES], cnt[CF_MAX_TYPES];
   ModelLds ml;
 };
@@ -783,7 +790,7 @@ __device__ void arrive(Sim &S, uint32_t r) {
     const int v = sh.route[t][alt][c];
     const int mc = sh.vminc[v];
     const uint64_t key = ((mc < 4 ? k0 : k1) >> (16 * (mc & 3))) & 0xFFFFull;
-    const int x = sh.vbase[v] + (int)((key * sh.vrep[v]) >> 16);
+    const int x = sh.vbase[v] + node_exec((uint32_t)key, sh.vrep1[v], (uint32_t)(sh.vrep[v] - sh.vrep1[v]), sh.vw[v]);
     ex = (ex & ~(0xFFull << (8 * c))) | ((uint64_t)x << (8 * c));
   }
   Rec R;
@@ -1624,11 +1631,22 @@ __device__ bool setup_plan(Sim &S, int p) {
   const int lane = lane_id();
   const int nv = ri(A.n_nodes[p]);
   if (nv < 1 || nv > CF_MAX_NODES) return false;
+  bool groups_ok = true;
   if (lane < CF_MAX_NODES) {
+    const uint32_t rep = lane < nv ? A.node_rep[lane * P + p] : 0;
+    const uint32_t rep2 = (lane < nv && A.node_rep2) ? A.node_rep2[lane * P + p] : 0;
     sh.vcomp[lane] = lane < nv ? A.node_comp[lane * P + p] : 0;
-    sh.vrep[lane] = lane < nv ? A.node_rep[lane * P + p] : 0;
+    sh.vrep[lane] = (uint8_t)(rep + rep2 < 255 ? rep + rep2 : 255);
+    sh.vrep1[lane] = (uint8_t)rep;
     sh.vbatch[lane] = lane < nv ? A.node_batch[lane * P + p] : 0;
+    sh.vbatch2[lane] = rep2 ? A.node_batch2[lane * P + p] : 0;
+    const uint32_t w = rep2 ? A.node_w[lane * P + p] : 0;
+    sh.vw[lane] = (uint8_t)w;
+    if (rep2 && (rep < 1 || w < 1 || w > 9 || sh.vbatch2[lane] < 1 || sh.vbatch2[lane] > CF_MAX_BATCH ||
+                 A.node_gpus2[lane * P + p] < 1))
+      groups_ok = false;
   }
+  if (__ballot(!groups_ok)) return false;
   for (int j = lane; j < CF_MAX_TYPES * 2 * CF_MAX_COMP; j += 64) (&sh.route[0][0][0])[j] = A.alt_node[j * P + p];
   if (lane < CF_MAX_TYPES) sh.nalt[lane] = lane < m.nt ? A.n_alt[lane * P + p] : 0;
   if (lane < 2 * CF_MAX_TYPES) (&sh.aw[0][0])[lane] = A.alt_w[lane * P + p];
@@ -1674,7 +1692,10 @@ __device__ bool setup_plan(Sim &S, int p) {
     for (uint32_t cc = cm; cc;) {
       const int c = __ffs(cc) - 1;
       cc &= cc - 1;
-      if (m.kind[c] == CF_LLM) run_need += sh.vrep[v] * (sh.vbatch[v] < m.cap[c] ? sh.vbatch[v] : m.cap[c]);
+      if (m.kind[c] == CF_LLM) {
+        run_need += sh.vrep1[v] * (sh.vbatch[v] < m.cap[c] ? sh.vbatch[v] : m.cap[c]);
+        run_need += (sh.vrep[v] - sh.vrep1[v]) * (sh.vbatch2[v] < m.cap[c] ? sh.vbatch2[v] : m.cap[c]);
+      }
       if ((m.gate_src_mask >> c) & 1u) ring_need += sh.vrep[v];
       if constexpr (G) {
         if (m.kind[c] == CF_LLM) llm_need += sh.vrep[v];
@@ -1710,7 +1731,8 @@ __device__ bool setup_plan(Sim &S, int p) {
     first += (lane - sh.vbase[v]) * __popc(sh.vcomp[v]);
     sh.ex_node[lane] = (uint8_t)v;
     if (m.tp_any) {
-      const uint32_t g = A.node_gpus[v * P + p];
+      const bool second = lane - sh.vbase[v] >= sh.vrep1[v];
+      const uint32_t g = second ? A.node_gpus2[v * P + p] : A.node_gpus[v * P + p];
       sh.ex_tp[lane] = (uint8_t)(g < 1 ? 0 : (g > 8 ? 7 : g - 1));
     }
     sh.ex_first[lane] = (uint16_t)first;
@@ -1742,7 +1764,9 @@ __device__ bool setup_plan(Sim &S, int p) {
       uint32_t cc = sh.vcomp[v];
       for (int q = 0; q < k; q++) cc &= cc - 1;
       c = __ffs(cc) - 1;
-      beff = sh.vbatch[v] < m.cap[c] ? sh.vbatch[v] : m.cap[c];
+      // the batch of the executor's configuration
+      const int bn = (s - acc) / per < sh.vrep1[v] ? sh.vbatch[v] : sh.vbatch2[v];
+      beff = bn < m.cap[c] ? bn : m.cap[c];
       llm = m.kind[c] == CF_LLM;
       thk = (m.gate_src_mask >> c) & 1u;
     }
@@ -2035,8 +2059,9 @@ __global__ void k_fine_reset3(unsigned int *v) {
 
 // stage instances, LLM stage instances and gate-source stage instances of
 // the largest selected plans (out[0..2]; malformed plans are skipped)
-__global__ void k_max_si(const uint8_t *n_nodes, const uint8_t *node_comp, const uint8_t *node_rep, int P,
-                         const int32_t *ids, int n, uint32_t llm_mask, uint32_t src_mask, unsigned int *out) {
+__global__ void k_max_si(const uint8_t *n_nodes, const uint8_t *node_comp, const uint8_t *node_rep,
+                         const uint8_t *node_rep2, int P, const int32_t *ids, int n, uint32_t llm_mask,
+                         uint32_t src_mask, unsigned int *out) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const int p = ids[i];
@@ -2045,7 +2070,8 @@ __global__ void k_max_si(const uint8_t *n_nodes, const uint8_t *node_comp, const
   if (nv < 1 || nv > CF_MAX_NODES) return;
   unsigned int nsi = 0, nl = 0, nt = 0;
   for (int v = 0; v < nv; v++) {
-    const unsigned int rep = node_rep[(size_t)v * P + p], cm = node_comp[(size_t)v * P + p];
+    const unsigned int rep = node_rep[(size_t)v * P + p] + (node_rep2 ? node_rep2[(size_t)v * P + p] : 0u);
+    const unsigned int cm = node_comp[(size_t)v * P + p];
     nsi += rep * (unsigned int)__popc(cm);
     nl += rep * (unsigned int)__popc(cm & llm_mask);
     nt += rep * (unsigned int)__popc(cm & src_mask);
@@ -2160,6 +2186,15 @@ cf_status eval_fine(const cf_model_desc *model, const cf_plan_table *plans, cons
   a.n_alt = plans->n_alt_dev;
   a.alt_w = plans->alt_w_dev;
   a.alt_node = plans->alt_node_dev;
+  {
+    const int ng = (plans->node_rep2_dev != nullptr) + (plans->node_batch2_dev != nullptr) +
+                   (plans->node_gpus2_dev != nullptr) + (plans->node_w_dev != nullptr);
+    if (ng != 0 && ng != 4) return set_error(CF_EINVAL, "second-configuration arrays: all four or none");
+  }
+  a.node_rep2 = plans->node_rep2_dev;
+  a.node_batch2 = plans->node_batch2_dev;
+  a.node_gpus2 = plans->node_gpus2_dev;
+  a.node_w = plans->node_w_dev;
   a.plan_ids = plan_ids_dev;
   a.n_plans = n_plans;
   a.rates = rates_dev;
@@ -2233,7 +2268,8 @@ cf_status eval_fine(const cf_model_desc *model, const cf_plan_table *plans, cons
     if (a.m.kind[c] == CF_LLM) llm_mask |= 1u << c;
   hipLaunchKernelGGL(k_fine_reset3, dim3(1), dim3(1), 0, s, max_si);
   hipLaunchKernelGGL(k_max_si, dim3((unsigned)((n_plans + 255) / 256)), dim3(256), 0, s, a.n_nodes, a.node_comp,
-                     a.node_rep, a.P, plan_ids_dev, n_plans, llm_mask, (uint32_t)a.m.gate_src_mask, max_si);
+                     a.node_rep, a.node_rep2, a.P, plan_ids_dev, n_plans, llm_mask, (uint32_t)a.m.gate_src_mask,
+                     max_si);
   unsigned int caps[3] = {0, 0, 0};
   st = hip_check(hipMemcpyAsync(caps, max_si, sizeof caps, hipMemcpyDeviceToHost, s), "copy stage count");
   if (st != CF_OK) return st;

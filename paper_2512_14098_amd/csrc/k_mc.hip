@@ -34,6 +34,8 @@ struct McView {
   int P;
   const uint8_t *n_nodes, *node_comp, *node_rep, *node_gpus, *n_alt, *alt_w, *alt_node;
   const uint16_t *node_batch;
+  const uint8_t *node_rep2, *node_gpus2, *node_w;  // a node's second configuration (NULL: none)
+  const uint16_t *node_batch2;
   const int32_t *ids;
   const double *rd;
   const uint64_t *moments;
@@ -136,6 +138,13 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
   __shared__ double tps_s[CF_MAX_COMP][8];         // iteration-time multipliers by GPUs per executor
   __shared__ uint16_t vbatch[CF_MAX_NODES];
   __shared__ uint16_t beff[CF_MAX_NODES][CF_MAX_COMP];
+  // a node's second configuration: executors vrep - vrep1 of batch vbatch2 and GPUs index vtp2,
+  // tenths vw of its requests to the first (0: one configuration), its demand and effective batches
+  __shared__ uint8_t vrep1[CF_MAX_NODES], vw[CF_MAX_NODES], vtp2[CF_MAX_NODES];
+  __shared__ uint16_t vbatch2[CF_MAX_NODES];
+  __shared__ uint16_t beff2[CF_MAX_NODES][CF_MAX_COMP];
+  __shared__ double u2_s[CF_MAX_NODES];
+  __shared__ int groups_bad;
   __shared__ uint8_t route[CF_MAX_TYPES][2][CF_MAX_COMP];
   __shared__ uint8_t nalt[CF_MAX_TYPES], aw[CF_MAX_TYPES][2];
   __shared__ double ex_s[CF_MAX_TYPES][CF_MAX_COMP], en_s[CF_MAX_TYPES][CF_MAX_COMP];
@@ -192,12 +201,24 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
   }
   const bool in_range = p >= 0 && p < V.P;
   const int nv = in_range ? V.n_nodes[p] : 0;
+  if (lane == 0) groups_bad = 0;
+  __syncthreads();
   if (in_range && lane < CF_MAX_NODES) {
+    const uint32_t rep = lane < nv ? V.node_rep[lane * P + p] : 0;
+    const uint32_t rep2 = (lane < nv && V.node_rep2) ? V.node_rep2[lane * P + p] : 0;
     vcomp[lane] = lane < nv ? V.node_comp[lane * P + p] : 0;
-    vrep[lane] = lane < nv ? V.node_rep[lane * P + p] : 0;
+    vrep[lane] = (uint8_t)(rep + rep2 < 255 ? rep + rep2 : 255);
+    vrep1[lane] = (uint8_t)rep;
     vbatch[lane] = lane < nv ? V.node_batch[lane * P + p] : 0;
     const uint32_t g = lane < nv ? V.node_gpus[lane * P + p] : 1u;
     vtp[lane] = (uint8_t)(g < 1 ? 0 : (g > 8 ? 7 : g - 1));
+    const uint32_t w = rep2 ? V.node_w[lane * P + p] : 0u;
+    const uint32_t b2 = rep2 ? V.node_batch2[lane * P + p] : 0u;
+    const uint32_t g2 = rep2 ? V.node_gpus2[lane * P + p] : 1u;
+    vw[lane] = (uint8_t)w;
+    vbatch2[lane] = (uint16_t)b2;
+    vtp2[lane] = (uint8_t)(g2 < 1 ? 0 : (g2 > 8 ? 7 : g2 - 1));
+    if (rep2 && (rep < 1 || w < 1 || w > 9 || b2 < 1 || b2 > CF_MAX_BATCH || g2 < 1)) atomicOr(&groups_bad, 1);
   }
   if (in_range) {
     for (int j = lane; j < CF_MAX_TYPES * 2 * CF_MAX_COMP; j += 64) (&route[0][0][0])[j] = V.alt_node[j * P + p];
@@ -207,7 +228,7 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
   __syncthreads();
   // validity (phase 1's), capacities, effective batches: one lane, phase 1's order
   if (lane == 0 && in_range) {
-    bool ok = nv >= 1 && nv <= CF_MAX_NODES;
+    bool ok = nv >= 1 && nv <= CF_MAX_NODES && !groups_bad;
     int execs = 0;
     for (int v = 0; v < nv && ok; v++) {
       const int cm = vcomp[v], rep = vrep[v], b = vbatch[v];
@@ -230,7 +251,7 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
       }
     }
     if (ok) {
-      for (int v = 0; v < CF_MAX_NODES; v++) u_s[v] = 0.0;
+      for (int v = 0; v < CF_MAX_NODES; v++) u_s[v] = u2_s[v] = 0.0;
       const double wsum = (double)m.wsum;
       for (int t = 0; t < m.nt; t++) {
         const double pi = (double)m.weight[t] / wsum;
@@ -244,24 +265,33 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
           for (int c = 0; c < m.nc; c++) {
             if (!((m.path[t] >> c) & 1u)) continue;
             const int v = route[t][a][c];
-            const int bn = vbatch[v];
-            const double B = (double)(bn < m.cap[c] ? bn : m.cap[c]);
-            double w = ((m.k0[c] / B) + m.k1[c] * ex_s[t][c]) + m.k2[c];
-            if (m.kind[c] == CF_LLM) w = w + (en_s[t][c] - 1.0) * ((m.d0[c] / B) + m.d1[c]);
-            if (m.tp_any) w = tps_s[c][vtp[v]] * w;
-            u_s[v] = u_s[v] + pq * w;
+            // seconds of executor time per request on each configuration of the node
+            for (int k = 0; k < (vw[v] ? 2 : 1); k++) {
+              const int bn = k ? vbatch2[v] : vbatch[v];
+              const double B = (double)(bn < m.cap[c] ? bn : m.cap[c]);
+              double w = ((m.k0[c] / B) + m.k1[c] * ex_s[t][c]) + m.k2[c];
+              if (m.kind[c] == CF_LLM) w = w + (en_s[t][c] - 1.0) * ((m.d0[c] / B) + m.d1[c]);
+              if (m.tp_any) w = tps_s[c][k ? vtp2[v] : vtp[v]] * w;
+              if (!vw[v]) u_s[v] = u_s[v] + pq * w;
+              else if (k == 0) u_s[v] = u_s[v] + (pq * ((double)vw[v] / 10.0)) * w;
+              else u2_s[v] = u2_s[v] + (pq * ((double)(10u - vw[v]) / 10.0)) * w;
+            }
           }
         }
       }
       const double R_d = V.rd[p];
       for (int v = 0; v < nv; v++) {
-        const double Rv = u_s[v] > 0.0 ? (double)vrep[v] / u_s[v] : __builtin_inf();
-        const double q = R_d / Rv;
-        for (int c = 0; c < m.nc; c++) {
-          const int bn = vbatch[v];
-          const int B = bn < m.cap[c] ? bn : m.cap[c];
-          const double bb = ceil((double)B * q);
-          beff[v][c] = (uint16_t)(bb < 1.0 ? 1 : (bb > (double)B ? B : (int)bb));
+        // effective batch per configuration: its share of the bottleneck's load
+        for (int k = 0; k < (vw[v] ? 2 : 1); k++) {
+          const double u = k ? u2_s[v] : u_s[v];
+          const double Rv = u > 0.0 ? (double)(k ? vrep[v] - vrep1[v] : vrep1[v]) / u : __builtin_inf();
+          const double q = R_d / Rv;
+          for (int c = 0; c < m.nc; c++) {
+            const int bn = k ? vbatch2[v] : vbatch[v];
+            const int B = bn < m.cap[c] ? bn : m.cap[c];
+            const double bb = ceil((double)B * q);
+            (k ? beff2 : beff)[v][c] = (uint16_t)(bb < 1.0 ? 1 : (bb > (double)B ? B : (int)bb));
+          }
         }
       }
       valid_s = 1;
@@ -309,7 +339,9 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
         const int v = route[t][alt][c];
         const int mc = vminc[v];
         const uint64_t key = ((mc < 4 ? k0 : k1) >> (16 * (mc & 3))) & 0xFFFFull;
-        ex[c] = vbase[v] + (int)((key * vrep[v]) >> 16);
+        const int j = node_exec((uint32_t)key, vrep1[v], (uint32_t)(vrep[v] - vrep1[v]), vw[v]);
+        const bool second = j >= vrep1[v];  // an executor of the node's second configuration
+        ex[c] = vbase[v] + j;
         // the last input to arrive
         double start = 0.0;
 #pragma unroll
@@ -320,8 +352,8 @@ __global__ void __launch_bounds__(64) k_mc(KModel m, McView V) {
           const double ready = gate_edge ? first[pc] + hop : fin[pc] + hop;
           start = ready > start ? ready : start;
         }
-        const int b = beff[v][c];
-        const double tps = tps_s[c][vtp[v]];
+        const int b = second ? beff2[v][c] : beff[v][c];
+        const double tps = tps_s[c][second ? vtp2[v] : vtp[v]];
         uint32_t x = 0;
         for (uint32_t sel = m.xsel[c]; sel; sel &= sel - 1) x += mc_attr(q, __ffs(sel) - 1);
         if (m.kind[c] != CF_LLM) {
@@ -559,6 +591,15 @@ cf_status eval_mc(const cf_model_desc *model, const cf_plan_table *plans, const 
   V.alt_w = plans->alt_w_dev;
   V.alt_node = plans->alt_node_dev;
   V.node_batch = plans->node_batch_dev;
+  {
+    const int ng = (plans->node_rep2_dev != nullptr) + (plans->node_batch2_dev != nullptr) +
+                   (plans->node_gpus2_dev != nullptr) + (plans->node_w_dev != nullptr);
+    if (ng != 0 && ng != 4) return set_error(CF_EINVAL, "second-configuration arrays: all four or none");
+  }
+  V.node_rep2 = plans->node_rep2_dev;
+  V.node_batch2 = plans->node_batch2_dev;
+  V.node_gpus2 = plans->node_gpus2_dev;
+  V.node_w = plans->node_w_dev;
   V.ids = plan_ids_dev;
   V.rd = rd_dev;
   V.moments = moments_dev;
