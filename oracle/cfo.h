@@ -214,8 +214,10 @@ int cfo_pareto(const double *g, int32_t n, int32_t T, uint8_t *keep);
 /* Plan enumeration (Sec. 4.2, Alg. 1; Eq. 1).  Options: GPU budget N,
  * subplans per logical plan (1 or 2), node sharing between the two
  * subplans, colocatable edges (colocatable[p] bit c: edge p -> c may be
- * merged), and per component its batch knobs and GPUs-per-executor options
- * (a node takes those of its lowest component). */
+ * merged), per component its batch knobs and GPUs-per-executor options
+ * (a node takes those of its lowest component), and het: a node may also
+ * hold executors of two of its configurations (Eq. 1's n_{v,k} for two k),
+ * with the share of its requests for the first in tenths. */
 typedef struct {
   int32_t n_gpus, k_s, share;
   uint32_t colocatable[CFO_MAXC];
@@ -223,6 +225,7 @@ typedef struct {
   uint16_t batch[CFO_MAXC][8];
   int32_t n_gpu_opt[CFO_MAXC];
   uint8_t gpu_opt[CFO_MAXC][4];
+  int32_t het;
 } cfo_enum_opts;
 
 /* a logical plan: nodes (component masks) and per type one or two
@@ -243,7 +246,8 @@ uint64_t cfo_enum_count(const cfo_model *m, const cfo_enum_opts *o, const cfo_lo
 int cfo_enum_plans(const cfo_model *m, const cfo_enum_opts *o, const cfo_logical *L, int32_t n_logical,
                    uint64_t first, int32_t count, uint8_t *n_nodes, uint8_t *node_comp, uint8_t *node_rep,
                    uint16_t *node_batch, uint8_t *node_gpus, uint8_t *n_alt, uint8_t *alt_w,
-                   uint8_t *alt_node);
+                   uint8_t *alt_node, uint8_t *node_rep2, uint16_t *node_batch2, uint8_t *node_gpus2,
+                   uint8_t *node_w);
 
 int cfo_select_topk(const double *rd, const uint8_t *flags, int32_t P, int32_t k,
                     int32_t *ids, int32_t *n_selected);

@@ -271,17 +271,30 @@ typedef uint64_t count_table[CFO_MAXV + 1][CFO_MAXN + 1];
 static uint64_t sat_add(uint64_t a, uint64_t b) { return a > UINT64_MAX - b ? UINT64_MAX : a + b; }
 static uint64_t sat_mul(uint64_t a, uint64_t b) { return (b != 0 && a > UINT64_MAX / b) ? UINT64_MAX : a * b; }
 
+/* A node's executor assignments, in this order: one configuration k with n >= 1
+ * executors (k, then n ascending); then, with het, two configurations k1 < k2 with
+ * n1, n2 >= 1 executors and w = 1..9 tenths of the node's requests for k1 (k1, k2,
+ * n1, n2, w ascending). */
 static void fill_counts(const cfo_logical *L, const cfo_enum_opts *o, count_table cnt) {
   const int N = o->n_gpus, V = L->n_nodes;
   for (int b = 0; b <= N; b++) cnt[V][b] = 1;
   for (int v = V - 1; v >= 0; v--) {
     const int c0 = lowest(L->node_comp[v]);
+    const int K = n_configs(o, c0);
     for (int b = 0; b <= N; b++) {
       uint64_t total = 0;
-      for (int k = 0; k < n_configs(o, c0); k++) {
+      for (int k = 0; k < K; k++) {
         const int g = config_gpus(o, c0, k);
         for (int n = 1; g * n <= b; n++) total = sat_add(total, cnt[v + 1][b - g * n]);
       }
+      if (o->het)
+        for (int k1 = 0; k1 < K; k1++)
+          for (int k2 = k1 + 1; k2 < K; k2++) {
+            const int g1 = config_gpus(o, c0, k1), g2 = config_gpus(o, c0, k2);
+            for (int n1 = 1; g1 * n1 + g2 <= b; n1++)
+              for (int n2 = 1; g1 * n1 + g2 * n2 <= b; n2++)
+                total = sat_add(total, sat_mul(9, cnt[v + 1][b - g1 * n1 - g2 * n2]));
+          }
       cnt[v][b] = total;
     }
   }
@@ -313,7 +326,10 @@ typedef struct {
   int32_t P;                /* output columns */
   uint8_t *n_nodes, *node_comp, *node_rep, *node_gpus, *n_alt, *alt_w, *alt_node;
   uint16_t *node_batch;
+  uint8_t *node_rep2, *node_gpus2, *node_w;
+  uint16_t *node_batch2;
   int kk[CFO_MAXV], nn[CFO_MAXV];
+  int kk2[CFO_MAXV], nn2[CFO_MAXV], ww[CFO_MAXV]; /* second configuration (nn2 = 0: none) */
   uint64_t R;
   uint64_t (*cnt)[CFO_MAXN + 1];
 } walk_t;
@@ -334,11 +350,19 @@ static void emit_routes(walk_t *w) {
         w->node_rep[v * P + p] = (uint8_t)w->nn[v];
         w->node_gpus[v * P + p] = (uint8_t)config_gpus(w->o, c0, w->kk[v]);
         w->node_batch[v * P + p] = (uint16_t)config_batch(w->o, c0, w->kk[v]);
+        w->node_rep2[v * P + p] = (uint8_t)w->nn2[v];
+        w->node_gpus2[v * P + p] = (uint8_t)(w->nn2[v] ? config_gpus(w->o, c0, w->kk2[v]) : 0);
+        w->node_batch2[v * P + p] = (uint16_t)(w->nn2[v] ? config_batch(w->o, c0, w->kk2[v]) : 0);
+        w->node_w[v * P + p] = (uint8_t)(w->nn2[v] ? w->ww[v] : 10);
       } else {
         w->node_comp[v * P + p] = 0;
         w->node_rep[v * P + p] = 0;
         w->node_gpus[v * P + p] = 0;
         w->node_batch[v * P + p] = 0;
+        w->node_rep2[v * P + p] = 0;
+        w->node_gpus2[v * P + p] = 0;
+        w->node_batch2[v * P + p] = 0;
+        w->node_w[v * P + p] = 10;
       }
     }
     /* routing digits: the lowest type is the most significant */
@@ -387,15 +411,40 @@ static void walk_nodes(walk_t *w, int v, int b) {
       }
       w->kk[v] = k;
       w->nn[v] = n;
+      w->nn2[v] = 0;
       walk_nodes(w, v + 1, b - g * n);
     }
   }
+  if (!w->o->het) return;
+  const int K = n_configs(w->o, c0);
+  for (int k1 = 0; k1 < K; k1++)
+    for (int k2 = k1 + 1; k2 < K; k2++) {
+      const int g1 = config_gpus(w->o, c0, k1), g2 = config_gpus(w->o, c0, k2);
+      for (int n1 = 1; g1 * n1 + g2 <= b; n1++)
+        for (int n2 = 1; g1 * n1 + g2 * n2 <= b; n2++)
+          for (int ws = 1; ws <= 9; ws++) {
+            if (w->idx >= w->end) return;
+            const int rest = b - g1 * n1 - g2 * n2;
+            const uint64_t sub = sat_mul(w->cnt[v + 1][rest], w->R);
+            if (w->idx + sub <= w->first) {
+              w->idx += sub;
+              continue;
+            }
+            w->kk[v] = k1;
+            w->nn[v] = n1;
+            w->kk2[v] = k2;
+            w->nn2[v] = n2;
+            w->ww[v] = ws;
+            walk_nodes(w, v + 1, rest);
+          }
+    }
 }
 
 int cfo_enum_plans(const cfo_model *m, const cfo_enum_opts *o, const cfo_logical *L, int32_t n_logical,
                    uint64_t first, int32_t count, uint8_t *n_nodes, uint8_t *node_comp, uint8_t *node_rep,
                    uint16_t *node_batch, uint8_t *node_gpus, uint8_t *n_alt, uint8_t *alt_w,
-                   uint8_t *alt_node) {
+                   uint8_t *alt_node, uint8_t *node_rep2, uint16_t *node_batch2, uint8_t *node_gpus2,
+                   uint8_t *node_w) {
   static count_table table;
   uint64_t base = 0;
   const uint64_t end = first + (uint64_t)count;
@@ -422,6 +471,10 @@ int cfo_enum_plans(const cfo_model *m, const cfo_enum_opts *o, const cfo_logical
       w.n_alt = n_alt;
       w.alt_w = alt_w;
       w.alt_node = alt_node;
+      w.node_rep2 = node_rep2;
+      w.node_batch2 = node_batch2;
+      w.node_gpus2 = node_gpus2;
+      w.node_w = node_w;
       w.R = routings(&L[i], m->n_types);
       w.cnt = table;
       walk_nodes(&w, 0, o->n_gpus);

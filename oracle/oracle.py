@@ -67,7 +67,7 @@ class EnumOpts(C.Structure):
     _fields_ = [("n_gpus", C.c_int32), ("k_s", C.c_int32), ("share", C.c_int32),
                 ("colocatable", C.c_uint32 * 8), ("n_batch", C.c_int32 * 8),
                 ("batch", (C.c_uint16 * 8) * 8), ("n_gpu_opt", C.c_int32 * 8),
-                ("gpu_opt", (C.c_uint8 * 4) * 8)]
+                ("gpu_opt", (C.c_uint8 * 4) * 8), ("het", C.c_int32)]
 
 
 class Logical(C.Structure):
@@ -408,6 +408,7 @@ def enum_opts(mcfg, spec, n_gpus):
     o = EnumOpts()
     names = {c["name"]: i for i, c in enumerate(mcfg["components"])}
     o.n_gpus, o.k_s, o.share = int(n_gpus), int(spec.get("k_s", 2)), int(bool(spec.get("share", True)))
+    o.het = int(bool(spec.get("het", False)))
     edges = spec.get("colocatable")
     if edges is None:
         edges = [e for t in mcfg["types"] for e in t.get("edges", [])]

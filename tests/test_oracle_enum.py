@@ -205,3 +205,83 @@ def test_omni_graph_invariants():
         for t in range(4):
             assert np.all(w[t, 0] + w[t, 1] == 10)
         assert len(_canon_rows(tab)) == 3000
+
+
+def _brute_plans_het(L, T, N, knobs, gopts):
+    """As _brute_plans with nodes of two configurations allowed (Eq. 1's n_{v,k} for two k):
+    after every one-configuration assignment of a node, its pairs of configurations k1 < k2
+    with n1, n2 >= 1 executors and w = 1..9 tenths for the first, in that order."""
+    V = L.n_nodes
+    per_node = []
+    for v in range(V):
+        mask = L.node_comp[v]
+        c0 = (mask & -mask).bit_length() - 1
+        per_node.append([(g, b) for g in gopts[c0] for b in knobs[c0]])
+
+    def node_options(v, budget):
+        cf = per_node[v]
+        for (g, b) in cf:
+            for n in range(1, budget // g + 1):
+                yield (n, b, g), g * n
+        for i1, i2 in itertools.combinations(range(len(cf)), 2):
+            (g1, b1), (g2, b2) = cf[i1], cf[i2]
+            for n1 in range(1, budget + 1):
+                for n2 in range(1, budget + 1):
+                    if g1 * n1 + g2 * n2 > budget:
+                        continue
+                    for w in range(1, 10):
+                        yield (n1, b1, g1, n2, b2, g2, w), g1 * n1 + g2 * n2
+
+    def assignments(v, budget):
+        if v == V:
+            yield []
+            return
+        for opt, cost in node_options(v, budget):
+            for rest in assignments(v + 1, budget - cost):
+                yield [opt] + rest
+
+    two = [t for t in range(T) if L.n_alt[t] == 2]
+    out = []
+    for asg in assignments(0, N):
+        for ws in itertools.product(range(1, 10), repeat=len(two)):
+            wt = dict(zip(two, ws))
+            nodes = [(L.node_comp[v],) + asg[v] if len(asg[v]) == 7 else
+                     (L.node_comp[v], asg[v][0], asg[v][1], asg[v][2]) for v in range(V)]
+            routes = []
+            for t in range(T):
+                alts = []
+                for a in range(L.n_alt[t]):
+                    w = 10 if L.n_alt[t] == 1 else (wt[t] if a == 0 else 10 - wt[t])
+                    alts.append((w, {c: L.alt_node[t][a][c] for c in range(8) if L.alt_node[t][a][c] != 255}))
+                routes.append(alts)
+            out.append(dict(nodes=nodes, routes=routes))
+    return out
+
+
+@pytest.mark.parametrize("N,gpus", [(3, {"E": [1, 2], "L": [1]}), (4, {"E": [1], "L": [1]})])
+def test_two_configuration_nodes_in_order_against_itertools(N, gpus):
+    cfg = load_config("c1")
+    spec = {"k_s": 2, "share": True, "batch": {"E": [16, 64], "L": [16, 64, 256]}, "gpus": gpus, "het": True}
+    m, o = O.make_model(cfg["model"]), O.enum_opts(cfg["model"], spec, N)
+    Ls = O.enum_logical(m, o)
+    knobs = {0: [16, 64], 1: [16, 64, 256]}
+    gopts = {0: gpus["E"], 1: gpus["L"]}
+    allp = []
+    for L in Ls:
+        plans = _brute_plans_het(L, 2, N, knobs, gopts)
+        assert O.enum_count(m, o, L) == len(plans)
+        allp += plans
+    total = len(allp)
+    assert total > 2000 and any(len(nd) == 8 for p in allp for nd in p["nodes"])
+    tab = O.enum_plans(m, o, Ls, 0, total)
+    _table_eq(tab, allp)
+    for first, count in ((1, 7), (total // 3, 500), (total - 3, 3)):
+        _table_eq(O.enum_plans(m, o, Ls, first, count), allp[first:first + count])
+    # every plan is valid for phase 1 and within the budget of Eq. (1) over both configurations
+    rd, bn, fl = O.eval_coarse(m, tab, O.trace_gen(m, [0], 2000)["moments"][0], N)
+    assert np.all((fl & 6) == 0)
+    # without the option the same space holds only the one-configuration plans, in order
+    o1 = O.enum_opts(cfg["model"], dict(spec, het=False), N)
+    one = [p for p in allp if all(len(nd) == 4 for nd in p["nodes"])]
+    assert sum(O.enum_count(m, o1, L) for L in Ls) == len(one)
+    _table_eq(O.enum_plans(m, o1, Ls, 0, len(one)), one)
