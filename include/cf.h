@@ -377,6 +377,10 @@ typedef struct cf_enum_opts {
   uint16_t batch[CF_MAX_COMP][8];
   int32_t n_gpu_opt[CF_MAX_COMP];
   uint8_t gpu_opt[CF_MAX_COMP][4];
+  /* 1: a node may also hold executors of two of its configurations (Eq. 1's
+   * n_{v,k} for two k), with 1..9 tenths of its requests for the first (the
+   * plan table's second-configuration arrays); 0: one configuration per node */
+  int32_t het;
 } cf_enum_opts;
 
 /* A logical plan (Alg. 1): nodes as component masks, and per type one or
@@ -411,10 +415,14 @@ cf_status cf_enum_logical(const cf_model_desc *model, const cf_enum_opts *opts, 
 /* Physical plans per logical plan (Eq. 1): node v takes a configuration k
  * (GPU option major, batch knob minor) and n_v >= 1 executors with
  * sum_v gpus_v n_v <= N; each type with two alternatives takes a weight w in
- * 1..9 tenths for its first (10 - w for the second).  The plans of logical
- * plan l are numbered offsets[l] .. offsets[l+1]-1: executor assignments
- * lexicographically in ((k_0, n_0), (k_1, n_1), ...), routing weights
- * lexicographically inside each (lowest type most significant).
+ * 1..9 tenths for its first (10 - w for the second).  With opts->het a node
+ * may instead take two configurations k1 < k2 with n1, n2 >= 1 executors and
+ * 1..9 tenths w of its requests for k1; a node's assignments are ordered
+ * (k, n) first, then (k1, k2, n1, n2, w), each lexicographically.  The plans
+ * of logical plan l are numbered offsets[l] .. offsets[l+1]-1: executor
+ * assignments lexicographically over the nodes in that per-node order,
+ * routing weights lexicographically inside each (lowest type most
+ * significant).
  * logical_dev: n_logical plans in device memory; writes offsets_dev[n_logical
  * + 1] (device) and the total to *total_host (synchronises the stream).
  * Errors: CF_EINVAL, CF_ECAPACITY (the total does not fit 64 bits). */
@@ -425,8 +433,11 @@ cf_status cf_enum_count(const cf_model_desc *model, const cf_enum_opts *opts, co
  * them; offsets_dev and total from it, with the same options and logical
  * plans) into columns 0..count-1 of the device plan table *out (out->P >=
  * count; its arrays are written, unused node slots 0, unused route entries
- * 255).  One thread per plan, asynchronous on stream.
- * Errors: CF_EINVAL (options, sizes, first + count > total). */
+ * 255; the second-configuration arrays, required with opts->het, are written
+ * when present: 0 executors and 10 tenths for a node of one configuration).
+ * One thread per plan, asynchronous on stream.
+ * Errors: CF_EINVAL (options, sizes, first + count > total, het without the
+ * second-configuration arrays). */
 cf_status cf_enum_plans(const cf_model_desc *model, const cf_enum_opts *opts, const cf_logical *logical_dev,
                         int32_t n_logical, const uint64_t *offsets_dev, uint64_t total, uint64_t first,
                         int32_t count, const cf_plan_table *out, void *stream);
@@ -445,7 +456,9 @@ cf_status cf_goodput_reduce(const cf_fine_out *fine, int32_t n_plans, int32_t K,
                             const double *rates_dev, uint32_t theta_num, uint32_t theta_den, int32_t n_req,
                             int32_t *kstar_dev, double *goodput_t_dev, double *goodput_dev, void *stream);
 
-/* Enumeration fused with phase 1: for physical plans first .. first+count-1
+/* Enumeration fused with phase 1 (one configuration per node: opts->het
+ * returns CF_EUNSUPPORTED; cf_enum_plans then cf_eval_coarse screen such
+ * plans): for physical plans first .. first+count-1
  * (numbered as cf_enum_plans numbers them), exactly what cf_eval_coarse
  * writes for those plans' table columns -- rd_dev[count], bottleneck_dev
  * [count], flags_dev[count] (device) -- without writing the plan table.

@@ -69,7 +69,7 @@ class cf_enum_opts(C.Structure):
     _fields_ = [("n_gpus", C.c_int32), ("k_s", C.c_int32), ("share", C.c_int32),
                 ("colocatable", C.c_uint32 * MAX_COMP), ("n_batch", C.c_int32 * MAX_COMP),
                 ("batch", (C.c_uint16 * 8) * MAX_COMP), ("n_gpu_opt", C.c_int32 * MAX_COMP),
-                ("gpu_opt", (C.c_uint8 * 4) * MAX_COMP)]
+                ("gpu_opt", (C.c_uint8 * 4) * MAX_COMP), ("het", C.c_int32)]
 
 
 LOGICAL_BYTES = 1 + 16 + 8 + 8 * 2 * 8  # sizeof(cf_logical)
@@ -302,15 +302,17 @@ class DevicePlans:
 
     SHAPES = {"n_nodes": (None, torch.uint8), "node_comp": (16, torch.uint8), "node_rep": (16, torch.uint8),
               "node_batch": (16, torch.int16), "node_gpus": (16, torch.uint8), "n_alt": (8, torch.uint8),
-              "alt_w": (16, torch.uint8), "alt_node": (128, torch.uint8)}
+              "alt_w": (16, torch.uint8), "alt_node": (128, torch.uint8), "node_rep2": (16, torch.uint8),
+              "node_batch2": (16, torch.int16), "node_gpus2": (16, torch.uint8), "node_w": (16, torch.uint8)}
 
     @classmethod
-    def empty(cls, P, device="cuda"):
-        """An unfilled device plan table of P columns (written by cf_enum_plans)."""
+    def empty(cls, P, device="cuda", groups=False):
+        """An unfilled device plan table of P columns (written by cf_enum_plans); groups: with
+        the second-configuration arrays (needed for plans of an enumeration with het)."""
         self = cls.__new__(cls)
         self.P, self.t, self.c = int(P), {}, cf_plan_table()
         self.c.P = self.P
-        for f in cls.FIELDS:
+        for f in cls.FIELDS + (cls.GROUP_FIELDS if groups else ()):
             rows, dt = cls.SHAPES[f]
             shape = (self.P,) if rows is None else (rows, self.P)
             self.t[f] = torch.empty(shape, dtype=dt, device=device)
@@ -321,9 +323,9 @@ class DevicePlans:
         """The table as an inputs.PlanTable (host copy)."""
         from .inputs.plans import PlanTable
         tab = PlanTable(self.P)
-        for f in self.FIELDS:
+        for f in self.FIELDS + tuple(g for g in self.GROUP_FIELDS if g in self.t):
             a = self.t[f].cpu().numpy()
-            setattr(tab, f, a.view(np.uint16) if f == "node_batch" else a)
+            setattr(tab, f, a.view(np.uint16) if f in ("node_batch", "node_batch2") else a)
         return tab
 
 
@@ -540,6 +542,7 @@ def enum_opts(mcfg, spec, n_gpus):
     o.n_gpus = int(n_gpus)
     o.k_s = int(spec.get("k_s", 2))
     o.share = 1 if spec.get("share", True) else 0
+    o.het = 1 if spec.get("het", False) else 0
     edges = spec.get("colocatable")
     if edges is None:
         edges = [e for ty in mcfg["types"] for e in ty.get("edges", [])]
@@ -579,7 +582,7 @@ def cf_enum_count(desc, opts, logical_dev):
 def cf_enum_plans(desc, opts, logical_dev, offsets, total, first, count, out=None):
     """Physical plans first..first+count-1 into a device plan table (new, or out)."""
     if out is None:
-        out = DevicePlans.empty(count, logical_dev.device)
+        out = DevicePlans.empty(count, logical_dev.device, groups=bool(opts.het))
     _check(_lib.cf_enum_plans(C.byref(desc), C.byref(opts), _p(logical_dev.contiguous()),
                               int(logical_dev.shape[0]), _p(offsets), C.c_uint64(int(total)),
                               C.c_uint64(int(first)), int(count), C.byref(out.c), _stream()), "cf_enum_plans")

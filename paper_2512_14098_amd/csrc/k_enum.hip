@@ -39,6 +39,7 @@ cf_status check_opts(const cf_model_desc *d, const cf_enum_opts *o) {
     return set_error(CF_EINVAL, "model sizes");
   if (o->n_gpus < 1 || o->n_gpus > kEnumMaxN) return set_error(CF_EINVAL, "n_gpus must be in 1..%d", kEnumMaxN);
   if (o->k_s < 1 || o->k_s > 2) return set_error(CF_EINVAL, "k_s must be 1 or 2");
+  if (o->het != 0 && o->het != 1) return set_error(CF_EINVAL, "het must be 0 or 1");
   for (int c = 0; c < d->n_comp; c++) {
     if (o->n_batch[c] < 1 || o->n_batch[c] > 8) return set_error(CF_EINVAL, "n_batch[%d]", c);
     for (int k = 0; k < o->n_batch[c]; k++)
@@ -134,6 +135,17 @@ __global__ void __launch_bounds__(128) k_enum_table(cf_enum_opts o, EnumView V) 
         for (int n = 1; g * n <= b; n++) per_cfg = sat_add(per_cfg, cnt[v + 1][b - g * n]);
         for (int bi = 0; bi < so.n_batch[c0]; bi++) tot = sat_add(tot, per_cfg);
       }
+      if (o.het) {
+        // two configurations k1 < k2 (GPU option major, batch minor), n1, n2 >= 1, 9 weights
+        const int nb = so.n_batch[c0], K = so.n_gpu[c0] * nb;
+        for (int k1 = 0; k1 < K; k1++)
+          for (int k2 = k1 + 1; k2 < K; k2++) {
+            const int g1 = so.gpu[c0][k1 / nb], g2 = so.gpu[c0][k2 / nb];
+            for (int n1 = 1; g1 * n1 + g2 <= b; n1++)
+              for (int n2 = 1; g1 * n1 + g2 * n2 <= b; n2++)
+                tot = sat_add(tot, sat_mul(9, cnt[v + 1][b - g1 * n1 - g2 * n2]));
+          }
+      }
       cnt[v][b] = tot;
     }
     __syncthreads();
@@ -179,6 +191,8 @@ struct PlanOut {
   int P;
   uint8_t *n_nodes, *node_comp, *node_rep, *node_gpus, *n_alt, *alt_w, *alt_node;
   uint16_t *node_batch;
+  uint8_t *node_rep2, *node_gpus2, *node_w;  // second configurations (NULL: not written)
+  uint16_t *node_batch2;
 };
 
 // The position of plan idx: its logical plan, routing digits and the cursor
@@ -223,12 +237,16 @@ __device__ Cursor locate(const EnumView &V, const uint64_t *offsets, uint64_t id
 struct NodeCfg {
   uint8_t comp, rep, gpus;
   uint16_t batch;
+  uint8_t rep2, gpus2, w;  // a second configuration (rep2 = 0: none, w = 10)
+  uint16_t batch2;
 };
 
 // Node v of the plan at cursor c: the candidates (k, n) in order own
-// cnt[v+1][b - gpus_k n] consecutive ranks each.
-__device__ NodeCfg place(const EnumView &V, const OptsLds &so, Cursor &c, int v) {
-  NodeCfg r = {0, 0, 0, 0};
+// cnt[v+1][b - gpus_k n] consecutive ranks each; with het, then the
+// candidates (k1, k2, n1, n2, w) own cnt[v+1][b - gpus_k1 n1 - gpus_k2 n2]
+// each.
+__device__ NodeCfg place(const EnumView &V, const OptsLds &so, Cursor &c, int v, bool het) {
+  NodeCfg r = {0, 0, 0, 0, 0, 0, 10, 0};
   if (v >= c.nv) return r;
   const cf_logical &L = V.logical[c.l];
   const uint64_t *tab = V.tab + (size_t)c.l * kTabSize + (size_t)(v + 1) * kTabStride;
@@ -250,6 +268,32 @@ __device__ NodeCfg place(const EnumView &V, const OptsLds &so, Cursor &c, int v)
         c.q -= k;
       }
     }
+  }
+  if (het) {
+    const int K = so.n_gpu[c0] * nb;
+    for (int k1 = 0; k1 < K; k1++)
+      for (int k2 = k1 + 1; k2 < K; k2++) {
+        const int g1 = so.gpu[c0][k1 / nb], g2 = so.gpu[c0][k2 / nb];
+        for (int n1 = 1; g1 * n1 + g2 <= c.b; n1++)
+          for (int n2 = 1; g1 * n1 + g2 * n2 <= c.b; n2++) {
+            const uint64_t k = tab[c.b - g1 * n1 - g2 * n2];
+            const uint64_t k9 = sat_mul(k, 9);  // the nine weights, k ranks each
+            if (c.q < k9) {
+              const uint64_t wi = c.q / k;
+              c.q -= wi * k;
+              r.rep = (uint8_t)n1;
+              r.gpus = (uint8_t)g1;
+              r.batch = so.batch[c0][k1 % nb];
+              r.rep2 = (uint8_t)n2;
+              r.gpus2 = (uint8_t)g2;
+              r.batch2 = so.batch[c0][k2 % nb];
+              r.w = (uint8_t)(wi + 1);
+              c.b -= g1 * n1 + g2 * n2;
+              return r;
+            }
+            c.q -= k9;
+          }
+      }
   }
   return r;
 }
@@ -291,7 +335,7 @@ __global__ void __launch_bounds__(256) k_enum_unrank(cf_enum_opts o, EnumView V,
   for (int v = 0; v < CF_MAX_NODES; v++) {
     NodeCfg nc[kPlansPerThread];
 #pragma unroll
-    for (int j = 0; j < kPlansPerThread; j++) nc[j] = same[j] ? nc[j - 1] : place(V, so, cur[j], v);
+    for (int j = 0; j < kPlansPerThread; j++) nc[j] = same[j] ? nc[j - 1] : place(V, so, cur[j], v, o.het != 0);
 #pragma unroll
     for (int j = 0; j < kPlansPerThread; j++) b8[j] = nc[j].comp;
     put8(out.node_comp + v * P, b8);
@@ -308,6 +352,20 @@ __global__ void __launch_bounds__(256) k_enum_unrank(cf_enum_opts o, EnumView V,
     } else {
       for (int j = 0; j < kPlansPerThread; j++)
         if (p0 + j < count) brow[p0 + j] = nc[j].batch;
+    }
+    if (out.node_rep2) {
+#pragma unroll
+      for (int j = 0; j < kPlansPerThread; j++) b8[j] = nc[j].rep2;
+      put8(out.node_rep2 + v * P, b8);
+#pragma unroll
+      for (int j = 0; j < kPlansPerThread; j++) b8[j] = nc[j].gpus2;
+      put8(out.node_gpus2 + v * P, b8);
+#pragma unroll
+      for (int j = 0; j < kPlansPerThread; j++) b8[j] = nc[j].w;
+      put8(out.node_w + v * P, b8);
+      uint16_t *b2row = out.node_batch2 + v * P;
+      for (int j = 0; j < kPlansPerThread; j++)
+        if (p0 + j < count) b2row[p0 + j] = nc[j].batch2;
     }
   }
   int i2[kPlansPerThread] = {0, 0, 0, 0};
@@ -365,7 +423,7 @@ __global__ void __launch_bounds__(kScrBlock) k_enum_screen(cf_enum_opts o, EnumV
   uint32_t rep[CF_MAX_NODES], gp[CF_MAX_NODES];
 #pragma unroll
   for (int v = 0; v < CF_MAX_NODES; v++) {
-    const NodeCfg nc = place(V, so, cur, v);
+    const NodeCfg nc = place(V, so, cur, v, false);
     rep[v] = nc.rep;
     gp[v] = nc.gpus;
     b_s[v][tid] = nc.batch;
@@ -601,6 +659,10 @@ extern "C" cf_status cf_enum_plans(const cf_model_desc *model, const cf_enum_opt
   if (!out->n_nodes_dev || !out->node_comp_dev || !out->node_rep_dev || !out->node_batch_dev ||
       !out->node_gpus_dev || !out->n_alt_dev || !out->alt_w_dev || !out->alt_node_dev)
     return set_error(CF_EINVAL, "NULL plan-table array");
+  const int ng = (out->node_rep2_dev != nullptr) + (out->node_batch2_dev != nullptr) +
+                 (out->node_gpus2_dev != nullptr) + (out->node_w_dev != nullptr);
+  if (ng != 0 && ng != 4) return set_error(CF_EINVAL, "second-configuration arrays: all four or none");
+  if (opts->het && ng == 0) return set_error(CF_EINVAL, "het plans need the second-configuration arrays");
   hipStream_t s = as_stream(stream);
   uint64_t *tab = nullptr, *totals = nullptr;
   if ((st = run_tables(opts, logical_dev, n_logical, &tab, &totals, s)) != CF_OK) return st;
@@ -620,6 +682,10 @@ extern "C" cf_status cf_enum_plans(const cf_model_desc *model, const cf_enum_opt
   o.n_alt = const_cast<uint8_t *>(out->n_alt_dev);
   o.alt_w = const_cast<uint8_t *>(out->alt_w_dev);
   o.alt_node = const_cast<uint8_t *>(out->alt_node_dev);
+  o.node_rep2 = const_cast<uint8_t *>(out->node_rep2_dev);
+  o.node_batch2 = const_cast<uint16_t *>(out->node_batch2_dev);
+  o.node_gpus2 = const_cast<uint8_t *>(out->node_gpus2_dev);
+  o.node_w = const_cast<uint8_t *>(out->node_w_dev);
   const unsigned threads = (unsigned)((count + kPlansPerThread - 1) / kPlansPerThread);
   hipLaunchKernelGGL(k_enum_unrank, dim3((threads + 255) / 256), dim3(256), 0, s, *opts, V, offsets_dev, first,
                      count, o);
@@ -633,6 +699,7 @@ extern "C" cf_status cf_enum_screen(const cf_model_desc *model, const cf_enum_op
   using namespace cf;
   cf_status st = check_opts(model, opts);
   if (st != CF_OK) return st;
+  if (opts->het) return set_error(CF_EUNSUPPORTED, "cf_enum_screen takes one configuration per node");
   KModel m;
   if ((st = lower_model(model, &m)) != CF_OK) return st;
   if (count < 0) return set_error(CF_EINVAL, "count < 0");

@@ -201,3 +201,35 @@ def test_topk_merge_edges(cf):
     assert rc == -1                                  # outputs alias the running list
     rc = cf._lib.cf_topk_merge(cf._p(r2), cf._p(g2), -1, cf._p(rd), cf._p(ids), 2, 0, 4, cf._p(buf), cf._p(bg), None)
     assert rc == -1                                  # a negative count
+
+
+@pytest.mark.parametrize("name,N,extra,window", [
+    ("c1", 4, {"gpus": {"E": [1, 2], "L": [1]}, "batch": {"E": [16, 64], "L": [16, 64, 256]}}, None),
+    ("c1", 8, {}, 20000),
+    ("c2", 10, {}, 5000),
+])
+def test_enum_two_configuration_nodes(cf, name, N, extra, window):
+    """Nodes of two configurations (het): counts and offsets, plan tables byte-identical to
+    the oracle's (whole space, or windows at evenly spaced starts of a large one), phase 1 of
+    the device table equal to the oracle's; the fused screen refuses het."""
+    _say(f"enum het {name} N={N}")
+    desc, opts, ldev, offsets, total, m, oo, Ls = _setup(cf, name, N, het=True, **extra)
+    counts = [O.enum_count(m, oo, L) for L in Ls]
+    assert total == sum(counts)
+    assert np.array_equal(offsets.cpu().numpy().view(np.uint64), np.concatenate([[0], np.cumsum(counts)]).astype(np.uint64))
+    starts = [0] if window is None else [0, total // 5, (2 * total) // 5, total // 2 + 3, total - window]
+    count = total if window is None else window
+    for s in starts:
+        got = cf.cf_enum_plans(desc, opts, ldev, offsets, total, s, count)
+        want = O.enum_plans(m, oo, Ls, s, count)
+        host = got.to_host()
+        for f in PlanTable.FIELDS:
+            assert np.array_equal(getattr(host, f), getattr(want, f)), (f, s)
+        assert np.any(want.node_rep2) or s == 0
+        mom = cf.cf_trace_gen(desc, [0], 2000)[1]
+        mom0 = O.trace_gen(m, [0], 2000)["moments"][0]
+        rd, bn, fl = cf.cf_eval_coarse(desc, got, mom[0], N)
+        w = O.eval_coarse(m, want, mom0, N)
+        assert np.array_equal(rd.cpu().numpy(), w[0]) and np.array_equal(fl.cpu().numpy(), w[2])
+    with pytest.raises(cf.CfError):
+        cf.cf_enum_screen(desc, opts, ldev, offsets, total, 0, 64, mom[0], N)
