@@ -38,33 +38,17 @@ MC_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_mc.hip", "paper_2512_14098_amd
 # WRITE_SIZE x 1.0, the scale factors a plain 1 GiB device copy gives), keyed by the kernel
 # source the counters were taken on and the workload (with its sample); any other source or
 # workload reports null
-_W_C1 = ("c1: MLLM graph E->L on 8 simulated GPUs (7B LLM, 600M ViT); ~1000 plans; 16-point rate grid; "
-         "32 seeds x 10000 requests")
-_W_C4_SEED0 = ("c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse screening of 10^6 "
-               "sampled plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 requests "
-               "(sample: first 1 of its 64 seeds)")
-_W_C3_SEED0 = ("c3: Text-to-image graph L -> 50-step diffusion G (1024^2) mixed 50/50 with text-only LLM requests "
-               "on 32 simulated GPUs; ~50000 sampled plans; 16 rates; 64 seeds x 50000 requests "
-               "(sample: first 1 of its 64 seeds)")
-_W_C2_SEEDS2 = ("c2: Omni graph (E_img, E_aud) -> thinker -> gated talker -> audio generator on 16 simulated GPUs; "
-                "~10000 sampled plans; 16 rates; 32 seeds x 20000 requests (sample: first 2 of its 32 seeds)")
-_W_C4_STEP = ('c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse screening of 10^6 sampl'
-              'ed plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 requests; each step: the trace of all 64 seeds, phase 1 over all 1000000 plans, the top 1000 and their 32-rate grid, phase 3 of every 4-th selected plan at every rate on one seed (plan slice g mod 4 of seed g div 4 at step g), their goodput reduction')
+_W_C4_STEP = ("c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse screening of 10^6 "
+              "sampled plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 requests; each step: "
+              "the trace of all 64 seeds, phase 1 over all 1000000 plans, the top 1000 and their 32-rate grid, "
+              "phase 3 of every selected plan at every rate on one seed (seed g at step g), their goodput reduction")
 MEASURED_TRAFFIC = {
-    ('c8fea1958289865f', _W_C4_STEP): 4.1436e+12,
-    ("c54c478f1dc57905", _W_C1): 2.0539e12,
-    ("c54c478f1dc57905", _W_C2_SEEDS2): 9.1424e11,
-    ("c54c478f1dc57905", _W_C3_SEED0): 1.9634e12,
-    ("c54c478f1dc57905", _W_C4_SEED0): 1.7606e13,
+    ("e499eed1d99c6565", _W_C4_STEP): 1.7718e13,
 }
 # VALU lane rate of the k_fine launch by rocprofv3 counters (SQ_INSTS_VALU x SQ_THREAD_CYCLES_VALU /
 # SQ_ACTIVE_INST_VALU / kernel time / PEAK_LANE_OPS), keyed like MEASURED_TRAFFIC
 MEASURED_LANE_FRAC = {
-    ('c8fea1958289865f', _W_C4_STEP): 0.1955,
-    ("c54c478f1dc57905", _W_C1): 0.4244,
-    ("c54c478f1dc57905", _W_C2_SEEDS2): 0.3076,
-    ("c54c478f1dc57905", _W_C3_SEED0): 0.3977,
-    ("c54c478f1dc57905", _W_C4_SEED0): 0.2844,
+    ("e499eed1d99c6565", _W_C4_STEP): 0.2846,
 }
 ENUM_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_enum.hip", "paper_2512_14098_amd/csrc/cf_internal.h",
                        "paper_2512_14098_amd/csrc/cf_phase1.h")
@@ -474,13 +458,16 @@ def enum_bench(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=-1,
+                    help="timed steps (default: 1 for the whole c4 workload, whose step is one seed of the fine "
+                         "stage, ~40 s; else 2)")
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", default="c4")
     ap.add_argument("--slices", type=int, default=-1, metavar="F",
                     help="each step simulates one slice of the fine stage: every F-th selected plan (all "
-                         "grid rates) on one seed, step g taking plan slice g %% F of seed g // F (default: 4 "
-                         "for the whole c4 workload, else none: every plan on every seed per step)")
+                         "grid rates) on one seed, step g taking plan slice g %% F of seed g // F (default: 1 "
+                         "for the whole c4 workload, i.e. every selected plan on one seed per step, else none: "
+                         "every plan on every seed per step)")
     ap.add_argument("--seeds", type=int, default=0, metavar="N",
                     help="simulate only the first N seeds of the workload (a sample of a workload "
                          "too large to run whole; stated in the output)")
@@ -513,6 +500,8 @@ def main():
     ap.add_argument("--mc-samples", type=int, default=1024, metavar="K")
     ap.add_argument("--mc-alpha", type=float, default=0.8)
     args = ap.parse_args()
+    if args.steps < 0 and (args.enum or args.phase2 or args.stress > 0):
+        args.steps = 2
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the library has no multi-GPU path (triples are "
               "independent; they would shard by contiguous blocks of the selected plans)",
@@ -567,7 +556,11 @@ def main():
         w.top_k = min(w.top_k, args.plans)
     F = args.slices
     if F < 0:
-        F = 4 if (args.config == "c4" and args.seeds == 0 and args.plans == 0 and not args.bisect) else 0
+        # c4 whole: one seed per step.  A launch of one seed's 32,000 triples keeps ~8 triples in turn on
+        # each resident wavefront; thinner slices end on their longest triple (~17 s) while the rest idle
+        F = 1 if (args.config == "c4" and args.seeds == 0 and args.plans == 0 and not args.bisect) else 0
+    if args.steps < 0:
+        args.steps = 1 if F > 0 else 2
     S = len(w.seeds)
 
     def set_slice(g):
@@ -615,7 +608,11 @@ def main():
     achieved = OPS_PER_EVENT * ev_step / fine_avg_s / 1e12
     n_sel = int(out["ids"].numel())
     workload = "%s: %s" % (args.config, w.cfg["summary"])
-    if F > 0:
+    if F == 1:
+        workload += ("; each step: the trace of all %d seeds, phase 1 over all %d plans, the top %d and their "
+                     "%d-rate grid, phase 3 of every selected plan at every rate on one seed (seed g at step g), "
+                     "their goodput reduction" % (S, w.tab.P, n_sel, w.K))
+    elif F > 0:
         workload += ("; each step: the trace of all %d seeds, phase 1 over all %d plans, the top %d and their "
                      "%d-rate grid, phase 3 of every %d-th selected plan at every rate on one seed (plan slice "
                      "g mod %d of seed g div %d at step g), their goodput reduction"
