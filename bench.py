@@ -38,17 +38,30 @@ MC_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_mc.hip", "paper_2512_14098_amd
 # WRITE_SIZE x 1.0, the scale factors a plain 1 GiB device copy gives), keyed by the kernel
 # source the counters were taken on and the workload (with its sample); any other source or
 # workload reports null
+_W_C1 = ("c1: MLLM graph E->L on 8 simulated GPUs (7B LLM, 600M ViT); ~1000 plans; 16-point rate grid; "
+         "32 seeds x 10000 requests")
+_W_C2_SEEDS2 = ("c2: Omni graph (E_img, E_aud) -> thinker -> gated talker -> audio generator on 16 simulated GPUs; "
+                "~10000 sampled plans; 16 rates; 32 seeds x 20000 requests (sample: first 2 of its 32 seeds)")
+_W_C3_SEED0 = ("c3: Text-to-image graph L -> 50-step diffusion G (1024^2) mixed 50/50 with text-only LLM requests "
+               "on 32 simulated GPUs; ~50000 sampled plans; 16 rates; 64 seeds x 50000 requests "
+               "(sample: first 1 of its 64 seeds)")
 _W_C4_STEP = ("c4: Full coarse-to-fine sweep of the omni graph on 64 simulated GPUs: coarse screening of 10^6 "
               "sampled plans, the top 1000 by R_d simulated at 32 rates x 64 seeds x 100000 requests; each step: "
               "the trace of all 64 seeds, phase 1 over all 1000000 plans, the top 1000 and their 32-rate grid, "
               "phase 3 of every selected plan at every rate on one seed (seed g at step g), their goodput reduction")
 MEASURED_TRAFFIC = {
     ("e499eed1d99c6565", _W_C4_STEP): 1.7718e13,
+    ("e499eed1d99c6565", _W_C1): 1.9291e12,
+    ("e499eed1d99c6565", _W_C2_SEEDS2): 9.3703e11,
+    ("e499eed1d99c6565", _W_C3_SEED0): 1.9566e12,
 }
 # VALU lane rate of the k_fine launch by rocprofv3 counters (SQ_INSTS_VALU x SQ_THREAD_CYCLES_VALU /
 # SQ_ACTIVE_INST_VALU / kernel time / PEAK_LANE_OPS), keyed like MEASURED_TRAFFIC
 MEASURED_LANE_FRAC = {
     ("e499eed1d99c6565", _W_C4_STEP): 0.2846,
+    ("e499eed1d99c6565", _W_C1): 0.4258,
+    ("e499eed1d99c6565", _W_C2_SEEDS2): 0.3077,
+    ("e499eed1d99c6565", _W_C3_SEED0): 0.3973,
 }
 ENUM_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_enum.hip", "paper_2512_14098_amd/csrc/cf_internal.h",
                        "paper_2512_14098_amd/csrc/cf_phase1.h")
