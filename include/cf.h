@@ -293,10 +293,10 @@ cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_table *plans,
  * per device (held from the library's load on that device until the
  * process ends) instead of the library's cached allocations, and no
  * hipMalloc, hipFree or allocating library routine is called.  The array
- * bounds the number of wavefronts (64 MiB / the state of one simulation,
- * about 0.9 MiB at 3,000 requests); a call whose single simulation does not
- * fit (about 60,000 requests and more) returns CF_ECAPACITY before any
- * launch.  Every call on a device shares that device's array and leaves its
+ * bounds the number of wavefronts (64 MiB, less the launch's (plan, rate)
+ * order of 4 bytes per pair, over the state of one simulation, about
+ * 0.9 MiB at 3,000 requests); a call whose single simulation does not fit
+ * (about 60,000 requests and more) returns CF_ECAPACITY before any launch.  Every call on a device shares that device's array and leaves its
  * contents behind (the call clears what must start at zero itself): calls
  * that overlap in time on one device race and must be serialised by the
  * caller.  Synchronises the stream, as cf_eval_fine does.

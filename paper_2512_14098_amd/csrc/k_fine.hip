@@ -142,6 +142,9 @@ struct FineArgs {
   int nsi_cap;  // stage instances provided in LDS
   int nl_cap, nt_cap;  // k_fine<true>: LLM stage instances and thinker ring slots provided in LDS
   uint64_t lim_instants;  // instants a simulation may take (a test limit; ~0 = none)
+  // order in which a seed's (plan, rate) pairs are taken: entry j is i * K + k
+  // (null: rate index first, then plan)
+  const uint32_t *order;
 };
 
 // model tables read with per-lane (divergent) indices
@@ -1913,12 +1916,22 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
     if (lane == 0) tk = atomicAdd(A.ticket, 1u);
     tk = ru(tk);
     if (tk >= A.total) break;
-    // seed-major, then rate, then plan: a triple costs more the lower its
-    // rate (less batching, more instants per request), so the costliest
-    // triples of a seed are taken first and the launch ends on cheap ones
+    // seed-major, then by rate: a triple costs more the lower its rate (less
+    // batching, more instants per request), so the costliest triples of a
+    // seed are taken first and the launch ends on cheap ones.  With an order
+    // table the pairs go by ascending rate over all plans, else by rate
+    // index, then plan.
     const int s = (int)(tk / per_seed);
     const unsigned int rem = tk % per_seed;
-    const int k = (int)(rem / (unsigned)A.n_plans), i = (int)(rem % (unsigned)A.n_plans);
+    int k, i;
+    if (A.order) {
+      const uint32_t e = ru(A.order[rem]);
+      i = (int)(e / (unsigned)A.K);
+      k = (int)(e % (unsigned)A.K);
+    } else {
+      k = (int)(rem / (unsigned)A.n_plans);
+      i = (int)(rem % (unsigned)A.n_plans);
+    }
     const int p = ri(A.plan_ids[i]);
     const size_t oidx = ((size_t)i * A.K + k) * A.S + s;
     S.soff = (size_t)s * A.n;
@@ -2057,6 +2070,35 @@ __global__ void k_fine_reset3(unsigned int *v) {
   v[2] = 0u;
 }
 
+// Position of each (plan, rate) pair when the pairs are sorted by ascending
+// rate, ties and NaN (last) by pair index: order[rank] = i * K + k.  One
+// thread per pair counts the pairs before it, reading them in LDS tiles.
+constexpr int kRankTile = 1024;
+__device__ __forceinline__ uint64_t rate_key(double r) {
+  uint64_t b = __builtin_bit_cast(uint64_t, r);
+  if (r != r) return ~0ull;  // NaN last
+  return (b >> 63) ? ~b : (b | (1ull << 63));  // IEEE order as unsigned order
+}
+__global__ void __launch_bounds__(256) k_rate_order(const double *__restrict__ rates, uint32_t n,
+                                                    uint32_t *__restrict__ order) {
+  __shared__ uint64_t tile[kRankTile];
+  const uint32_t e = blockIdx.x * blockDim.x + threadIdx.x;
+  const uint64_t key = e < n ? rate_key(rates[e]) : 0ull;
+  uint32_t rank = 0;
+  for (uint32_t base = 0; base < n; base += kRankTile) {
+    __syncthreads();
+    for (uint32_t t = threadIdx.x; t < kRankTile; t += blockDim.x)
+      tile[t] = base + t < n ? rate_key(rates[base + t]) : ~0ull;
+    __syncthreads();
+    const uint32_t lim = n - base < (uint32_t)kRankTile ? n - base : (uint32_t)kRankTile;
+    for (uint32_t t = 0; t < lim; t++) {
+      const uint64_t o = tile[t];
+      rank += (o < key || (o == key && base + t < e)) ? 1u : 0u;
+    }
+  }
+  if (e < n) order[rank] = e;
+}
+
 // stage instances, LLM stage instances and gate-source stage instances of
 // the largest selected plans (out[0..2]; malformed plans are skipped)
 __global__ void k_max_si(const uint8_t *n_nodes, const uint8_t *node_comp, const uint8_t *node_rep,
@@ -2148,6 +2190,9 @@ cf_status fixed_scratch_of(char **ptr) {
 }
 
 constexpr size_t kFineHdr = 8192;  // ticket, stage counts, the argument block
+// launches of at most this many (plan, rate) pairs take them by ascending rate
+// (k_rate_order: quadratic in the pairs, ~1 ms at the limit)
+constexpr size_t kOrderMax = 1u << 17;
 
 // cf_eval_fine and cf_eval_fine_noalloc: with fixed == nullptr the call's
 // scratch comes from the library's cached allocations, else from the fixed
@@ -2239,14 +2284,19 @@ cf_status eval_fine(const cf_model_desc *model, const cf_plan_table *plans, cons
   static_assert(sizeof(FineArgs) + 512 <= kFineHdr, "FineArgs must fit the scratch header");
   char *scr;
   size_t hdr = kFineHdr;
+  const size_t npairs = (size_t)n_plans * (size_t)K;
+  const size_t order_bytes = npairs <= kOrderMax ? (sizeof(uint32_t) * npairs + 255) & ~(size_t)255 : 0;
+  size_t order_off = 0;
   if (fixed) {
-    // the target table (if any) follows the header; the slabs of as many
-    // wavefronts as fit follow it
+    // the target table (if any) and the pair order follow the header; the
+    // slabs of as many wavefronts as fit follow them
     if (out->n_bins > 0) {
       st = check_targets(a.m.nt, out->n_bins, out->hist_targets_host);
       if (st != CF_OK) return st;
       hdr += (sizeof(double) * (size_t)a.m.nt * (size_t)out->n_bins * 4 + 255) & ~(size_t)255;
     }
+    order_off = hdr;
+    hdr += order_bytes;
     if (fixed_cap < hdr + a.L.bytes)
       return set_error(CF_ECAPACITY, "one simulation of %d requests needs %zu bytes of scratch; the fixed scratch holds %zu",
                        trace->n_req, hdr + a.L.bytes, fixed_cap);
@@ -2254,6 +2304,8 @@ cf_status eval_fine(const cf_model_desc *model, const cf_plan_table *plans, cons
     if ((size_t)waves > fit) waves = (long long)fit;
     scr = fixed;
   } else {
+    order_off = hdr;
+    hdr += order_bytes;
     scr = (char *)scratch_get(SCR_FINE, hdr + (size_t)waves * a.L.bytes, &st);
     if (!scr) return st;
   }
@@ -2262,6 +2314,13 @@ cf_status eval_fine(const cf_model_desc *model, const cf_plan_table *plans, cons
   FineArgs *args_dev = (FineArgs *)(scr + 512);
   a.slab = scr + hdr;
   hipStream_t s = as_stream(stream);
+  a.order = nullptr;
+  if (order_bytes) {
+    uint32_t *order = (uint32_t *)(scr + order_off);
+    hipLaunchKernelGGL(k_rate_order, dim3((unsigned)((npairs + 255) / 256)), dim3(256), 0, s, rates_dev,
+                       (uint32_t)npairs, order);
+    a.order = order;
+  }
   // size the LDS stage table from the largest selected plan
   uint32_t llm_mask = 0;
   for (int c = 0; c < a.m.nc; c++)
