@@ -83,9 +83,7 @@ def test_trace_parity(cf, name, seeds, n):
 def test_coarse_select_grid_parity(cf, name):
     _say(f"coarse {name}")
     cfg = load_config(name)
-    if name == "c4" and not os.environ.get("CF_FULL_C4"):
-        cfg["plans"]["sampled"]["total"] = 100000  # first 1e5 plans of the c4 sampler
-    tab = make_plans(cfg)
+    tab = make_plans(cfg)  # c4: all 10^6 sampled plans
     m = O.make_model(cfg["model"])
     desc = cf.model_desc(cfg["model"])
     tr, mom = cf.cf_trace_gen(desc, [0], 4000)

@@ -203,11 +203,13 @@ def _enc_queue(dist):
                  [rtype("a", ["S"], aud_in=dist)])
 
 
-@pytest.mark.parametrize("rho,dist", [(0.3, {"exp": 1000}), (0.6, {"exp": 1000}),
-                                      (0.6, {"const": 1000}), (0.5, {"lognormal_s": [0.0, 0.5]})])
+@pytest.mark.parametrize("rho,dist", [(0.3, {"exp": 1000}), (0.6, {"exp": 1000}), (0.9, {"exp": 1000}),
+                                      (0.6, {"const": 1000}), (0.9, {"const": 1000}),
+                                      (0.5, {"lognormal_s": [0.0, 0.5]})])
 def test_mg1_pollaczek_khinchine(rho, dist):
     plan = one_plan([(1, 1, 1)], [[(10, {0: 0})]])
-    seeds, n = list(range(16)), 20000
+    # near saturation the sample mean converges slowly: more and longer seeds
+    seeds, n = (list(range(32)), 50000) if rho > 0.8 else (list(range(16)), 20000)
     mc = _enc_queue(dist)
     m = O.make_model(mc)
     tr = O.trace_gen(m, seeds, n)
