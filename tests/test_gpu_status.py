@@ -154,6 +154,46 @@ def test_invalid_rates_and_plan_ids_match_the_oracle(cf):
     assert np.all(g.cpu().numpy()[1:] == 0.0)
 
 
+def test_every_pair_simulated_once_whatever_the_rates(cf):
+    """The launch takes a seed's (plan, rate) pairs by ascending rate: repeated rates, signed
+    zeros, infinities and NaNs of either sign still give every triple exactly its own result."""
+    _say("status: pair order with repeated and non-finite rates")
+    cfg = load_config("c0")
+    tab = make_plans(cfg)
+    desc = cf.model_desc(cfg["model"])
+    n = 300
+    tr, _ = cf.cf_trace_gen(desc, [0, 1], n)
+    neg_nan = np.frombuffer(np.uint64(0xFFF8000000000001).tobytes(), np.float64)[0]
+    ids = np.array([0, 1, 2, 3, 4, 5, 0], np.int32)
+    rates = np.array([[2.0, 2.0, np.nan, 4.0, -0.0],
+                      [0.0, 2.0, 2.0, neg_nan, 8.0],
+                      [np.inf, -np.inf, 1.0, 1.0, 1.0],
+                      [np.nan, np.nan, 4.0, 4.0, 2.0],
+                      [1.0, 2.0, 4.0, 8.0, 16.0],
+                      [-1.0, 1e-300, 2.0, neg_nan, 2.0],
+                      [2.0, 2.0, np.nan, 4.0, -0.0]])
+    out = _np(cf.cf_eval_fine(desc, cf.DevicePlans(tab), torch.from_numpy(ids).cuda(),
+                              torch.from_numpy(rates).cuda(), tr))
+    m = O.make_model(cfg["model"])
+    otr = O.trace_gen(m, [0, 1], n)
+    st = out["status"].view(np.uint32)
+    for i in range(len(ids)):
+        for k in range(rates.shape[1]):
+            for s_ in range(2):
+                r = float(rates[i, k])
+                if np.isfinite(r) and r > 0:
+                    o = O.sim_triple(m, tab, int(ids[i]), r, otr, s_)
+                    assert st[i, k, s_] == o["status"], (i, k, s_)
+                    assert np.array_equal(out["met"][i, k, s_].view(np.uint32), o["met"]), (i, k, s_)
+                    assert np.array_equal(out["cnt"][i, k, s_].view(np.uint32), o["cnt"]), (i, k, s_)
+                    assert out["events"][i, k, s_].view(np.uint64) == o["events"], (i, k, s_)
+                else:
+                    assert st[i, k, s_] == ST_INVALID, (i, k, s_)
+    # the first and last rows are the same plan at the same rates
+    for key in ("met", "cnt", "events", "status"):
+        assert np.array_equal(out[key][0], out[key][6])
+
+
 def test_bad_limits_and_flags_are_rejected(cf):
     cfg = load_config("c0")
     tab = make_plans(cfg)
