@@ -194,6 +194,33 @@ def test_every_pair_simulated_once_whatever_the_rates(cf):
         assert np.array_equal(out[key][0], out[key][6])
 
 
+def test_launch_above_the_ordered_pair_limit(cf):
+    """Above 2^17 (plan, rate) pairs per seed the launch takes them by rate index, then plan:
+    8,200 copies of c0's plans x 16 rates, every copy equal to its first occurrence, the first
+    occurrences equal to the oracle."""
+    _say("status: launch of 131,200 pairs (unordered)")
+    cfg = load_config("c0")
+    tab = make_plans(cfg)
+    desc = cf.model_desc(cfg["model"])
+    n, P, K = 40, 8200, 16
+    tr, _ = cf.cf_trace_gen(desc, [3], n)
+    ids = (np.arange(P) % tab.P).astype(np.int32)
+    base = np.array([0.5 * 1.25 ** k for k in range(K)])
+    rates = np.tile(base, (P, 1))
+    out = _np(cf.cf_eval_fine(desc, cf.DevicePlans(tab), torch.from_numpy(ids).cuda(),
+                              torch.from_numpy(rates).cuda(), tr))
+    assert P * K > (1 << 17)
+    for key in ("met", "cnt", "events", "status"):
+        first = out[key][: tab.P]
+        assert np.array_equal(out[key], np.concatenate([first] * (P // tab.P) + [first[: P % tab.P]])), key
+    m = O.make_model(cfg["model"])
+    want = O.eval_fine(m, tab, ids[: tab.P], np.ascontiguousarray(rates[: tab.P]), O.trace_gen(m, [3], n))
+    assert np.array_equal(out["met"][: tab.P].view(np.uint32), want[0])
+    assert np.array_equal(out["cnt"][: tab.P].view(np.uint32), want[1])
+    assert np.array_equal(out["events"][: tab.P].view(np.uint64), want[2])
+    assert np.array_equal(out["status"][: tab.P].view(np.uint32), want[3])
+
+
 def test_bad_limits_and_flags_are_rejected(cf):
     cfg = load_config("c0")
     tab = make_plans(cfg)
