@@ -840,9 +840,14 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
     const bool valid = j < n;
     uint32_t r = 0;
     Rec R = {0, 0, 0};
+    uint32_t a_no = 0;  // prefill: the request's output-length attribute at c
+    uint64_t tkv = 0;   // the request's arrival tick
     if (valid) {
       r = mem[j];
+      // loads that depend on the request id only, issued with its record
       R = rec_get(S, r);
+      tkv = gload(S.A->ticks, S.soff + r);
+      if (kind == IT_PREFILL) a_no = attr(S, r, ml.nout_attr[c]);
     }
     const int t = rtype(R.misc);
     bool fin = valid;
@@ -850,7 +855,7 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
     int ta = 0;
     uint32_t key = 0, gw = 0, gq = 0;
     if (valid && kind == IT_PREFILL) {
-      const uint32_t no = nout_of(S, r, t, c);
+      const uint32_t no = ((ml.pfo[t] >> c) & 1u) ? 1u : (a_no < 1u ? 1u : a_no);  // nout_of(S, r, t, c)
       if (c == ml.ttft_c[t]) {
         S.tim[r].tfirst = now;
         S.tim[r].tlast = now;
@@ -972,7 +977,7 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
       bool ok = false;
       int hbin = 0;
       if (done) {
-        const double a = arrival_time(S, r);
+        const double a = ((double)tkv * 0x1p-32) / S.lam;  // arrival_time(S, r)
         double ttft = 0.0, tpot = 0.0, media = 0.0;
         const int tc = ml.ttft_c[t];
         if (tc >= 0) {
@@ -1129,12 +1134,15 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
 
 template <bool G>
 __device__ int runnable_kind(Sim &S, int x, int si, int c) {
+  // the stage's fields are read together (one LDS latency), the LLM ones
+  // before they are known to be needed
   const uint8_t fl = S.si.flags[si];
   const int qn = S.si.qn[si];
-  if (!(fl & SF_LLM)) return qn > 0 ? IT_BATCH : -1;
+  const int beff = S.si.beff[si];
   const int lx = lx_of<G>(S.si, si);
+  if (!(fl & SF_LLM)) return qn > 0 ? IT_BATCH : -1;
   const int rn = S.si.rn[lx];
-  if (qn > 0 && rn < (int)S.si.beff[si]) return IT_PREFILL;
+  if (qn > 0 && rn < beff) return IT_PREFILL;
   if (rn == 0) return -1;
   if (!(fl & SF_GATED)) return IT_DECODE;
   const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lx];
