@@ -158,8 +158,9 @@ struct ModelLds {
 
 struct WaveShared {
   uint32_t ex_st[CF_MAX_EXEC];  // busy:1 ran:1 kind:2 rr:4 cur:4 nmem:9
-  uint16_t ex_first[CF_MAX_EXEC];
-  uint8_t ex_ns[CF_MAX_EXEC], ex_node[CF_MAX_EXEC];
+  // an executor's first stage instance (bits 0..15), its stage count (bits
+  // 16..23) and its node (bits 24..31): one LDS word read at once
+  uint32_t ex_geo[CF_MAX_EXEC];
   uint8_t ex_tp[CF_MAX_EXEC];  // GPUs per executor as min(g, 8) - 1 (iteration-time multiplier index)
   uint8_t route[CF_MAX_TYPES][2][CF_MAX_COMP];
   uint8_t nalt[CF_MAX_TYPES], aw[CF_MAX_TYPES][2];
@@ -441,8 +442,9 @@ __device__ __forceinline__ double arrival_time(const Sim &S, uint32_t r) {
 __device__ __forceinline__ int ex_byte(uint64_t ex, int c) { return (int)((ex >> (8 * c)) & 0xFFu); }
 __device__ __forceinline__ int rtype(uint32_t misc) { return (int)((misc >> 8) & 7u); }
 __device__ __forceinline__ int stage_of(const Sim &S, int x, int c) {
-  const int v = S.sh->ex_node[x];
-  return S.sh->ex_first[x] + __popc((uint32_t)S.sh->vcomp[v] & ((1u << c) - 1u));
+  const uint32_t geo = S.sh->ex_geo[x];
+  const int v = (int)(geo >> 24);
+  return (int)(geo & 0xFFFFu) + __popc((uint32_t)S.sh->vcomp[v] & ((1u << c) - 1u));
 }
 
 // ------------------------------------------------------------------ pool / queues
@@ -1193,7 +1195,8 @@ struct GateView {
   bool joint;
 };
 __device__ __forceinline__ GateView local_gate_view(const Sim &S, int x, int si) {
-  const int ns = S.sh->ex_ns[x], first = S.sh->ex_first[x];
+  const uint32_t geo = S.sh->ex_geo[x];
+  const int ns = (int)((geo >> 16) & 0xFFu), first = (int)(geo & 0xFFFFu);
   const int lth = S.si.lsi[si];
   const uint32_t next = S.si.iter[lth] + 1u;
   uint32_t qmin = kNone, kta = kNone;
@@ -1276,7 +1279,7 @@ __device__ __forceinline__ bool start_joint(Sim &S, int x, int lth, int sth, int
   S.r_dur2 = lane_id() == x ? d2 : S.r_dur2;
   itgt_set<true>(S, x, n);  // steps of the run, thinker first
   xt_set<true, XT_END>(S, x, t);
-  const uint32_t lta = (uint32_t)(sta - sh.ex_first[x]);
+  const uint32_t lta = (uint32_t)(sta - (int)(sh.ex_geo[x] & 0xFFFFu));
   sh.ex_st[x] = (sh.ex_st[x] & 2u) | 1u | (IT_JOINT << 2) | ((uint32_t)lth << 4) | ((uint32_t)lth << 8) | EX_RUN |
                 (lta << 22);
   return true;
@@ -1286,7 +1289,8 @@ template <bool G>
 __device__ __forceinline__ void try_start(Sim &S, int x) {
   WaveShared &sh = *S.sh;
   const uint32_t st = sh.ex_st[x];
-  const int ns = sh.ex_ns[x], first = sh.ex_first[x];
+  const uint32_t geo = sh.ex_geo[x];
+  const int ns = (int)((geo >> 16) & 0xFFu), first = (int)(geo & 0xFFFFu);
   const int rr = (st >> 4) & 15u;
   for (int i = 0; i < ns; i++) {
     int l = (rr == 15) ? i : rr + 1 + i;  // rr < ns, i < ns
@@ -1336,7 +1340,7 @@ __device__ void cut_run(Sim &S, int x) {
   WaveShared &sh = *S.sh;
   const uint32_t st = sh.ex_st[x];
   if (!(st & EX_RUN) || !(xt_get<G, XT_END>(S, x) > S.now)) return;
-  const int si = sh.ex_first[x] + ((st >> 8) & 15u);
+  const int si = (int)(sh.ex_geo[x] & 0xFFFFu) + ((st >> 8) & 15u);
   if constexpr (G) {
     if (((st >> 2) & 3u) == IT_JOINT) {
       const uint32_t n = itgt_get<true>(S, x);
@@ -1461,7 +1465,7 @@ __device__ void finish_slots(Sim &S, int x, int si, int c, const bool *fin) {
 // finishing requests finish.
 __device__ __forceinline__ void complete_joint(Sim &S, int x, uint32_t st) {
   WaveShared &sh = *S.sh;
-  const int first = sh.ex_first[x];
+  const int first = (int)(sh.ex_geo[x] & 0xFFFFu);
   const int lth = (st >> 8) & 15u, lta = (st >> 22) & 15u;
   const int sth = first + lth, sta = first + lta;
   const uint32_t n = itgt_get<true>(S, x);
@@ -1525,7 +1529,7 @@ __device__ __forceinline__ void complete_iter(Sim &S, int x) {
       return;
     }
   }
-  const int si = sh.ex_first[x] + l;
+  const int si = (int)(sh.ex_geo[x] & 0xFFFFu) + l;
   const int c = S.si.comp[si];
   const uint8_t fl = S.si.flags[si];
   sh.ex_st[x] = (st & ~(1u | EX_RUN)) | 2u;  // idle, has run
@@ -1601,7 +1605,8 @@ __device__ __forceinline__ bool gate_wake(Sim &S, int y) {
   double w = __builtin_inf();
   bool now_el = false;
   if (!(st & 1u) || (st & EX_RUN)) {
-    const int ns = sh.ex_ns[y], first = sh.ex_first[y];
+    const uint32_t geo = sh.ex_geo[y];
+    const int ns = (int)((geo >> 16) & 0xFFu), first = (int)(geo & 0xFFFFu);
     bool undecided = false;
     for (int g = first; g < first + ns; g++) {
       if (!(S.si.flags[g] & SF_GATED)) continue;
@@ -1740,14 +1745,12 @@ __device__ bool setup_plan(Sim &S, int p) {
     int first = 0;
     for (int u = 0; u < v; u++) first += sh.vrep[u] * __popc(sh.vcomp[u]);
     first += (lane - sh.vbase[v]) * __popc(sh.vcomp[v]);
-    sh.ex_node[lane] = (uint8_t)v;
     if (m.tp_any) {
       const bool second = lane - sh.vbase[v] >= sh.vrep1[v];
       const uint32_t g = second ? A.node_gpus2[v * P + p] : A.node_gpus[v * P + p];
       sh.ex_tp[lane] = (uint8_t)(g < 1 ? 0 : (g > 8 ? 7 : g - 1));
     }
-    sh.ex_first[lane] = (uint16_t)first;
-    sh.ex_ns[lane] = (uint8_t)__popc(sh.vcomp[v]);
+    sh.ex_geo[lane] = (uint32_t)first | ((uint32_t)__popc(sh.vcomp[v]) << 16) | ((uint32_t)v << 24);
     sh.ex_st[lane] = 15u << 4;  // idle, never ran, no stage run yet
     if constexpr (!G) {
       S.xt[XT_END * CF_MAX_EXEC + lane] = __builtin_inf();
