@@ -181,12 +181,15 @@ struct WaveShared {
 // instances only, at index lsi[si], and the thinker-only fields (sched,
 // watch) per thinker ring slot hist[lsi[si]].
 struct SiLds {
-  uint8_t *comp, *flags;
+  uint8_t *comp, *flags;  // k_fine<false>
+  // k_fine<true>: a stage instance's constant fields in one word: flags
+  // (bits 0..7), component (8..11), batch (12..20), LLM index (21..31; kNoLsi:
+  // not an LLM stage)
+  uint32_t *word;
   uint8_t *qhp, *qtp;  // k_fine<false>: queue head and tail positions in their chunks
   int *qhc, *qtc;      // k_fine<false>: queue head and tail chunks
   uint32_t *qh, *qt;   // k_fine<true>: queue head and tail, chunk and position packed by qend
-  uint16_t *beff;
-  uint16_t *lsi;    // k_fine<true>: index of an LLM stage instance in the LLM-only fields
+  uint16_t *beff;   // k_fine<false>
   int16_t *hist;
   int *qn, *roff, *rn;
   uint32_t *iter, *minfin;
@@ -195,7 +198,7 @@ struct SiLds {
 };
 constexpr size_t kSiBytes = 1 + 1 + 1 + 1 + 2 + 2 + 4 * 7;
 // k_fine<true>: bytes per stage instance, per LLM stage instance, per thinker slot
-constexpr size_t kSiBytesG = 4 * 3 + 2 * 2 + 2, kLlmBytesG = 4 * 4 + 2, kThBytesG = 8 + 4;
+constexpr size_t kSiBytesG = 4 * 4, kLlmBytesG = 4 * 4 + 2, kThBytesG = 8 + 4;
 // a queue end, chunk c (-1: none) and position p <= kChunk in it, as one word
 // (chunk indices stay below 2^25: at most 2^26 requests on 8 components)
 __device__ __forceinline__ uint32_t qend(int c, int p) { return ((uint32_t)(c + 1) << 7) | (uint32_t)p; }
@@ -215,10 +218,29 @@ struct WaveLds<true> {
   WaveShared w;
 };
 
+constexpr uint32_t kNoLsi = 0x7FFu;
+static_assert(CF_MAX_COMP <= 16 && CF_MAX_BATCH < 512 && CF_MAX_EXEC * CF_MAX_COMP < (int)kNoLsi,
+              "stage word fields");
+// a stage instance's index in the LLM-only fields (k_fine<false>: its own)
 template <bool G>
 __device__ __forceinline__ int lx_of(const SiLds &si, int s) {
-  if constexpr (G) return si.lsi[s];
+  if constexpr (G) return (int)(si.word[s] >> 21);
   else return s;
+}
+template <bool G>
+__device__ __forceinline__ uint32_t si_flags(const SiLds &si, int s) {
+  if constexpr (G) return si.word[s] & 0xFFu;
+  else return si.flags[s];
+}
+template <bool G>
+__device__ __forceinline__ int si_comp(const SiLds &si, int s) {
+  if constexpr (G) return (int)((si.word[s] >> 8) & 15u);
+  else return si.comp[s];
+}
+template <bool G>
+__device__ __forceinline__ int si_beff(const SiLds &si, int s) {
+  if constexpr (G) return (int)((si.word[s] >> 12) & 0x1FFu);
+  else return si.beff[s];
 }
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x; }
@@ -656,7 +678,7 @@ __device__ __forceinline__ double token_vis(const Sim &S, uint32_t r, uint32_t m
   } else if ((misc & MISC_TH_DONE) && k == nth) {
     e = S.tim[r].tlast;
   } else {
-    const int lx = S.si.lsi[stage_of(S, xth, th)];
+    const int lx = lx_of<true>(S.si, stage_of(S, xth, th));
     const int slot = S.si.hist[lx];
     const uint32_t q = S.tim[r].thjoin + k - 1u;
     if (q > S.si.sched[slot]) {
@@ -833,7 +855,7 @@ template <bool G>
 __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr<uint32_t> mem) {
   const KModel &m = S.A->m;
   const ModelLds &ml = S.sh->ml;
-  const bool gated = S.si.flags[si] & SF_GATED;
+  const bool gated = si_flags<G>(S.si, si) & SF_GATED;
   const int lx = (G && kind != IT_PREFILL) ? 0 : lx_of<G>(S.si, si);  // LLM fields: prefill only
   const uint32_t iter_s = S.si.iter[lx];
   const double now = S.now;
@@ -871,7 +893,7 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
       key = gated ? (1u | (no << 16)) : iter_s + no - 1u;
       if (gated && ml.ta_c[t] == c) {
         const int th = ml.th_c[t], xth = ex_byte(R.ex, th);
-        gw = RG_GATED | ((uint32_t)S.si.lsi[stage_of(S, xth, th)] << 22) | ((uint32_t)xth << 16) |
+        gw = RG_GATED | ((uint32_t)lx_of<G>(S.si, stage_of(S, xth, th)) << 22) | ((uint32_t)xth << 16) |
              nout_of(S, r, t, th);
         gq = S.tim[r].thjoin;
       }
@@ -1019,10 +1041,11 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
   WaveShared &sh = *S.sh;
   double dur;
   int nmem = 0;
-  const int lx = (G && !(S.si.flags[si] & SF_LLM)) ? 0 : lx_of<G>(S.si, si);
+  const uint32_t fl = si_flags<G>(S.si, si);
+  const int lx = (G && !(fl & SF_LLM)) ? 0 : lx_of<G>(S.si, si);
   if (kind != IT_DECODE) {
     const int qn = S.si.qn[si];
-    const int beff = S.si.beff[si];
+    const int beff = si_beff<G>(S.si, si);
     const int room = kind == IT_PREFILL ? beff - S.si.rn[lx] : beff;
     const int n = qn < room ? qn : room;
     const GPtr<uint32_t> dst = S.mem + (uint32_t)(x * CF_MAX_BATCH);
@@ -1037,12 +1060,12 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     xs = dpp_sum_u32(xs);
     dur = (m.k0[c] + m.k1[c] * (double)xs) + m.k2[c] * (double)n;
     if (m.tp_any) dur = m.tps[c][sh.ex_tp[x]] * dur;
-    if (S.si.flags[si] & SF_ENC) {
+    if (fl & SF_ENC) {
       const bool ran = (sh.ex_st[x] >> 1) & 1u;
       if (!ran || xt_get<G, XT_LAST>(S, x) < S.now) dur = dur + m.cpu_pre;
     }
     nmem = n;
-  } else if (!(S.si.flags[si] & SF_GATED)) {
+  } else if (!(fl & SF_GATED)) {
     const int rn = S.si.rn[lx];
     dur = m.d0[c] + m.d1[c] * (double)rn;
     if (m.tp_any) dur = m.tps[c][sh.ex_tp[x]] * dur;
@@ -1067,7 +1090,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     if constexpr (G) {
       // k_fine<true>: a thinker stage records the predicted end of every
       // step of the run in its ring, one step per lane
-      if (S.si.flags[si] & SF_THINKER) {
+      if (fl & SF_THINKER) {
         const int slot = S.si.hist[lx];
         const GPtr<double> h = S.hist + (uint32_t)(slot * kRing);
         for (uint32_t i = (uint32_t)lane_id(); i <= itgt - (it0 + 1u); i += 64u) {
@@ -1120,7 +1143,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     if (m.tp_any) dur = m.tps[c][sh.ex_tp[x]] * dur;
     nmem = (int)cntm;
     if constexpr (G) {
-      if (S.si.flags[si] & SF_THINKER) {  // a gated stage that is also a gate source
+      if (fl & SF_THINKER) {  // a gated stage that is also a gate source
         const uint32_t it1 = S.si.iter[lx] + 1u;
         const int slot = S.si.hist[lx];
         if (lane_id() == 0) S.hist[(uint32_t)(slot * kRing) + (it1 & (kRing - 1))] = S.now + dur;
@@ -1138,9 +1161,9 @@ template <bool G>
 __device__ int runnable_kind(Sim &S, int x, int si, int c) {
   // the stage's fields are read together (one LDS latency), the LLM ones
   // before they are known to be needed
-  const uint8_t fl = S.si.flags[si];
+  const uint32_t fl = si_flags<G>(S.si, si);
   const int qn = S.si.qn[si];
-  const int beff = S.si.beff[si];
+  const int beff = si_beff<G>(S.si, si);
   const int lx = lx_of<G>(S.si, si);
   if (!(fl & SF_LLM)) return qn > 0 ? IT_BATCH : -1;
   const int rn = S.si.rn[lx];
@@ -1197,14 +1220,14 @@ struct GateView {
 __device__ __forceinline__ GateView local_gate_view(const Sim &S, int x, int si) {
   const uint32_t geo = S.sh->ex_geo[x];
   const int ns = (int)((geo >> 16) & 0xFFu), first = (int)(geo & 0xFFFFu);
-  const int lth = S.si.lsi[si];
+  const int lth = lx_of<true>(S.si, si);
   const uint32_t next = S.si.iter[lth] + 1u;
   uint32_t qmin = kNone, kta = kNone;
   int gsi = -1, nbusy = 0;
   bool other = false;  // a running request that does not wait for the next step of si
   for (int g = first; g < first + ns; g++) {
-    if (!(S.si.flags[g] & SF_GATED)) continue;
-    const int lg = S.si.lsi[g];
+    if (!(si_flags<true>(S.si, g) & SF_GATED)) continue;
+    const int lg = lx_of<true>(S.si, g);
     const int rn = S.si.rn[lg];
     if (rn == 0) continue;
     nbusy++;
@@ -1253,8 +1276,8 @@ __device__ __forceinline__ GateView local_gate_view(const Sim &S, int x, int si)
 __device__ __forceinline__ bool start_joint(Sim &S, int x, int lth, int sth, int sta, uint32_t kta) {
   const KModel &m = S.A->m;
   WaveShared &sh = *S.sh;
-  const int cth = S.si.comp[sth], cta = S.si.comp[sta];
-  const int lx = S.si.lsi[sth], lg = S.si.lsi[sta];
+  const int cth = si_comp<true>(S.si, sth), cta = si_comp<true>(S.si, sta);
+  const int lx = lx_of<true>(S.si, sth), lg = lx_of<true>(S.si, sta);
   double d1 = m.d0[cth] + m.d1[cth] * (double)S.si.rn[lx];
   double d2 = m.d0[cta] + m.d1[cta] * (double)S.si.rn[lg];
   if (m.tp_any) {
@@ -1296,27 +1319,27 @@ __device__ __forceinline__ void try_start(Sim &S, int x) {
     int l = (rr == 15) ? i : rr + 1 + i;  // rr < ns, i < ns
     if (l >= ns) l -= ns;
     const int si = first + l;
-    const int kind = runnable_kind<G>(S, x, si, S.si.comp[si]);
+    const int kind = runnable_kind<G>(S, x, si, si_comp<G>(S.si, si));
     if (kind >= 0) {
       bool lazy = false;
       uint32_t bound = kNone;
-      const uint8_t fl = S.si.flags[si];
-      const uint8_t no_run = G ? SF_GATED : (SF_THINKER | SF_GATED);
+      const uint32_t fl = si_flags<G>(S.si, si);
+      const uint32_t no_run = G ? SF_GATED : (SF_THINKER | SF_GATED);
       if (kind == IT_DECODE && !(fl & no_run) &&
-          (S.si.qn[si] == 0 || S.si.rn[lx_of<G>(S.si, si)] >= (int)S.si.beff[si])) {
+          (S.si.qn[si] == 0 || S.si.rn[lx_of<G>(S.si, si)] >= si_beff<G>(S.si, si))) {
         lazy = true;  // ... unless a stage checked after this one has work
         for (int i2 = i + 1; i2 < ns && lazy; i2++) {
           int l2 = (rr == 15) ? i2 : rr + 1 + i2;
           if (l2 >= ns) l2 -= ns;
-          if (runnable_kind<G>(S, x, first + l2, S.si.comp[first + l2]) >= 0) lazy = false;
+          if (runnable_kind<G>(S, x, first + l2, si_comp<G>(S.si, first + l2)) >= 0) lazy = false;
         }
         if constexpr (G) {
           if (lazy && (fl & SF_THINKER)) {
-            bound = S.si.iter[S.si.lsi[si]] + kThRun;
+            bound = S.si.iter[lx_of<G>(S.si, si)] + kThRun;
             if ((S.ta_exec_mask >> x) & 1ull) {
               const GateView gv = local_gate_view(S, x, si);
               if (gv.joint && start_joint(S, x, l, si, gv.gsi, gv.kta)) {
-                notify(S, S.si.hist[S.si.lsi[si]]);
+                notify(S, S.si.hist[lx_of<G>(S.si, si)]);
                 return;
               }
               bound = gv.qmin < bound ? gv.qmin : bound;
@@ -1324,9 +1347,9 @@ __device__ __forceinline__ void try_start(Sim &S, int x) {
           }
         }
       }
-      start_iter<G>(S, x, l, si, S.si.comp[si], kind, lazy, bound);
+      start_iter<G>(S, x, l, si, si_comp<G>(S.si, si), kind, lazy, bound);
       if constexpr (G) {
-        if ((fl & SF_THINKER) && kind == IT_DECODE) notify(S, S.si.hist[S.si.lsi[si]]);
+        if ((fl & SF_THINKER) && kind == IT_DECODE) notify(S, S.si.hist[lx_of<G>(S.si, si)]);
       }
       return;
     }
@@ -1354,7 +1377,7 @@ __device__ void cut_run(Sim &S, int x) {
       xt_set<true, XT_END>(S, x, t);
       itgt_set<true>(S, x, j);
       if (j < n) {
-        const int lx = S.si.lsi[si];
+        const int lx = lx_of<true>(S.si, si);
         const int slot = S.si.hist[lx];
         S.si.sched[slot] = S.si.iter[lx] + ((j + 1u) >> 1);
         notify(S, slot);
@@ -1373,7 +1396,7 @@ __device__ void cut_run(Sim &S, int x) {
   itgt_set<G>(S, x, j);
   if (j <= it0 + 1u) sh.ex_st[x] = st & ~EX_RUN;
   if constexpr (G) {
-    if ((S.si.flags[si] & SF_THINKER) && j < itgt) {
+    if ((si_flags<G>(S.si, si) & SF_THINKER) && j < itgt) {
       const int slot = S.si.hist[lx];
       S.si.sched[slot] = j;
       notify(S, slot);
@@ -1394,7 +1417,7 @@ __device__ void run_compact(Sim &S, int si, const bool *drop) {
   const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
   const GPtr<uint32_t> rg = S.run_g + (uint32_t)S.si.roff[lx];
   const GPtr<uint32_t> rq = S.run_q + (uint32_t)S.si.roff[lx];
-  const bool gated = G && (S.si.flags[si] & SF_GATED);  // k_fine<true>: gate words move with their slots
+  const bool gated = G && (si_flags<G>(S.si, si) & SF_GATED);  // k_fine<true>: gate words move with their slots
   uint32_t vr[CF_MAX_BATCH / 64], vk[CF_MAX_BATCH / 64], vg[CF_MAX_BATCH / 64], vq[CF_MAX_BATCH / 64];
   bool keep[CF_MAX_BATCH / 64];
 #pragma unroll
@@ -1434,7 +1457,7 @@ __device__ void run_compact(Sim &S, int si, const bool *drop) {
   }
   __syncthreads();
   S.si.rn[lx] = (int)w;
-  if (!(S.si.flags[si] & SF_GATED)) S.si.minfin[lx] = dpp_min_u32(mn);
+  if (!(si_flags<G>(S.si, si) & SF_GATED)) S.si.minfin[lx] = dpp_min_u32(mn);
 }
 
 // collects the running slots flagged in fin[] (slot order) into mem,
@@ -1475,15 +1498,15 @@ __device__ __forceinline__ void complete_joint(Sim &S, int x, uint32_t st) {
   xt_set<true, XT_LAST>(S, x, S.now);
   S.dirty |= 1ull << x;
   // thinker
-  const int lx = S.si.lsi[sth];
-  const int cth = S.si.comp[sth];
+  const int lx = lx_of<true>(S.si, sth);
+  const int cth = si_comp<true>(S.si, sth);
   const int rn = S.si.rn[lx];
   const uint32_t it = S.si.iter[lx] + nth_s;
   S.si.iter[lx] = it;
   S.events += (uint64_t)rn * (uint64_t)nth_s;
   // talker
-  const int lg = S.si.lsi[sta];
-  const int cta = S.si.comp[sta];
+  const int lg = lx_of<true>(S.si, sta);
+  const int cta = si_comp<true>(S.si, sta);
   const int rng = S.si.rn[lg];
   const GPtr<uint32_t> rkg = S.run_k + (uint32_t)S.si.roff[lg];
   bool fin[CF_MAX_BATCH / 64];
@@ -1530,8 +1553,8 @@ __device__ __forceinline__ void complete_iter(Sim &S, int x) {
     }
   }
   const int si = (int)(sh.ex_geo[x] & 0xFFFFu) + l;
-  const int c = S.si.comp[si];
-  const uint8_t fl = S.si.flags[si];
+  const int c = si_comp<G>(S.si, si);
+  const uint32_t fl = si_flags<G>(S.si, si);
   sh.ex_st[x] = (st & ~(1u | EX_RUN)) | 2u;  // idle, has run
   xt_set<G, XT_LAST>(S, x, S.now);
   S.dirty |= 1ull << x;
@@ -1609,8 +1632,8 @@ __device__ __forceinline__ bool gate_wake(Sim &S, int y) {
     const int ns = (int)((geo >> 16) & 0xFFu), first = (int)(geo & 0xFFFFu);
     bool undecided = false;
     for (int g = first; g < first + ns; g++) {
-      if (!(S.si.flags[g] & SF_GATED)) continue;
-      const int lg = S.si.lsi[g];
+      if (!(si_flags<true>(S.si, g) & SF_GATED)) continue;
+      const int lg = lx_of<true>(S.si, g);
       const int rn = S.si.rn[lg];
       const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lg];
       const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lg];
@@ -1789,11 +1812,14 @@ __device__ bool setup_plan(Sim &S, int p) {
     const uint32_t ho = wave_excl_scan(thk ? 1u : 0u, tot_h);
     if constexpr (G) lo = wave_excl_scan(llm ? 1u : 0u, tot_l);
     if (s < nsi) {
-      S.si.comp[s] = (uint8_t)c;
-      S.si.flags[s] = (uint8_t)((llm ? SF_LLM : 0) | (((m.gated_mask >> c) & 1u) ? SF_GATED : 0) |
-                                (thk ? SF_THINKER : 0) | (m.kind[c] == CF_ENC ? SF_ENC : 0) |
-                                (m.kind[c] == CF_GEN ? SF_GEN : 0));
-      S.si.beff[s] = (uint16_t)beff;
+      const uint32_t fl = (llm ? SF_LLM : 0) | (((m.gated_mask >> c) & 1u) ? SF_GATED : 0) |
+                          (thk ? SF_THINKER : 0) | (m.kind[c] == CF_ENC ? SF_ENC : 0) |
+                          (m.kind[c] == CF_GEN ? SF_GEN : 0);
+      if constexpr (!G) {
+        S.si.comp[s] = (uint8_t)c;
+        S.si.flags[s] = (uint8_t)fl;
+        S.si.beff[s] = (uint16_t)beff;
+      }
       S.si.qn[s] = 0;
       if constexpr (G) {
         S.si.qh[s] = qend(-1, 0);
@@ -1806,7 +1832,7 @@ __device__ bool setup_plan(Sim &S, int p) {
       }
       if constexpr (G) {
         const int ls = l_carry + (int)lo, slot = hs_carry + (int)ho;
-        S.si.lsi[s] = llm ? (uint16_t)ls : (uint16_t)0xFFFFu;
+        S.si.word[s] = fl | ((uint32_t)c << 8) | ((uint32_t)beff << 12) | ((llm ? (uint32_t)ls : kNoLsi) << 21);
         if (llm) {
           S.si.rn[ls] = 0;
           S.si.iter[ls] = 0;
@@ -1864,11 +1890,8 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
       S.si.iter = (uint32_t *)p; p += 4 * lcap;
       S.si.minfin = (uint32_t *)p; p += 4 * lcap;
       S.si.sched = (uint32_t *)p; p += 4 * tcap;
-      S.si.beff = (uint16_t *)p; p += 2 * cap;
-      S.si.lsi = (uint16_t *)p; p += 2 * cap;
+      S.si.word = (uint32_t *)p; p += 4 * cap;
       S.si.hist = (int16_t *)p; p += 2 * lcap;
-      S.si.comp = (uint8_t *)p; p += cap;
-      S.si.flags = (uint8_t *)p; p += cap;
     } else {
       S.si.qhc = (int *)p; p += 4 * cap;
       S.si.qtc = (int *)p; p += 4 * cap;
