@@ -158,8 +158,9 @@ struct ModelLds {
 
 struct WaveShared {
   uint32_t ex_st[CF_MAX_EXEC];  // busy:1 ran:1 kind:2 rr:4 cur:4 nmem:9
-  // an executor's first stage instance (bits 0..15), its stage count (bits
-  // 16..23) and its node (bits 24..31): one LDS word read at once
+  // an executor's first stage instance (bits 0..15), its node's component set
+  // (bits 16..23: its stages in component order) and its node (bits 24..31):
+  // one LDS word read at once
   uint32_t ex_geo[CF_MAX_EXEC];
   uint8_t ex_tp[CF_MAX_EXEC];  // GPUs per executor as min(g, 8) - 1 (iteration-time multiplier index)
   uint8_t route[CF_MAX_TYPES][2][CF_MAX_COMP];
@@ -465,8 +466,7 @@ __device__ __forceinline__ int ex_byte(uint64_t ex, int c) { return (int)((ex >>
 __device__ __forceinline__ int rtype(uint32_t misc) { return (int)((misc >> 8) & 7u); }
 __device__ __forceinline__ int stage_of(const Sim &S, int x, int c) {
   const uint32_t geo = S.sh->ex_geo[x];
-  const int v = (int)(geo >> 24);
-  return (int)(geo & 0xFFFFu) + __popc((uint32_t)S.sh->vcomp[v] & ((1u << c) - 1u));
+  return (int)(geo & 0xFFFFu) + __popc((geo >> 16) & 0xFFu & ((1u << c) - 1u));
 }
 
 // ------------------------------------------------------------------ pool / queues
@@ -1219,7 +1219,7 @@ struct GateView {
 };
 __device__ __forceinline__ GateView local_gate_view(const Sim &S, int x, int si) {
   const uint32_t geo = S.sh->ex_geo[x];
-  const int ns = (int)((geo >> 16) & 0xFFu), first = (int)(geo & 0xFFFFu);
+  const int ns = __popc((geo >> 16) & 0xFFu), first = (int)(geo & 0xFFFFu);
   const int lth = lx_of<true>(S.si, si);
   const uint32_t next = S.si.iter[lth] + 1u;
   uint32_t qmin = kNone, kta = kNone;
@@ -1313,7 +1313,7 @@ __device__ __forceinline__ void try_start(Sim &S, int x) {
   WaveShared &sh = *S.sh;
   const uint32_t st = sh.ex_st[x];
   const uint32_t geo = sh.ex_geo[x];
-  const int ns = (int)((geo >> 16) & 0xFFu), first = (int)(geo & 0xFFFFu);
+  const int ns = __popc((geo >> 16) & 0xFFu), first = (int)(geo & 0xFFFFu);
   const int rr = (st >> 4) & 15u;
   for (int i = 0; i < ns; i++) {
     int l = (rr == 15) ? i : rr + 1 + i;  // rr < ns, i < ns
@@ -1629,7 +1629,7 @@ __device__ __forceinline__ bool gate_wake(Sim &S, int y) {
   bool now_el = false;
   if (!(st & 1u) || (st & EX_RUN)) {
     const uint32_t geo = sh.ex_geo[y];
-    const int ns = (int)((geo >> 16) & 0xFFu), first = (int)(geo & 0xFFFFu);
+    const int ns = __popc((geo >> 16) & 0xFFu), first = (int)(geo & 0xFFFFu);
     bool undecided = false;
     for (int g = first; g < first + ns; g++) {
       if (!(si_flags<true>(S.si, g) & SF_GATED)) continue;
@@ -1773,7 +1773,7 @@ __device__ bool setup_plan(Sim &S, int p) {
       const uint32_t g = second ? A.node_gpus2[v * P + p] : A.node_gpus[v * P + p];
       sh.ex_tp[lane] = (uint8_t)(g < 1 ? 0 : (g > 8 ? 7 : g - 1));
     }
-    sh.ex_geo[lane] = (uint32_t)first | ((uint32_t)__popc(sh.vcomp[v]) << 16) | ((uint32_t)v << 24);
+    sh.ex_geo[lane] = (uint32_t)first | ((uint32_t)sh.vcomp[v] << 16) | ((uint32_t)v << 24);
     sh.ex_st[lane] = 15u << 4;  // idle, never ran, no stage run yet
     if constexpr (!G) {
       S.xt[XT_END * CF_MAX_EXEC + lane] = __builtin_inf();
