@@ -1496,6 +1496,7 @@ __device__ __forceinline__ void complete_joint(Sim &S, int x, uint32_t st) {
   const uint32_t llast = (n & 1u) ? (uint32_t)lth : (uint32_t)lta;
   sh.ex_st[x] = (st & ~(1u | EX_RUN | (15u << 4) | (15u << 22))) | 2u | (llast << 4);
   xt_set<true, XT_LAST>(S, x, S.now);
+  xt_set<true, XT_END>(S, x, __builtin_inf());  // idle: no pending end
   S.dirty |= 1ull << x;
   // thinker
   const int lx = lx_of<true>(S.si, sth);
@@ -1557,6 +1558,7 @@ __device__ __forceinline__ void complete_iter(Sim &S, int x) {
   const uint32_t fl = si_flags<G>(S.si, si);
   sh.ex_st[x] = (st & ~(1u | EX_RUN)) | 2u;  // idle, has run
   xt_set<G, XT_LAST>(S, x, S.now);
+  xt_set<G, XT_END>(S, x, __builtin_inf());  // idle: no pending end
   S.dirty |= 1ull << x;
   if (kind == IT_BATCH || kind == IT_PREFILL) {
     S.events += (uint64_t)nmem;
@@ -1998,7 +2000,8 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
       for (;;) {
         // --- next pending time
         double te = __builtin_inf();
-        if (lane < S.nx && (sh.ex_st[lane] & 1u)) te = xt_own<G, XT_END>(S);
+        // an idle executor's end is +inf (so are the lanes past the plan's executors)
+        if (lane < S.nx) te = xt_own<G, XT_END>(S);
         if constexpr (G) {
           if (lane < S.nx) {
             const double wk = S.r_wake;
@@ -2016,7 +2019,7 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
         }
         // --- step 1: iterations ending at t, ascending executor
         if (te == t) {
-          uint64_t done = __ballot(lane < S.nx && (sh.ex_st[lane] & 1u) && xt_own<G, XT_END>(S) == t);
+          uint64_t done = __ballot(lane < S.nx && xt_own<G, XT_END>(S) == t);
           if constexpr (G) {
             // wake times due: the executor examines its stages in step 3
             const bool wk = lane < S.nx && S.r_wake == t;
