@@ -102,9 +102,15 @@ struct __attribute__((aligned(32))) Tim {
   double tfirst, tlast, tmedia;
   uint32_t thjoin, pad;
 };
+// a request's record and times side by side: one 64-byte block holds both
+struct __attribute__((aligned(64))) Req {
+  Rec r;
+  Tim t;
+};
+static_assert(sizeof(Req) == 64, "request block");
 
 struct Layout {
-  size_t rec, tim;
+  size_t req;
   size_t run_r, run_k, run_g, run_q, hist, mem, dl_t, dl_v, pool, pool_next, pool_free;
   size_t bytes;
   int run_cap, hist_slots, n_chunks;
@@ -336,8 +342,7 @@ struct Sim {
   const FineArgs *A;
   WaveShared *sh;
   SiLds si;
-  GPtr<Rec> rec;
-  GPtr<Tim> tim;
+  GPtr<Req> req;
   GPtr<double> hist, dl_t;
   GPtr<uint32_t> run_r, run_k, run_g, run_q, mem, dl_v, pool;
   GPtr<int> pool_next, pool_free;
@@ -416,7 +421,7 @@ __device__ __forceinline__ double xt_own(const Sim &S) {
 }
 
 __device__ __forceinline__ Rec rec_get(const Sim &S, uint32_t r) {
-  CF_GLOBAL Rec &q = S.rec[r];
+  CF_GLOBAL Rec &q = S.req[r].r;
   Rec R;
   R.ex = q.ex;
   R.join = q.join;
@@ -424,7 +429,7 @@ __device__ __forceinline__ Rec rec_get(const Sim &S, uint32_t r) {
   return R;
 }
 __device__ __forceinline__ void rec_put(const Sim &S, uint32_t r, const Rec &R) {
-  CF_GLOBAL Rec &q = S.rec[r];
+  CF_GLOBAL Rec &q = S.req[r].r;
   q.ex = R.ex;
   q.join = R.join;
   q.misc = R.misc;
@@ -631,12 +636,12 @@ __device__ __forceinline__ bool token_visible(const Sim &S, uint32_t r, uint32_t
   const double delta = (xth == x) ? 0.0 : S.A->m.comm;
   double e;
   if (k <= 1) {
-    e = S.tim[r].tfirst;
+    e = S.req[r].t.tfirst;
   } else if ((misc & MISC_TH_DONE) && k == nth) {
-    e = S.tim[r].tlast;
+    e = S.req[r].t.tlast;
   } else {
     const int si = stage_of(S, xth, th);
-    const uint32_t q = S.tim[r].thjoin + k - 1u;
+    const uint32_t q = S.req[r].t.thjoin + k - 1u;
     const uint32_t it = S.si.iter[si];
     if (q > it) return false;
     const GPtr<double> h = S.hist + (uint32_t)(S.si.hist[si] * kHist);
@@ -674,13 +679,13 @@ __device__ __forceinline__ double token_vis(const Sim &S, uint32_t r, uint32_t m
   wsi = -1;
   double e;
   if (k <= 1) {
-    e = S.tim[r].tfirst;
+    e = S.req[r].t.tfirst;
   } else if ((misc & MISC_TH_DONE) && k == nth) {
-    e = S.tim[r].tlast;
+    e = S.req[r].t.tlast;
   } else {
     const int lx = lx_of<true>(S.si, stage_of(S, xth, th));
     const int slot = S.si.hist[lx];
-    const uint32_t q = S.tim[r].thjoin + k - 1u;
+    const uint32_t q = S.req[r].t.thjoin + k - 1u;
     if (q > S.si.sched[slot]) {
       wsi = slot;
       return __builtin_inf();
@@ -736,7 +741,7 @@ __device__ __forceinline__ double slot_vis_g(const Sim &S, uint32_t r, uint32_t 
   const double delta = (xth == x) ? 0.0 : S.A->m.comm;
   double e;
   if (k <= 1) {
-    e = S.tim[r].tfirst;
+    e = S.req[r].t.tfirst;
   } else {
     const int lx = (int)((g >> 22) & 511u);
     const int slot = S.si.hist[lx];
@@ -752,8 +757,8 @@ __device__ __forceinline__ double slot_vis_g(const Sim &S, uint32_t r, uint32_t 
       e = h[q & (kRing - 1)];
     } else if (it - q < (uint32_t)kKeep) {
       e = h[q & (kRing - 1)];
-    } else if (k == nth && (S.rec[r].misc & MISC_TH_DONE)) {
-      e = S.tim[r].tlast;
+    } else if (k == nth && (S.req[r].r.misc & MISC_TH_DONE)) {
+      e = S.req[r].t.tlast;
     } else {
       e = h[(it - (kKeep - 1)) & (kRing - 1)];  // oldest kept step: token k is no later
       if (!(e + delta <= S.now)) {
@@ -840,7 +845,7 @@ __device__ void dl_deliver(Sim &S, uint32_t r, int c2) {
   const uint64_t ex = ru64(R.ex);
   const uint32_t join = ru(R.join) + (1u << (4 * c2));
   const uint32_t misc = ru(R.misc);
-  if (lane_id() == 0) S.rec[r].join = join;
+  if (lane_id() == 0) S.req[r].r.join = join;
   const int t = rtype(misc);
   if (((join >> (4 * c2)) & 15u) == S.A->m.npar[t][c2]) enqueue1<G>(S, r, c2, ex_byte(ex, c2));
 }
@@ -881,11 +886,11 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
     if (valid && kind == IT_PREFILL) {
       const uint32_t no = ((ml.pfo[t] >> c) & 1u) ? 1u : (a_no < 1u ? 1u : a_no);  // nout_of(S, r, t, c)
       if (c == ml.ttft_c[t]) {
-        S.tim[r].tfirst = now;
-        S.tim[r].tlast = now;
+        S.req[r].t.tfirst = now;
+        S.req[r].t.tlast = now;
       }
       if (c == ml.th_c[t]) {
-        S.tim[r].thjoin = iter_s;
+        S.req[r].t.thjoin = iter_s;
         stream = true;
         ta = ml.ta_c[t];
       }
@@ -895,10 +900,10 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
         const int th = ml.th_c[t], xth = ex_byte(R.ex, th);
         gw = RG_GATED | ((uint32_t)lx_of<G>(S.si, stage_of(S, xth, th)) << 22) | ((uint32_t)xth << 16) |
              nout_of(S, r, t, th);
-        gq = S.tim[r].thjoin;
+        gq = S.req[r].t.thjoin;
       }
     } else if (valid && kind == IT_FINISH) {
-      if (c == ml.ttft_c[t]) S.tim[r].tlast = now;
+      if (c == ml.ttft_c[t]) S.req[r].t.tlast = now;
     }
     const bool append = valid && kind == IT_PREFILL && !fin;
     // delayed deliveries: the streaming one first, then remote children
@@ -957,14 +962,14 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
     if (fin && valid) {
       if (c == ml.th_c[t]) misc |= MISC_TH_DONE;
       if ((ml.outm[t] >> c) & 1u) {
-        if (ml.kind[c] == CF_GEN) S.tim[r].tmedia = now;
+        if (ml.kind[c] == CF_GEN) S.req[r].t.tmedia = now;
         misc -= 1u;
         done = (misc & MISC_OUTS) == 0;
       }
     }
     if (valid) {
-      S.rec[r].join = join;
-      S.rec[r].misc = misc;
+      S.req[r].r.join = join;
+      S.req[r].r.misc = misc;
     }
     // running-set appends (prefill), in member order
     const uint64_t abal = __ballot(append);
@@ -1005,13 +1010,13 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
         double ttft = 0.0, tpot = 0.0, media = 0.0;
         const int tc = ml.ttft_c[t];
         if (tc >= 0) {
-          const double tf = S.tim[r].tfirst;
+          const double tf = S.req[r].t.tfirst;
           ttft = tf - a;
           const uint32_t n1 = nout_of(S, r, t, tc);
-          if (n1 > 1) tpot = (S.tim[r].tlast - tf) / (double)(n1 - 1);
+          if (n1 > 1) tpot = (S.req[r].t.tlast - tf) / (double)(n1 - 1);
         }
         const double e2e = now - a;
-        if (ml.gen_out[t]) media = S.tim[r].tmedia - a;
+        if (ml.gen_out[t]) media = S.req[r].t.tmedia - a;
         ok = ttft <= ml.slo[t][0] && tpot <= ml.slo[t][1] && e2e <= ml.slo[t][2] && media <= ml.slo[t][3];
         if (S.hrow) hbin = target_bin(S.A->tg, S.A->nb, t, ttft, tpot, e2e, media);
         if (S.lat_slot >= 0) {
@@ -1932,8 +1937,7 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
   if (lane < CF_MAX_TYPES * 4) (&sh.ml.slo[0][0])[lane] = (&m.slo[0][0])[lane];
   char *slab = A.slab + (size_t)blockIdx.x * A.L.bytes;
   const Layout &L = A.L;
-  S.rec = gptr_at<Rec>(slab, L.rec);
-  S.tim = gptr_at<Tim>(slab, L.tim);
+  S.req = gptr_at<Req>(slab, L.req);
   S.run_r = gptr_at<uint32_t>(slab, L.run_r);
   S.run_k = gptr_at<uint32_t>(slab, L.run_k);
   S.run_g = gptr_at<uint32_t>(slab, L.run_g);
@@ -2175,8 +2179,7 @@ Layout make_layout(const KModel &m, int n) {
   }
   L.run_cap = CF_MAX_EXEC * per_exec_run;
   L.hist_slots = CF_MAX_EXEC * n_th;
-  L.rec = take(sizeof(Rec) * (size_t)n);
-  L.tim = take(sizeof(Tim) * (size_t)n);
+  L.req = take(sizeof(Req) * (size_t)n);
   L.run_r = take(4 * (size_t)L.run_cap);
   L.run_k = take(4 * (size_t)L.run_cap);
   L.run_g = take(4 * (size_t)L.run_cap);
