@@ -111,7 +111,7 @@ static_assert(sizeof(Req) == 64, "request block");
 
 struct Layout {
   size_t req;
-  size_t run_r, run_k, run_g, run_q, hist, mem, dl_t, dl_v, pool, pool_next, pool_free;
+  size_t run, hist, mem, dl_t, dl_v, pool, pool_next, pool_free;
   size_t bytes;
   int run_cap, hist_slots, n_chunks;
   uint32_t dl_mask;
@@ -332,6 +332,18 @@ template <typename T>
 __device__ __forceinline__ GPtr<T> gptr_at(char *base, size_t off) {
   return GPtr<T>{(CF_GLOBAL T *)(base + off)};
 }
+// One word of the running slots, which lie interleaved in the slab
+// (k_fine<true>: request, key, gate word, join step; k_fine<false>: request,
+// key): slot i's word is 4 << sh bytes after slot i - 1's, so a slot's words
+// share a cache line.
+struct SlotPtr {
+  CF_GLOBAL uint32_t *p;
+  uint32_t sh;
+  __device__ __forceinline__ CF_GLOBAL uint32_t &operator[](uint32_t i) const {
+    return *(CF_GLOBAL uint32_t *)((CF_GLOBAL char *)p + ((i << sh) << 2));
+  }
+  __device__ __forceinline__ SlotPtr operator+(uint32_t i) const { return SlotPtr{&(*this)[i], sh}; }
+};
 // element o of a read-only input array
 template <typename T>
 __device__ __forceinline__ T gload(const T *p, size_t o) {
@@ -344,7 +356,8 @@ struct Sim {
   SiLds si;
   GPtr<Req> req;
   GPtr<double> hist, dl_t;
-  GPtr<uint32_t> run_r, run_k, run_g, run_q, mem, dl_v, pool;
+  SlotPtr run_r, run_k, run_g, run_q;
+  GPtr<uint32_t> mem, dl_v, pool;
   GPtr<int> pool_next, pool_free;
   size_t soff;
   double lam, now, dl_head_t, t_arr;
@@ -1115,10 +1128,10 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
   } else {
     // gated stage: mark the eligible running requests
     const int rn = S.si.rn[lx];
-    const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lx];
-    const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
-    const GPtr<uint32_t> rg = S.run_g + (uint32_t)S.si.roff[lx];
-    const GPtr<uint32_t> rq = S.run_q + (uint32_t)S.si.roff[lx];
+    const SlotPtr rr = S.run_r + (uint32_t)S.si.roff[lx];
+    const SlotPtr rk = S.run_k + (uint32_t)S.si.roff[lx];
+    const SlotPtr rg = S.run_g + (uint32_t)S.si.roff[lx];
+    const SlotPtr rq = S.run_q + (uint32_t)S.si.roff[lx];
     uint32_t cntm = 0;
     if (G && S.gmark_si == si) {
       cntm = S.gmark_n;  // marked by runnable_kind in this instant
@@ -1175,10 +1188,10 @@ __device__ int runnable_kind(Sim &S, int x, int si, int c) {
   if (qn > 0 && rn < beff) return IT_PREFILL;
   if (rn == 0) return -1;
   if (!(fl & SF_GATED)) return IT_DECODE;
-  const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lx];
-  const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
-  const GPtr<uint32_t> rg = S.run_g + (uint32_t)S.si.roff[lx];
-  const GPtr<uint32_t> rq = S.run_q + (uint32_t)S.si.roff[lx];
+  const SlotPtr rr = S.run_r + (uint32_t)S.si.roff[lx];
+  const SlotPtr rk = S.run_k + (uint32_t)S.si.roff[lx];
+  const SlotPtr rg = S.run_g + (uint32_t)S.si.roff[lx];
+  const SlotPtr rq = S.run_q + (uint32_t)S.si.roff[lx];
   bool any = false, undecided = false;
   if constexpr (G) {
     // k_fine<true>: mark every eligible slot now; a decode step started on
@@ -1237,9 +1250,9 @@ __device__ __forceinline__ GateView local_gate_view(const Sim &S, int x, int si)
     if (rn == 0) continue;
     nbusy++;
     gsi = g;
-    const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lg];
-    const GPtr<uint32_t> rg = S.run_g + (uint32_t)S.si.roff[lg];
-    const GPtr<uint32_t> rq = S.run_q + (uint32_t)S.si.roff[lg];
+    const SlotPtr rk = S.run_k + (uint32_t)S.si.roff[lg];
+    const SlotPtr rg = S.run_g + (uint32_t)S.si.roff[lg];
+    const SlotPtr rq = S.run_q + (uint32_t)S.si.roff[lg];
     for (int b = 0; b < rn; b += 64) {
       const int j = b + lane_id();
       if (j < rn) {
@@ -1418,10 +1431,10 @@ template <bool G>
 __device__ void run_compact(Sim &S, int si, const bool *drop) {
   const int lx = lx_of<G>(S.si, si);
   const int rn = S.si.rn[lx];
-  const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lx];
-  const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
-  const GPtr<uint32_t> rg = S.run_g + (uint32_t)S.si.roff[lx];
-  const GPtr<uint32_t> rq = S.run_q + (uint32_t)S.si.roff[lx];
+  const SlotPtr rr = S.run_r + (uint32_t)S.si.roff[lx];
+  const SlotPtr rk = S.run_k + (uint32_t)S.si.roff[lx];
+  const SlotPtr rg = S.run_g + (uint32_t)S.si.roff[lx];
+  const SlotPtr rq = S.run_q + (uint32_t)S.si.roff[lx];
   const bool gated = G && (si_flags<G>(S.si, si) & SF_GATED);  // k_fine<true>: gate words move with their slots
   uint32_t vr[CF_MAX_BATCH / 64], vk[CF_MAX_BATCH / 64], vg[CF_MAX_BATCH / 64], vq[CF_MAX_BATCH / 64];
   bool keep[CF_MAX_BATCH / 64];
@@ -1471,7 +1484,7 @@ template <bool G>
 __device__ void finish_slots(Sim &S, int x, int si, int c, const bool *fin) {
   const int lx = lx_of<G>(S.si, si);
   const int rn = S.si.rn[lx];
-  const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lx];
+  const SlotPtr rr = S.run_r + (uint32_t)S.si.roff[lx];
   const GPtr<uint32_t> mem = S.mem + (uint32_t)(x * CF_MAX_BATCH);
   uint32_t nf = 0;
 #pragma unroll
@@ -1514,7 +1527,7 @@ __device__ __forceinline__ void complete_joint(Sim &S, int x, uint32_t st) {
   const int lg = lx_of<true>(S.si, sta);
   const int cta = si_comp<true>(S.si, sta);
   const int rng = S.si.rn[lg];
-  const GPtr<uint32_t> rkg = S.run_k + (uint32_t)S.si.roff[lg];
+  const SlotPtr rkg = S.run_k + (uint32_t)S.si.roff[lg];
   bool fin[CF_MAX_BATCH / 64];
 #pragma unroll
   for (int p = 0; p < CF_MAX_BATCH / 64; p++) {
@@ -1531,7 +1544,7 @@ __device__ __forceinline__ void complete_joint(Sim &S, int x, uint32_t st) {
   __syncthreads();
   if (n & 1u) {
     if (it == S.si.minfin[lx]) {
-      const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
+      const SlotPtr rk = S.run_k + (uint32_t)S.si.roff[lx];
 #pragma unroll
       for (int p = 0; p < CF_MAX_BATCH / 64; p++) {
         const int j = p * 64 + lane_id();
@@ -1581,7 +1594,7 @@ __device__ __forceinline__ void complete_iter(Sim &S, int x) {
   if constexpr (!G) {
     if ((fl & SF_THINKER) && lane_id() == 0) S.hist[(uint32_t)(S.si.hist[si] * kHist) + (it & (kHist - 1))] = S.now;
   }
-  const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lx];
+  const SlotPtr rk = S.run_k + (uint32_t)S.si.roff[lx];
   if (!(fl & SF_GATED)) {
     S.events += (uint64_t)rn * (uint64_t)(it - it0);
     if (it == S.si.minfin[lx]) {
@@ -1642,10 +1655,10 @@ __device__ __forceinline__ bool gate_wake(Sim &S, int y) {
       if (!(si_flags<true>(S.si, g) & SF_GATED)) continue;
       const int lg = lx_of<true>(S.si, g);
       const int rn = S.si.rn[lg];
-      const GPtr<uint32_t> rr = S.run_r + (uint32_t)S.si.roff[lg];
-      const GPtr<uint32_t> rk = S.run_k + (uint32_t)S.si.roff[lg];
-      const GPtr<uint32_t> rg = S.run_g + (uint32_t)S.si.roff[lg];
-      const GPtr<uint32_t> rq = S.run_q + (uint32_t)S.si.roff[lg];
+      const SlotPtr rr = S.run_r + (uint32_t)S.si.roff[lg];
+      const SlotPtr rk = S.run_k + (uint32_t)S.si.roff[lg];
+      const SlotPtr rg = S.run_g + (uint32_t)S.si.roff[lg];
+      const SlotPtr rq = S.run_q + (uint32_t)S.si.roff[lg];
       for (int b = 0; b < rn; b += 64) {
         const int j = b + lane_id();
         if (j < rn) {
@@ -1938,10 +1951,15 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
   char *slab = A.slab + (size_t)blockIdx.x * A.L.bytes;
   const Layout &L = A.L;
   S.req = gptr_at<Req>(slab, L.req);
-  S.run_r = gptr_at<uint32_t>(slab, L.run_r);
-  S.run_k = gptr_at<uint32_t>(slab, L.run_k);
-  S.run_g = gptr_at<uint32_t>(slab, L.run_g);
-  S.run_q = gptr_at<uint32_t>(slab, L.run_q);
+  {
+    // running slots interleaved: 4 words per slot (k_fine<true>), 2 (k_fine<false>)
+    constexpr uint32_t sh = G ? 2u : 1u;
+    CF_GLOBAL uint32_t *run = (CF_GLOBAL uint32_t *)(slab + L.run);
+    S.run_r = SlotPtr{run, sh};
+    S.run_k = SlotPtr{run + 1, sh};
+    S.run_g = SlotPtr{G ? run + 2 : run, sh};
+    S.run_q = SlotPtr{G ? run + 3 : run, sh};
+  }
   S.hist = gptr_at<double>(slab, L.hist);
   S.mem = gptr_at<uint32_t>(slab, L.mem);
   S.dl_t = gptr_at<double>(slab, L.dl_t);
@@ -2180,10 +2198,7 @@ Layout make_layout(const KModel &m, int n) {
   L.run_cap = CF_MAX_EXEC * per_exec_run;
   L.hist_slots = CF_MAX_EXEC * n_th;
   L.req = take(sizeof(Req) * (size_t)n);
-  L.run_r = take(4 * (size_t)L.run_cap);
-  L.run_k = take(4 * (size_t)L.run_cap);
-  L.run_g = take(4 * (size_t)L.run_cap);
-  L.run_q = take(4 * (size_t)L.run_cap);
+  L.run = take((m.gated_mask ? 16 : 8) * (size_t)L.run_cap);
   L.hist = take(8 * (size_t)L.hist_slots * (m.gated_mask ? kRing : kHist) + 8);
   L.mem = take(4 * (size_t)CF_MAX_EXEC * CF_MAX_BATCH);
   size_t dl = 4096;
