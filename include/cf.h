@@ -277,10 +277,12 @@ cf_status cf_rate_grid(const double *rd_dev, const int32_t *ids_dev, int32_t n, 
  * *out (device arrays, caller-owned).  flags: CF_FULL, or CF_DUMP_LAT to
  * also write out->lat_dev for the out->n_lat triples listed in
  * out->lat_triples_dev (both required with the flag, ignored without it);
- * CF_EARLY_EXIT is not built and returns CF_EUNSUPPORTED.  Synchronises
- * the stream (the argument block is copied from host memory).
- * Errors: CF_EINVAL (descriptor, sizes, flags), CF_ECAPACITY, CF_ENOMEM,
- * CF_EUNSUPPORTED. */
+ * CF_EARLY_EXIT is not built and returns CF_EUNSUPPORTED.  Every array of
+ * *trace but n_img_dev is read (a request's lengths are copied beside its
+ * record when it arrives).  Synchronises the stream (the argument block is
+ * copied from host memory).
+ * Errors: CF_EINVAL (descriptor, sizes, flags, NULL trace arrays),
+ * CF_ECAPACITY, CF_ENOMEM, CF_EUNSUPPORTED. */
 cf_status cf_eval_fine(const cf_model_desc *model, const cf_plan_table *plans,
                        const int32_t *plan_ids_dev, int32_t n_plans, const double *rates_dev,
                        int32_t K, const cf_trace *trace, uint32_t flags, const cf_fine_out *out,

@@ -102,12 +102,15 @@ struct __attribute__((aligned(32))) Tim {
   double tfirst, tlast, tmedia;
   uint32_t thjoin, pad;
 };
-// a request's record and times side by side: one 64-byte block holds both
+// a request's record, its length attributes (copied from the trace at its
+// arrival) and its times side by side: one 64-byte block holds them all
 struct __attribute__((aligned(64))) Req {
   Rec r;
+  uint16_t prompt, out, patches, pad;
+  uint32_t aud_in, aud_out;
   Tim t;
 };
-static_assert(sizeof(Req) == 64, "request block");
+static_assert(sizeof(Req) == 64 && __builtin_offsetof(Req, t) == 32, "request block");
 
 struct Layout {
   size_t req;
@@ -449,17 +452,17 @@ __device__ __forceinline__ void rec_put(const Sim &S, uint32_t r, const Rec &R) 
 }
 
 // ------------------------------------------------------------------ trace
+// attribute a of arrived request r, from its block
 __device__ __forceinline__ uint32_t attr(const Sim &S, uint32_t r, int a) {
-  const size_t o = S.soff + r;
-  const FineArgs &A = *S.A;
+  const CF_GLOBAL Req &q = S.req[r];
   switch (a) {
-    case CF_ATTR_PROMPT: return gload(A.prompt, o);
-    case CF_ATTR_OUT: return gload(A.out, o);
-    case CF_ATTR_PATCHES: return gload(A.patches, o);
-    case CF_ATTR_AUDIN_MS: return gload(A.aud_in, o);
-    case CF_ATTR_AUDOUT_MS: return gload(A.aud_out, o);
-    case CF_ATTR_AUDIN_TOK: return (gload(A.aud_in, o) + 79u) / 80u;
-    case CF_ATTR_AUDOUT_TOK: return (gload(A.aud_out, o) + 79u) / 80u;
+    case CF_ATTR_PROMPT: return q.prompt;
+    case CF_ATTR_OUT: return q.out;
+    case CF_ATTR_PATCHES: return q.patches;
+    case CF_ATTR_AUDIN_MS: return q.aud_in;
+    case CF_ATTR_AUDOUT_MS: return q.aud_out;
+    case CF_ATTR_AUDIN_TOK: return (q.aud_in + 79u) / 80u;
+    case CF_ATTR_AUDOUT_TOK: return (q.aud_out + 79u) / 80u;
     default: return 0;
   }
 }
@@ -815,6 +818,8 @@ __device__ void arrive(Sim &S, uint32_t r) {
   const uint8_t tv = gload(A.type, o);
   const uint64_t k0v = gload(A.rkey0, o), k1v = gload(A.rkey1, o);
   const uint32_t akv = gload(A.akey, o);
+  const uint16_t prv = gload(A.prompt, o), ouv = gload(A.out, o), pav = gload(A.patches, o);
+  const uint32_t aiv = gload(A.aud_in, o), aov = gload(A.aud_out, o);
   const int t = ri(tv);
   if (t >= m.nt) {
     S.status |= CF_ST_INVALID;
@@ -842,7 +847,16 @@ __device__ void arrive(Sim &S, uint32_t r) {
   R.ex = ex;
   R.join = 0;
   R.misc = (uint32_t)__popc(m.outm[t]) | ((uint32_t)t << 8);
-  if (lane_id() == 0) rec_put(S, r, R);
+  if (lane_id() == 0) {
+    rec_put(S, r, R);
+    // the length attributes, read by the stages from the request's block
+    CF_GLOBAL Req &q = S.req[r];
+    q.prompt = prv;
+    q.out = ouv;
+    q.patches = pav;
+    q.aud_in = aiv;
+    q.aud_out = aov;
+  }
   uint32_t src = m.srcm[t];
   while (src) {
     const int c = __ffs(src) - 1;
@@ -2260,6 +2274,10 @@ cf_status eval_fine(const cf_model_desc *model, const cf_plan_table *plans, cons
   cf_status st = lower_model(model, &a.m);
   if (st != CF_OK) return st;
   if (!plans || !trace || !out) return set_error(CF_EINVAL, "NULL argument");
+  if (trace->n_req > 0 && (!trace->arr_ticks_dev || !trace->type_dev || !trace->patches_dev || !trace->prompt_dev ||
+                           !trace->out_dev || !trace->aud_in_ms_dev || !trace->aud_out_ms_dev ||
+                           !trace->rkey0_dev || !trace->rkey1_dev || !trace->akey_dev))
+    return set_error(CF_EINVAL, "NULL trace array");
   if (flags & ~(CF_DUMP_LAT | CF_EARLY_EXIT)) return set_error(CF_EINVAL, "unknown flags");
   if (flags & CF_EARLY_EXIT) return set_error(CF_EUNSUPPORTED, "CF_EARLY_EXIT is not built");
   const bool dump = (flags & CF_DUMP_LAT) != 0;
