@@ -231,3 +231,13 @@ def test_bad_limits_and_flags_are_rejected(cf):
     for lim in ({"delay": 3}, {"delay": 1}, {"chunks": -1}):
         with pytest.raises(cf.CfError):
             cf.cf_eval_fine(desc, cf.DevicePlans(tab), ids, rates, tr, limits=lim)
+    # every trace array the simulation reads must be given
+    for f in ("aud_out_ms", "prompt", "akey"):
+        saved = getattr(tr.c, f + "_dev")
+        setattr(tr.c, f + "_dev", None)
+        try:
+            with pytest.raises(cf.CfError, match="NULL trace array"):
+                cf.cf_eval_fine(desc, cf.DevicePlans(tab), ids, rates, tr)
+        finally:
+            setattr(tr.c, f + "_dev", saved)
+    cf.cf_eval_fine(desc, cf.DevicePlans(tab), ids, rates, tr)
