@@ -102,6 +102,11 @@ struct __attribute__((aligned(32))) Tim {
   double tfirst, tlast, tmedia;
   uint32_t thjoin, pad;
 };
+// a delay-line entry: due time and what is delivered (one 16-byte block)
+struct __attribute__((aligned(16))) DlEnt {
+  double t;
+  uint32_t v, pad;
+};
 // a request's record, its length attributes (copied from the trace at its
 // arrival) and its times side by side: one 64-byte block holds them all
 struct __attribute__((aligned(64))) Req {
@@ -114,7 +119,7 @@ static_assert(sizeof(Req) == 64 && __builtin_offsetof(Req, t) == 32, "request bl
 
 struct Layout {
   size_t req;
-  size_t run, hist, mem, dl_t, dl_v, pool, pool_next, pool_free;
+  size_t run, hist, mem, dl, pool, pool_next, pool_free;
   size_t bytes;
   int run_cap, hist_slots, n_chunks;
   uint32_t dl_mask;
@@ -358,9 +363,10 @@ struct Sim {
   WaveShared *sh;
   SiLds si;
   GPtr<Req> req;
-  GPtr<double> hist, dl_t;
+  GPtr<double> hist;
+  GPtr<DlEnt> dl;
   SlotPtr run_r, run_k, run_g, run_q;
-  GPtr<uint32_t> mem, dl_v, pool;
+  GPtr<uint32_t> mem, pool;
   GPtr<int> pool_next, pool_free;
   size_t soff;
   double lam, now, dl_head_t, t_arr;
@@ -639,8 +645,8 @@ __device__ __forceinline__ void dl_push1(Sim &S, double due, uint32_t v) {
     return;
   }
   if (lane_id() == 0) {
-    S.dl_t[S.dl_tail & S.A->L.dl_mask] = due;
-    S.dl_v[S.dl_tail & S.A->L.dl_mask] = v;
+    S.dl[S.dl_tail & S.A->L.dl_mask].t = due;
+    S.dl[S.dl_tail & S.A->L.dl_mask].v = v;
   }
   if (S.dl_head == S.dl_tail) S.dl_head_t = due;
   S.dl_tail++;
@@ -832,16 +838,20 @@ __device__ void arrive(Sim &S, uint32_t r) {
     const uint64_t w0 = sh.aw[t][0], w1 = sh.aw[t][1];
     alt = ((((uint64_t)ak) * (w0 + w1)) >> 32) < w0 ? 0 : 1;
   }
-  uint64_t ex = ~0ull;
-  uint32_t path = m.path[t];
-  while (path) {
-    const int c = __ffs(path) - 1;
-    path &= path - 1;
-    const int v = sh.route[t][alt][c];
+  // the executor of every component of the path at once, lane c for component c
+  const uint32_t path = m.path[t];
+  uint32_t xl = 0xFFu;
+  if (lane_id() < CF_MAX_COMP && ((path >> lane_id()) & 1u)) {
+    const int v = sh.route[t][alt][lane_id()];
     const int mc = sh.vminc[v];
     const uint64_t key = ((mc < 4 ? k0 : k1) >> (16 * (mc & 3))) & 0xFFFFull;
-    const int x = sh.vbase[v] + node_exec((uint32_t)key, sh.vrep1[v], (uint32_t)(sh.vrep[v] - sh.vrep1[v]), sh.vw[v]);
-    ex = (ex & ~(0xFFull << (8 * c))) | ((uint64_t)x << (8 * c));
+    xl = sh.vbase[v] + node_exec((uint32_t)key, sh.vrep1[v], (uint32_t)(sh.vrep[v] - sh.vrep1[v]), sh.vw[v]);
+  }
+  uint64_t ex = ~0ull;
+  for (uint32_t pc = path; pc; pc &= pc - 1) {
+    const int c = __ffs(pc) - 1;
+    const uint64_t x = (uint32_t)__builtin_amdgcn_readlane((int)xl, c);
+    ex = (ex & ~(0xFFull << (8 * c))) | (x << (8 * c));
   }
   Rec R;
   R.ex = ex;
@@ -961,15 +971,15 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
       const double due = now + m.comm;
       uint32_t pos = S.dl_tail + dl_off;
       if (stream_remote) {
-        S.dl_t[pos & S.A->L.dl_mask] = due;
-        S.dl_v[pos & S.A->L.dl_mask] = (r << 4) | (DL_DELIVER << 3) | (uint32_t)ta;
+        S.dl[pos & S.A->L.dl_mask].t = due;
+        S.dl[pos & S.A->L.dl_mask].v = (r << 4) | (DL_DELIVER << 3) | (uint32_t)ta;
         pos++;
       }
       for (uint32_t cc = rc; cc;) {
         const int c2 = __ffs(cc) - 1;
         cc &= cc - 1;
-        S.dl_t[pos & S.A->L.dl_mask] = due;
-        S.dl_v[pos & S.A->L.dl_mask] = (r << 4) | (DL_DELIVER << 3) | (uint32_t)c2;
+        S.dl[pos & S.A->L.dl_mask].t = due;
+        S.dl[pos & S.A->L.dl_mask].v = (r << 4) | (DL_DELIVER << 3) | (uint32_t)c2;
         pos++;
       }
       if (S.dl_head == S.dl_tail) S.dl_head_t = due;
@@ -1976,8 +1986,7 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
   }
   S.hist = gptr_at<double>(slab, L.hist);
   S.mem = gptr_at<uint32_t>(slab, L.mem);
-  S.dl_t = gptr_at<double>(slab, L.dl_t);
-  S.dl_v = gptr_at<uint32_t>(slab, L.dl_v);
+  S.dl = gptr_at<DlEnt>(slab, L.dl);
   S.pool = gptr_at<uint32_t>(slab, L.pool);
   S.pool_next = gptr_at<int>(slab, L.pool_next);
   S.pool_free = gptr_at<int>(slab, L.pool_free);
@@ -2070,9 +2079,9 @@ __global__ void __launch_bounds__(64, G ? 4 : 7) k_fine(const FineArgs *__restri
         }
         // --- step 2: delayed deliveries due at t (production order), then arrivals at t
         while (S.dl_head != S.dl_tail && S.dl_head_t == t) {
-          const uint32_t v = ru(S.dl_v[S.dl_head & L.dl_mask]);
+          const uint32_t v = ru(S.dl[S.dl_head & L.dl_mask].v);
           S.dl_head++;
-          S.dl_head_t = S.dl_head != S.dl_tail ? rdb(S.dl_t[S.dl_head & L.dl_mask]) : __builtin_inf();
+          S.dl_head_t = S.dl_head != S.dl_tail ? rdb(S.dl[S.dl_head & L.dl_mask].t) : __builtin_inf();
           if (((v >> 3) & 1u) == DL_TICK) S.dirty |= S.ta_exec_mask;
           else dl_deliver<G>(S, v >> 4, (int)(v & 7u));
         }
@@ -2218,8 +2227,7 @@ Layout make_layout(const KModel &m, int n) {
   size_t dl = 4096;
   while (dl < 2 * (size_t)n + 8192) dl <<= 1;
   L.dl_mask = (uint32_t)(dl - 1);
-  L.dl_t = take(8 * dl);
-  L.dl_v = take(4 * dl);
+  L.dl = take(sizeof(DlEnt) * dl);
   const int maxq = m.max_path > 0 ? m.max_path : 1;
   L.n_chunks = (int)(((size_t)n * maxq + kChunk - 1) / kChunk) + 2 * kMaxSI + 16;
   L.pool = take(4 * (size_t)L.n_chunks * kChunk);
