@@ -352,6 +352,19 @@ struct SlotPtr {
   }
   __device__ __forceinline__ SlotPtr operator+(uint32_t i) const { return SlotPtr{&(*this)[i], sh}; }
 };
+// k_fine<true>: the four words of a running slot, read in one 16-byte load
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+struct Slot4 {
+  uint32_t r, k, g, q;
+};
+__device__ __forceinline__ Slot4 slot_get(const SlotPtr &rr, uint32_t j) {
+  const u32x4 v = *(const CF_GLOBAL u32x4 *)((CF_GLOBAL char *)rr.p + (j << 4));
+  return Slot4{v.x, v.y, v.z, v.w};
+}
+__device__ __forceinline__ void slot_put(const SlotPtr &rr, uint32_t j, const Slot4 &w) {
+  const u32x4 v = {w.r, w.k, w.g, w.q};
+  *(CF_GLOBAL u32x4 *)((CF_GLOBAL char *)rr.p + (j << 4)) = v;
+}
 // element o of a read-only input array
 template <typename T>
 __device__ __forceinline__ T gload(const T *p, size_t o) {
@@ -751,35 +764,31 @@ __device__ __forceinline__ double slot_vis(const Sim &S, uint32_t r, uint32_t to
 // k_fine<true>: slot_vis from the slot's gate word g and thinker join step
 // q0, without reading the request's record or trace: the step's ring entry
 // is the time of its token (for a finished thinker's last token too, while
-// that step is kept in the ring).
+// that step is kept in the ring).  The thinker's ring slot, step counter,
+// schedule and ring entry are read before the case is known, so the reads
+// overlap; comm is the model's transfer delay.
 __device__ __forceinline__ double slot_vis_g(const Sim &S, uint32_t r, uint32_t g, uint32_t q0, uint32_t tok, int x,
-                                             int &xth, int &wsi, bool &undecided) {
+                                             double comm, int &xth, int &wsi, bool &undecided) {
   xth = x;
   wsi = -1;
   if (!(g & RG_GATED)) return -__builtin_inf();
   xth = (int)((g >> 16) & 63u);
   const uint32_t nth = g & 0xFFFFu;
   const uint32_t k = tok + 1u < nth ? tok + 1u : nth;
-  const double delta = (xth == x) ? 0.0 : S.A->m.comm;
-  double e;
-  if (k <= 1) {
-    e = S.req[r].t.tfirst;
-  } else {
-    const int lx = (int)((g >> 22) & 511u);
-    const int slot = S.si.hist[lx];
-    const uint32_t q = q0 + k - 1u;
-    if (q > S.si.sched[slot]) {
-      wsi = slot;
-      return __builtin_inf();
-    }
-    const uint32_t it = S.si.iter[lx];
-    const GPtr<double> h = S.hist + (uint32_t)(slot * kRing);
-    if (q > it) {
-      wsi = slot;  // predicted end of a step of the running decode run
-      e = h[q & (kRing - 1)];
-    } else if (it - q < (uint32_t)kKeep) {
-      e = h[q & (kRing - 1)];
-    } else if (k == nth && (S.req[r].r.misc & MISC_TH_DONE)) {
+  const double delta = (xth == x) ? 0.0 : comm;
+  if (k <= 1) return S.req[r].t.tfirst + delta;
+  const int lx = (int)((g >> 22) & 511u);
+  const int slot = S.si.hist[lx];
+  const uint32_t it = S.si.iter[lx];
+  const uint32_t q = q0 + k - 1u;
+  const GPtr<double> h = S.hist + (uint32_t)(slot * kRing);
+  const double hq = h[q & (kRing - 1)];  // every kept or scheduled step's entry
+  const bool pend = q > S.si.sched[slot];  // the step is not scheduled yet
+  const bool pred = q > it;                // predicted end of a step of the running decode run
+  wsi = (pend || pred) ? slot : -1;
+  double e = hq;
+  if (!pend && !pred && it - q >= (uint32_t)kKeep) {
+    if (k == nth && (S.req[r].r.misc & MISC_TH_DONE)) {
       e = S.req[r].t.tlast;
     } else {
       e = h[(it - (kKeep - 1)) & (kRing - 1)];  // oldest kept step: token k is no later
@@ -789,7 +798,7 @@ __device__ __forceinline__ double slot_vis_g(const Sim &S, uint32_t r, uint32_t 
       }
     }
   }
-  return e + delta;
+  return pend ? __builtin_inf() : e + delta;
 }
 
 template <bool G>
@@ -1154,22 +1163,24 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
     const int rn = S.si.rn[lx];
     const SlotPtr rr = S.run_r + (uint32_t)S.si.roff[lx];
     const SlotPtr rk = S.run_k + (uint32_t)S.si.roff[lx];
-    const SlotPtr rg = S.run_g + (uint32_t)S.si.roff[lx];
-    const SlotPtr rq = S.run_q + (uint32_t)S.si.roff[lx];
     uint32_t cntm = 0;
     if (G && S.gmark_si == si) {
       cntm = S.gmark_n;  // marked by runnable_kind in this instant
     } else {
+      const double comm = m.comm;
       bool undecided = false;
       for (int b = 0; b < rn; b += 64) {
         const int j = b + lane_id();
         if (j < rn) {
-          const uint32_t v = rk[j];
+          uint32_t v;
           bool el;
           if constexpr (G) {
+            const Slot4 w = slot_get(rr, (uint32_t)j);
+            v = w.k;
             int xth, wsi;
-            el = slot_vis_g(S, rr[j], rg[j], rq[j], v & RK_TOK, x, xth, wsi, undecided) <= S.now;
+            el = slot_vis_g(S, w.r, w.g, w.q, v & RK_TOK, x, comm, xth, wsi, undecided) <= S.now;
           } else {
+            v = rk[j];
             el = eligible<G>(S, rr[j], v & RK_TOK, c, x, undecided);
           }
           rk[j] = el ? (v | MARK) : (v & ~MARK);
@@ -1214,19 +1225,19 @@ __device__ int runnable_kind(Sim &S, int x, int si, int c) {
   if (!(fl & SF_GATED)) return IT_DECODE;
   const SlotPtr rr = S.run_r + (uint32_t)S.si.roff[lx];
   const SlotPtr rk = S.run_k + (uint32_t)S.si.roff[lx];
-  const SlotPtr rg = S.run_g + (uint32_t)S.si.roff[lx];
-  const SlotPtr rq = S.run_q + (uint32_t)S.si.roff[lx];
   bool any = false, undecided = false;
   if constexpr (G) {
     // k_fine<true>: mark every eligible slot now; a decode step started on
     // this stage in the same instant takes the marks as they are
     uint32_t cnt = 0;
+    const double comm = S.A->m.comm;
     for (int b = 0; b < rn; b += 64) {
       const int j = b + lane_id();
       if (j < rn) {
-        const uint32_t v = rk[j];
+        const Slot4 w = slot_get(rr, (uint32_t)j);
+        const uint32_t v = w.k;
         int xth, wsi;
-        const bool el = slot_vis_g(S, rr[j], rg[j], rq[j], v & RK_TOK, x, xth, wsi, undecided) <= S.now;
+        const bool el = slot_vis_g(S, w.r, w.g, w.q, v & RK_TOK, x, comm, xth, wsi, undecided) <= S.now;
         rk[j] = el ? (v | MARK) : (v & ~MARK);
         cnt += el ? 1u : 0u;
       }
@@ -1274,19 +1285,18 @@ __device__ __forceinline__ GateView local_gate_view(const Sim &S, int x, int si)
     if (rn == 0) continue;
     nbusy++;
     gsi = g;
-    const SlotPtr rk = S.run_k + (uint32_t)S.si.roff[lg];
-    const SlotPtr rg = S.run_g + (uint32_t)S.si.roff[lg];
-    const SlotPtr rq = S.run_q + (uint32_t)S.si.roff[lg];
+    const SlotPtr rr = S.run_r + (uint32_t)S.si.roff[lg];
     for (int b = 0; b < rn; b += 64) {
       const int j = b + lane_id();
       if (j < rn) {
-        const uint32_t v = rk[j], g = rg[j];
+        const Slot4 w = slot_get(rr, (uint32_t)j);
+        const uint32_t v = w.k, g = w.g;
         const uint32_t tok = v & RK_TOK;
         bool waits_next = false;
         if ((g & RG_GATED) && (int)((g >> 22) & 511u) == lth && (int)((g >> 16) & 63u) == x) {
           const uint32_t nth = g & 0xFFFFu;
           const uint32_t k = tok + 1u < nth ? tok + 1u : nth;
-          const uint32_t q = rq[j] + k - 1u;
+          const uint32_t q = w.q + k - 1u;
           // a thinker on this executor has finished once its last step is completed
           if (k > 1u && !(k == nth && q < next)) {
             qmin = q < qmin ? q : qmin;
@@ -1457,9 +1467,7 @@ __device__ void run_compact(Sim &S, int si, const bool *drop) {
   const int rn = S.si.rn[lx];
   const SlotPtr rr = S.run_r + (uint32_t)S.si.roff[lx];
   const SlotPtr rk = S.run_k + (uint32_t)S.si.roff[lx];
-  const SlotPtr rg = S.run_g + (uint32_t)S.si.roff[lx];
-  const SlotPtr rq = S.run_q + (uint32_t)S.si.roff[lx];
-  const bool gated = G && (si_flags<G>(S.si, si) & SF_GATED);  // k_fine<true>: gate words move with their slots
+  // k_fine<true>: a slot's four words move together (one 16-byte load and store)
   uint32_t vr[CF_MAX_BATCH / 64], vk[CF_MAX_BATCH / 64], vg[CF_MAX_BATCH / 64], vq[CF_MAX_BATCH / 64];
   bool keep[CF_MAX_BATCH / 64];
 #pragma unroll
@@ -1471,11 +1479,15 @@ __device__ void run_compact(Sim &S, int si, const bool *drop) {
     vg[p] = 0;
     vq[p] = 0;
     if (j < rn) {
-      vr[p] = rr[j];
-      vk[p] = rk[j];
-      if (gated) {
-        vg[p] = rg[j];
-        vq[p] = rq[j];
+      if constexpr (G) {
+        const Slot4 w = slot_get(rr, (uint32_t)j);
+        vr[p] = w.r;
+        vk[p] = w.k;
+        vg[p] = w.g;
+        vq[p] = w.q;
+      } else {
+        vr[p] = rr[j];
+        vk[p] = rk[j];
       }
       keep[p] = !drop[p];
     }
@@ -1487,11 +1499,11 @@ __device__ void run_compact(Sim &S, int si, const bool *drop) {
     const uint64_t bal = __ballot(keep[p]);
     if (keep[p]) {
       const uint32_t d = w + lanes_below(bal);
-      rr[d] = vr[p];
-      rk[d] = vk[p];
-      if (gated) {
-        rg[d] = vg[p];
-        rq[d] = vq[p];
+      if constexpr (G) {
+        slot_put(rr, d, Slot4{vr[p], vk[p], vg[p], vq[p]});
+      } else {
+        rr[d] = vr[p];
+        rk[d] = vk[p];
       }
       mn = vk[p] < mn ? vk[p] : mn;
     }
@@ -1674,20 +1686,19 @@ __device__ __forceinline__ bool gate_wake(Sim &S, int y) {
   if (!(st & 1u) || (st & EX_RUN)) {
     const uint32_t geo = sh.ex_geo[y];
     const int ns = __popc((geo >> 16) & 0xFFu), first = (int)(geo & 0xFFFFu);
+    const double comm = S.A->m.comm;
     bool undecided = false;
     for (int g = first; g < first + ns; g++) {
       if (!(si_flags<true>(S.si, g) & SF_GATED)) continue;
       const int lg = lx_of<true>(S.si, g);
       const int rn = S.si.rn[lg];
       const SlotPtr rr = S.run_r + (uint32_t)S.si.roff[lg];
-      const SlotPtr rk = S.run_k + (uint32_t)S.si.roff[lg];
-      const SlotPtr rg = S.run_g + (uint32_t)S.si.roff[lg];
-      const SlotPtr rq = S.run_q + (uint32_t)S.si.roff[lg];
       for (int b = 0; b < rn; b += 64) {
         const int j = b + lane_id();
         if (j < rn) {
+          const Slot4 sw = slot_get(rr, (uint32_t)j);
           int xth, wsi;
-          const double tv = slot_vis_g(S, rr[j], rg[j], rq[j], rk[j] & RK_TOK, y, xth, wsi, undecided);
+          const double tv = slot_vis_g(S, sw.r, sw.g, sw.q, sw.k & RK_TOK, y, comm, xth, wsi, undecided);
           if (xth != y) {
             if (wsi >= 0) atomicOr((unsigned long long *)&S.si.watch[wsi], 1ull << y);
             if (tv <= S.now) now_el = true;
