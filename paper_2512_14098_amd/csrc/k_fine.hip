@@ -1183,7 +1183,7 @@ __device__ void start_iter(Sim &S, int x, int l, int si, int c, int kind, bool l
             v = rk[j];
             el = eligible<G>(S, rr[j], v & RK_TOK, c, x, undecided);
           }
-          rk[j] = el ? (v | MARK) : (v & ~MARK);
+          if (el != ((v & MARK) != 0)) rk[j] = v ^ MARK;  // only a changed mark is written
           cntm += el ? 1u : 0u;
         }
       }
@@ -1238,7 +1238,7 @@ __device__ int runnable_kind(Sim &S, int x, int si, int c) {
         const uint32_t v = w.k;
         int xth, wsi;
         const bool el = slot_vis_g(S, w.r, w.g, w.q, v & RK_TOK, x, comm, xth, wsi, undecided) <= S.now;
-        rk[j] = el ? (v | MARK) : (v & ~MARK);
+        if (el != ((v & MARK) != 0)) rk[j] = v ^ MARK;  // only a changed mark is written
         cnt += el ? 1u : 0u;
       }
     }
