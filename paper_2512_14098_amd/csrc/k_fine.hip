@@ -897,13 +897,16 @@ __device__ void dl_deliver(Sim &S, uint32_t r, int c2) {
 }
 
 // Lane-parallel processing of the n members mem[0..n) of a completed
-// iteration of stage si (component c) on executor x, in member order.
+// iteration of stage si (component c) on executor x, in member order.  With
+// rs, the members are instead the running slots j < n of rs whose page bit
+// j / 64 is set in fbits (the slot order is the member order).
 //   IT_BATCH:   ENC/GEN members finish c;
 //   IT_PREFILL: members get their first token (TTFT stamps, thinker's
 //               streaming delivery to the talker) and finish or join Run;
 //   IT_FINISH:  decode members that produced their last token finish c.
 template <bool G>
-__device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr<uint32_t> mem) {
+__device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr<uint32_t> mem,
+                             const SlotPtr *rs = nullptr, uint32_t fbits = 0u) {
   const KModel &m = S.A->m;
   const ModelLds &ml = S.sh->ml;
   const bool gated = si_flags<G>(S.si, si) & SF_GATED;
@@ -912,13 +915,14 @@ __device__ void members_done(Sim &S, int x, int si, int c, int kind, int n, GPtr
   const double now = S.now;
   for (int b = 0; b < n; b += 64) {
     const int j = b + lane_id();
-    const bool valid = j < n;
+    const bool valid = j < n && (!rs || ((fbits >> (b >> 6)) & 1u));
+    if (rs && !__ballot(valid)) continue;  // a page of slots with none finishing
     uint32_t r = 0;
     Rec R = {0, 0, 0};
     uint32_t a_no = 0;  // prefill: the request's output-length attribute at c
     uint64_t tkv = 0;   // the request's arrival tick
     if (valid) {
-      r = mem[j];
+      r = rs ? (*rs)[j] : mem[j];
       // loads that depend on the request id only, issued with its record
       R = rec_get(S, r);
       tkv = gload(S.A->ticks, S.soff + r);
@@ -1514,25 +1518,34 @@ __device__ void run_compact(Sim &S, int si, const bool *drop) {
   if (!(si_flags<G>(S.si, si) & SF_GATED)) S.si.minfin[lx] = dpp_min_u32(mn);
 }
 
-// collects the running slots flagged in fin[] (slot order) into mem,
-// processes them as finishing members, and drops them from the running set
+// processes the running slots flagged in fin[] as finishing members (slot
+// order), and drops them from the running set.  k_fine<false> takes them
+// straight from their slots; k_fine<true> first collects them into mem (the
+// shorter members_done loop measures faster there).
 template <bool G>
 __device__ void finish_slots(Sim &S, int x, int si, int c, const bool *fin) {
   const int lx = lx_of<G>(S.si, si);
   const int rn = S.si.rn[lx];
   const SlotPtr rr = S.run_r + (uint32_t)S.si.roff[lx];
-  const GPtr<uint32_t> mem = S.mem + (uint32_t)(x * CF_MAX_BATCH);
-  uint32_t nf = 0;
+  if constexpr (G) {
+    const GPtr<uint32_t> mem = S.mem + (uint32_t)(x * CF_MAX_BATCH);
+    uint32_t nf = 0;
 #pragma unroll
-  for (int p = 0; p < CF_MAX_BATCH / 64; p++) {
-    const int j = p * 64 + lane_id();
-    const bool f = j < rn && fin[p];
-    const uint64_t bal = __ballot(f);
-    if (f) mem[nf + lanes_below(bal)] = rr[j];
-    nf += (uint32_t)__popcll(bal);
+    for (int p = 0; p < CF_MAX_BATCH / 64; p++) {
+      const int j = p * 64 + lane_id();
+      const bool f = j < rn && fin[p];
+      const uint64_t bal = __ballot(f);
+      if (f) mem[nf + lanes_below(bal)] = rr[j];
+      nf += (uint32_t)__popcll(bal);
+    }
+    __syncthreads();
+    members_done<G>(S, x, si, c, IT_FINISH, (int)nf, mem);
+  } else {
+    uint32_t fbits = 0;
+#pragma unroll
+    for (int p = 0; p < CF_MAX_BATCH / 64; p++) fbits |= (fin[p] ? 1u : 0u) << p;
+    members_done<G>(S, x, si, c, IT_FINISH, rn, S.mem, &rr, fbits);
   }
-  __syncthreads();
-  members_done<G>(S, x, si, c, IT_FINISH, (int)nf, mem);
   run_compact<G>(S, si, fin);
 }
 
