@@ -1347,12 +1347,21 @@ __device__ __forceinline__ bool start_joint(Sim &S, int x, int lth, int sth, int
   if (2u * kta < n) n = 2u * kta;
   const int slot = S.si.hist[lx];
   const GPtr<double> h = S.hist + (uint32_t)(slot * kRing);
-  double t = S.now;
-  for (uint32_t i = 1; i <= n; i++) {
-    t = t + ((i & 1u) ? d1 : d2);
-    if ((i & 1u) && lane_id() == 0) h[(it0 + ((i + 1u) >> 1)) & (kRing - 1)] = t;
+  // thinker step s, then talker step s while the run lasts; lane j keeps the
+  // end of the j-th thinker step of the current block of 64, written to the
+  // ring when the block is complete
+  const uint32_t nth = (n + 1u) >> 1;
+  double t = S.now, tl = 0.0;
+  for (uint32_t s = 1; s <= nth; s++) {
+    t = t + d1;
+    const uint32_t j = (s - 1u) & 63u;
+    tl = (uint32_t)lane_id() == j ? t : tl;
+    if (j == 63u || s == nth) {
+      if ((uint32_t)lane_id() <= j) h[(it0 + s - j + (uint32_t)lane_id()) & (kRing - 1)] = tl;
+    }
+    if (2u * s <= n) t = t + d2;
   }
-  S.si.sched[slot] = it0 + ((n + 1u) >> 1);
+  S.si.sched[slot] = it0 + nth;
   xt_set<true, XT_T0>(S, x, S.now);
   xt_set<true, XT_DUR>(S, x, d1);
   S.r_dur2 = lane_id() == x ? d2 : S.r_dur2;
