@@ -50,18 +50,18 @@ _W_C4_STEP = ("c4: Full coarse-to-fine sweep of the omni graph on 64 simulated G
               "the trace of all 64 seeds, phase 1 over all 1000000 plans, the top 1000 and their 32-rate grid, "
               "phase 3 of every selected plan at every rate on one seed (seed g at step g), their goodput reduction")
 MEASURED_TRAFFIC = {
-    ("9953da8079ca9c5c", _W_C4_STEP): 1.4857e13,
-    ("9953da8079ca9c5c", _W_C1): 8.4902e11,
-    ("9953da8079ca9c5c", _W_C2_SEEDS2): 7.9134e11,
-    ("9953da8079ca9c5c", _W_C3_SEED0): 1.7986e12,
+    ("7ed4a4b598700ba3", _W_C4_STEP): 1.4861e13,
+    ("7ed4a4b598700ba3", _W_C1): 8.4908e11,
+    ("7ed4a4b598700ba3", _W_C2_SEEDS2): 7.9068e11,
+    ("7ed4a4b598700ba3", _W_C3_SEED0): 1.8009e12,
 }
 # VALU lane rate of the k_fine launch by rocprofv3 counters (SQ_INSTS_VALU x SQ_THREAD_CYCLES_VALU /
 # SQ_ACTIVE_INST_VALU / kernel time / PEAK_LANE_OPS), keyed like MEASURED_TRAFFIC
 MEASURED_LANE_FRAC = {
-    ("9953da8079ca9c5c", _W_C4_STEP): 0.3747,
-    ("9953da8079ca9c5c", _W_C1): 0.4311,
-    ("9953da8079ca9c5c", _W_C2_SEEDS2): 0.4017,
-    ("9953da8079ca9c5c", _W_C3_SEED0): 0.3960,
+    ("7ed4a4b598700ba3", _W_C4_STEP): 0.3829,
+    ("7ed4a4b598700ba3", _W_C1): 0.4314,
+    ("7ed4a4b598700ba3", _W_C2_SEEDS2): 0.4059,
+    ("7ed4a4b598700ba3", _W_C3_SEED0): 0.3950,
 }
 ENUM_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_enum.hip", "paper_2512_14098_amd/csrc/cf_internal.h",
                        "paper_2512_14098_amd/csrc/cf_phase1.h")
