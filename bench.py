@@ -66,10 +66,10 @@ MEASURED_LANE_FRAC = {
 ENUM_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_enum.hip", "paper_2512_14098_amd/csrc/cf_internal.h",
                        "paper_2512_14098_amd/csrc/cf_phase1.h")
 # bytes per k_enum_unrank launch of 2^25 plans (the write counter reads exactly the table bytes)
-ENUM_MEASURED_TRAFFIC = {("960f3fbf7af75a5d", 1 << 25): 7.8190e9}
+ENUM_MEASURED_TRAFFIC = {("7c49ce14ae2f9bb3", 1 << 25): 7.8195e9}
 MC_MEASURED_TRAFFIC = {
-    ("dfdb2b4408dfe475", "c4 phase 2: the 17444 plans phase 1 keeps of 1000000, 1024 sampled requests (seed 0), "
-     "alpha 0.8, then Pareto pruning"): 3.7237e8,
+    ("7c84b8868934b26b", "c4 phase 2: the 17471 plans phase 1 keeps of 1000000, 1024 sampled requests (seed 0), "
+     "alpha 0.8, then Pareto pruning"): 3.7331e8,
 }
 
 
