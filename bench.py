@@ -66,7 +66,7 @@ MEASURED_LANE_FRAC = {
 ENUM_KERNEL_SOURCES = ("paper_2512_14098_amd/csrc/k_enum.hip", "paper_2512_14098_amd/csrc/cf_internal.h",
                        "paper_2512_14098_amd/csrc/cf_phase1.h")
 # bytes per k_enum_unrank launch of 2^25 plans (the write counter reads exactly the table bytes)
-ENUM_MEASURED_TRAFFIC = {("7c49ce14ae2f9bb3", 1 << 25): 7.8195e9}
+ENUM_MEASURED_TRAFFIC = {("b9ac6efd2fcc5a5b", 1 << 25): 7.8191e9}
 MC_MEASURED_TRAFFIC = {
     ("7c84b8868934b26b", "c4 phase 2: the 17471 plans phase 1 keeps of 1000000, 1024 sampled requests (seed 0), "
      "alpha 0.8, then Pareto pruning"): 3.7331e8,

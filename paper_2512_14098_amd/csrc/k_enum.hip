@@ -301,7 +301,10 @@ __device__ NodeCfg place(const EnumView &V, const OptsLds &so, Cursor &c, int v,
 // Four consecutive plans per thread, each slot row written with one 32-bit
 // store (64-bit for the batch row): a wavefront writes 256 bytes of a row
 // per instruction.  Needs out.P % 4 == 0; the last thread writes bytes.
+// HET: the space has nodes of two configurations (o.het); without them the
+// walk over configuration pairs is not compiled in.
 constexpr int kPlansPerThread = 4;
+template <bool HET>
 __global__ void __launch_bounds__(256) k_enum_unrank(cf_enum_opts o, EnumView V, const uint64_t *offsets,
                                                     uint64_t first, int count, PlanOut out) {
   __shared__ OptsLds so;
@@ -335,7 +338,7 @@ __global__ void __launch_bounds__(256) k_enum_unrank(cf_enum_opts o, EnumView V,
   for (int v = 0; v < CF_MAX_NODES; v++) {
     NodeCfg nc[kPlansPerThread];
 #pragma unroll
-    for (int j = 0; j < kPlansPerThread; j++) nc[j] = same[j] ? nc[j - 1] : place(V, so, cur[j], v, o.het != 0);
+    for (int j = 0; j < kPlansPerThread; j++) nc[j] = same[j] ? nc[j - 1] : place(V, so, cur[j], v, HET);
 #pragma unroll
     for (int j = 0; j < kPlansPerThread; j++) b8[j] = nc[j].comp;
     put8(out.node_comp + v * P, b8);
@@ -687,8 +690,12 @@ extern "C" cf_status cf_enum_plans(const cf_model_desc *model, const cf_enum_opt
   o.node_gpus2 = const_cast<uint8_t *>(out->node_gpus2_dev);
   o.node_w = const_cast<uint8_t *>(out->node_w_dev);
   const unsigned threads = (unsigned)((count + kPlansPerThread - 1) / kPlansPerThread);
-  hipLaunchKernelGGL(k_enum_unrank, dim3((threads + 255) / 256), dim3(256), 0, s, *opts, V, offsets_dev, first,
-                     count, o);
+  if (opts->het)
+    hipLaunchKernelGGL(k_enum_unrank<true>, dim3((threads + 255) / 256), dim3(256), 0, s, *opts, V, offsets_dev, first,
+                       count, o);
+  else
+    hipLaunchKernelGGL(k_enum_unrank<false>, dim3((threads + 255) / 256), dim3(256), 0, s, *opts, V, offsets_dev,
+                       first, count, o);
   return hip_check(hipGetLastError(), "cf_enum_plans launch");
 }
 
